@@ -1,0 +1,309 @@
+"""Plain fp64 CPU oracle for the fused hybrid causal-attention layer of
+Selective Attention Freezing ("When Can Attention Heads Be Statically
+Defined?").
+
+TEST INFRASTRUCTURE ONLY.  Only the test suite, ``__graft_entry__.smoke()``
+and the ``cpu_baseline`` leg of ``bench.py`` may import or call this module.
+The GPU product path never imports it, and this module imports nothing from
+the product package: the two share no code.  Inputs reach both sides from the
+seeded generators in ``paper_2609_34650_amd.inputs``, which hold none of the
+method's arithmetic.
+
+Everything here evaluates the plain dense definitions in float64, one
+(batch, head) slice at a time, materialising each causal weight matrix:
+
+* Ordinary head (Appendix "Attention notation and calibration",
+  Eqs. standard-head): ``S = Q K^T / sqrt(d_h)``, ``A = softmax_causal(S)``
+  with the diagonal visible, ``Z = A V``.
+* Replaced (fixed) head (Section "Fixed-pattern construction and fitting",
+  Eq. compact-prior): with 1-based key index ``alpha(1..T)`` and offset index
+  ``rho(0..T-1)``, ``P(i, j) = exp(alpha(j) + rho(i - j)) / Z(i)`` for
+  ``j <= i`` and 0 otherwise, where ``Z(i)`` sums the numerator over
+  ``j <= i``.  There is no ``1/sqrt(d_h)`` on these logits.  The output is
+  ``P V`` (Section "Replacing Attention with a Fixed Pattern").
+* Backward of the loss ``sum(O * dO)``: for a fixed head only the value
+  gradient ``dV = P^T dO`` exists (Section "Replacement schedules and fused
+  execution", paragraph "Fused computation"); its query and key slots get
+  zero gradients (Appendix "Mixed-head execution and numerical checks").
+  For an ordinary head the gradients are the chain rule through softmax.
+
+Readings of points the paper leaves open (each is listed in the design doc):
+
+* 0-based storage: ``a[j] = alpha(j + 1)`` and ``r[delta] = rho(delta)``.
+* The per-row log-normaliser is returned as ``LSE`` (natural log): for an
+  ordinary head ``logsumexp_j S[i, j]`` over ``j <= i``, for a fixed head
+  ``log Z(i)``.
+* A prior vector longer than the sequence is used through its prefix.
+
+Rows of a causal weight matrix are independent of one another (each query row
+is normalised on its own), so every function may evaluate the rows in blocks
+to bound memory; ``row_block`` never changes a result beyond float64
+rounding of independent rows.
+"""
+
+from __future__ import annotations
+
+import math
+import os
+from typing import Optional, Sequence, Tuple
+
+import numpy as np
+
+__all__ = [
+    "fixed_logits",
+    "fixed_pattern",
+    "fixed_log_normaliser",
+    "ordinary_logits",
+    "head_forward",
+    "head_backward",
+    "layer_forward",
+    "layer_backward",
+    "layer_forward_backward_parallel",
+]
+
+_F64 = np.float64
+
+
+def _as64(x) -> np.ndarray:
+    return np.asarray(x, dtype=_F64)
+
+
+# ---------------------------------------------------------------------------
+# Logit matrices (causal; -inf above the diagonal)
+# ---------------------------------------------------------------------------
+
+def fixed_logits(a, r, rows: np.ndarray, n_keys: int) -> np.ndarray:
+    """Logits ``L[i, j] = a[j] + r[i - j]`` of a fixed head for the query rows
+    ``rows`` against keys ``0..n_keys-1``; ``-inf`` where ``j > i``.
+
+    Eq. compact-prior: the numerator of ``P(i, j)`` is
+    ``exp(alpha(j) + rho(i - j))`` for ``j <= i``; no temperature is applied.
+    """
+    a = _as64(a)
+    r = _as64(r)
+    rows = np.asarray(rows, dtype=np.int64)
+    j = np.arange(n_keys, dtype=np.int64)
+    offset = rows[:, None] - j[None, :]            # i - j
+    visible = offset >= 0                          # causal: j <= i
+    out = np.full(offset.shape, -np.inf, dtype=_F64)
+    out[visible] = a[np.broadcast_to(j[None, :], offset.shape)[visible]] + r[offset[visible]]
+    return out
+
+
+def ordinary_logits(q, k, rows: np.ndarray) -> np.ndarray:
+    """Scores ``S[i, j] = q_i . k_j / sqrt(d_h)`` for the query rows ``rows``;
+    ``-inf`` where ``j > i`` (Eqs. standard-head; causal softmax masks future
+    keys and keeps the diagonal)."""
+    q = _as64(q)
+    k = _as64(k)
+    d = q.shape[1]
+    rows = np.asarray(rows, dtype=np.int64)
+    s = (q[rows] @ k.T) / math.sqrt(d)
+    j = np.arange(k.shape[0], dtype=np.int64)
+    s[j[None, :] > rows[:, None]] = -np.inf
+    return s
+
+
+def _row_logsumexp(logits: np.ndarray) -> np.ndarray:
+    """Natural-log row normaliser ``log sum_j exp(L[i, j])`` (each row has at
+    least its diagonal entry finite)."""
+    m = np.max(logits, axis=1)
+    return m + np.log(np.sum(np.exp(logits - m[:, None]), axis=1))
+
+
+def fixed_log_normaliser(a, r, n: Optional[int] = None) -> np.ndarray:
+    """``log Z(i)`` of Eq. compact-prior for ``i = 0..n-1``."""
+    a = _as64(a)
+    n = a.shape[0] if n is None else n
+    rows = np.arange(n)
+    return _row_logsumexp(fixed_logits(a, r, rows, n))
+
+
+def fixed_pattern(a, r, n: Optional[int] = None) -> np.ndarray:
+    """Dense ``n x n`` compact pattern ``P`` of Eq. compact-prior (lower
+    triangular, rows sum to one)."""
+    a = _as64(a)
+    n = a.shape[0] if n is None else n
+    rows = np.arange(n)
+    L = fixed_logits(a, r, rows, n)
+    return np.exp(L - _row_logsumexp(L)[:, None])
+
+
+# ---------------------------------------------------------------------------
+# One (batch, head) slice
+# ---------------------------------------------------------------------------
+
+def _probs_block(q, k, fixed: bool, a, r, rows, n) -> Tuple[np.ndarray, np.ndarray]:
+    """Causal weights of the given query rows and their log-normalisers."""
+    if fixed:
+        L = fixed_logits(a, r, rows, n)
+    else:
+        L = ordinary_logits(q, k, rows)
+    lse = _row_logsumexp(L)
+    return np.exp(L - lse[:, None]), lse
+
+
+def head_forward(q, k, v, fixed: bool, a=None, r=None,
+                 row_block: int = 512) -> Tuple[np.ndarray, np.ndarray]:
+    """Forward of one head: returns ``O`` ``[n, d]`` and ``LSE`` ``[n]``.
+
+    Ordinary: ``O = softmax_causal(Q K^T / sqrt(d)) V``.  Fixed: ``O = P V``
+    with ``P`` from ``a`` and ``r``; ``q`` and ``k`` are not read.
+    """
+    v = _as64(v)
+    n = v.shape[0]
+    if fixed:
+        a = _as64(a)[:n]
+        r = _as64(r)[:n]
+    o = np.empty_like(v)
+    lse = np.empty(n, dtype=_F64)
+    for start in range(0, n, row_block):
+        rows = np.arange(start, min(n, start + row_block))
+        p, lse_blk = _probs_block(q, k, fixed, a, r, rows, n)
+        o[rows] = p @ v
+        lse[rows] = lse_blk
+    return o, lse
+
+
+def head_backward(q, k, v, do, fixed: bool, a=None, r=None,
+                  row_block: int = 512) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
+    """Gradients of ``sum(O * dO)`` for one head: ``dQ, dK, dV``.
+
+    Fixed head: ``dV = P^T dO`` and ``dQ = dK = 0`` (the pattern takes no
+    gradient).  Ordinary head: ``dV = P^T dO``, ``dP = dO V^T``,
+    ``D_i = sum_j P_ij dP_ij``, ``dS = P * (dP - D)``,
+    ``dQ = dS K / sqrt(d)``, ``dK = dS^T Q / sqrt(d)``.  ``D`` is taken from
+    its definition, not from the ``rowsum(dO * O)`` identity that a kernel
+    would use.
+    """
+    v = _as64(v)
+    do = _as64(do)
+    n, d = v.shape
+    dv = np.zeros_like(v)
+    if fixed:
+        a = _as64(a)[:n]
+        r = _as64(r)[:n]
+        for start in range(0, n, row_block):
+            rows = np.arange(start, min(n, start + row_block))
+            p, _ = _probs_block(None, None, True, a, r, rows, n)
+            dv += p.T @ do[rows]
+        return np.zeros((n, d)), np.zeros((n, d)), dv
+    q = _as64(q)
+    k = _as64(k)
+    dq = np.zeros_like(q)
+    dk = np.zeros_like(k)
+    scale = 1.0 / math.sqrt(d)
+    for start in range(0, n, row_block):
+        rows = np.arange(start, min(n, start + row_block))
+        p, _ = _probs_block(q, k, False, None, None, rows, n)
+        dv += p.T @ do[rows]
+        dp = do[rows] @ v.T
+        D = np.sum(p * dp, axis=1)
+        ds = p * (dp - D[:, None])
+        dq[rows] = (ds @ k) * scale
+        dk += (ds.T @ q[rows]) * scale
+    return dq, dk, dv
+
+
+# ---------------------------------------------------------------------------
+# Whole layer [B, H, N, d]
+# ---------------------------------------------------------------------------
+
+def _check_layer(Q, K, V, is_fixed, a, r):
+    V = np.asarray(V)
+    B, H, N, d = V.shape
+    is_fixed = np.asarray(is_fixed).astype(bool).reshape(-1)
+    if is_fixed.shape[0] != H:
+        raise ValueError("is_fixed must have one flag per head")
+    if is_fixed.any():
+        if a is None or r is None:
+            raise ValueError("a fixed head needs both preference vectors")
+        if np.asarray(a).shape[0] != H or np.asarray(r).shape[0] != H:
+            raise ValueError("a and r are [H, >=N]")
+        if np.asarray(a).shape[1] < N or np.asarray(r).shape[1] < N:
+            raise ValueError("a and r must cover N positions")
+    if not is_fixed.all():
+        if Q is None or K is None:
+            raise ValueError("ordinary heads need Q and K")
+    return B, H, N, d, is_fixed
+
+
+def layer_forward(Q, K, V, is_fixed, a=None, r=None, row_block: int = 512,
+                  heads: Optional[Sequence[Tuple[int, int]]] = None):
+    """Forward of the hybrid layer.  Returns ``O`` ``[B,H,N,d]`` and ``LSE``
+    ``[B,H,N]`` in float64.  If ``heads`` lists ``(b, h)`` pairs, only those
+    slices are computed and the rest of the outputs are NaN."""
+    B, H, N, d, is_fixed = _check_layer(Q, K, V, is_fixed, a, r)
+    O = np.full((B, H, N, d), np.nan)
+    LSE = np.full((B, H, N), np.nan)
+    todo = heads if heads is not None else [(b, h) for b in range(B) for h in range(H)]
+    for b, h in todo:
+        fx = bool(is_fixed[h])
+        o, lse = head_forward(
+            None if fx else Q[b, h], None if fx else K[b, h], V[b, h], fx,
+            a[h] if fx else None, r[h] if fx else None, row_block)
+        O[b, h] = o
+        LSE[b, h] = lse
+    return O, LSE
+
+
+def layer_backward(Q, K, V, dO, is_fixed, a=None, r=None, row_block: int = 512,
+                   heads: Optional[Sequence[Tuple[int, int]]] = None):
+    """Gradients ``dQ, dK, dV`` ``[B,H,N,d]`` (float64) of ``sum(O * dO)``.
+    Fixed heads get exact zeros in ``dQ`` and ``dK``."""
+    B, H, N, d, is_fixed = _check_layer(Q, K, V, is_fixed, a, r)
+    dQ = np.full((B, H, N, d), np.nan)
+    dK = np.full((B, H, N, d), np.nan)
+    dV = np.full((B, H, N, d), np.nan)
+    todo = heads if heads is not None else [(b, h) for b in range(B) for h in range(H)]
+    for b, h in todo:
+        fx = bool(is_fixed[h])
+        dq, dk, dv = head_backward(
+            None if fx else Q[b, h], None if fx else K[b, h], V[b, h], dO[b, h], fx,
+            a[h] if fx else None, r[h] if fx else None, row_block)
+        dQ[b, h] = dq
+        dK[b, h] = dk
+        dV[b, h] = dv
+    return dQ, dK, dV
+
+
+# ---------------------------------------------------------------------------
+# Process-parallel driver (used to time the oracle as a CPU baseline)
+# ---------------------------------------------------------------------------
+
+def _slice_job(args):
+    q, k, v, do, fx, a, r, row_block, backward = args
+    o, lse = head_forward(q, k, v, fx, a, r, row_block)
+    if backward:
+        head_backward(q, k, v, do, fx, a, r, row_block)
+    return o.shape[0]
+
+
+def layer_forward_backward_parallel(Q, K, V, dO, is_fixed, a, r,
+                                    heads: Sequence[Tuple[int, int]],
+                                    backward: bool = True, workers: Optional[int] = None,
+                                    row_block: int = 512) -> int:
+    """Run forward (+ backward) for the listed ``(b, h)`` slices on a process
+    pool, one slice per task.  Returns the number of worker processes used.
+    Each worker is expected to run single-threaded BLAS (the caller sets the
+    thread environment before the pool starts)."""
+    import multiprocessing as mp
+
+    is_fixed = np.asarray(is_fixed).astype(bool)
+    jobs = []
+    for b, h in heads:
+        fx = bool(is_fixed[h])
+        jobs.append((None if fx else Q[b, h], None if fx else K[b, h], V[b, h],
+                     dO[b, h] if dO is not None else None, fx,
+                     a[h] if fx else None, r[h] if fx else None, row_block, backward))
+    if workers is None:
+        workers = len(os.sched_getaffinity(0))
+    workers = max(1, min(workers, len(jobs)))
+    if workers == 1:
+        for j in jobs:
+            _slice_job(j)
+        return 1
+    ctx = mp.get_context("fork")
+    with ctx.Pool(workers) as pool:
+        pool.map(_slice_job, jobs, chunksize=1)
+    return workers
