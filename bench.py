@@ -1,0 +1,273 @@
+#!/usr/bin/env python3
+"""Benchmark of the fused hybrid causal-attention layer (forward + backward)
+on one MI355X.
+
+One step = one full layer: the forward launch followed by the three backward
+launches, over one batch of synthetic inputs already resident in HBM.  The
+default workload is the 124M-style layer: B=8, H=12 with 3 fixed heads (25 %),
+N=4096, d=64, bf16 with float32 accumulation.
+
+Prints one JSON line with:
+* ``value`` / ``ms_per_step``: wall milliseconds per layer (fwd+bwd) over the
+  timed steps (lower is better);
+* ``tflops`` and ``mfma_util``: algorithmic FLOP per layer / time, and its
+  fraction of the MI355X dense bf16 MFMA peak;
+* ``kernels``: average duration of each launch, measured with HIP events on
+  the stream the library launches on;
+* ``roofline``: the dominant launch's algorithmic FLOP / its duration;
+* ``speedup_vs_all_ordinary``: the same kernels with every head ordinary, at
+  the same shape, timed in alternating (ABBA) blocks;
+* ``cpu_baseline``: the fp64 oracle timed on this host's cores on a bounded
+  sample of (batch, head) slices, scaled to one layer.
+
+FLOP rule: one causal N x N x d contraction counts 2*d*N(N+1)/2.  An ordinary
+head counts 7 (2 forward, 5 backward: S recompute, dP, dV, dK, dQ); a fixed
+head counts 2 (P V forward, P^T dO backward).
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+from paper_2609_34650_amd import inputs as gen  # noqa: E402
+
+METRIC = "hybrid-attn fwd+bwd ms/layer + MFMA util, H=12 (25% fixed), N=4096, d=64"
+PEAK_BF16_TFLOPS = 2500.0
+PEAK_F32_TFLOPS = 157.3
+PEAK_HBM_GBS = 8000.0
+MAX_HOST_WORKERS = 16
+
+
+def contraction_flop(N: int, d: int) -> float:
+    return 2.0 * d * N * (N + 1) / 2.0
+
+
+def layer_flop(B: int, H: int, N: int, d: int, n_fixed: int, backward: bool = True):
+    """Algorithmic FLOP per launch: dict stage -> FLOP."""
+    c = contraction_flop(N, d) * B
+    n_ord = H - n_fixed
+    out = {"fwd": c * (2 * n_ord + 1 * n_fixed)}
+    if backward:
+        out["bwd_pre"] = 0.0
+        out["bwd_dkdv"] = c * (4 * n_ord + 1 * n_fixed)
+        out["bwd_dq"] = c * (1 * n_ord)
+    return out
+
+
+def stage_bytes(B: int, H: int, N: int, d: int, n_fixed: int, elem: int):
+    """Minimum HBM bytes per launch (each tensor read or written once)."""
+    t = B * N * d * elem          # one [N, d] slice per batch element
+    row = B * N * 4               # one float32 row vector per batch element
+    n_ord = H - n_fixed
+    return {
+        "fwd": n_ord * (3 * t + t + row) + n_fixed * (t + t + row),
+        "bwd_pre": n_ord * (2 * t + row),
+        "bwd_dkdv": n_ord * (4 * t + 2 * row + 2 * t) + n_fixed * (t + row + 2 * t),
+        "bwd_dq": n_ord * (4 * t + 2 * row + t) + n_fixed * t,
+    }
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="gpt124m_4k", choices=sorted(gen.WORKLOADS))
+    ap.add_argument("--cpu-baseline", dest="cpu_baseline", action="store_true", default=True)
+    ap.add_argument("--no-cpu-baseline", dest="cpu_baseline", action="store_false")
+    ap.add_argument("--cpu-slices", type=int, default=0,
+                    help="(batch, head) slices the oracle baseline runs (0: one per worker, twice)")
+    ap.add_argument("--compare-ordinary", dest="compare", action="store_true", default=True)
+    ap.add_argument("--no-compare-ordinary", dest="compare", action="store_false")
+    return ap.parse_args()
+
+
+class Layer:
+    """Device buffers and the launch sequence of one layer."""
+
+    def __init__(self, torch, inp, dtype, backward):
+        from paper_2609_34650_amd import binding
+        self.torch = torch
+        self.b = binding
+        dev = torch.device("cuda", 0)
+        tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+        self.Q = torch.from_numpy(inp["Q"]).to(dev).to(tdt)
+        self.K = torch.from_numpy(inp["K"]).to(dev).to(tdt)
+        self.V = torch.from_numpy(inp["V"]).to(dev).to(tdt)
+        self.dO = torch.from_numpy(inp["dO"]).to(dev).to(tdt) if backward else None
+        self.a = torch.from_numpy(inp["a"]).to(dev)
+        self.r = torch.from_numpy(inp["r"]).to(dev)
+        B, H, N, d = self.V.shape
+        self.O = torch.empty_like(self.V)
+        self.LSE = torch.empty((B, H, N), dtype=torch.float32, device=dev)
+        self.backward = backward
+        if backward:
+            self.dQ, self.dK, self.dV = (torch.empty_like(self.V) for _ in range(3))
+            nbytes = binding.saf_hybrid_attn_bwd_workspace_bytes(tdt, B, H, N, d)
+            self.ws = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+        self.stages = ["fwd"] + (["bwd_pre", "bwd_dkdv", "bwd_dq"] if backward else [])
+
+    def step(self, flags, events=None):
+        b = self.b
+        ev = events
+        if ev is not None:
+            ev[0].record()
+        b.saf_hybrid_attn_fwd(self.Q, self.K, self.V, flags, self.a, self.r, O=self.O, LSE=self.LSE)
+        if ev is not None:
+            ev[1].record()
+        if self.backward:
+            for i, st in enumerate((b.SAF_BWD_PREPROCESS, b.SAF_BWD_DKDV, b.SAF_BWD_DQ)):
+                b.saf_hybrid_attn_bwd_stage(st, self.Q, self.K, self.V, self.O, self.dO, self.LSE, flags,
+                                            self.a, self.r, self.dQ, self.dK, self.dV, self.ws)
+                if ev is not None:
+                    ev[2 + i].record()
+
+
+def timed_block(torch, layer, flags, steps, with_events):
+    """Run `steps` steps between two device synchronisations; returns wall ms
+    per step and, if requested, per-stage event milliseconds per step."""
+    n_ev = len(layer.stages) + 1
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(n_ev)] for _ in range(steps)] if with_events else None
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(steps):
+        layer.step(flags, evs[s] if with_events else None)
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) * 1e3 / steps
+    per_stage = None
+    if with_events:
+        per_stage = {}
+        for i, name in enumerate(layer.stages):
+            per_stage[name] = float(np.mean([e[i].elapsed_time(e[i + 1]) for e in evs]))
+    return wall, per_stage
+
+
+def cpu_baseline(inp, w, slices_req):
+    """The fp64 oracle (as it stands) on a sample of (b, h) slices, one slice
+    per task on a process pool; returns the JSON object."""
+    from oracle import saf_oracle as orc
+    try:
+        from threadpoolctl import threadpool_limits
+    except ImportError:  # pragma: no cover
+        threadpool_limits = None
+    workers = max(1, min(MAX_HOST_WORKERS, len(os.sched_getaffinity(0))))
+    all_slices = [(b, h) for b in range(w.B) for h in range(w.H)]
+    n = slices_req if slices_req > 0 else min(len(all_slices), 2 * workers)
+    sample = all_slices[:n]
+    n_fixed = int(sum(inp["is_fixed"][h] for _, h in sample))
+    ctx = threadpool_limits(limits=1) if threadpool_limits else None
+    t0 = time.perf_counter()
+    try:
+        used = orc.layer_forward_backward_parallel(inp["Q"], inp["K"], inp["V"], inp.get("dO"), inp["is_fixed"],
+                                                   inp["a"], inp["r"], heads=sample, backward=w.backward,
+                                                   workers=workers)
+    finally:
+        if ctx is not None:
+            ctx.unregister() if hasattr(ctx, "unregister") else None
+    wall = time.perf_counter() - t0
+    per_layer_ms = wall * 1e3 * len(all_slices) / len(sample)
+    return {
+        "value": round(per_layer_ms, 1),
+        "unit": "ms/layer",
+        "cores": used,
+        "kind": "oracle",
+        "sample": (f"{len(sample)} of {len(all_slices)} (batch, head) slices ({n_fixed} fixed), "
+                   f"fp64 dense {'fwd+bwd' if w.backward else 'fwd'}, {wall:.1f} s wall on {used} "
+                   f"processes, scaled by {len(all_slices)}/{len(sample)}"),
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; multi-GPU runs are not part of it",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+    import torch
+    if not torch.cuda.is_available():
+        print(json.dumps({"error": "no GPU visible"}))
+        sys.exit(1)
+    from paper_2609_34650_amd import binding
+    binding.load()
+
+    w = gen.WORKLOADS[args.workload]
+    inp = gen.workload_inputs(w)
+    H, B, N, d = w.H, w.B, w.N, w.d
+    n_fixed = int(inp["is_fixed"].sum())
+    hybrid_flags = inp["is_fixed"].copy()
+    ordinary_flags = np.zeros_like(hybrid_flags)
+    layer = Layer(torch, inp, w.dtype, w.backward)
+
+    for _ in range(args.warmup):
+        layer.step(hybrid_flags)
+        if args.compare:
+            layer.step(ordinary_flags)
+    torch.cuda.synchronize()
+
+    # Timed region: exactly `steps` hybrid layers.
+    ms, per_stage = timed_block(torch, layer, hybrid_flags, args.steps, with_events=True)
+
+    flop = layer_flop(B, H, N, d, n_fixed, w.backward)
+    total_flop = sum(flop.values())
+    peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
+    tflops = total_flop / (ms * 1e-3) / 1e12
+    elem = 2 if w.dtype == "bf16" else 4
+    sbytes = stage_bytes(B, H, N, d, n_fixed, elem)
+    dominant = max(per_stage, key=per_stage.get)
+    dom_tflops = flop[dominant] / (per_stage[dominant] * 1e-3) / 1e12
+
+    result = {
+        "metric": METRIC,
+        "value": round(ms, 4),
+        "unit": "ms/layer",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": f"{w.name}: hybrid causal attention layer fwd+bwd" if w.backward
+                   else f"{w.name}: hybrid causal attention layer fwd",
+                   "B": B, "H": H, "n_fixed": n_fixed, "fixed_heads": [int(h) for h in np.flatnonzero(hybrid_flags)],
+                   "N": N, "d": d, "passes": "fwd+bwd" if w.backward else "fwd", "parallelism": "single GPU"},
+        "tflops": round(tflops, 1),
+        "mfma_util": round(tflops / peak, 4),
+        "kernels": {k: {"ms": round(v, 4), "tflops": round(flop[k] / (v * 1e-3) / 1e12, 1),
+                        "min_hbm_gbs": round(sbytes[k] / (v * 1e-3) / 1e9, 1)} for k, v in per_stage.items()},
+        "roofline": {"bound": "mfma", "kernel": dominant, "achieved": round(dom_tflops, 1), "peak": peak,
+                     "unit": "TFLOP/s", "frac": round(dom_tflops / peak, 4), "traffic": None},
+    }
+
+    if args.compare:
+        # ABBA blocks: hybrid, all-ordinary, all-ordinary, hybrid.
+        blk = max(1, args.steps // 2)
+        t = {"h": [], "o": []}
+        for tag, fl in (("h", hybrid_flags), ("o", ordinary_flags), ("o", ordinary_flags), ("h", hybrid_flags)):
+            t[tag].append(timed_block(torch, layer, fl, blk, with_events=False)[0])
+        ms_h, ms_o = float(np.mean(t["h"])), float(np.mean(t["o"]))
+        flop_o = sum(layer_flop(B, H, N, d, 0, w.backward).values())
+        result["all_ordinary"] = {"ms": round(ms_o, 4), "tflops": round(flop_o / (ms_o * 1e-3) / 1e12, 1),
+                                  "hybrid_ms_same_blocks": round(ms_h, 4)}
+        result["speedup_vs_all_ordinary"] = round(ms_o / ms_h, 4)
+
+    if args.cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(inp, w, args.cpu_slices)
+
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,147 @@
+/*
+ * saf.h -- C ABI of libsaf.so: the fused hybrid causal-attention layer of
+ * Selective Attention Freezing ("When Can Attention Heads Be Statically
+ * Defined?"), forward and backward, for AMD Instinct MI355X (gfx950).
+ *
+ * One layer has H heads.  An ordinary head computes causal softmax attention
+ * (Appendix "Attention notation and calibration", Eqs. standard-head):
+ *     S = Q K^T / sqrt(d),  A = softmax_causal(S),  O = A V.
+ * A fixed ("replaced") head mixes values with a fixed causal row-stochastic
+ * pattern built from two length-N preference vectors (Section
+ * "Fixed-pattern construction and fitting", Eq. compact-prior), with 0-based
+ * storage a[j] = alpha(j+1) and r[delta] = rho(delta):
+ *     P(i, j) = exp(a[j] + r[i - j]) / Z(i)  for j <= i,  0 for j > i,
+ *     Z(i)    = sum_{j <= i} exp(a[j] + r[i - j]),         O = P V.
+ * Fixed heads never read Q or K, take no 1/sqrt(d), and the pattern takes no
+ * gradient: the backward gives a fixed head only dV = P^T dO and writes exact
+ * zeros into its dQ and dK slices (Section "Replacement schedules and fused
+ * execution", paragraph "Fused computation"; Appendix "Mixed-head execution
+ * and numerical checks").
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Tensors Q, K, V, O, dO, dQ, dK, dV are DEVICE pointers to contiguous
+ *   [B, H, N, d] arrays of the element type `dt` (row-major, d fastest), each
+ *   16-byte aligned.  LSE is a DEVICE pointer to contiguous [B, H, N] float32.
+ * - a and r are DEVICE pointers to float32 [H, ld_prior] arrays (ld_prior >=
+ *   N; only the first N entries of each row are read; rows of ordinary heads
+ *   are never read).  They are shared by every batch element.  Entries must be
+ *   finite.
+ * - head_is_fixed is a HOST pointer to H bytes: 0 = ordinary, 1 = fixed.
+ * - The caller owns every buffer.  The library never allocates or frees
+ *   device memory, keeps no mutable global state, never synchronises the
+ *   stream, and only enqueues kernels on `stream` (0 = the null stream).
+ *   Outputs are overwritten, never accumulated into.
+ * - Arguments are checked before anything is enqueued; on any error nothing
+ *   is launched and nothing is written.  A kernel fault surfaces at the
+ *   caller's next synchronisation, not here.
+ * - Limits of this build: d == 64, 1 <= H <= 64, N <= 2^24.  B, H or N equal
+ *   to 0 is an empty problem: SAF_OK, nothing launched.
+ * - Numerics: products on MFMA in the element type with float32 accumulation;
+ *   softmax statistics, LSE and the fixed-head normalisers in float32.  Results
+ *   are rounded once to the element type (nearest even for bf16).
+ */
+#ifndef SAF_H
+#define SAF_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    SAF_DTYPE_F32 = 0,  /* float32 activations, float32 MFMA (v_mfma_f32_32x32x2_f32) */
+    SAF_DTYPE_BF16 = 1  /* bfloat16 activations, bf16 MFMA with float32 accumulation */
+} saf_dtype_t;
+
+typedef enum {
+    SAF_OK = 0,
+    SAF_ERR_NULL = 1,          /* a required pointer is NULL */
+    SAF_ERR_SHAPE = 2,         /* negative size, N > 2^24, ld_prior < N, or workspace too small */
+    SAF_ERR_UNSUPPORTED = 3,   /* unknown dtype, d != 64, H > 64 */
+    SAF_ERR_MISSING_PRIOR = 4, /* a head is fixed but a or r is NULL */
+    SAF_ERR_LAUNCH = 5,        /* the HIP runtime rejected a kernel launch */
+    SAF_ERR_ALIGNMENT = 6,     /* a tensor pointer is not 16-byte aligned */
+    SAF_ERR_FLAG = 7           /* head_is_fixed holds a byte other than 0 or 1 */
+} saf_status_t;
+
+/*
+ * Forward of the hybrid layer (Section "Replacement schedules and fused
+ * execution"; Appendix "Mixed-head execution and numerical checks"): one
+ * kernel launch in which every workgroup takes one (batch, head, block of
+ * queries) and the head's flag selects its path; outputs land in the original
+ * head order.
+ *   Q, K : [B,H,N,d] `dt`; read for ordinary heads only (fixed-head slices may
+ *          hold anything, NaN included).  May be NULL if every head is fixed.
+ *   V    : [B,H,N,d] `dt`.
+ *   O    : [B,H,N,d] `dt`, written.
+ *   LSE  : [B,H,N] float32, written: natural-log row normaliser,
+ *          log sum_{j<=i} exp(S[i,j]) for ordinary heads, log Z(i) for fixed.
+ */
+saf_status_t saf_hybrid_attn_fwd(saf_dtype_t dt,
+                                 const void* Q, const void* K, const void* V,
+                                 const uint8_t* head_is_fixed,
+                                 const float* a, const float* r, int ld_prior,
+                                 int B, int H, int N, int d,
+                                 void* O, float* LSE,
+                                 hipStream_t stream);
+
+/* Bytes of device workspace saf_hybrid_attn_bwd needs (a multiple of 256).
+ * Returns 0 for an empty or invalid problem. */
+size_t saf_hybrid_attn_bwd_workspace_bytes(saf_dtype_t dt, int B, int H, int N, int d);
+
+/*
+ * Backward of the hybrid layer for the loss sum(O * dO) (Appendix "Mixed-head
+ * execution and numerical checks": key-block programs produce dV for every
+ * head and dK for ordinary heads; a separate query-block pass produces dQ for
+ * ordinary heads only).  Three launches: a row pre-pass D_i = sum_c dO*O for
+ * ordinary heads, the key-block pass, the query-block pass.
+ *   Q, K, V, O, dO : [B,H,N,d] `dt` (O and LSE as written by the forward).
+ *   LSE            : [B,H,N] float32 from the forward.
+ *   dQ, dK, dV     : [B,H,N,d] `dt`, written; fixed heads get exact zeros in
+ *                    dQ and dK.
+ *   workspace      : DEVICE, >= saf_hybrid_attn_bwd_workspace_bytes(), owned
+ *                    by the caller, 256-byte aligned; its contents on entry
+ *                    are ignored.
+ */
+saf_status_t saf_hybrid_attn_bwd(saf_dtype_t dt,
+                                 const void* Q, const void* K, const void* V,
+                                 const void* O, const void* dO, const float* LSE,
+                                 const uint8_t* head_is_fixed,
+                                 const float* a, const float* r, int ld_prior,
+                                 int B, int H, int N, int d,
+                                 void* dQ, void* dK, void* dV,
+                                 void* workspace, size_t workspace_bytes,
+                                 hipStream_t stream);
+
+/* The three launches of saf_hybrid_attn_bwd, enqueued one at a time (same
+ * arguments and contract).  Running SAF_BWD_PREPROCESS, then SAF_BWD_DKDV and
+ * SAF_BWD_DQ (in either order) on one stream with one workspace equals
+ * saf_hybrid_attn_bwd.  DKDV writes dK and dV; DQ writes dQ. */
+typedef enum {
+    SAF_BWD_PREPROCESS = 0,
+    SAF_BWD_DKDV = 1,
+    SAF_BWD_DQ = 2
+} saf_bwd_stage_t;
+
+saf_status_t saf_hybrid_attn_bwd_stage(saf_bwd_stage_t stage, saf_dtype_t dt,
+                                       const void* Q, const void* K, const void* V,
+                                       const void* O, const void* dO, const float* LSE,
+                                       const uint8_t* head_is_fixed,
+                                       const float* a, const float* r, int ld_prior,
+                                       int B, int H, int N, int d,
+                                       void* dQ, void* dK, void* dV,
+                                       void* workspace, size_t workspace_bytes,
+                                       hipStream_t stream);
+
+/* Static text for a status code ("unknown status" for anything else). */
+const char* saf_status_str(saf_status_t s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SAF_H */

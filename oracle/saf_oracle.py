@@ -144,24 +144,27 @@ def _probs_block(q, k, fixed: bool, a, r, rows, n) -> Tuple[np.ndarray, np.ndarr
 
 
 def head_forward(q, k, v, fixed: bool, a=None, r=None,
-                 row_block: int = 512) -> Tuple[np.ndarray, np.ndarray]:
+                 row_block: int = 512, rows=None) -> Tuple[np.ndarray, np.ndarray]:
     """Forward of one head: returns ``O`` ``[n, d]`` and ``LSE`` ``[n]``.
 
     Ordinary: ``O = softmax_causal(Q K^T / sqrt(d)) V``.  Fixed: ``O = P V``
-    with ``P`` from ``a`` and ``r``; ``q`` and ``k`` are not read.
+    with ``P`` from ``a`` and ``r``; ``q`` and ``k`` are not read.  If
+    ``rows`` lists query positions, only those rows are evaluated and the
+    results have one entry per listed row.
     """
     v = _as64(v)
     n = v.shape[0]
     if fixed:
         a = _as64(a)[:n]
         r = _as64(r)[:n]
-    o = np.empty_like(v)
-    lse = np.empty(n, dtype=_F64)
-    for start in range(0, n, row_block):
-        rows = np.arange(start, min(n, start + row_block))
-        p, lse_blk = _probs_block(q, k, fixed, a, r, rows, n)
-        o[rows] = p @ v
-        lse[rows] = lse_blk
+    want = np.arange(n) if rows is None else np.asarray(rows, dtype=np.int64).reshape(-1)
+    o = np.empty((want.shape[0], v.shape[1]), dtype=_F64)
+    lse = np.empty(want.shape[0], dtype=_F64)
+    for start in range(0, want.shape[0], row_block):
+        sel = slice(start, min(want.shape[0], start + row_block))
+        p, lse_blk = _probs_block(q, k, fixed, a, r, want[sel], n)
+        o[sel] = p @ v
+        lse[sel] = lse_blk
     return o, lse
 
 

@@ -1,0 +1,257 @@
+"""Thin ctypes binding to libsaf.so (C ABI in ``include/saf.h``).
+
+Only argument marshalling happens here: tensor checks, pointers, the head
+flags and the caller's current HIP stream.  Every step of the layer runs in
+the library's kernels; there is no fallback.  If ``libsaf.so`` is missing or
+fails to load, every call raises.
+
+Function names match the C entry points.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence, Tuple
+
+import numpy as np
+import torch
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsaf.so")
+
+SAF_DTYPE_F32 = 0
+SAF_DTYPE_BF16 = 1
+SAF_BWD_PREPROCESS = 0
+SAF_BWD_DKDV = 1
+SAF_BWD_DQ = 2
+
+STATUS = {
+    0: "SAF_OK",
+    1: "SAF_ERR_NULL",
+    2: "SAF_ERR_SHAPE",
+    3: "SAF_ERR_UNSUPPORTED",
+    4: "SAF_ERR_MISSING_PRIOR",
+    5: "SAF_ERR_LAUNCH",
+    6: "SAF_ERR_ALIGNMENT",
+    7: "SAF_ERR_FLAG",
+}
+
+EXPORTS = (
+    "saf_hybrid_attn_fwd",
+    "saf_hybrid_attn_bwd_workspace_bytes",
+    "saf_hybrid_attn_bwd",
+    "saf_hybrid_attn_bwd_stage",
+    "saf_status_str",
+)
+
+
+class SafError(RuntimeError):
+    def __init__(self, code: int, what: str):
+        self.code = code
+        super().__init__(f"{what}: {STATUS.get(code, code)} ({status_str(code)})")
+
+
+_lib = None
+
+
+def lib_path() -> str:
+    return _LIB_PATH
+
+
+def load() -> ctypes.CDLL:
+    """Load libsaf.so once; raise if it is not built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        raise RuntimeError(
+            f"{_LIB_PATH} is not built; run `python -m paper_2609_34650_amd.build` "
+            "(there is no non-HIP fallback)")
+    lib = ctypes.CDLL(_LIB_PATH)
+    vp, i, f32p, u8p = ctypes.c_void_p, ctypes.c_int, ctypes.POINTER(ctypes.c_float), ctypes.c_void_p
+    lib.saf_hybrid_attn_fwd.restype = ctypes.c_int
+    lib.saf_hybrid_attn_fwd.argtypes = [i, vp, vp, vp, u8p, vp, vp, i, i, i, i, i, vp, vp, vp]
+    lib.saf_hybrid_attn_bwd_workspace_bytes.restype = ctypes.c_size_t
+    lib.saf_hybrid_attn_bwd_workspace_bytes.argtypes = [i, i, i, i, i]
+    bwd_args = [i, vp, vp, vp, vp, vp, vp, u8p, vp, vp, i, i, i, i, i, vp, vp, vp, vp, ctypes.c_size_t, vp]
+    lib.saf_hybrid_attn_bwd.restype = ctypes.c_int
+    lib.saf_hybrid_attn_bwd.argtypes = bwd_args
+    lib.saf_hybrid_attn_bwd_stage.restype = ctypes.c_int
+    lib.saf_hybrid_attn_bwd_stage.argtypes = [i] + bwd_args
+    lib.saf_status_str.restype = ctypes.c_char_p
+    lib.saf_status_str.argtypes = [i]
+    del f32p
+    _lib = lib
+    return lib
+
+
+def status_str(code: int) -> str:
+    return load().saf_status_str(int(code)).decode()
+
+
+# ---------------------------------------------------------------------------
+# Marshalling helpers
+# ---------------------------------------------------------------------------
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return SAF_DTYPE_BF16
+    if t.dtype == torch.float32:
+        return SAF_DTYPE_F32
+    raise TypeError(f"activations must be bfloat16 or float32, got {t.dtype}")
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _check_act(name: str, t: Optional[torch.Tensor], shape, dtype, device, allow_none=False):
+    if t is None:
+        if allow_none:
+            return
+        raise ValueError(f"{name} is required")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} has dtype {t.dtype}, expected {dtype}")
+    if t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous [B, H, N, d]")
+
+
+def _flags(head_is_fixed, H: int) -> np.ndarray:
+    if isinstance(head_is_fixed, torch.Tensor):
+        head_is_fixed = head_is_fixed.detach().cpu().numpy()
+    flags = np.ascontiguousarray(np.asarray(head_is_fixed, dtype=np.uint8).reshape(-1))
+    if flags.shape[0] != H:
+        raise ValueError(f"head_is_fixed has {flags.shape[0]} entries for {H} heads")
+    return flags
+
+
+def _prior(name: str, t: Optional[torch.Tensor], H: int, N: int, device) -> Tuple[Optional[int], int]:
+    if t is None:
+        return None, N
+    if t.dim() != 2 or t.shape[0] != H or t.shape[1] < N:
+        raise ValueError(f"{name} must be [H, >=N] float32, got {tuple(t.shape)}")
+    if t.dtype != torch.float32:
+        raise TypeError(f"{name} must be float32")
+    if t.device != device or t.stride(1) != 1 or t.stride(0) < N:
+        raise ValueError(f"{name} must be on {device} with unit stride along positions")
+    return t.data_ptr(), t.stride(0)
+
+
+def _stream(device) -> int:
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def _raise(code: int, what: str):
+    if code != 0:
+        raise SafError(code, what)
+
+
+# ---------------------------------------------------------------------------
+# Entry points
+# ---------------------------------------------------------------------------
+
+def saf_hybrid_attn_fwd(Q: Optional[torch.Tensor], K: Optional[torch.Tensor], V: torch.Tensor,
+                        head_is_fixed: Sequence[int], a: Optional[torch.Tensor] = None,
+                        r: Optional[torch.Tensor] = None, O: Optional[torch.Tensor] = None,
+                        LSE: Optional[torch.Tensor] = None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Forward of the hybrid layer on the current stream.  Returns ``(O, LSE)``.
+    ``Q`` and ``K`` may be ``None`` when every head is fixed."""
+    lib = load()
+    B, H, N, d = V.shape
+    dev = V.device
+    _check_act("V", V, V.shape, V.dtype, dev)
+    _check_act("Q", Q, V.shape, V.dtype, dev, allow_none=True)
+    _check_act("K", K, V.shape, V.dtype, dev, allow_none=True)
+    if O is None:
+        O = torch.empty_like(V)
+    if LSE is None:
+        LSE = torch.empty((B, H, N), dtype=torch.float32, device=dev)
+    _check_act("O", O, V.shape, V.dtype, dev)
+    _check_act("LSE", LSE, (B, H, N), torch.float32, dev)
+    flags = _flags(head_is_fixed, H)
+    pa, lda = _prior("a", a, H, N, dev)
+    pr, ldr = _prior("r", r, H, N, dev)
+    if pa is not None and pr is not None and lda != ldr:
+        raise ValueError("a and r must share one row stride")
+    code = lib.saf_hybrid_attn_fwd(
+        _dtype_code(V), _ptr(Q), _ptr(K), _ptr(V), flags.ctypes.data, pa, pr, lda,
+        B, H, N, d, _ptr(O), _ptr(LSE), _stream(dev))
+    _raise(code, "saf_hybrid_attn_fwd")
+    return O, LSE
+
+
+def saf_hybrid_attn_bwd_workspace_bytes(dtype: torch.dtype, B: int, H: int, N: int, d: int) -> int:
+    code = SAF_DTYPE_BF16 if dtype == torch.bfloat16 else SAF_DTYPE_F32
+    return int(load().saf_hybrid_attn_bwd_workspace_bytes(code, B, H, N, d))
+
+
+def _bwd_common(Q, K, V, O, dO, LSE, head_is_fixed, a, r, dQ, dK, dV, workspace):
+    B, H, N, d = V.shape
+    dev = V.device
+    for name, t in (("V", V), ("O", O), ("dO", dO)):
+        _check_act(name, t, V.shape, V.dtype, dev)
+    _check_act("Q", Q, V.shape, V.dtype, dev, allow_none=True)
+    _check_act("K", K, V.shape, V.dtype, dev, allow_none=True)
+    _check_act("LSE", LSE, (B, H, N), torch.float32, dev)
+    dQ = torch.empty_like(V) if dQ is None else dQ
+    dK = torch.empty_like(V) if dK is None else dK
+    dV = torch.empty_like(V) if dV is None else dV
+    for name, t in (("dQ", dQ), ("dK", dK), ("dV", dV)):
+        _check_act(name, t, V.shape, V.dtype, dev)
+    nbytes = saf_hybrid_attn_bwd_workspace_bytes(V.dtype, B, H, N, d)
+    if workspace is None:
+        workspace = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=dev)
+    flags = _flags(head_is_fixed, H)
+    pa, lda = _prior("a", a, H, N, dev)
+    pr, ldr = _prior("r", r, H, N, dev)
+    if pa is not None and pr is not None and lda != ldr:
+        raise ValueError("a and r must share one row stride")
+    args = [_dtype_code(V), _ptr(Q), _ptr(K), _ptr(V), _ptr(O), _ptr(dO), _ptr(LSE), flags.ctypes.data,
+            pa, pr, lda, B, H, N, d, _ptr(dQ), _ptr(dK), _ptr(dV), workspace.data_ptr(),
+            workspace.numel() * workspace.element_size(), _stream(dev)]
+    return args, (dQ, dK, dV), flags, workspace
+
+
+def saf_hybrid_attn_bwd(Q, K, V, O, dO, LSE, head_is_fixed, a=None, r=None, dQ=None, dK=None, dV=None,
+                        workspace: Optional[torch.Tensor] = None):
+    """Backward of the hybrid layer for ``sum(O * dO)`` on the current
+    stream.  Returns ``(dQ, dK, dV)``; fixed heads get zeros in dQ and dK."""
+    lib = load()
+    args, outs, _flags_keep, _ws_keep = _bwd_common(Q, K, V, O, dO, LSE, head_is_fixed, a, r, dQ, dK, dV,
+                                                    workspace)
+    _raise(lib.saf_hybrid_attn_bwd(*args), "saf_hybrid_attn_bwd")
+    return outs
+
+
+def saf_hybrid_attn_bwd_stage(stage: int, Q, K, V, O, dO, LSE, head_is_fixed, a=None, r=None, dQ=None,
+                              dK=None, dV=None, workspace: Optional[torch.Tensor] = None):
+    """One of the three launches of the backward (``SAF_BWD_PREPROCESS``,
+    ``SAF_BWD_DKDV``, ``SAF_BWD_DQ``); returns ``(dQ, dK, dV)`` as passed or
+    allocated.  Pass the same ``workspace`` to every stage."""
+    lib = load()
+    args, outs, _flags_keep, _ws_keep = _bwd_common(Q, K, V, O, dO, LSE, head_is_fixed, a, r, dQ, dK, dV,
+                                                    workspace)
+    _raise(lib.saf_hybrid_attn_bwd_stage(int(stage), *args), "saf_hybrid_attn_bwd_stage")
+    return outs
+
+
+class HybridAttention(torch.autograd.Function):
+    """Autograd wrapper over the forward/backward pair.  ``a`` and ``r`` take no
+    gradient; fixed heads return zero gradients for Q and K."""
+
+    @staticmethod
+    def forward(ctx, Q, K, V, head_is_fixed, a, r):
+        O, LSE = saf_hybrid_attn_fwd(Q, K, V, head_is_fixed, a, r)
+        ctx.save_for_backward(Q, K, V, O, LSE, a, r)
+        ctx.flags = _flags(head_is_fixed, V.shape[1])
+        return O
+
+    @staticmethod
+    def backward(ctx, dO):
+        Q, K, V, O, LSE, a, r = ctx.saved_tensors
+        dQ, dK, dV = saf_hybrid_attn_bwd(Q, K, V, O, dO.contiguous(), LSE, ctx.flags, a, r)
+        return dQ, dK, dV, None, None, None

@@ -1,0 +1,227 @@
+// Host side of libsaf.so: argument checks and kernel launches for the C ABI
+// declared in include/saf.h.  No allocation, no synchronisation, no global
+// mutable state.
+#include "saf.h"
+
+#include <math.h>
+#include <stdint.h>
+
+#include "saf_bwd.h"
+#include "saf_fwd.h"
+
+#define SAF_EXPORT extern "C" __attribute__((visibility("default")))
+
+namespace {
+
+constexpr int kMaxN = 1 << 24;
+
+struct Problem {
+    uint64_t fixed_mask = 0;
+    bool any_fixed = false;
+    bool any_ordinary = false;
+    bool empty = false;
+};
+
+bool aligned16(const void* ptr) { return (reinterpret_cast<uintptr_t>(ptr) & 15u) == 0; }
+
+// Checks shared by forward and backward.  Fills `pr`; SAF_OK with pr->empty
+// set means there is nothing to do.
+saf_status_t check_common(saf_dtype_t dt, const uint8_t* head_is_fixed, const float* a, const float* r,
+                          int ld_prior, int B, int H, int N, int d, Problem* pr) {
+    if (dt != SAF_DTYPE_F32 && dt != SAF_DTYPE_BF16) return SAF_ERR_UNSUPPORTED;
+    if (B < 0 || H < 0 || N < 0 || d < 0) return SAF_ERR_SHAPE;
+    if (d != saf::HEAD_DIM) return SAF_ERR_UNSUPPORTED;
+    if (H > 64) return SAF_ERR_UNSUPPORTED;
+    if (N > kMaxN) return SAF_ERR_SHAPE;
+    if ((int64_t)B * H * ((N + 127) / 128) > INT32_MAX) return SAF_ERR_SHAPE;
+    if (B == 0 || H == 0 || N == 0) {
+        pr->empty = true;
+        return SAF_OK;
+    }
+    if (head_is_fixed == nullptr) return SAF_ERR_NULL;
+    for (int h = 0; h < H; ++h) {
+        if (head_is_fixed[h] > 1) return SAF_ERR_FLAG;
+        if (head_is_fixed[h]) {
+            pr->fixed_mask |= (1ull << h);
+            pr->any_fixed = true;
+        } else {
+            pr->any_ordinary = true;
+        }
+    }
+    if (pr->any_fixed) {
+        if (a == nullptr || r == nullptr) return SAF_ERR_MISSING_PRIOR;
+        if (ld_prior < N) return SAF_ERR_SHAPE;
+    }
+    return SAF_OK;
+}
+
+saf_status_t launched() { return hipGetLastError() == hipSuccess ? SAF_OK : SAF_ERR_LAUNCH; }
+
+template <typename T>
+saf_status_t launch_fwd(const saf::FwdArgs& args, hipStream_t stream) {
+    const unsigned grid = (unsigned)((size_t)args.n_qblocks * args.B * args.H);
+    hipLaunchKernelGGL(saf::fwd_kernel<T>, dim3(grid), dim3(saf::FWD_THREADS), 0, stream, args);
+    return launched();
+}
+
+size_t workspace_bytes(int B, int H, int N) {
+    const size_t d_bytes = (size_t)B * H * N * sizeof(float);
+    return (d_bytes + 255) & ~(size_t)255;
+}
+
+template <typename T>
+saf_status_t launch_bwd_stage(saf_bwd_stage_t stage, const saf::BwdArgs& base, hipStream_t stream) {
+    saf::BwdArgs args = base;
+    if (stage == SAF_BWD_PREPROCESS) {
+        const size_t rows = (size_t)args.B * args.H * args.N;
+        const unsigned grid = (unsigned)((rows + saf::PRE_ROWS - 1) / saf::PRE_ROWS);
+        hipLaunchKernelGGL(saf::bwd_pre_kernel<T>, dim3(grid), dim3(saf::PRE_THREADS), 0, stream, args);
+    } else if (stage == SAF_BWD_DKDV) {
+        args.n_blocks = (args.N + saf::KV_BN - 1) / saf::KV_BN;
+        const unsigned grid = (unsigned)((size_t)args.n_blocks * args.B * args.H);
+        hipLaunchKernelGGL(saf::bwd_kv_kernel<T>, dim3(grid), dim3(saf::KV_THREADS), 0, stream, args);
+    } else {
+        args.n_blocks = (args.N + saf::DQ_BM - 1) / saf::DQ_BM;
+        const unsigned grid = (unsigned)((size_t)args.n_blocks * args.B * args.H);
+        hipLaunchKernelGGL(saf::bwd_dq_kernel<T>, dim3(grid), dim3(saf::DQ_THREADS), 0, stream, args);
+    }
+    return launched();
+}
+
+saf_status_t check_bwd(saf_bwd_stage_t stage, saf_dtype_t dt, const void* Q, const void* K, const void* V,
+                       const void* O, const void* dO, const float* LSE, const uint8_t* head_is_fixed,
+                       const float* a, const float* r, int ld_prior, int B, int H, int N, int d, void* dQ,
+                       void* dK, void* dV, void* workspace, size_t workspace_bytes_given, Problem* pr) {
+    if (stage != SAF_BWD_PREPROCESS && stage != SAF_BWD_DKDV && stage != SAF_BWD_DQ) return SAF_ERR_UNSUPPORTED;
+    saf_status_t st = check_common(dt, head_is_fixed, a, r, ld_prior, B, H, N, d, pr);
+    if (st != SAF_OK || pr->empty) return st;
+    if (V == nullptr || O == nullptr || dO == nullptr || LSE == nullptr || dQ == nullptr || dK == nullptr ||
+        dV == nullptr || workspace == nullptr)
+        return SAF_ERR_NULL;
+    if (pr->any_ordinary && (Q == nullptr || K == nullptr)) return SAF_ERR_NULL;
+    if (!aligned16(V) || !aligned16(O) || !aligned16(dO) || !aligned16(dQ) || !aligned16(dK) || !aligned16(dV) ||
+        !aligned16(LSE) || (Q && !aligned16(Q)) || (K && !aligned16(K)) ||
+        (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
+        return SAF_ERR_ALIGNMENT;
+    if (workspace_bytes_given < workspace_bytes(B, H, N)) return SAF_ERR_SHAPE;
+    return SAF_OK;
+}
+
+saf::BwdArgs make_bwd_args(const void* Q, const void* K, const void* V, const void* O, const void* dO,
+                           const float* LSE, const float* a, const float* r, int ld_prior, int B, int H, int N,
+                           void* dQ, void* dK, void* dV, void* workspace, const Problem& pr) {
+    saf::BwdArgs args;
+    args.q = Q;
+    args.k = K;
+    args.v = V;
+    args.o = O;
+    args.dO = dO;
+    args.lse = LSE;
+    args.a = a;
+    args.r = r;
+    args.dq = dQ;
+    args.dk = dK;
+    args.dv = dV;
+    args.dsum = reinterpret_cast<float*>(workspace);
+    args.fixed_mask = pr.fixed_mask;
+    args.B = B;
+    args.H = H;
+    args.N = N;
+    args.ld_prior = ld_prior;
+    args.n_blocks = 0;
+    args.scale = 1.0f / sqrtf((float)saf::HEAD_DIM);
+    args.scale_log2 = saf::LOG2E / sqrtf((float)saf::HEAD_DIM);
+    return args;
+}
+
+saf_status_t run_bwd_stage(saf_bwd_stage_t stage, saf_dtype_t dt, const saf::BwdArgs& args, hipStream_t stream) {
+    return dt == SAF_DTYPE_BF16 ? launch_bwd_stage<saf::bf16>(stage, args, stream)
+                                : launch_bwd_stage<float>(stage, args, stream);
+}
+
+}  // namespace
+
+SAF_EXPORT saf_status_t saf_hybrid_attn_fwd(saf_dtype_t dt, const void* Q, const void* K, const void* V,
+                                            const uint8_t* head_is_fixed, const float* a, const float* r,
+                                            int ld_prior, int B, int H, int N, int d, void* O, float* LSE,
+                                            hipStream_t stream) {
+    Problem pr;
+    saf_status_t st = check_common(dt, head_is_fixed, a, r, ld_prior, B, H, N, d, &pr);
+    if (st != SAF_OK || pr.empty) return st;
+    if (V == nullptr || O == nullptr || LSE == nullptr) return SAF_ERR_NULL;
+    if (pr.any_ordinary && (Q == nullptr || K == nullptr)) return SAF_ERR_NULL;
+    if (!aligned16(V) || !aligned16(O) || !aligned16(LSE) || (Q && !aligned16(Q)) || (K && !aligned16(K)))
+        return SAF_ERR_ALIGNMENT;
+
+    saf::FwdArgs args;
+    args.q = Q;
+    args.k = K;
+    args.v = V;
+    args.a = a;
+    args.r = r;
+    args.o = O;
+    args.lse = LSE;
+    args.fixed_mask = pr.fixed_mask;
+    args.B = B;
+    args.H = H;
+    args.N = N;
+    args.ld_prior = ld_prior;
+    args.n_qblocks = (N + saf::FWD_BM - 1) / saf::FWD_BM;
+    args.scale_log2 = saf::LOG2E / sqrtf((float)saf::HEAD_DIM);
+    return dt == SAF_DTYPE_BF16 ? launch_fwd<saf::bf16>(args, stream) : launch_fwd<float>(args, stream);
+}
+
+SAF_EXPORT size_t saf_hybrid_attn_bwd_workspace_bytes(saf_dtype_t dt, int B, int H, int N, int d) {
+    if (dt != SAF_DTYPE_F32 && dt != SAF_DTYPE_BF16) return 0;
+    if (B <= 0 || H <= 0 || N <= 0 || d != saf::HEAD_DIM || H > 64 || N > kMaxN) return 0;
+    return workspace_bytes(B, H, N);
+}
+
+SAF_EXPORT saf_status_t saf_hybrid_attn_bwd_stage(saf_bwd_stage_t stage, saf_dtype_t dt, const void* Q,
+                                                  const void* K, const void* V, const void* O, const void* dO,
+                                                  const float* LSE, const uint8_t* head_is_fixed, const float* a,
+                                                  const float* r, int ld_prior, int B, int H, int N, int d,
+                                                  void* dQ, void* dK, void* dV, void* workspace,
+                                                  size_t workspace_bytes_given, hipStream_t stream) {
+    Problem pr;
+    saf_status_t st = check_bwd(stage, dt, Q, K, V, O, dO, LSE, head_is_fixed, a, r, ld_prior, B, H, N, d, dQ, dK,
+                                dV, workspace, workspace_bytes_given, &pr);
+    if (st != SAF_OK || pr.empty) return st;
+    const saf::BwdArgs args =
+        make_bwd_args(Q, K, V, O, dO, LSE, a, r, ld_prior, B, H, N, dQ, dK, dV, workspace, pr);
+    return run_bwd_stage(stage, dt, args, stream);
+}
+
+SAF_EXPORT saf_status_t saf_hybrid_attn_bwd(saf_dtype_t dt, const void* Q, const void* K, const void* V,
+                                            const void* O, const void* dO, const float* LSE,
+                                            const uint8_t* head_is_fixed, const float* a, const float* r,
+                                            int ld_prior, int B, int H, int N, int d, void* dQ, void* dK,
+                                            void* dV, void* workspace, size_t workspace_bytes_given,
+                                            hipStream_t stream) {
+    Problem pr;
+    saf_status_t st = check_bwd(SAF_BWD_PREPROCESS, dt, Q, K, V, O, dO, LSE, head_is_fixed, a, r, ld_prior, B, H,
+                                N, d, dQ, dK, dV, workspace, workspace_bytes_given, &pr);
+    if (st != SAF_OK || pr.empty) return st;
+    const saf::BwdArgs args =
+        make_bwd_args(Q, K, V, O, dO, LSE, a, r, ld_prior, B, H, N, dQ, dK, dV, workspace, pr);
+    const saf_bwd_stage_t order[3] = {SAF_BWD_PREPROCESS, SAF_BWD_DKDV, SAF_BWD_DQ};
+    for (saf_bwd_stage_t s : order) {
+        st = run_bwd_stage(s, dt, args, stream);
+        if (st != SAF_OK) return st;
+    }
+    return SAF_OK;
+}
+
+SAF_EXPORT const char* saf_status_str(saf_status_t s) {
+    switch (s) {
+        case SAF_OK: return "ok";
+        case SAF_ERR_NULL: return "a required pointer is NULL";
+        case SAF_ERR_SHAPE: return "invalid size (negative, N > 2^24, ld_prior < N, or workspace too small)";
+        case SAF_ERR_UNSUPPORTED: return "unsupported dtype, head dimension (d must be 64) or head count (H <= 64)";
+        case SAF_ERR_MISSING_PRIOR: return "a head is fixed but a or r is NULL";
+        case SAF_ERR_LAUNCH: return "kernel launch failed";
+        case SAF_ERR_ALIGNMENT: return "a tensor pointer is not 16-byte aligned (workspace: 256-byte)";
+        case SAF_ERR_FLAG: return "head_is_fixed holds a byte other than 0 or 1";
+    }
+    return "unknown status";
+}

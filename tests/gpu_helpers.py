@@ -1,0 +1,101 @@
+"""Helpers shared by the GPU tests: move seeded inputs to the device, run the
+C ABI through the binding, and compare with the fp64 oracle at the stated
+tolerances.
+
+Tolerances (elementwise, on O, LSE, dQ, dK, dV):
+* float32 path: ``max |gpu - oracle| <= 1e-4``;
+* bf16 path:    ``|gpu - oracle| <= 1e-2 + 2e-2 * |oracle|``.
+"""
+
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import pytest
+
+F32_ATOL = 1e-4
+BF16_ATOL = 1e-2
+BF16_RTOL = 2e-2
+
+
+def torch_cuda():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.fail("GPU test run without a visible GPU")
+    return torch
+
+
+def announce(msg: str):
+    print(f"[gpu-case] {msg}", flush=True)
+    sys.stdout.flush()
+
+
+def to_device(inp: dict, dtype: str):
+    torch = torch_cuda()
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    dev = torch.device("cuda", 0)
+    out = {}
+    for k in ("Q", "K", "V", "dO"):
+        if k in inp:
+            out[k] = torch.from_numpy(inp[k]).to(dev).to(tdt).contiguous()
+    out["a"] = torch.from_numpy(np.ascontiguousarray(inp["a"])).to(dev)
+    out["r"] = torch.from_numpy(np.ascontiguousarray(inp["r"])).to(dev)
+    out["is_fixed"] = inp["is_fixed"]
+    return out
+
+
+def run_gpu(inp: dict, dtype: str, backward: bool = True):
+    """Forward (+ backward) through the C ABI; returns float64 numpy arrays."""
+    torch = torch_cuda()
+    from paper_2609_34650_amd import binding
+    t = to_device(inp, dtype)
+    O, LSE = binding.saf_hybrid_attn_fwd(t["Q"], t["K"], t["V"], t["is_fixed"], t["a"], t["r"])
+    res = {"O": O, "LSE": LSE}
+    if backward:
+        dQ, dK, dV = binding.saf_hybrid_attn_bwd(t["Q"], t["K"], t["V"], O, t["dO"], LSE, t["is_fixed"],
+                                                 t["a"], t["r"])
+        res.update(dQ=dQ, dK=dK, dV=dV)
+    torch.cuda.synchronize()
+    return {k: v.float().cpu().numpy().astype(np.float64) for k, v in res.items()}
+
+
+def check_close(name: str, got: np.ndarray, ref: np.ndarray, dtype: str):
+    assert got.shape == ref.shape, (name, got.shape, ref.shape)
+    assert np.isfinite(got).all(), f"{name}: non-finite GPU values"
+    err = np.abs(got - ref)
+    if dtype == "f32":
+        worst = float(err.max()) if err.size else 0.0
+        assert worst <= F32_ATOL, f"{name}: max abs err {worst:.3e} > {F32_ATOL}"
+    else:
+        bound = BF16_ATOL + BF16_RTOL * np.abs(ref)
+        ratio = err / bound
+        if ratio.size:
+            i = np.unravel_index(int(np.argmax(ratio)), ratio.shape)
+            assert ratio[i] <= 1.0, (f"{name}: |gpu-oracle| = {err[i]:.3e} at {i} exceeds "
+                                     f"1e-2 + 2e-2*|{ref[i]:.3e}|")
+    return float(err.max()) if err.size else 0.0
+
+
+def compare_layer(gpu: dict, inp: dict, dtype: str, backward: bool = True, heads=None):
+    """Compare every listed (b, h) slice (all if ``heads`` is None)."""
+    from oracle import saf_oracle as orc
+    O, LSE = orc.layer_forward(inp["Q"], inp["K"], inp["V"], inp["is_fixed"], inp["a"], inp["r"],
+                               heads=heads)
+    refs = {"O": O, "LSE": LSE}
+    if backward:
+        dQ, dK, dV = orc.layer_backward(inp["Q"], inp["K"], inp["V"], inp["dO"], inp["is_fixed"], inp["a"],
+                                        inp["r"], heads=heads)
+        refs.update(dQ=dQ, dK=dK, dV=dV)
+    errs = {}
+    sel = heads if heads is not None else [(b, h) for b in range(O.shape[0]) for h in range(O.shape[1])]
+    for name, ref in refs.items():
+        got = np.stack([gpu[name][b, h] for b, h in sel])
+        want = np.stack([ref[b, h] for b, h in sel])
+        errs[name] = check_close(name, got, want, dtype)
+    if backward:
+        fixed = np.asarray(inp["is_fixed"]).astype(bool)
+        for b, h in sel:
+            if fixed[h]:
+                assert not gpu["dQ"][b, h].any() and not gpu["dK"][b, h].any(), "fixed head dQ/dK not zero"
+    return errs

@@ -1,0 +1,123 @@
+"""C ABI checks that need no GPU: libsaf.so loads, exports exactly the entry
+points include/saf.h declares, and rejects bad arguments with the documented
+status before anything is launched.  Device pointers here are fake (aligned
+integers that are never dereferenced: every call below fails validation)."""
+
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "saf.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    from paper_2609_34650_amd import binding
+    return binding.load()
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(saf_\w+)\s*\(", text)))
+
+
+def test_header_declares_the_binding_exports():
+    from paper_2609_34650_amd import binding
+    assert _declared() == sorted(binding.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol_and_nothing_else(lib):
+    out = subprocess.run(["nm", "-D", "--defined-only", lib._name], capture_output=True, text=True, check=True)
+    exported = sorted(ln.split()[-1] for ln in out.stdout.splitlines() if ln.split()[-1].startswith("saf_"))
+    assert exported == _declared()
+    for name in _declared():
+        assert getattr(lib, name) is not None
+
+
+FAKE = 1 << 20  # aligned, never dereferenced
+
+
+def _fwd(lib, dt=1, Q=FAKE, K=FAKE, V=FAKE, flags=(0, 1), a=FAKE, r=FAKE, ld=None, B=1, N=8, d=64,
+         O=FAKE, LSE=FAKE):
+    f = np.asarray(flags, dtype=np.uint8)
+    H = f.shape[0]
+    ld = N if ld is None else ld
+    return lib.saf_hybrid_attn_fwd(dt, Q, K, V, f.ctypes.data if H else None, a, r, ld, B, H, N, d, O, LSE,
+                                   None)
+
+
+def _bwd(lib, stage=None, dt=1, Q=FAKE, K=FAKE, V=FAKE, O=FAKE, dO=FAKE, LSE=FAKE, flags=(0, 1), a=FAKE,
+         r=FAKE, ld=None, B=1, N=8, d=64, dQ=FAKE, dK=FAKE, dV=FAKE, ws=FAKE, ws_bytes=None):
+    f = np.asarray(flags, dtype=np.uint8)
+    H = f.shape[0]
+    ld = N if ld is None else ld
+    if ws_bytes is None:
+        ws_bytes = lib.saf_hybrid_attn_bwd_workspace_bytes(dt, B, H, N, d)
+    args = [dt, Q, K, V, O, dO, LSE, f.ctypes.data, a, r, ld, B, H, N, d, dQ, dK, dV, ws, ws_bytes, None]
+    if stage is None:
+        return lib.saf_hybrid_attn_bwd(*args)
+    return lib.saf_hybrid_attn_bwd_stage(stage, *args)
+
+
+def test_forward_argument_errors(lib):
+    assert _fwd(lib, dt=7) == 3                       # unknown dtype
+    assert _fwd(lib, d=32) == 3                       # only d = 64
+    assert _fwd(lib, d=128) == 3
+    assert _fwd(lib, flags=[0] * 65) == 3             # H > 64
+    assert _fwd(lib, N=-1) == 2
+    assert _fwd(lib, B=-2) == 2
+    assert _fwd(lib, N=(1 << 24) + 1) == 2
+    assert _fwd(lib, a=None) == 4                     # a fixed head needs a and r
+    assert _fwd(lib, r=None) == 4
+    assert _fwd(lib, ld=7) == 2                       # prior shorter than N
+    assert _fwd(lib, V=None) == 1
+    assert _fwd(lib, O=None) == 1
+    assert _fwd(lib, LSE=None) == 1
+    assert _fwd(lib, Q=None) == 1                     # an ordinary head needs Q and K
+    assert _fwd(lib, K=None) == 1
+    assert _fwd(lib, V=FAKE + 8) == 6                 # 16-byte alignment
+    assert _fwd(lib, LSE=FAKE + 4) == 6
+    assert _fwd(lib, flags=(0, 2)) == 7               # flags are 0 or 1
+    assert lib.saf_hybrid_attn_fwd(1, FAKE, FAKE, FAKE, None, FAKE, FAKE, 8, 1, 2, 8, 64, FAKE, FAKE, None) == 1
+
+
+def test_empty_problems_are_no_ops(lib):
+    assert _fwd(lib, B=0) == 0
+    assert _fwd(lib, N=0, V=None, O=None) == 0
+    assert lib.saf_hybrid_attn_fwd(1, None, None, None, None, None, None, 0, 4, 0, 16, 64, None, None, None) == 0
+
+
+def test_backward_argument_errors(lib):
+    for stage in (None, 0, 1, 2):
+        assert _bwd(lib, stage, dt=9) == 3
+        assert _bwd(lib, stage, d=96) == 3
+        assert _bwd(lib, stage, a=None) == 4
+        assert _bwd(lib, stage, dO=None) == 1
+        assert _bwd(lib, stage, ws=None) == 1
+        assert _bwd(lib, stage, ws=FAKE + 16) == 6    # workspace is 256-byte aligned
+        assert _bwd(lib, stage, ws_bytes=0) == 2       # workspace too small
+        assert _bwd(lib, stage, dK=FAKE + 2) == 6
+        assert _bwd(lib, stage, flags=(3, 0)) == 7
+        assert _bwd(lib, stage, B=0) == 0
+    assert _bwd(lib, 5) == 3                           # unknown stage
+
+
+def test_workspace_size(lib):
+    assert lib.saf_hybrid_attn_bwd_workspace_bytes(1, 8, 12, 4096, 64) == 8 * 12 * 4096 * 4
+    assert lib.saf_hybrid_attn_bwd_workspace_bytes(0, 1, 1, 3, 64) == 256
+    assert lib.saf_hybrid_attn_bwd_workspace_bytes(1, 1, 1, 1, 32) == 0
+    assert lib.saf_hybrid_attn_bwd_workspace_bytes(1, 0, 1, 1, 64) == 0
+    assert lib.saf_hybrid_attn_bwd_workspace_bytes(4, 1, 1, 1, 64) == 0
+
+
+def test_status_strings(lib):
+    from paper_2609_34650_amd import binding
+    for code in range(8):
+        assert binding.status_str(code) and binding.status_str(code) != "unknown status"
+    assert binding.status_str(99) == "unknown status"

@@ -1,0 +1,298 @@
+"""GPU parity: the HIP path through the C ABI against the fp64 oracle on the
+same seeded inputs.
+
+Small shapes compare every element of O, LSE, dQ, dK, dV; they span several
+tiles and ragged tails.  The full-size workloads (124M-style 4K layer, 1B-style
+8K layer, 32K prefill, replacement-rate sweep) run in the launch configuration
+the benchmark times and compare whole sampled (batch, head) slices, or sampled
+query rows for the 32K forward.
+"""
+
+import numpy as np
+import pytest
+
+from gpu_helpers import announce, check_close, compare_layer, run_gpu, to_device, torch_cuda
+from paper_2609_34650_amd import inputs as gen
+
+pytestmark = pytest.mark.gpu
+
+
+def _inp(B, H, N, fixed, dtype, seed=11, backward=True, prior_len=None):
+    return gen.make_inputs(B, H, N, 64, fixed, dtype, seed=seed, stream_id=100 + N, backward=backward,
+                           prior_len=prior_len)
+
+
+def test_tiny_f32_workload_all_elements():
+    w = gen.WORKLOADS["tiny_f32"]
+    announce(f"{w.name} B={w.B} H={w.H} N={w.N}")
+    inp = gen.workload_inputs(w)
+    errs = compare_layer(run_gpu(inp, "f32"), inp, "f32")
+    print(errs)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_paper_unaligned_shape(dtype):
+    """B=2, T=129, H=4, d=64, prior length 192, heads 1 and 3 fixed (the mixed
+    layer of the paper's gradient-agreement check)."""
+    announce(f"paper shape {dtype}")
+    inp = _inp(2, 4, 129, [1, 3], dtype, prior_len=192)
+    compare_layer(run_gpu(inp, dtype), inp, dtype)
+
+
+@pytest.mark.parametrize("N", [1, 2, 31, 32, 33, 63, 64, 65, 127, 128, 129, 191, 255, 256, 257, 300])
+def test_edge_lengths_f32(N):
+    announce(f"edge f32 N={N}")
+    inp = _inp(1, 3, N, [1], "f32")
+    compare_layer(run_gpu(inp, "f32"), inp, "f32")
+
+
+@pytest.mark.parametrize("N", [1, 33, 65, 129, 383])
+def test_edge_lengths_bf16(N):
+    announce(f"edge bf16 N={N}")
+    inp = _inp(2, 3, N, [0], "bf16")
+    compare_layer(run_gpu(inp, "bf16"), inp, "bf16")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("fixed", [[], [0, 1, 2, 3]], ids=["all_ordinary", "all_fixed"])
+def test_uniform_head_sets(dtype, fixed):
+    announce(f"head set {fixed} {dtype}")
+    inp = _inp(2, 4, 200, fixed, dtype)
+    compare_layer(run_gpu(inp, dtype), inp, dtype)
+
+
+def test_bf16_several_tiles_ragged():
+    announce("bf16 B=2 H=4 N=1000")
+    inp = _inp(2, 4, 1000, [1, 2], "bf16")
+    print(compare_layer(run_gpu(inp, "bf16"), inp, "bf16"))
+
+
+def test_fuzz_head_states_f32():
+    """Fifty random (B, H, N, fixed set) draws, including empty and full fixed
+    sets, against the oracle (the paper's 50-operation state fuzz)."""
+    rng = np.random.default_rng(5)
+    for it in range(50):
+        B = int(rng.integers(1, 3))
+        H = int(rng.integers(1, 6))
+        N = int(rng.integers(1, 160))
+        kind = it % 5
+        if kind == 0:
+            fixed = []
+        elif kind == 1:
+            fixed = list(range(H))
+        else:
+            fixed = [h for h in range(H) if rng.random() < 0.5]
+        announce(f"fuzz {it}: B={B} H={H} N={N} fixed={fixed}")
+        inp = gen.make_inputs(B, H, N, 64, fixed, "f32", seed=1000 + it, stream_id=9)
+        compare_layer(run_gpu(inp, "f32"), inp, "f32")
+
+
+# ---------------------------------------------------------------------------
+# Full-size workloads (sampled slices)
+# ---------------------------------------------------------------------------
+
+def _sample_heads(w, inp, count_each=2, seed=0):
+    rng = np.random.default_rng(seed)
+    fixed = [h for h in range(w.H) if inp["is_fixed"][h]]
+    ordinary = [h for h in range(w.H) if not inp["is_fixed"][h]]
+    out = []
+    for pool in (fixed, ordinary):
+        for h in rng.permutation(pool)[:count_each]:
+            out.append((int(rng.integers(0, w.B)), int(h)))
+    # The last batch element and the first head are always covered.
+    out.append((w.B - 1, 0))
+    return sorted(set(out))
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("name", ["gpt124m_4k", "gpt1b_8k", "sweep124m_0", "sweep124m_6", "sweep124m_12"])
+def test_full_size_workload_sampled_heads(name):
+    w = gen.WORKLOADS[name]
+    announce(f"{name} B={w.B} H={w.H} N={w.N}")
+    inp = gen.workload_inputs(w)
+    gpu = run_gpu(inp, w.dtype, backward=True)
+    heads = _sample_heads(w, inp, count_each=1 if w.N > 4096 else 2)
+    announce(f"{name} oracle on {heads}")
+    print(compare_layer(gpu, inp, w.dtype, backward=True, heads=heads))
+
+
+@pytest.mark.slow
+def test_prefill_32k_sampled_rows():
+    from oracle import saf_oracle as orc
+    w = gen.WORKLOADS["prefill_32k"]
+    announce(f"{w.name} B={w.B} H={w.H} N={w.N} forward")
+    inp = gen.workload_inputs(w)
+    gpu = run_gpu(inp, w.dtype, backward=False)
+    rng = np.random.default_rng(3)
+    rows = np.unique(np.concatenate([[0, 1, 63, 64, 4095, w.N - 1], rng.integers(0, w.N, 40)]))
+    fixed = [h for h in range(w.H) if inp["is_fixed"][h]]
+    ordinary = [h for h in range(w.H) if not inp["is_fixed"][h]]
+    for h in (fixed[0], ordinary[0], ordinary[-1]):
+        fx = bool(inp["is_fixed"][h])
+        o, lse = orc.head_forward(None if fx else inp["Q"][0, h], None if fx else inp["K"][0, h],
+                                  inp["V"][0, h], fx, inp["a"][h], inp["r"][h], rows=rows, row_block=8)
+        check_close(f"O[h={h}]", gpu["O"][0, h][rows], o, "bf16")
+        check_close(f"LSE[h={h}]", gpu["LSE"][0, h][rows], lse, "bf16")
+
+
+# ---------------------------------------------------------------------------
+# Metamorphic and structural checks
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_fixed_heads_never_read_q_k(dtype):
+    torch = torch_cuda()
+    from paper_2609_34650_amd import binding
+    announce(f"NaN in fixed Q/K {dtype}")
+    inp = _inp(2, 4, 300, [0, 2], dtype)
+    t = to_device(inp, dtype)
+    O0, L0 = binding.saf_hybrid_attn_fwd(t["Q"], t["K"], t["V"], t["is_fixed"], t["a"], t["r"])
+    G0 = binding.saf_hybrid_attn_bwd(t["Q"], t["K"], t["V"], O0, t["dO"], L0, t["is_fixed"], t["a"], t["r"])
+    Qn, Kn = t["Q"].clone(), t["K"].clone()
+    Qn[:, [0, 2]] = float("nan")
+    Kn[:, [0, 2]] = float("nan")
+    O1, L1 = binding.saf_hybrid_attn_fwd(Qn, Kn, t["V"], t["is_fixed"], t["a"], t["r"])
+    G1 = binding.saf_hybrid_attn_bwd(Qn, Kn, t["V"], O1, t["dO"], L1, t["is_fixed"], t["a"], t["r"])
+    torch.cuda.synchronize()
+    assert torch.equal(O0, O1) and torch.equal(L0, L1)
+    for g0, g1 in zip(G0, G1):
+        assert torch.isfinite(g1).all()
+        assert torch.equal(g0, g1)
+
+
+def test_shift_invariance_on_gpu():
+    """a + 100 and r - 3 leave O and dV unchanged and move LSE by 97 for fixed
+    heads; a naive float32 exp(a) would overflow."""
+    announce("shift invariance")
+    inp = _inp(1, 3, 257, [0, 1, 2], "f32")
+    base = run_gpu(inp, "f32")
+    shifted = dict(inp)
+    shifted["a"] = (inp["a"] + 100.0).astype(np.float32)
+    shifted["r"] = (inp["r"] - 3.0).astype(np.float32)
+    moved = run_gpu(shifted, "f32")
+    check_close("O", moved["O"], base["O"], "f32")
+    check_close("dV", moved["dV"], base["dV"], "f32")
+    check_close("LSE", moved["LSE"] - 97.0, base["LSE"], "f32")
+    compare_layer(moved, shifted, "f32")
+
+
+def test_identity_and_uniform_patterns_on_gpu():
+    """Closed forms through the kernel: r = (0, -1e4, ...) gives O = V and
+    dV = dO; a = r = 0 gives prefix means."""
+    announce("closed forms")
+    N = 190
+    inp = _inp(1, 2, N, [0, 1], "f32")
+    inp["r"][0] = -1e4
+    inp["r"][0, 0] = 0.0
+    inp["a"][1] = 0.0
+    inp["r"][1] = 0.0
+    g = run_gpu(inp, "f32")
+    check_close("O=V", g["O"][0, 0], inp["V"][0, 0].astype(np.float64), "f32")
+    check_close("dV=dO", g["dV"][0, 0], inp["dO"][0, 0].astype(np.float64), "f32")
+    cnt = np.arange(1, N + 1)[:, None]
+    check_close("prefix mean", g["O"][0, 1], np.cumsum(inp["V"][0, 1].astype(np.float64), 0) / cnt, "f32")
+    check_close("LSE=log(i+1)", g["LSE"][0, 1], np.log(np.arange(1, N + 1)), "f32")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_deterministic_repeat(dtype):
+    torch = torch_cuda()
+    from paper_2609_34650_amd import binding
+    announce(f"determinism {dtype}")
+    inp = _inp(2, 4, 333, [1], dtype)
+    t = to_device(inp, dtype)
+    outs = []
+    for _ in range(2):
+        O, L = binding.saf_hybrid_attn_fwd(t["Q"], t["K"], t["V"], t["is_fixed"], t["a"], t["r"])
+        G = binding.saf_hybrid_attn_bwd(t["Q"], t["K"], t["V"], O, t["dO"], L, t["is_fixed"], t["a"], t["r"])
+        outs.append((O, L) + tuple(G))
+    torch.cuda.synchronize()
+    for x, y in zip(*outs):
+        assert torch.equal(x, y)
+
+
+def test_stages_equal_full_backward():
+    torch = torch_cuda()
+    from paper_2609_34650_amd import binding
+    announce("bwd stages")
+    inp = _inp(1, 3, 260, [2], "bf16")
+    t = to_device(inp, "bf16")
+    O, L = binding.saf_hybrid_attn_fwd(t["Q"], t["K"], t["V"], t["is_fixed"], t["a"], t["r"])
+    full = binding.saf_hybrid_attn_bwd(t["Q"], t["K"], t["V"], O, t["dO"], L, t["is_fixed"], t["a"], t["r"])
+    nbytes = binding.saf_hybrid_attn_bwd_workspace_bytes(torch.bfloat16, 1, 3, 260, 64)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device=O.device)
+    dQ, dK, dV = (torch.empty_like(O) for _ in range(3))
+    for st in (binding.SAF_BWD_PREPROCESS, binding.SAF_BWD_DQ, binding.SAF_BWD_DKDV):
+        binding.saf_hybrid_attn_bwd_stage(st, t["Q"], t["K"], t["V"], O, t["dO"], L, t["is_fixed"], t["a"],
+                                          t["r"], dQ, dK, dV, ws)
+    torch.cuda.synchronize()
+    for x, y in zip(full, (dQ, dK, dV)):
+        assert torch.equal(x, y)
+
+
+def _guarded(torch, shape, dtype, dev, guard=4096):
+    n = int(np.prod(shape))
+    buf = torch.full((n + 2 * guard,), 12345.0, dtype=dtype, device=dev)
+    return buf, buf[guard:guard + n].view(shape)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_no_writes_outside_outputs(dtype):
+    """Canary bands around every output stay untouched; the interior equals a
+    normal run."""
+    torch = torch_cuda()
+    from paper_2609_34650_amd import binding
+    announce(f"canaries {dtype}")
+    B, H, N = 2, 3, 97
+    inp = _inp(B, H, N, [1], dtype)
+    t = to_device(inp, dtype)
+    tdt, dev = t["V"].dtype, t["V"].device
+    bufs = {}
+    bufs["O"], O = _guarded(torch, (B, H, N, 64), tdt, dev)
+    bufs["L"], L = _guarded(torch, (B, H, N), torch.float32, dev)
+    bufs["dQ"], dQ = _guarded(torch, (B, H, N, 64), tdt, dev)
+    bufs["dK"], dK = _guarded(torch, (B, H, N, 64), tdt, dev)
+    bufs["dV"], dV = _guarded(torch, (B, H, N, 64), tdt, dev)
+    binding.saf_hybrid_attn_fwd(t["Q"], t["K"], t["V"], t["is_fixed"], t["a"], t["r"], O=O, LSE=L)
+    binding.saf_hybrid_attn_bwd(t["Q"], t["K"], t["V"], O, t["dO"], L, t["is_fixed"], t["a"], t["r"], dQ, dK, dV)
+    torch.cuda.synchronize()
+    for name, buf in bufs.items():
+        g = 4096
+        assert (buf[:g] == 12345.0).all() and (buf[-g:] == 12345.0).all(), f"{name} guard band written"
+    ref = run_gpu(inp, dtype)
+    assert np.array_equal(O.float().cpu().numpy(), ref["O"].astype(np.float32))
+    assert np.array_equal(dK.float().cpu().numpy(), ref["dK"].astype(np.float32))
+
+
+def test_rejected_call_writes_nothing():
+    torch = torch_cuda()
+    from paper_2609_34650_amd import binding
+    announce("error path")
+    inp = _inp(1, 2, 64, [1], "bf16")
+    t = to_device(inp, "bf16")
+    O = torch.full_like(t["V"], 7.0)
+    L = torch.full((1, 2, 64), 7.0, device=O.device)
+    with pytest.raises(binding.SafError) as e:
+        binding.saf_hybrid_attn_fwd(t["Q"], t["K"], t["V"], t["is_fixed"], None, t["r"], O=O, LSE=L)
+    assert e.value.code == 4
+    with pytest.raises(binding.SafError) as e:
+        binding.saf_hybrid_attn_fwd(t["Q"], t["K"], t["V"], [0, 3], t["a"], t["r"], O=O, LSE=L)
+    assert e.value.code == 7
+    torch.cuda.synchronize()
+    assert (O == 7.0).all() and (L == 7.0).all()
+
+
+def test_autograd_wrapper_matches_abi():
+    torch = torch_cuda()
+    from paper_2609_34650_amd import binding
+    announce("autograd wrapper")
+    inp = _inp(1, 2, 150, [0], "f32")
+    t = to_device(inp, "f32")
+    q, k, v = (t[x].clone().requires_grad_(True) for x in ("Q", "K", "V"))
+    o = binding.HybridAttention.apply(q, k, v, t["is_fixed"], t["a"], t["r"])
+    o.backward(t["dO"])
+    ref = run_gpu(inp, "f32")
+    torch.cuda.synchronize()
+    assert np.array_equal(o.detach().cpu().numpy(), ref["O"].astype(np.float32))
+    assert np.array_equal(v.grad.cpu().numpy(), ref["dV"].astype(np.float32))
+    assert np.array_equal(q.grad.cpu().numpy(), ref["dQ"].astype(np.float32))

@@ -303,6 +303,18 @@ def test_row_blocking_does_not_change_results():
             np.testing.assert_allclose(g2, g1, rtol=1e-12, atol=1e-13)
 
 
+def test_sampled_rows_match_full_head():
+    n, d = 70, 4
+    q, k, v = _rand(n, d), _rand(n, d), _rand(n, d)
+    a, r = _rand(n), _rand(n)
+    rows = np.array([0, 5, 69, 33, 33])
+    for fixed in (False, True):
+        o, l = orc.head_forward(q, k, v, fixed, a, r)
+        os_, ls = orc.head_forward(q, k, v, fixed, a, r, rows=rows, row_block=2)
+        np.testing.assert_allclose(os_, o[rows], rtol=1e-14, atol=1e-15)
+        np.testing.assert_allclose(ls, l[rows], rtol=1e-14)
+
+
 def test_sampled_heads_match_full_layer():
     B, H, N, d = 2, 3, 12, 4
     Q, K, V, dO = (_rand(B, H, N, d) for _ in range(4))
