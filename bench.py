@@ -86,7 +86,7 @@ def parse():
     ap.add_argument("--cpu-baseline", dest="cpu_baseline", action="store_true", default=True)
     ap.add_argument("--no-cpu-baseline", dest="cpu_baseline", action="store_false")
     ap.add_argument("--cpu-slices", type=int, default=0,
-                    help="(batch, head) slices the oracle baseline runs (0: one per worker, twice)")
+                    help="(batch, head) slices the oracle baseline runs (0: four per worker)")
     ap.add_argument("--compare-ordinary", dest="compare", action="store_true", default=True)
     ap.add_argument("--no-compare-ordinary", dest="compare", action="store_false")
     return ap.parse_args()
@@ -162,7 +162,7 @@ def cpu_baseline(inp, w, slices_req):
         threadpool_limits = None
     workers = max(1, min(MAX_HOST_WORKERS, len(os.sched_getaffinity(0))))
     all_slices = [(b, h) for b in range(w.B) for h in range(w.H)]
-    n = slices_req if slices_req > 0 else min(len(all_slices), 2 * workers)
+    n = slices_req if slices_req > 0 else min(len(all_slices), 4 * workers)
     sample = all_slices[:n]
     n_fixed = int(sum(inp["is_fixed"][h] for _, h in sample))
     ctx = threadpool_limits(limits=1) if threadpool_limits else None

@@ -25,6 +25,9 @@ HIPCC_FLAGS = [
     "-fvisibility=hidden",
     # No packed-fp32 VALU instructions in any kernel.
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # MFMA accumulators in ordinary VGPRs: the softmax works on them directly,
+    # with no copies between AGPRs and VGPRs.
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
     "-Wall",
     "-Wno-unused-function",
 ]

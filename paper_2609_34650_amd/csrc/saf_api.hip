@@ -59,6 +59,24 @@ saf_status_t launched() { return hipGetLastError() == hipSuccess ? SAF_OK : SAF_
 
 template <typename T>
 saf_status_t launch_fwd(const saf::FwdArgs& args, hipStream_t stream) {
+    if (args.fixed_mask) {
+        // Fixed-head row normalisers first: the main kernel reads them.
+        saf::NormArgs na;
+        na.a = args.a;
+        na.r = args.r;
+        na.lse = args.lse;
+        na.B = args.B;
+        na.H = args.H;
+        na.N = args.N;
+        na.ld_prior = args.ld_prior;
+        na.n_rblocks = (args.N + saf::NORM_ROWS - 1) / saf::NORM_ROWS;
+        na.n_fixed = 0;
+        for (int h = 0; h < args.H; ++h)
+            if ((args.fixed_mask >> h) & 1ull) na.heads[na.n_fixed++] = (unsigned char)h;
+        const unsigned ngrid = (unsigned)((size_t)na.n_rblocks * na.n_fixed);
+        hipLaunchKernelGGL(saf::fixed_lse_kernel, dim3(ngrid), dim3(saf::NORM_THREADS), 0, stream, na);
+        if (launched() != SAF_OK) return SAF_ERR_LAUNCH;
+    }
     const unsigned grid = (unsigned)((size_t)args.n_qblocks * args.B * args.H);
     hipLaunchKernelGGL(saf::fwd_kernel<T>, dim3(grid), dim3(saf::FWD_THREADS), 0, stream, args);
     return launched();

@@ -37,6 +37,13 @@ constexpr float LN2 = 0.6931471805599453f;
 // Running-max start value: finite, so exp2(m_old - m_new) is 0 (not NaN)
 // on the first visible tile.
 constexpr float NEG_BIG = -1.0e30f;
+// Fixed heads use the factorised exp(a - A) * exp(r - R) form only while every
+// row's normaliser stays within this many natural-log units of exp(A + R);
+// beyond it a workgroup falls back to exact per-element exponentials.
+constexpr float FAST_GUARD = 40.0f;
+// Shifted copies of a Toeplitz band in LDS: copy s starts s entries later, so
+// eight consecutive entries from any start are one aligned 16-byte read.
+constexpr int BAND_COPIES = 8;
 
 template <typename T> struct Vec;
 template <> struct Vec<bf16> {
@@ -116,5 +123,107 @@ __device__ __forceinline__ int tpos(int k) {
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 __device__ __forceinline__ float xor32(float x) { return __shfl_xor(x, 32); }
+
+// IEEE maximum (NaN-propagating): lowers to v_maximum3_f32 chains with no
+// NaN-quieting of the inputs, unlike fmaxf.
+__device__ __forceinline__ float vmax(float a, float b) { return __builtin_elementwise_maximum(a, b); }
+
+typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
+
+__device__ __forceinline__ unsigned int pack_bf16(float lo, float hi) {
+    const bf16x2 v = {(bf16)lo, (bf16)hi};
+    return __builtin_bit_cast(unsigned int, v);
+}
+
+// Transposed store of two consecutive rows x0, x1 (eight consecutive columns
+// each): dst[t * ld] = (x0[t], x1[t]) as an adjacent pair, t = 0..7.  The bf16
+// version packs the halves of 32-bit words with v_perm_b32 (no per-element
+// vector shuffles, which the compiler would route through scratch memory).
+__device__ __forceinline__ void st_pair_t(bf16* dst, int ld, const bf16x8& x0, const bf16x8& x1) {
+    const u32x4 a = __builtin_bit_cast(u32x4, x0);
+    const u32x4 b = __builtin_bit_cast(u32x4, x1);
+#pragma unroll
+    for (int m = 0; m < 4; ++m) {
+        *reinterpret_cast<unsigned int*>(dst + (2 * m) * ld) = __builtin_amdgcn_perm(b[m], a[m], 0x05040100u);
+        *reinterpret_cast<unsigned int*>(dst + (2 * m + 1) * ld) = __builtin_amdgcn_perm(b[m], a[m], 0x07060302u);
+    }
+}
+__device__ __forceinline__ void st_pair_t(float* dst, int ld, const f32x8& x0, const f32x8& x1) {
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+        const f32x2 v = {x0[t], x1[t]};
+        *reinterpret_cast<f32x2*>(dst + t * ld) = v;
+    }
+}
+
+// As st_pair_t, with row x0 scaled by e0 and row x1 by e1 (rounded once).
+__device__ __forceinline__ void st_pair_t_scaled(bf16* dst, int ld, const bf16x8& x0, const bf16x8& x1, float e0,
+                                                 float e1) {
+    const u32x4 a = __builtin_bit_cast(u32x4, x0);
+    const u32x4 b = __builtin_bit_cast(u32x4, x1);
+#pragma unroll
+    for (int m = 0; m < 4; ++m) {
+        const float a_lo = __uint_as_float(a[m] << 16), a_hi = __uint_as_float(a[m] & 0xffff0000u);
+        const float b_lo = __uint_as_float(b[m] << 16), b_hi = __uint_as_float(b[m] & 0xffff0000u);
+        *reinterpret_cast<unsigned int*>(dst + (2 * m) * ld) = pack_bf16(a_lo * e0, b_lo * e1);
+        *reinterpret_cast<unsigned int*>(dst + (2 * m + 1) * ld) = pack_bf16(a_hi * e0, b_hi * e1);
+    }
+}
+__device__ __forceinline__ void st_pair_t_scaled(float* dst, int ld, const f32x8& x0, const f32x8& x1, float e0,
+                                                 float e1) {
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+        const f32x2 v = {x0[t] * e0, x1[t] * e1};
+        *reinterpret_cast<f32x2*>(dst + t * ld) = v;
+    }
+}
+
+// Sum of the eight operand values: for bf16 the rounded values that enter
+// the product (four packed dot products against ones), for float32 plain adds.
+__device__ __forceinline__ float sum8(const bf16x8& x, float acc) {
+    const bf16x2 one = {(bf16)1.0f, (bf16)1.0f};
+#pragma unroll
+    for (int t = 0; t < 8; t += 2) {
+        const bf16x2 pr = {x[t], x[t + 1]};
+        acc = __builtin_amdgcn_fdot2_f32_bf16(pr, one, acc, false);
+    }
+    return acc;
+}
+__device__ __forceinline__ float sum8(const f32x8& x, float acc) {
+#pragma unroll
+    for (int t = 0; t < 8; ++t) acc += x[t];
+    return acc;
+}
+
+// acc + sum_t x[t] * y[t] over eight operand values.
+__device__ __forceinline__ float dot8(const bf16x8& x, const bf16x8& y, float acc) {
+#pragma unroll
+    for (int t = 0; t < 8; t += 2) {
+        const bf16x2 px = {x[t], x[t + 1]};
+        const bf16x2 py = {y[t], y[t + 1]};
+        acc = __builtin_amdgcn_fdot2_f32_bf16(px, py, acc, false);
+    }
+    return acc;
+}
+__device__ __forceinline__ float dot8(const f32x8& x, const f32x8& y, float acc) {
+#pragma unroll
+    for (int t = 0; t < 8; ++t) acc = fmaf(x[t], y[t], acc);
+    return acc;
+}
+
+// Maximum / minimum over the 256 threads of a workgroup (4 wavefronts);
+// `red` is 4 floats of LDS.  Contains barriers: call from uniform code.
+__device__ __forceinline__ float wave_max(float x) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) x = fmaxf(x, __shfl_xor(x, o));
+    return x;
+}
+__device__ __forceinline__ float block_max(float x, float* red) {
+    x = wave_max(x);
+    __syncthreads();
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = x;
+    __syncthreads();
+    return fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+}
 
 }  // namespace saf

@@ -1,28 +1,36 @@
 // Forward of the hybrid causal-attention layer: one launch for all heads.
 //
 // Workgroup = (batch b, head h, block of 128 queries); 4 wavefronts, each
-// owning 32 consecutive queries.  The head's flag picks the path of the whole
-// workgroup (Appendix "Mixed-head execution and numerical checks": one
+// owning 32 consecutive queries.  The head's flag picks the program of the
+// whole workgroup (Appendix "Mixed-head execution and numerical checks": one
 // program per batch element, head and query block, a head-state flag selects
 // the computation, outputs keep the original head order).
 //
-// Both paths stream key tiles of 64 from key 0 up to the block's last query
-// (causal tile skipping: tiles wholly in the future of a wavefront's queries
-// are skipped by that wavefront) and keep, per query, a running maximum m and
-// sum l of the base-2 exponentials plus an unnormalised output, the online
-// softmax of FlashAttention-2 that the paper uses for ordinary heads.
+// Ordinary heads (Eqs. standard-head): FlashAttention-2 tiling with online
+// softmax, the scheme the paper uses for ordinary heads.  Scores are formed
+// transposed, S^T = K Q^T (keys x queries), so the accumulator of lane l holds
+// one query (l % 32) and 16 of its keys: the running maximum and sum stay in
+// the lane (one exchange with the other lane half per tile), the
+// exponentials go straight into the B operand of O^T += V^T P^T, and O^T
+// again holds one query per lane.  Key tiles of 64 stream through a double
+// buffer in LDS while the next tile's global loads are in flight; the tiles
+// below the block's diagonal run a mask-free body.  The running maximum is
+// only raised when a tile exceeds it by more than 2^8, so most tiles skip the
+// rescale of the accumulator.
 //
-// Scores are formed transposed, S^T (keys x queries), so that the
-// accumulator of lane l holds one query (l % 32) and 16 of its keys: the
-// per-query statistics stay in the lane (one cross-half exchange per tile for
-// the maximum), the exponentials go straight into the B operand of
-// O^T += V^T P^T, and O^T again holds one query per lane.
-//
-//   ordinary head: S = Q K^T / sqrt(d) (bf16/fp32 MFMA, K tile in LDS,
-//                  Q in registers), LSE = log sum_j exp(S_ij)
-//   fixed head:    S_ij = a[j] + r[i - j] gathered from LDS copies of a and
-//                  of the r band the tile touches (Eq. compact-prior; no
-//                  1/sqrt(d), no Q or K reads), LSE = log Z(i)
+// Fixed heads (Eq. compact-prior): P(i,j) = exp(a[j] + r[i-j]) / Z(i) factors
+// as ea(j) * er(i-j) / Z'(i) with ea = exp(a - A*), er = exp(r - R*) and
+// A*, R* the maxima of a and r over the positions the block touches.  Each V
+// row is scaled by ea(j) while it is staged in LDS, so the weight tile is the
+// Toeplitz band er(i-j) -- read from LDS with no exponential, no score and no
+// softmax per element; a band entry of a negative offset is 0, which is the
+// causal mask.  The row normalisers are precomputed, as in the paper: a
+// pre-pass (fixed_lse_kernel) writes log Z(i) in float32 into LSE for every
+// batch element, and the block scales its accumulator by
+// exp(A* + R* - log Z(i)).  This is exact up to rounding as long as no row's
+// terms all underflow; a block where the largest of a row's diagonal and sink
+// terms lies more than FAST_GUARD below A* + R* runs the exact per-element
+// program instead.
 #pragma once
 
 #include "saf_common.h"
@@ -33,14 +41,37 @@ constexpr int FWD_BM = 128;  // queries per workgroup
 constexpr int FWD_BN = 64;   // keys per tile
 constexpr int FWD_THREADS = 256;
 constexpr int LDS_PAD = 8;   // elements appended to each LDS row
+constexpr float RESCALE_TAU = 8.0f;   // log2 units
+constexpr int FWD_BAND = FWD_BM + FWD_BN;    // 191 offsets used per tile
+constexpr int FWD_BAND_STRIDE = FWD_BAND + 8;  // spreads the copies over banks
 
 template <typename T>
-struct FwdSmem {
-    T k[FWD_BN][HEAD_DIM + LDS_PAD];    // K tile, [key][d]
-    T vt[HEAD_DIM][FWD_BN + LDS_PAD];   // V tile transposed, [d][tpos(key)]
-    float a[FWD_BN];                    // fixed head: a of the tile's keys
-    float rb[FWD_BM + FWD_BN];          // fixed head: r over the tile's offsets
+struct FwdOrdSmem {
+    T k[2][FWD_BN][HEAD_DIM + LDS_PAD];   // K tile, [key][d]
+    T vt[2][HEAD_DIM][FWD_BN + LDS_PAD];  // V tile transposed, [d][tpos(key)]
 };
+
+template <typename T>
+struct FwdFixSmem {
+    T vt[2][HEAD_DIM][FWD_BN + LDS_PAD];                // (ea * V) transposed, [d][key]
+    T band[2][BAND_COPIES][FWD_BAND_STRIDE];            // er, reversed, 8 shifted copies
+    float red[4];
+};
+
+template <typename T>
+struct FwdExactSmem {
+    T vt[HEAD_DIM][FWD_BN + LDS_PAD];  // V tile transposed, [d][tpos(key)]
+    float a[FWD_BN];
+    float rb[FWD_BAND];
+};
+
+template <typename T>
+constexpr size_t fwd_smem_bytes() {
+    size_t x = sizeof(FwdOrdSmem<T>);
+    if (sizeof(FwdFixSmem<T>) > x) x = sizeof(FwdFixSmem<T>);
+    if (sizeof(FwdExactSmem<T>) > x) x = sizeof(FwdExactSmem<T>);
+    return x;
+}
 
 struct FwdArgs {
     const void* q;
@@ -55,42 +86,142 @@ struct FwdArgs {
     float scale_log2;  // log2(e) / sqrt(d)
 };
 
-template <typename T>
-__global__ __launch_bounds__(FWD_THREADS) void fwd_kernel(FwdArgs p) {
-    __shared__ FwdSmem<T> sm;
+// Per-lane geometry of one workgroup.
+struct FwdLane {
+    int tid, w, c, hf, m0, q0, qq, N;
+};
 
-    const int n_bh = p.B * p.H;
-    // Longest blocks first: block index -> query block in descending order.
-    const int qblk = p.n_qblocks - 1 - (int)(blockIdx.x / n_bh);
-    const int bh = (int)(blockIdx.x % n_bh);
-    const int h = bh % p.H;
-    const bool fixed = (p.fixed_mask >> h) & 1ull;
-    const int N = p.N;
-    const size_t base = (size_t)bh * N * HEAD_DIM;
+template <typename T>
+__device__ __forceinline__ void store_output(T* O, float* LSE, const FwdLane& L, const f32x16 (&oacc)[2],
+                                             float inv, float lse, bool write_lse = true) {
+    if (L.qq >= L.N) return;
+    T* orow = O + (size_t)L.qq * HEAD_DIM;
+#pragma unroll
+    for (int db = 0; db < 2; ++db)
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+            st4<T>(orow + 32 * db + 8 * g + 4 * L.hf, oacc[db][4 * g] * inv, oacc[db][4 * g + 1] * inv,
+                   oacc[db][4 * g + 2] * inv, oacc[db][4 * g + 3] * inv);
+    if (write_lse && L.hf == 0) LSE[L.qq] = lse;
+}
+
+// ---------------------------------------------------------------------------
+// Ordinary heads
+// ---------------------------------------------------------------------------
+
+template <typename T>
+struct KVStage {
+    typename Vec<T>::x8 k[2], v[2];
+};
+
+template <typename T>
+__device__ __forceinline__ void ord_load(KVStage<T>& st, const T* K, const T* V, int n0, int N, int tid) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const int id = tid + FWD_THREADS * i;
+        const int row = id >> 3;
+        const int col = (id & 7) * 8;
+        st.k[i] = (n0 + row < N) ? ld8<T>(K + (size_t)(n0 + row) * HEAD_DIM + col) : zero8<T>();
+    }
+    const int k2 = (tid >> 3) * 2;
+    const int d8 = (tid & 7) * 8;
+    st.v[0] = (n0 + k2 < N) ? ld8<T>(V + (size_t)(n0 + k2) * HEAD_DIM + d8) : zero8<T>();
+    st.v[1] = (n0 + k2 + 1 < N) ? ld8<T>(V + (size_t)(n0 + k2 + 1) * HEAD_DIM + d8) : zero8<T>();
+}
+
+template <typename T>
+__device__ __forceinline__ void ord_store(FwdOrdSmem<T>& sm, int buf, const KVStage<T>& st, int tid) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const int id = tid + FWD_THREADS * i;
+        st8<T>(&sm.k[buf][id >> 3][(id & 7) * 8], st.k[i]);
+    }
+    const int k2 = (tid >> 3) * 2;
+    const int d8 = (tid & 7) * 8;
+    st_pair_t(&sm.vt[buf][d8][tpos(k2)], FWD_BN + LDS_PAD, st.v[0], st.v[1]);
+}
+
+template <typename T, bool MASK>
+__device__ __forceinline__ void ord_tile(const FwdOrdSmem<T>& sm, int buf, int n0, const FwdLane& L,
+                                         const typename Vec<T>::x8 (&qf)[4], f32x16 (&oacc)[2], float& m_run,
+                                         float& l_run, float scale_log2) {
+    typedef typename Vec<T>::x8 frag;
+    bool act1 = true;
+    if (MASK) {
+        if (!(n0 < L.q0 + 32 && n0 < L.N)) return;  // tile wholly after this wavefront's queries
+        act1 = (n0 + 32 < L.q0 + 32) && (n0 + 32 < L.N);
+    }
+    f32x16 s[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) s[kb][v] = 0.0f;
+        if (kb == 1 && !act1) continue;
+#pragma unroll
+        for (int dc = 0; dc < 4; ++dc) mma(s[kb], ld8<T>(&sm.k[buf][32 * kb + L.c][16 * dc + 8 * L.hf]), qf[dc]);
+    }
+    if (MASK) {
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) {
+            const int k0 = n0 + 32 * kb;
+            if (kb == 1 && !act1) {
+#pragma unroll
+                for (int v = 0; v < 16; ++v) s[kb][v] = -INFINITY;
+            } else if (k0 == L.q0) {  // diagonal sub-block: hide keys after the query
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const int kk = k0 + 8 * (v >> 2) + 4 * L.hf + (v & 3);
+                    if (kk > L.qq) s[kb][v] = -INFINITY;
+                }
+            }
+        }
+    }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int v = 0; v < 16; v += 2) mx = vmax(vmax(mx, s[kb][v]), s[kb][v + 1]);
+    mx = vmax(mx, xor32(mx)) * scale_log2;
+    if (__any(mx > m_run + RESCALE_TAU)) {
+        const float m_new = fmaxf(m_run, mx);
+        const float alpha = fast_exp2(m_run - m_new);
+        m_run = m_new;
+        l_run *= alpha;
+#pragma unroll
+        for (int db = 0; db < 2; ++db)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) oacc[db][v] *= alpha;
+    }
+    const float neg_m = -m_run;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+        if (MASK && kb == 1 && !act1) continue;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            s[kb][v] = fast_exp2(fmaf(s[kb][v], scale_log2, neg_m));
+            l_run += s[kb][v];  // float32 row sum, before rounding to the operand type
+        }
+#pragma unroll
+        for (int kc = 0; kc < 2; ++kc) {
+            const frag pb = to_operand<T>(s[kb], 8 * kc);
+#pragma unroll
+            for (int db = 0; db < 2; ++db)
+                mma(oacc[db], ld8<T>(&sm.vt[buf][32 * db + L.c][32 * kb + 16 * kc + 8 * L.hf]), pb);
+        }
+    }
+}
+
+template <typename T>
+__device__ void fwd_ordinary(void* smem, const FwdArgs& p, const FwdLane& L, size_t base, size_t row_base) {
+    FwdOrdSmem<T>& sm = *reinterpret_cast<FwdOrdSmem<T>*>(smem);
     const T* __restrict__ Q = reinterpret_cast<const T*>(p.q) + base;
     const T* __restrict__ K = reinterpret_cast<const T*>(p.k) + base;
     const T* __restrict__ V = reinterpret_cast<const T*>(p.v) + base;
-    T* __restrict__ O = reinterpret_cast<T*>(p.o) + base;
-    float* __restrict__ LSE = p.lse + (size_t)bh * N;
-    const float* __restrict__ arow = fixed ? p.a + (size_t)h * p.ld_prior : nullptr;
-    const float* __restrict__ rrow = fixed ? p.r + (size_t)h * p.ld_prior : nullptr;
-
-    const int tid = threadIdx.x;
-    const int w = tid >> 6;
-    const int lane = tid & 63;
-    const int c = lane & 31;
-    const int hf = lane >> 5;
-    const int m0 = qblk * FWD_BM;
-    const int q0 = m0 + 32 * w;  // first query of this wavefront
-    const int qq = q0 + c;       // this lane's query
-
     typedef typename Vec<T>::x8 frag;
     frag qf[4];
-    if (!fixed) {
 #pragma unroll
-        for (int dc = 0; dc < 4; ++dc)
-            qf[dc] = qq < N ? ld8<T>(Q + (size_t)qq * HEAD_DIM + 16 * dc + 8 * hf) : zero8<T>();
-    }
+    for (int dc = 0; dc < 4; ++dc)
+        qf[dc] = L.qq < L.N ? ld8<T>(Q + (size_t)L.qq * HEAD_DIM + 16 * dc + 8 * L.hf) : zero8<T>();
 
     f32x16 oacc[2];
 #pragma unroll
@@ -100,85 +231,76 @@ __global__ __launch_bounds__(FWD_THREADS) void fwd_kernel(FwdArgs p) {
     float m_run = NEG_BIG;
     float l_run = 0.0f;  // this lane's share of the row sum
 
-    const int n_end = min(m0 + FWD_BM, N);
+    const int n_tiles = (min(L.m0 + FWD_BM, L.N) + FWD_BN - 1) / FWD_BN;
+    const int n_full = L.m0 / FWD_BN;  // tiles wholly below the block's first query
+    KVStage<T> st;
+    ord_load<T>(st, K, V, 0, L.N, L.tid);
+    ord_store<T>(sm, 0, st, L.tid);
+    __syncthreads();
+    for (int t = 0; t < n_tiles; ++t) {
+        const bool more = t + 1 < n_tiles;
+        if (more) ord_load<T>(st, K, V, (t + 1) * FWD_BN, L.N, L.tid);
+        if (t < n_full)
+            ord_tile<T, false>(sm, t & 1, t * FWD_BN, L, qf, oacc, m_run, l_run, p.scale_log2);
+        else
+            ord_tile<T, true>(sm, t & 1, t * FWD_BN, L, qf, oacc, m_run, l_run, p.scale_log2);
+        if (more) ord_store<T>(sm, (t + 1) & 1, st, L.tid);
+        __syncthreads();
+    }
+    const float l_tot = l_run + xor32(l_run);
+    store_output<T>(reinterpret_cast<T*>(p.o) + base, p.lse + row_base, L, oacc, 1.0f / l_tot,
+                    (m_run + __log2f(l_tot)) * LN2);
+}
+
+// ---------------------------------------------------------------------------
+// Fixed heads, exact per-element program (fallback)
+// ---------------------------------------------------------------------------
+
+template <typename T>
+__device__ void fwd_fixed_exact(void* smem, const FwdArgs& p, const FwdLane& L, size_t base, size_t row_base,
+                                const float* arow, const float* rrow) {
+    FwdExactSmem<T>& sm = *reinterpret_cast<FwdExactSmem<T>*>(smem);
+    const T* __restrict__ V = reinterpret_cast<const T*>(p.v) + base;
+    typedef typename Vec<T>::x8 frag;
+    const int N = L.N;
+    f32x16 oacc[2];
+#pragma unroll
+    for (int db = 0; db < 2; ++db)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) oacc[db][v] = 0.0f;
+    float m_run = NEG_BIG;
+    float l_run = 0.0f;
+    const int n_end = min(L.m0 + FWD_BM, N);
     for (int n0 = 0; n0 < n_end; n0 += FWD_BN) {
         __syncthreads();
-        if (!fixed) {
-#pragma unroll
-            for (int i = 0; i < 2; ++i) {
-                const int id = tid + FWD_THREADS * i;
-                const int row = id >> 3;
-                const int col = (id & 7) * 8;
-                frag x = (n0 + row < N) ? ld8<T>(K + (size_t)(n0 + row) * HEAD_DIM + col) : zero8<T>();
-                st8<T>(&sm.k[row][col], x);
-            }
-        }
         {
-            const int k2 = (tid >> 3) * 2;  // key pair (k2, k2 + 1)
-            const int d8 = (tid & 7) * 8;
+            const int k2 = (L.tid >> 3) * 2;
+            const int d8 = (L.tid & 7) * 8;
             frag x0 = (n0 + k2 < N) ? ld8<T>(V + (size_t)(n0 + k2) * HEAD_DIM + d8) : zero8<T>();
             frag x1 = (n0 + k2 + 1 < N) ? ld8<T>(V + (size_t)(n0 + k2 + 1) * HEAD_DIM + d8) : zero8<T>();
-            const int pos = tpos(k2);
-#pragma unroll
-            for (int t = 0; t < 8; ++t) st2<T>(&sm.vt[d8 + t][pos], x0[t], x1[t]);
+            st_pair_t(&sm.vt[d8][tpos(k2)], FWD_BN + LDS_PAD, x0, x1);
         }
-        if (fixed) {
-            if (tid < FWD_BN) sm.a[tid] = (n0 + tid < N) ? arow[n0 + tid] : -INFINITY;
-            // Offsets i - j over the tile: m0 - n0 - 63 .. m0 - n0 + 127.
-            for (int x = tid; x < FWD_BM + FWD_BN - 1; x += FWD_THREADS) {
-                const int delta = m0 - n0 - (FWD_BN - 1) + x;
-                sm.rb[x] = (delta >= 0 && delta < N) ? rrow[delta] : -INFINITY;
-            }
+        if (L.tid < FWD_BN) sm.a[L.tid] = (n0 + L.tid < N) ? arow[n0 + L.tid] : -INFINITY;
+        for (int x = L.tid; x < FWD_BAND - 1; x += FWD_THREADS) {
+            const int delta = L.m0 - n0 - (FWD_BN - 1) + x;  // offsets m0-n0-63 .. m0-n0+127
+            sm.rb[x] = (delta >= 0 && delta < N) ? rrow[delta] : -INFINITY;
         }
         __syncthreads();
-
-        // 32-key sub-blocks of this tile that hold a key <= some query of
-        // this wavefront (both start at multiples of 32).
-        bool act[2];
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-            const int k0 = n0 + 32 * kb;
-            act[kb] = (k0 < q0 + 32) && (k0 < N);
-        }
-        if (!act[0]) continue;
-
+        if (!(n0 < L.q0 + 32)) continue;
         f32x16 s[2];
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-            if (!act[kb]) continue;
-            const int k0 = n0 + 32 * kb;
-            if (!fixed) {
+        for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-                for (int v = 0; v < 16; ++v) s[kb][v] = 0.0f;
-#pragma unroll
-                for (int dc = 0; dc < 4; ++dc)
-                    mma(s[kb], ld8<T>(&sm.k[32 * kb + c][16 * dc + 8 * hf]), qf[dc]);
-#pragma unroll
-                for (int v = 0; v < 16; ++v) s[kb][v] *= p.scale_log2;
-            } else {
-#pragma unroll
-                for (int v = 0; v < 16; ++v) {
-                    const int kl = 32 * kb + 8 * (v >> 2) + 4 * hf + (v & 3);  // key within tile
-                    const int x = (qq - m0) - kl + (FWD_BN - 1);               // band index of qq - (n0 + kl)
-                    s[kb][v] = (sm.a[kl] + sm.rb[x]) * LOG2E;
-                }
+            for (int v = 0; v < 16; ++v) {
+                const int kl = 32 * kb + 8 * (v >> 2) + 4 * L.hf + (v & 3);
+                const int x = (L.qq - L.m0) - kl + (FWD_BN - 1);
+                s[kb][v] = (sm.a[kl] + sm.rb[x]) * LOG2E;
             }
-            if (k0 == q0) {  // diagonal sub-block: hide keys after the query
-#pragma unroll
-                for (int v = 0; v < 16; ++v) {
-                    const int kk = k0 + 8 * (v >> 2) + 4 * hf + (v & 3);
-                    if (kk > qq) s[kb][v] = -INFINITY;
-                }
-            }
-        }
-
         float mx = -INFINITY;
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-            if (!act[kb]) continue;
+        for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
             for (int v = 0; v < 16; ++v) mx = fmaxf(mx, s[kb][v]);
-        }
         mx = fmaxf(mx, xor32(mx));
         const float m_new = fmaxf(m_run, mx);
         const float alpha = fast_exp2(m_run - m_new);
@@ -188,40 +310,290 @@ __global__ __launch_bounds__(FWD_THREADS) void fwd_kernel(FwdArgs p) {
         for (int db = 0; db < 2; ++db)
 #pragma unroll
             for (int v = 0; v < 16; ++v) oacc[db][v] *= alpha;
-
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb) {
-            if (!act[kb]) continue;
-            float ls = 0.0f;
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
                 const float e = fast_exp2(s[kb][v] - m_new);
                 s[kb][v] = e;
-                ls += e;
+                l_run += e;
             }
-            l_run += ls;
 #pragma unroll
             for (int kc = 0; kc < 2; ++kc) {
                 const frag pb = to_operand<T>(s[kb], 8 * kc);
 #pragma unroll
                 for (int db = 0; db < 2; ++db)
-                    mma(oacc[db], ld8<T>(&sm.vt[32 * db + c][32 * kb + 16 * kc + 8 * hf]), pb);
+                    mma(oacc[db], ld8<T>(&sm.vt[32 * db + L.c][32 * kb + 16 * kc + 8 * L.hf]), pb);
             }
         }
     }
-
+    // LSE of fixed heads comes from the normaliser pre-pass.
     const float l_tot = l_run + xor32(l_run);
-    if (qq < N) {
-        const float inv = 1.0f / l_tot;
-        T* orow = O + (size_t)qq * HEAD_DIM;
+    store_output<T>(reinterpret_cast<T*>(p.o) + base, p.lse + row_base, L, oacc, 1.0f / l_tot, 0.0f, false);
+}
+
+// ---------------------------------------------------------------------------
+// Fixed heads, factorised program
+// ---------------------------------------------------------------------------
+
+template <typename T>
+struct FixStage {
+    typename Vec<T>::x8 v[2];
+    float a[2];
+    float rb;
+};
+
+template <typename T>
+__device__ __forceinline__ void fix_load(FixStage<T>& st, const T* V, const float* arow, const float* rrow, int n0,
+                                         int m0, int N, int tid) {
+    const int k2 = (tid >> 3) * 2;
+    const int d8 = (tid & 7) * 8;
+    st.v[0] = (n0 + k2 < N) ? ld8<T>(V + (size_t)(n0 + k2) * HEAD_DIM + d8) : zero8<T>();
+    st.v[1] = (n0 + k2 + 1 < N) ? ld8<T>(V + (size_t)(n0 + k2 + 1) * HEAD_DIM + d8) : zero8<T>();
+    st.a[0] = (n0 + k2 < N) ? arow[n0 + k2] : -INFINITY;
+    st.a[1] = (n0 + k2 + 1 < N) ? arow[n0 + k2 + 1] : -INFINITY;
+    // Band entry u holds offset (m0 - n0 + 127) - u.
+    const int delta = m0 - n0 + (FWD_BM - 1) - tid;
+    st.rb = (tid < FWD_BAND - 1 && delta >= 0 && delta < N) ? rrow[delta] : -INFINITY;
+}
+
+template <typename T>
+__device__ __forceinline__ void fix_store(FwdFixSmem<T>& sm, int buf, const FixStage<T>& st, int tid, float a_sh,
+                                          float r_sh) {
+    const int k2 = (tid >> 3) * 2;
+    const int d8 = (tid & 7) * 8;
+    const float e0 = fast_exp2(fmaf(st.a[0], LOG2E, -a_sh));
+    const float e1 = fast_exp2(fmaf(st.a[1], LOG2E, -a_sh));
+    st_pair_t_scaled(&sm.vt[buf][d8][k2], FWD_BN + LDS_PAD, st.v[0], st.v[1], e0, e1);
+    if (tid < FWD_BAND - 1) {
+        const T e = (T)fast_exp2(fmaf(st.rb, LOG2E, -r_sh));
 #pragma unroll
-        for (int db = 0; db < 2; ++db)
-#pragma unroll
-            for (int g = 0; g < 4; ++g)
-                st4<T>(orow + 32 * db + 8 * g + 4 * hf, oacc[db][4 * g] * inv, oacc[db][4 * g + 1] * inv,
-                       oacc[db][4 * g + 2] * inv, oacc[db][4 * g + 3] * inv);
-        if (hf == 0) LSE[qq] = (m_run + __log2f(l_tot)) * LN2;
+        for (int s = 0; s < BAND_COPIES; ++s)
+            if (tid >= s) sm.band[buf][s][tid - s] = e;
     }
+}
+
+template <typename T, bool MASK>
+__device__ __forceinline__ void fix_tile(const FwdFixSmem<T>& sm, int buf, int n0, const FwdLane& L,
+                                         f32x16 (&oacc)[2]) {
+    typedef typename Vec<T>::x8 frag;
+    const int ql = 32 * L.w + L.c;  // query within the block
+#pragma unroll
+    for (int G = 0; G < 4; ++G) {
+        if (MASK && n0 + 16 * G > L.q0 + 31) continue;  // chunk wholly after this wavefront's queries
+        const int u0 = (FWD_BM - 1) - ql + 16 * G + 8 * L.hf;
+        const int s = u0 & 7;
+        const frag b = ld8<T>(&sm.band[buf][s][u0 - s]);
+#pragma unroll
+        for (int db = 0; db < 2; ++db) mma(oacc[db], ld8<T>(&sm.vt[buf][32 * db + L.c][16 * G + 8 * L.hf]), b);
+    }
+}
+
+template <typename T>
+__device__ void fwd_fixed(void* smem, const FwdArgs& p, const FwdLane& L, size_t base, size_t row_base, int h) {
+    FwdFixSmem<T>& sm = *reinterpret_cast<FwdFixSmem<T>*>(smem);
+    const T* __restrict__ V = reinterpret_cast<const T*>(p.v) + base;
+    const float* __restrict__ arow = p.a + (size_t)h * p.ld_prior;
+    const float* __restrict__ rrow = p.r + (size_t)h * p.ld_prior;
+    const int N = L.N;
+    const int m1 = min(L.m0 + FWD_BM, N);
+
+    // Shifts: maxima of a and r over the positions this block touches.
+    float am = -INFINITY, rm = -INFINITY;
+    for (int j = L.tid; j < m1; j += FWD_THREADS) {
+        am = fmaxf(am, arow[j]);
+        rm = fmaxf(rm, rrow[j]);
+    }
+    const float A = block_max(am, sm.red);
+    const float R = block_max(rm, sm.red);
+    // Guard: every row's diagonal or sink term within FAST_GUARD of A + R,
+    // so Z'(i) >= exp(-FAST_GUARD) and no row underflows.
+    bool ok = true;
+    if (L.tid < FWD_BM && L.m0 + L.tid < N) {
+        const int i = L.m0 + L.tid;
+        ok = fmaxf(arow[i] + rrow[0], arow[0] + rrow[i]) - A - R >= -FAST_GUARD;
+    }
+    if (!__syncthreads_and(ok)) {
+        fwd_fixed_exact<T>(smem, p, L, base, row_base, arow, rrow);
+        return;
+    }
+    const float a_sh = A * LOG2E, r_sh = R * LOG2E;
+
+    f32x16 oacc[2];
+#pragma unroll
+    for (int db = 0; db < 2; ++db)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) oacc[db][v] = 0.0f;
+    const int n_tiles = (m1 + FWD_BN - 1) / FWD_BN;
+    const int n_full = L.m0 / FWD_BN;
+    FixStage<T> st;
+    fix_load<T>(st, V, arow, rrow, 0, L.m0, N, L.tid);
+    fix_store<T>(sm, 0, st, L.tid, a_sh, r_sh);
+    __syncthreads();
+    for (int t = 0; t < n_tiles; ++t) {
+        const bool more = t + 1 < n_tiles;
+        if (more) fix_load<T>(st, V, arow, rrow, (t + 1) * FWD_BN, L.m0, N, L.tid);
+        if (t < n_full)
+            fix_tile<T, false>(sm, t & 1, t * FWD_BN, L, oacc);
+        else
+            fix_tile<T, true>(sm, t & 1, t * FWD_BN, L, oacc);
+        if (more) fix_store<T>(sm, (t + 1) & 1, st, L.tid, a_sh, r_sh);
+        __syncthreads();
+    }
+    // 1 / Z'(i) = exp(A + R - log Z(i)), with log Z from the normaliser pre-pass.
+    const float lse = L.qq < N ? p.lse[row_base + L.qq] : 0.0f;
+    const float inv = fast_exp2((A + R - lse) * LOG2E);
+    store_output<T>(reinterpret_cast<T*>(p.o) + base, p.lse + row_base, L, oacc, inv, 0.0f, false);
+}
+
+// ---------------------------------------------------------------------------
+// Fixed-head normaliser pre-pass: LSE[b, h, i] = log Z(i) for every batch
+// element b (Z depends on a and r only).  Workgroup = (fixed head, 32 rows);
+// eight threads share a row and each sums a 64-key slice of every 512-key
+// tile: Z'(i) = sum_j ea(j) er(i - j) in float32, with ea = exp(a - A_t) and
+// er = exp(r - R_t) shifted by the tile's maxima A_t, R_t; the tiles combine
+// online under the largest shift M seen so far, so log Z = M + log Z'.  A
+// row whose Z' ends below 2^-80 (its terms underflowed) is summed exactly,
+// with a running maximum.
+// ---------------------------------------------------------------------------
+constexpr int NORM_THREADS = 256;
+constexpr int NORM_ROWS = 32;
+constexpr int NORM_PARTS = NORM_THREADS / NORM_ROWS;     // threads per row
+constexpr int NORM_KT = 512;                             // keys per tile
+constexpr int NORM_PART_KEYS = NORM_KT / NORM_PARTS;     // 64
+constexpr int NORM_BAND = NORM_ROWS + NORM_KT - 1;       // offsets per tile
+
+struct NormArgs {
+    const float* a;
+    const float* r;
+    float* lse;
+    int B, H, N, ld_prior, n_rblocks, n_fixed;
+    unsigned char heads[64];  // the fixed heads, ascending
+};
+
+__global__ __launch_bounds__(NORM_THREADS) void fixed_lse_kernel(NormArgs p) {
+    __shared__ __attribute__((aligned(16))) float ea_s[NORM_KT];
+    __shared__ float er_s[NORM_BAND + 1];
+    __shared__ float red[2][4];
+    __shared__ float zs[NORM_PARTS][NORM_ROWS];
+    const int rblk = p.n_rblocks - 1 - (int)(blockIdx.x / p.n_fixed);  // longest first
+    const int h = p.heads[blockIdx.x % p.n_fixed];
+    const int tid = threadIdx.x;
+    const int row = tid % NORM_ROWS;
+    const int part = tid / NORM_ROWS;
+    const int N = p.N;
+    const float* __restrict__ arow = p.a + (size_t)h * p.ld_prior;
+    const float* __restrict__ rrow = p.r + (size_t)h * p.ld_prior;
+    const int i0 = rblk * NORM_ROWS;
+    const int m1 = min(i0 + NORM_ROWS, N);
+    const int i = i0 + row;
+
+    float M = -INFINITY;  // shift of S (uniform over the workgroup)
+    float S = 0.0f;       // this thread's share of Z(i) * exp(-M)
+    for (int j0 = 0; j0 < m1; j0 += NORM_KT) {
+        float av[NORM_KT / NORM_THREADS], rv[3];
+        float amx = -INFINITY, rmx = -INFINITY;
+#pragma unroll
+        for (int k = 0; k < NORM_KT / NORM_THREADS; ++k) {
+            const int j = j0 + tid + NORM_THREADS * k;
+            av[k] = j < m1 ? arow[j] : -INFINITY;
+            amx = fmaxf(amx, av[k]);
+        }
+#pragma unroll
+        for (int k = 0; k < 3; ++k) {
+            const int x = tid + NORM_THREADS * k;  // er_s[x] = er(i0 - j0 - 511 + x)
+            const int delta = i0 - j0 - (NORM_KT - 1) + x;
+            rv[k] = (x < NORM_BAND && delta >= 0 && delta < N) ? rrow[delta] : -INFINITY;
+            rmx = fmaxf(rmx, rv[k]);
+        }
+        amx = wave_max(amx);
+        rmx = wave_max(rmx);
+        if ((tid & 63) == 0) {
+            red[0][tid >> 6] = amx;
+            red[1][tid >> 6] = rmx;
+        }
+        __syncthreads();
+        const float At = fmaxf(fmaxf(red[0][0], red[0][1]), fmaxf(red[0][2], red[0][3]));
+        const float Rt = fmaxf(fmaxf(red[1][0], red[1][1]), fmaxf(red[1][2], red[1][3]));
+#pragma unroll
+        for (int k = 0; k < NORM_KT / NORM_THREADS; ++k)
+            ea_s[tid + NORM_THREADS * k] = fast_exp2((av[k] - At) * LOG2E);
+#pragma unroll
+        for (int k = 0; k < 3; ++k) {
+            const int x = tid + NORM_THREADS * k;
+            if (x < NORM_BAND) er_s[x] = fast_exp2((rv[k] - Rt) * LOG2E);
+        }
+        __syncthreads();
+        const float ct = At + Rt;
+        if (ct > M) {
+            S *= fast_exp2((M - ct) * LOG2E);
+            M = ct;
+        }
+        const int jb = part * NORM_PART_KEYS;
+        const int xb = row - jb + (NORM_KT - 1);  // er_s index of key j0 + jb for row i
+        float z0 = 0.0f, z1 = 0.0f, z2 = 0.0f, z3 = 0.0f;
+#pragma unroll
+        for (int m = 0; m < NORM_PART_KEYS; m += 4) {
+            const f32x4 e = *reinterpret_cast<const f32x4*>(&ea_s[jb + m]);
+            z0 = fmaf(e[0], er_s[xb - m], z0);
+            z1 = fmaf(e[1], er_s[xb - m - 1], z1);
+            z2 = fmaf(e[2], er_s[xb - m - 2], z2);
+            z3 = fmaf(e[3], er_s[xb - m - 3], z3);
+        }
+        S = fmaf((z0 + z1) + (z2 + z3), fast_exp2((ct - M) * LOG2E), S);
+        __syncthreads();
+    }
+    zs[part][row] = S;
+    __syncthreads();
+    if (part != 0 || i >= N) return;
+    float z = 0.0f;
+#pragma unroll
+    for (int q = 0; q < NORM_PARTS; ++q) z += zs[q][row];
+    float lse;
+    if (z >= 0x1p-80f) {
+        lse = M + __log2f(z) * LN2;
+    } else {
+        float m = -INFINITY, s = 0.0f;
+        for (int j = 0; j <= i; ++j) {
+            const float x = arow[j] + rrow[i - j];
+            if (x > m) {
+                s = s * expf(m - x) + 1.0f;
+                m = x;
+            } else {
+                s += expf(x - m);
+            }
+        }
+        lse = m + logf(s);
+    }
+    for (int b = 0; b < p.B; ++b) p.lse[((size_t)b * p.H + h) * N + i] = lse;
+}
+
+// ---------------------------------------------------------------------------
+
+template <typename T>
+__global__ __launch_bounds__(FWD_THREADS) void fwd_kernel(FwdArgs p) {
+    __shared__ __attribute__((aligned(16))) char smem[fwd_smem_bytes<T>()];
+    const int n_bh = p.B * p.H;
+    // Longest blocks first: block index -> query block in descending order.
+    const int qblk = p.n_qblocks - 1 - (int)(blockIdx.x / n_bh);
+    const int bh = (int)(blockIdx.x % n_bh);
+    const int h = bh % p.H;
+    const bool fixed = (p.fixed_mask >> h) & 1ull;
+    FwdLane L;
+    L.tid = threadIdx.x;
+    L.w = L.tid >> 6;
+    L.c = L.tid & 31;
+    L.hf = (L.tid >> 5) & 1;
+    L.m0 = qblk * FWD_BM;
+    L.q0 = L.m0 + 32 * L.w;
+    L.qq = L.q0 + L.c;
+    L.N = p.N;
+    const size_t base = (size_t)bh * p.N * HEAD_DIM;
+    const size_t row_base = (size_t)bh * p.N;
+    if (fixed)
+        fwd_fixed<T>(smem, p, L, base, row_base, h);
+    else
+        fwd_ordinary<T>(smem, p, L, base, row_base);
 }
 
 }  // namespace saf
