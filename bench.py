@@ -46,6 +46,7 @@ PEAK_BF16_TFLOPS = 2500.0
 PEAK_F32_TFLOPS = 157.3
 PEAK_HBM_GBS = 8000.0
 MAX_HOST_WORKERS = 16
+COPY_CALIBRATION_BYTES = 64 << 20
 
 
 def contraction_flop(N: int, d: int) -> float:
@@ -89,6 +90,9 @@ def parse():
                     help="(batch, head) slices the oracle baseline runs (0: four per worker)")
     ap.add_argument("--compare-ordinary", dest="compare", action="store_true", default=True)
     ap.add_argument("--no-compare-ordinary", dest="compare", action="store_false")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run one plain 64 MiB device copy before the timed steps (a known-size reference "
+                         "for HBM byte counters in a profiler run)")
     return ap.parse_args()
 
 
@@ -207,6 +211,14 @@ def main():
     hybrid_flags = inp["is_fixed"].copy()
     ordinary_flags = np.zeros_like(hybrid_flags)
     layer = Layer(torch, inp, w.dtype, w.backward)
+
+    if args.copy_calibration:
+        src = torch.empty(COPY_CALIBRATION_BYTES // 4, dtype=torch.float32, device="cuda").fill_(1.0)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     for _ in range(args.warmup):
         layer.step(hybrid_flags)

@@ -77,10 +77,11 @@ __global__ __launch_bounds__(PRE_THREADS) void bwd_pre_kernel(BwdArgs p) {
 // key (l % 32) and 16 queries of each 32-query half: P and dS feed directly
 // into the B operand of dV^T += dO^T P and dK^T += Q^T dS, whose accumulators
 // again hold one key per lane.  K and V of the wavefront's keys stay in
-// registers; Q and dO tiles are staged in LDS twice, row-major (A operand of S
-// and dP) and transposed (A operand of the dV/dK products), in a double buffer
-// filled from registers loaded one tile ahead.  The first four tiles meet the
-// diagonal and run a masked body; the rest run mask-free.
+// registers; Q and dO tiles are copied by buffer loads straight into
+// column-slab LDS tiles (A operands of S and dP, and, through transposing
+// reads, of the dV/dK products), double-buffered so the next tile is in
+// flight while this one is used.  The first tiles meet the diagonal and run a
+// masked body; the rest run mask-free.
 //
 // Fixed heads: dV[j] = sum_i P(i,j) dO[i] with P(i,j) = ea(j) er(i-j) g(i),
 // ea = exp(a - A), er = exp(r - R), g(i) = exp(A + R - log Z(i)) (A: maximum
@@ -91,53 +92,23 @@ __global__ __launch_bounds__(PRE_THREADS) void bwd_pre_kernel(BwdArgs p) {
 // offsets hold 0, the causal mask), and the accumulator is scaled by ea(j) at
 // the end: no exponential per element.  The band is kept as a bf16 high part
 // plus a bf16 low part (er - hi), two products per chunk, so each term is
-// rounded once (in g * dO), as in the exact program.  If some row's log Z lies more than
-// FAST_GUARD below A + R (g could overflow), the block runs the exact
-// per-element program instead.  dK of a fixed head is written as zeros.
+// rounded once (in g * dO), as in the exact program.  If some row's log Z
+// lies more than FAST_GUARD below A + R (g could overflow), the block runs
+// the exact per-element program instead.  dK of a fixed head is written as
+// zeros.
 // ---------------------------------------------------------------------------
-constexpr int KV_KB = 1;                 // 32-key sub-blocks per wavefront
-constexpr int KV_BN = 4 * 32 * KV_KB;    // keys per workgroup
-constexpr int KV_BM = 64;                // queries per tile
+constexpr int KV_KB = 1;               // 32-key sub-blocks per wavefront
+constexpr int KV_BN = 4 * 32 * KV_KB;  // keys per workgroup
+constexpr int KV_BM = TILE_ROWS;       // queries per tile
 constexpr int KV_THREADS = 256;
-constexpr int KV_PAD = 8;
-constexpr int KV_MASK_TILES = KV_BN / KV_BM;  // tiles that meet the diagonal
-constexpr int KV_BAND = KV_BM + KV_BN - 1;    // offsets per tile
+constexpr int KV_MASK_TILES = KV_BN / KV_BM;               // tiles that meet the diagonal
+constexpr int KV_BAND = KV_BM + KV_BN - 1;                 // offsets per tile
 constexpr int KV_BAND_STRIDE = (KV_BAND + 8) / 8 * 8 + 8;  // every copy 16-byte aligned
-
-template <typename T>
-struct KvOrdSmem {
-    T q[2][KV_BM][HEAD_DIM + KV_PAD];
-    T dO[2][KV_BM][HEAD_DIM + KV_PAD];
-    T qt[2][HEAD_DIM][KV_BM + KV_PAD];    // [d][tpos(query)]
-    T dOt[2][HEAD_DIM][KV_BM + KV_PAD];
-    float lse[2][KV_BM];                  // LSE * log2(e); +inf past N
-    float dsum[2][KV_BM];                 // D; 0 past N
-};
-
-template <typename T>
-struct KvFixSmem {
-    T dogt[2][HEAD_DIM][KV_BM + KV_PAD];          // (g * dO) transposed, [d][query]
-    T band[2][2][BAND_COPIES][KV_BAND_STRIDE];    // [buf][hi, lo] er(delta_lo + x + s) in copy s
-    float red[4];
-};
-
-template <typename T>
-struct KvExactSmem {
-    T dOt[HEAD_DIM][KV_BM + KV_PAD];  // [d][tpos(query)]
-    float lse[KV_BM];
-    float rb[KV_BAND + 1];            // r(delta_lo + x), -inf outside [0, N)
-};
-
-template <typename T>
-constexpr size_t kv_smem_bytes() {
-    size_t x = sizeof(KvOrdSmem<T>);
-    if (sizeof(KvFixSmem<T>) > x) x = sizeof(KvFixSmem<T>);
-    if (sizeof(KvExactSmem<T>) > x) x = sizeof(KvExactSmem<T>);
-    return x;
-}
+static_assert(2 * BAND_COPIES * KV_BAND_STRIDE <= tile_elems<bf16>(), "hi/lo band copies fit in a tile");
+static_assert((KV_BM + KV_BAND + 1) * 4 <= tile_elems<bf16>() * 2, "exact-program rows fit in a tile");
 
 struct KvLane {
-    int tid, w, c, hf, n0, kw, N;
+    int tid, w, lane, c, hf, n0, kw, N;
 };
 
 template <typename T>
@@ -174,51 +145,13 @@ __device__ __forceinline__ void kv_store_zero(T* base, const KvLane& L) {
 
 // --- ordinary heads ---------------------------------------------------------
 
-template <typename T>
-struct KvStage {
-    typename Vec<T>::x8 q[2], g[2];
-    float lse, dsum;
-};
-
-template <typename T>
-__device__ __forceinline__ void kv_load(KvStage<T>& st, const T* Q, const T* dO, const float* LSE, const float* Dsum,
-                                        int mq, int N, int tid) {
-    const int r2 = (tid >> 3) * 2;
-    const int d8 = (tid & 7) * 8;
-#pragma unroll
-    for (int k = 0; k < 2; ++k) {
-        const bool ok = mq + r2 + k < N;
-        st.q[k] = ok ? ld8<T>(Q + (size_t)(mq + r2 + k) * HEAD_DIM + d8) : zero8<T>();
-        st.g[k] = ok ? ld8<T>(dO + (size_t)(mq + r2 + k) * HEAD_DIM + d8) : zero8<T>();
-    }
-    if (tid < KV_BM) {
-        const bool ok = mq + tid < N;
-        st.lse = ok ? LSE[mq + tid] * LOG2E : INFINITY;
-        st.dsum = ok ? Dsum[mq + tid] : 0.0f;
-    }
-}
-
-template <typename T>
-__device__ __forceinline__ void kv_store(KvOrdSmem<T>& sm, int buf, const KvStage<T>& st, int tid) {
-    const int r2 = (tid >> 3) * 2;
-    const int d8 = (tid & 7) * 8;
-#pragma unroll
-    for (int k = 0; k < 2; ++k) {
-        st8<T>(&sm.q[buf][r2 + k][d8], st.q[k]);
-        st8<T>(&sm.dO[buf][r2 + k][d8], st.g[k]);
-    }
-    st_pair_t(&sm.qt[buf][d8][tpos(r2)], KV_BM + KV_PAD, st.q[0], st.q[1]);
-    st_pair_t(&sm.dOt[buf][d8][tpos(r2)], KV_BM + KV_PAD, st.g[0], st.g[1]);
-    if (tid < KV_BM) {
-        sm.lse[buf][tid] = st.lse;
-        sm.dsum[buf][tid] = st.dsum;
-    }
-}
-
+// One query tile: qt / gt are the Q / dO tiles, rows holds LSE * log2(e)
+// (first KV_BM floats) and D (next KV_BM).
 template <typename T, bool MASK>
-__device__ __forceinline__ void kv_tile(const KvOrdSmem<T>& sm, int buf, int mq, const KvLane& L,
-                                        const typename Vec<T>::x8 (&kf)[KV_KB][4], const typename Vec<T>::x8 (&vf)[KV_KB][4],
-                                        f32x16 (&dv)[KV_KB][2], f32x16 (&dk)[KV_KB][2], float scale_log2) {
+__device__ __forceinline__ void kv_tile(const T* qt, const T* gt, const float* rows, int mq, const KvLane& L,
+                                        const typename Vec<T>::x8 (&kf)[KV_KB][4],
+                                        const typename Vec<T>::x8 (&vf)[KV_KB][4], f32x16 (&dv)[KV_KB][2],
+                                        f32x16 (&dk)[KV_KB][2], float scale_log2) {
     typedef typename Vec<T>::x8 frag;
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
@@ -228,7 +161,7 @@ __device__ __forceinline__ void kv_tile(const KvOrdSmem<T>& sm, int buf, int mq,
         {
             frag qa[4];
 #pragma unroll
-            for (int dc = 0; dc < 4; ++dc) qa[dc] = ld8<T>(&sm.q[buf][32 * qb + L.c][16 * dc + 8 * L.hf]);
+            for (int dc = 0; dc < 4; ++dc) qa[dc] = ld_row<T>(qt, 32 * qb + L.c, 16 * dc + 8 * L.hf);
 #pragma unroll
             for (int kb = 0; kb < KV_KB; ++kb) {
 #pragma unroll
@@ -240,7 +173,7 @@ __device__ __forceinline__ void kv_tile(const KvOrdSmem<T>& sm, int buf, int mq,
         {
             frag ga[4];
 #pragma unroll
-            for (int dc = 0; dc < 4; ++dc) ga[dc] = ld8<T>(&sm.dO[buf][32 * qb + L.c][16 * dc + 8 * L.hf]);
+            for (int dc = 0; dc < 4; ++dc) ga[dc] = ld_row<T>(gt, 32 * qb + L.c, 16 * dc + 8 * L.hf);
 #pragma unroll
             for (int kb = 0; kb < KV_KB; ++kb) {
 #pragma unroll
@@ -251,8 +184,8 @@ __device__ __forceinline__ void kv_tile(const KvOrdSmem<T>& sm, int buf, int mq,
         }
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
-            const f32x4 l4 = *reinterpret_cast<const f32x4*>(&sm.lse[buf][32 * qb + 8 * g + 4 * L.hf]);
-            const f32x4 d4 = *reinterpret_cast<const f32x4*>(&sm.dsum[buf][32 * qb + 8 * g + 4 * L.hf]);
+            const f32x4 l4 = *reinterpret_cast<const f32x4*>(rows + 32 * qb + 8 * g + 4 * L.hf);
+            const f32x4 d4 = *reinterpret_cast<const f32x4*>(rows + KV_BM + 32 * qb + 8 * g + 4 * L.hf);
 #pragma unroll
             for (int kb = 0; kb < KV_KB; ++kb)
 #pragma unroll
@@ -269,12 +202,11 @@ __device__ __forceinline__ void kv_tile(const KvOrdSmem<T>& sm, int buf, int mq,
         }
 #pragma unroll
         for (int kc = 0; kc < 2; ++kc) {
-            const int col = 32 * qb + 16 * kc + 8 * L.hf;
-            frag gt[2], qt[2];
+            frag gta[2], qta[2];
 #pragma unroll
             for (int db = 0; db < 2; ++db) {
-                gt[db] = ld8<T>(&sm.dOt[buf][32 * db + L.c][col]);
-                qt[db] = ld8<T>(&sm.qt[buf][32 * db + L.c][col]);
+                gta[db] = ld_tile_t<true>(gt, 32 * qb + 16 * kc, 32 * db);
+                qta[db] = ld_tile_t<true>(qt, 32 * qb + 16 * kc, 32 * db);
             }
 #pragma unroll
             for (int kb = 0; kb < KV_KB; ++kb) {
@@ -282,8 +214,8 @@ __device__ __forceinline__ void kv_tile(const KvOrdSmem<T>& sm, int buf, int mq,
                 const frag sb = to_operand<T>(dp[kb], 8 * kc);
 #pragma unroll
                 for (int db = 0; db < 2; ++db) {
-                    mma(dv[kb][db], gt[db], pb);
-                    mma(dk[kb][db], qt[db], sb);
+                    mma(dv[kb][db], gta[db], pb);
+                    mma(dk[kb][db], qta[db], sb);
                 }
             }
         }
@@ -291,12 +223,13 @@ __device__ __forceinline__ void kv_tile(const KvOrdSmem<T>& sm, int buf, int mq,
 }
 
 template <typename T>
-__device__ void kv_ordinary(void* smem, const BwdArgs& p, const KvLane& L, size_t base, size_t row_base) {
-    KvOrdSmem<T>& sm = *reinterpret_cast<KvOrdSmem<T>*>(smem);
-    const T* __restrict__ Q = reinterpret_cast<const T*>(p.q) + base;
+__device__ __forceinline__ void kv_ordinary(const Tiles<T>& sm, const BwdArgs& p, const KvLane& L, size_t base,
+                                            size_t row_base) {
+    // Tiles: Q in t[0] / t[1], dO in t[2] / t[3]; LSE and D rows in aux[0] / aux[1].
     const T* __restrict__ K = reinterpret_cast<const T*>(p.k) + base;
     const T* __restrict__ V = reinterpret_cast<const T*>(p.v) + base;
-    const T* __restrict__ dO = reinterpret_cast<const T*>(p.dO) + base;
+    const __amdgpu_buffer_rsrc_t rq = slice_rsrc<T>(reinterpret_cast<const T*>(p.q) + base, L.N);
+    const __amdgpu_buffer_rsrc_t rg = slice_rsrc<T>(reinterpret_cast<const T*>(p.dO) + base, L.N);
     const float* __restrict__ LSE = p.lse + row_base;
     const float* __restrict__ Dsum = p.dsum + row_base;
     typedef typename Vec<T>::x8 frag;
@@ -322,19 +255,32 @@ __device__ void kv_ordinary(void* smem, const BwdArgs& p, const KvLane& L, size_
             }
 
     const int n_tiles = (L.N - L.n0 + KV_BM - 1) / KV_BM;
-    KvStage<T> st;
-    kv_load<T>(st, Q, dO, LSE, Dsum, L.n0, L.N, L.tid);
-    kv_store<T>(sm, 0, st, L.tid);
-    __syncthreads();
-    for (int t = 0; t < n_tiles; ++t) {
-        const bool more = t + 1 < n_tiles;
+    auto load = [&](T* qd, T* gd, float* rows, int t) {
         const int mq = L.n0 + t * KV_BM;
-        if (more) kv_load<T>(st, Q, dO, LSE, Dsum, mq + KV_BM, L.N, L.tid);
+        tile_load_lds<T>(qd, rq, mq, L.w, L.lane);
+        tile_load_lds<T>(gd, rg, mq, L.w, L.lane);
+        if (L.tid < KV_BM) {
+            const bool ok = mq + L.tid < L.N;
+            rows[L.tid] = ok ? LSE[mq + L.tid] * LOG2E : INFINITY;
+            rows[KV_BM + L.tid] = ok ? Dsum[mq + L.tid] : 0.0f;
+        }
+    };
+    auto compute = [&](const T* qt, const T* gt, const float* rows, int t) {
+        const int mq = L.n0 + t * KV_BM;
         if (t < KV_MASK_TILES)
-            kv_tile<T, true>(sm, t & 1, mq, L, kf, vf, dv, dk, p.scale_log2);
+            kv_tile<T, true>(qt, gt, rows, mq, L, kf, vf, dv, dk, p.scale_log2);
         else
-            kv_tile<T, false>(sm, t & 1, mq, L, kf, vf, dv, dk, p.scale_log2);
-        if (more) kv_store<T>(sm, (t + 1) & 1, st, L.tid);
+            kv_tile<T, false>(qt, gt, rows, mq, L, kf, vf, dv, dk, p.scale_log2);
+    };
+    load(sm.t[0], sm.t[2], sm.aux[0], 0);
+    __syncthreads();
+    for (int t = 0; t < n_tiles; t += 2) {
+        if (t + 1 < n_tiles) load(sm.t[1], sm.t[3], sm.aux[1], t + 1);
+        compute(sm.t[0], sm.t[2], sm.aux[0], t);
+        __syncthreads();
+        if (t + 1 >= n_tiles) break;
+        if (t + 2 < n_tiles) load(sm.t[0], sm.t[2], sm.aux[0], t + 2);
+        compute(sm.t[1], sm.t[3], sm.aux[1], t + 1);
         __syncthreads();
     }
     float one[KV_KB], ks[KV_KB];
@@ -350,9 +296,13 @@ __device__ void kv_ordinary(void* smem, const BwdArgs& p, const KvLane& L, size_
 // --- fixed heads: exact per-element program (fallback) ----------------------
 
 template <typename T>
-__device__ void kv_fixed_exact(void* smem, const BwdArgs& p, const KvLane& L, size_t base, size_t row_base,
-                               const float* arow, const float* rrow) {
-    KvExactSmem<T>& sm = *reinterpret_cast<KvExactSmem<T>*>(smem);
+__device__ __forceinline__ void kv_fixed_exact(const Tiles<T>& sm, const BwdArgs& p, const KvLane& L, size_t base,
+                                               size_t row_base, const float* arow, const float* rrow) {
+    // Tiles: dO in t[0]; LSE * log2(e) of the tile's rows and r over its
+    // offsets in t[1].
+    T* gt = sm.t[0];
+    float* lse = reinterpret_cast<float*>(sm.t[1]);
+    float* rb = lse + KV_BM;
     const T* __restrict__ dO = reinterpret_cast<const T*>(p.dO) + base;
     const float* __restrict__ LSE = p.lse + row_base;
     typedef typename Vec<T>::x8 frag;
@@ -370,19 +320,20 @@ __device__ void kv_fixed_exact(void* smem, const BwdArgs& p, const KvLane& L, si
         for (int db = 0; db < 2; ++db)
 #pragma unroll
             for (int v = 0; v < 16; ++v) dv[kb][db][v] = 0.0f;
+    const int row = unit_row<T>(L.w, L.lane);
     for (int mq = L.n0; mq < N; mq += KV_BM) {
         __syncthreads();
-        {
-            const int r2 = (L.tid >> 3) * 2;
-            const int d8 = (L.tid & 7) * 8;
-            const frag g0 = mq + r2 < N ? ld8<T>(dO + (size_t)(mq + r2) * HEAD_DIM + d8) : zero8<T>();
-            const frag g1 = mq + r2 + 1 < N ? ld8<T>(dO + (size_t)(mq + r2 + 1) * HEAD_DIM + d8) : zero8<T>();
-            st_pair_t(&sm.dOt[d8][tpos(r2)], KV_BM + KV_PAD, g0, g1);
+#pragma unroll
+        for (int k = 0; k < tile_units<T>(); ++k) {
+            const int col = unit_col<T>(L.w, L.lane, k);
+            const u32x4 z = {0u, 0u, 0u, 0u};
+            const u32x4 x = mq + row < N ? ld_unit(dO + (size_t)(mq + row) * HEAD_DIM + col) : z;
+            *reinterpret_cast<u32x4*>(gt + toff<T>(row, col)) = x;
         }
-        if (L.tid < KV_BM) sm.lse[L.tid] = mq + L.tid < N ? LSE[mq + L.tid] * LOG2E : INFINITY;
+        if (L.tid < KV_BM) lse[L.tid] = mq + L.tid < N ? LSE[mq + L.tid] * LOG2E : INFINITY;
         for (int x = L.tid; x < KV_BAND; x += KV_THREADS) {
             const int delta = mq - L.n0 - (KV_BN - 1) + x;
-            sm.rb[x] = (delta >= 0 && delta < N) ? rrow[delta] : -INFINITY;
+            rb[x] = (delta >= 0 && delta < N) ? rrow[delta] : -INFINITY;
         }
         __syncthreads();
 #pragma unroll
@@ -397,20 +348,19 @@ __device__ void kv_fixed_exact(void* smem, const BwdArgs& p, const KvLane& L, si
                 for (int v = 0; v < 16; ++v) {
                     const int ql = 32 * qb + 8 * (v >> 2) + 4 * L.hf + (v & 3);
                     const int x = ql - kl + (KV_BN - 1);
-                    pm[kb][v] = fast_exp2(fmaf(a_key[kb] + sm.rb[x], LOG2E, -sm.lse[ql]));
+                    pm[kb][v] = fast_exp2(fmaf(a_key[kb] + rb[x], LOG2E, -lse[ql]));
                 }
             }
 #pragma unroll
             for (int kc = 0; kc < 2; ++kc) {
-                const int col = 32 * qb + 16 * kc + 8 * L.hf;
-                frag gt[2];
+                frag gta[2];
 #pragma unroll
-                for (int db = 0; db < 2; ++db) gt[db] = ld8<T>(&sm.dOt[32 * db + L.c][col]);
+                for (int db = 0; db < 2; ++db) gta[db] = ld_tile_t<true>(gt, 32 * qb + 16 * kc, 32 * db);
 #pragma unroll
                 for (int kb = 0; kb < KV_KB; ++kb) {
                     const frag pb = to_operand<T>(pm[kb], 8 * kc);
 #pragma unroll
-                    for (int db = 0; db < 2; ++db) mma(dv[kb][db], gt[db], pb);
+                    for (int db = 0; db < 2; ++db) mma(dv[kb][db], gta[db], pb);
                 }
             }
         }
@@ -426,38 +376,43 @@ __device__ void kv_fixed_exact(void* smem, const BwdArgs& p, const KvLane& L, si
 
 template <typename T>
 struct KvFixStage {
-    typename Vec<T>::x8 g[2];
-    float lse[2];
-    float rb[2];
+    u32x4 g[tile_units<T>()];  // this lane's 16-byte units of the dO tile (one row)
+    float lse;                 // log Z of that row
+    float rb[2];               // band entries
 };
 
 template <typename T>
 __device__ __forceinline__ void kvf_load(KvFixStage<T>& st, const T* dO, const float* LSE, const float* rrow, int mq,
-                                         int n0, int N, int tid) {
-    const int r2 = (tid >> 3) * 2;
-    const int d8 = (tid & 7) * 8;
+                                         const KvLane& L) {
+    const int q = mq + unit_row<T>(L.w, L.lane);
+    const bool ok = q < L.N;
+#pragma unroll
+    for (int k = 0; k < tile_units<T>(); ++k) {
+        const u32x4 z = {0u, 0u, 0u, 0u};
+        st.g[k] = ok ? ld_unit(dO + (size_t)q * HEAD_DIM + unit_col<T>(L.w, L.lane, k)) : z;
+    }
+    st.lse = ok ? LSE[q] : INFINITY;
 #pragma unroll
     for (int k = 0; k < 2; ++k) {
-        const bool ok = mq + r2 + k < N;
-        st.g[k] = ok ? ld8<T>(dO + (size_t)(mq + r2 + k) * HEAD_DIM + d8) : zero8<T>();
-        st.lse[k] = ok ? LSE[mq + r2 + k] : INFINITY;
-        const int x = tid + KV_THREADS * k;
-        const int delta = mq - n0 - (KV_BN - 1) + x;
-        st.rb[k] = (x < KV_BAND && delta >= 0 && delta < N) ? rrow[delta] : -INFINITY;
+        const int x = L.tid + KV_THREADS * k;
+        const int delta = mq - L.n0 - (KV_BN - 1) + x;
+        st.rb[k] = (x < KV_BAND && delta >= 0 && delta < L.N) ? rrow[delta] : -INFINITY;
     }
 }
 
+// band: copy s of the high parts at s * KV_BAND_STRIDE, of the low parts at
+// (BAND_COPIES + s) * KV_BAND_STRIDE.
 template <typename T>
-__device__ __forceinline__ void kvf_store(KvFixSmem<T>& sm, int buf, const KvFixStage<T>& st, int tid, float g_sh,
+__device__ __forceinline__ void kvf_store(T* dog, T* band, const KvFixStage<T>& st, const KvLane& L, float g_sh,
                                           float r_sh) {
-    const int r2 = (tid >> 3) * 2;
-    const int d8 = (tid & 7) * 8;
-    const float g0 = fast_exp2(fmaf(-st.lse[0], LOG2E, g_sh));
-    const float g1 = fast_exp2(fmaf(-st.lse[1], LOG2E, g_sh));
-    st_pair_t_scaled(&sm.dogt[buf][d8][r2], KV_BM + KV_PAD, st.g[0], st.g[1], g0, g1);
+    const float g = fast_exp2(fmaf(-st.lse, LOG2E, g_sh));
+    const int row = unit_row<T>(L.w, L.lane);
+#pragma unroll
+    for (int k = 0; k < tile_units<T>(); ++k)
+        st_unit_scaled(dog + toff<T>(row, unit_col<T>(L.w, L.lane, k)), st.g[k], g);
 #pragma unroll
     for (int k = 0; k < 2; ++k) {
-        const int x = tid + KV_THREADS * k;
+        const int x = L.tid + KV_THREADS * k;
         if (x < KV_BAND) {
             const float e = fast_exp2(fmaf(st.rb[k], LOG2E, -r_sh));
             const T hi = (T)e;
@@ -465,15 +420,15 @@ __device__ __forceinline__ void kvf_store(KvFixSmem<T>& sm, int buf, const KvFix
 #pragma unroll
             for (int s = 0; s < BAND_COPIES; ++s)
                 if (x >= s) {
-                    sm.band[buf][0][s][x - s] = hi;
-                    sm.band[buf][1][s][x - s] = lo;
+                    band[s * KV_BAND_STRIDE + x - s] = hi;
+                    band[(BAND_COPIES + s) * KV_BAND_STRIDE + x - s] = lo;
                 }
         }
     }
 }
 
 template <typename T, bool MASK>
-__device__ __forceinline__ void kvf_tile(const KvFixSmem<T>& sm, int buf, int mq, const KvLane& L,
+__device__ __forceinline__ void kvf_tile(const T* dog, const T* band, int mq, const KvLane& L,
                                          f32x16 (&dv)[KV_KB][2]) {
     typedef typename Vec<T>::x8 frag;
 #pragma unroll
@@ -483,20 +438,20 @@ __device__ __forceinline__ void kvf_tile(const KvFixSmem<T>& sm, int buf, int mq
 #pragma unroll
         for (int kc = 0; kc < 2; ++kc) {
             const int col = 32 * qb + 16 * kc + 8 * L.hf;  // first query (within the tile) of this lane's slots
-            frag gt[2];
+            frag gta[2];
 #pragma unroll
-            for (int db = 0; db < 2; ++db) gt[db] = ld8<T>(&sm.dogt[buf][32 * db + L.c][col]);
+            for (int db = 0; db < 2; ++db) gta[db] = ld_tile_t<false>(dog, 32 * qb + 16 * kc, 32 * db);
 #pragma unroll
             for (int kb = 0; kb < KV_KB; ++kb) {
                 const int kl = L.kw - L.n0 + 32 * kb + L.c;
                 const int u0 = col - kl + (KV_BN - 1);  // band index of offset (mq + col) - (n0 + kl)
                 const int s = u0 & 7;
-                const frag bh = ld8<T>(&sm.band[buf][0][s][u0 - s]);
-                const frag bl = ld8<T>(&sm.band[buf][1][s][u0 - s]);
+                const frag bh = ld8<T>(band + s * KV_BAND_STRIDE + u0 - s);
+                const frag bl = ld8<T>(band + (BAND_COPIES + s) * KV_BAND_STRIDE + u0 - s);
 #pragma unroll
                 for (int db = 0; db < 2; ++db) {
-                    mma(dv[kb][db], gt[db], bh);
-                    mma(dv[kb][db], gt[db], bl);
+                    mma(dv[kb][db], gta[db], bh);
+                    mma(dv[kb][db], gta[db], bl);
                 }
             }
         }
@@ -504,8 +459,9 @@ __device__ __forceinline__ void kvf_tile(const KvFixSmem<T>& sm, int buf, int mq
 }
 
 template <typename T>
-__device__ void kv_fixed(void* smem, const BwdArgs& p, const KvLane& L, size_t base, size_t row_base, int h) {
-    KvFixSmem<T>& sm = *reinterpret_cast<KvFixSmem<T>*>(smem);
+__device__ __forceinline__ void kv_fixed(const Tiles<T>& sm, const BwdArgs& p, const KvLane& L, size_t base,
+                                         size_t row_base, int h) {
+    // Tiles: g * dO in t[0] / t[1], the hi/lo band in t[2] / t[3].
     const T* __restrict__ dO = reinterpret_cast<const T*>(p.dO) + base;
     const float* __restrict__ LSE = p.lse + row_base;
     const float* __restrict__ arow = p.a + (size_t)h * p.ld_prior;
@@ -514,7 +470,9 @@ __device__ void kv_fixed(void* smem, const BwdArgs& p, const KvLane& L, size_t b
 
     // A: max of a over the block's keys; R: max of r over the offsets the
     // block meets (0 .. N - 1 - n0); lo: min of log Z over its rows.
-    float am = L.n0 + L.tid < N ? arow[L.n0 + L.tid] : -INFINITY;
+    float am = -INFINITY;
+    for (int j = L.tid; j < KV_BN; j += KV_THREADS)
+        if (L.n0 + j < N) am = fmaxf(am, arow[L.n0 + j]);
     float rm = -INFINITY, lo = INFINITY;
     for (int j = L.tid; j < N - L.n0; j += KV_THREADS) {
         rm = fmaxf(rm, rrow[j]);
@@ -524,7 +482,7 @@ __device__ void kv_fixed(void* smem, const BwdArgs& p, const KvLane& L, size_t b
     const float R = block_max(rm, sm.red);
     const float LO = -block_max(-lo, sm.red);
     if (!(LO - A - R >= -FAST_GUARD)) {  // some g(i) could overflow
-        kv_fixed_exact<T>(smem, p, L, base, row_base, arow, rrow);
+        kv_fixed_exact<T>(sm, p, L, base, row_base, arow, rrow);
         return;
     }
     const float g_sh = (A + R) * LOG2E, r_sh = R * LOG2E, a_sh = A * LOG2E;
@@ -538,19 +496,26 @@ __device__ void kv_fixed(void* smem, const BwdArgs& p, const KvLane& L, size_t b
             for (int v = 0; v < 16; ++v) dv[kb][db][v] = 0.0f;
 
     const int n_tiles = (N - L.n0 + KV_BM - 1) / KV_BM;
-    KvFixStage<T> st;
-    kvf_load<T>(st, dO, LSE, rrow, L.n0, L.n0, N, L.tid);
-    kvf_store<T>(sm, 0, st, L.tid, g_sh, r_sh);
-    __syncthreads();
-    for (int t = 0; t < n_tiles; ++t) {
-        const bool more = t + 1 < n_tiles;
+    auto compute = [&](const T* dog, const T* band, int t) {
         const int mq = L.n0 + t * KV_BM;
-        if (more) kvf_load<T>(st, dO, LSE, rrow, mq + KV_BM, L.n0, N, L.tid);
         if (t < KV_MASK_TILES)
-            kvf_tile<T, true>(sm, t & 1, mq, L, dv);
+            kvf_tile<T, true>(dog, band, mq, L, dv);
         else
-            kvf_tile<T, false>(sm, t & 1, mq, L, dv);
-        if (more) kvf_store<T>(sm, (t + 1) & 1, st, L.tid, g_sh, r_sh);
+            kvf_tile<T, false>(dog, band, mq, L, dv);
+    };
+    KvFixStage<T> st;
+    kvf_load<T>(st, dO, LSE, rrow, L.n0, L);
+    kvf_store<T>(sm.t[0], sm.t[2], st, L, g_sh, r_sh);
+    __syncthreads();
+    for (int t = 0; t < n_tiles; t += 2) {
+        if (t + 1 < n_tiles) kvf_load<T>(st, dO, LSE, rrow, L.n0 + (t + 1) * KV_BM, L);
+        compute(sm.t[0], sm.t[2], t);
+        if (t + 1 < n_tiles) kvf_store<T>(sm.t[1], sm.t[3], st, L, g_sh, r_sh);
+        __syncthreads();
+        if (t + 1 >= n_tiles) break;
+        if (t + 2 < n_tiles) kvf_load<T>(st, dO, LSE, rrow, L.n0 + (t + 2) * KV_BM, L);
+        compute(sm.t[1], sm.t[3], t + 1);
+        if (t + 2 < n_tiles) kvf_store<T>(sm.t[0], sm.t[2], st, L, g_sh, r_sh);
         __syncthreads();
     }
     float ea[KV_KB];
@@ -564,8 +529,15 @@ __device__ void kv_fixed(void* smem, const BwdArgs& p, const KvLane& L, size_t b
 }
 
 template <typename T>
-__global__ __launch_bounds__(KV_THREADS) void bwd_kv_kernel(BwdArgs p) {
-    __shared__ __attribute__((aligned(16))) char smem[kv_smem_bytes<T>()];
+__global__ __launch_bounds__(KV_THREADS) __attribute__((amdgpu_waves_per_eu(sizeof(T) == 2 ? 2 : 1))) void bwd_kv_kernel(BwdArgs p) {
+    __shared__ __attribute__((aligned(16))) T t0[tile_elems<T>()];
+    __shared__ __attribute__((aligned(16))) T t1[tile_elems<T>()];
+    __shared__ __attribute__((aligned(16))) T t2[tile_elems<T>()];
+    __shared__ __attribute__((aligned(16))) T t3[tile_elems<T>()];
+    __shared__ __attribute__((aligned(16))) float x0[2 * KV_BM];
+    __shared__ __attribute__((aligned(16))) float x1[2 * KV_BM];
+    __shared__ float red[4];
+    const Tiles<T> sm = {{t0, t1, t2, t3}, {x0, x1}, red};
     const int n_bh = p.B * p.H;
     const int kblk = (int)(blockIdx.x / n_bh);  // ascending: longest first
     const int bh = (int)(blockIdx.x % n_bh);
@@ -573,6 +545,7 @@ __global__ __launch_bounds__(KV_THREADS) void bwd_kv_kernel(BwdArgs p) {
     KvLane L;
     L.tid = threadIdx.x;
     L.w = L.tid >> 6;
+    L.lane = L.tid & 63;
     L.c = L.tid & 31;
     L.hf = (L.tid >> 5) & 1;
     L.n0 = kblk * KV_BN;
@@ -581,34 +554,72 @@ __global__ __launch_bounds__(KV_THREADS) void bwd_kv_kernel(BwdArgs p) {
     const size_t base = (size_t)bh * p.N * HEAD_DIM;
     const size_t row_base = (size_t)bh * p.N;
     if ((p.fixed_mask >> h) & 1ull)
-        kv_fixed<T>(smem, p, L, base, row_base, h);
+        kv_fixed<T>(sm, p, L, base, row_base, h);
     else
-        kv_ordinary<T>(smem, p, L, base, row_base);
+        kv_ordinary<T>(sm, p, L, base, row_base);
 }
 
 // ---------------------------------------------------------------------------
 // Query-block pass (ordinary heads): workgroup = (b, h, 128 queries); 4
-// wavefronts x 32 queries, streaming key tiles of 64 up to the diagonal.
+// wavefronts x 32 queries, streaming key tiles of 64 up to the diagonal,
+// copied by buffer loads straight into double-buffered column-slab LDS tiles.
 // S^T (keys x queries) puts one query per lane, so LSE and D are per-lane
-// scalars and dS^T feeds the B operand of dQ^T += K^T dS^T.  Workgroups of
-// fixed heads only write zeros.
+// scalars and dS^T feeds the B operand of dQ^T += K^T dS^T (K^T through
+// transposing LDS reads).  Tiles below the block's first query run a
+// mask-free body.  Workgroups of fixed heads only write zeros.
 // ---------------------------------------------------------------------------
 constexpr int DQ_BM = 128;
-constexpr int DQ_BN = 64;
+constexpr int DQ_BN = TILE_ROWS;
 constexpr int DQ_THREADS = 256;
-constexpr int DQ_PAD = 8;
 
-template <typename T>
-struct DqSmem {
-    T k[DQ_BN][HEAD_DIM + DQ_PAD];
-    T v[DQ_BN][HEAD_DIM + DQ_PAD];
-    T kt[HEAD_DIM][DQ_BN + DQ_PAD];
+struct DqLane {
+    int tid, w, lane, c, hf, m0, q0, qq, N;
 };
+
+template <typename T, bool MASK>
+__device__ __forceinline__ void dq_tile(const T* kt, const T* vt, int n0, const DqLane& L,
+                                        const typename Vec<T>::x8 (&qf)[4], const typename Vec<T>::x8 (&gf)[4],
+                                        float lse2, float dsum, f32x16 (&dq)[2], float scale_log2) {
+    typedef typename Vec<T>::x8 frag;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+        const int k0 = n0 + 32 * kb;
+        if (MASK && !(k0 < L.q0 + 32 && k0 < L.N)) continue;  // keys wholly after this wavefront's queries
+        f32x16 s, dp;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            s[v] = 0.0f;
+            dp[v] = 0.0f;
+        }
+#pragma unroll
+        for (int dc = 0; dc < 4; ++dc) {
+            mma(s, ld_row<T>(kt, 32 * kb + L.c, 16 * dc + 8 * L.hf), qf[dc]);
+            mma(dp, ld_row<T>(vt, 32 * kb + L.c, 16 * dc + 8 * L.hf), gf[dc]);
+        }
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            float pv = fast_exp2(fmaf(s[v], scale_log2, -lse2));
+            if (MASK && k0 == L.q0) {
+                const int kk = k0 + 8 * (v >> 2) + 4 * L.hf + (v & 3);
+                if (kk > L.qq) pv = 0.0f;
+            }
+            s[v] = pv * (dp[v] - dsum);  // dS^T
+        }
+#pragma unroll
+        for (int kc = 0; kc < 2; ++kc) {
+            const frag sb = to_operand<T>(s, 8 * kc);
+#pragma unroll
+            for (int db = 0; db < 2; ++db) mma(dq[db], ld_tile_t<true>(kt, 32 * kb + 16 * kc, 32 * db), sb);
+        }
+    }
+}
 
 template <typename T>
 __global__ __launch_bounds__(DQ_THREADS) void bwd_dq_kernel(BwdArgs p) {
-    __shared__ DqSmem<T> sm;
-
+    __shared__ __attribute__((aligned(16))) T t0[tile_elems<T>()];
+    __shared__ __attribute__((aligned(16))) T t1[tile_elems<T>()];
+    __shared__ __attribute__((aligned(16))) T t2[tile_elems<T>()];
+    __shared__ __attribute__((aligned(16))) T t3[tile_elems<T>()];
     const int n_bh = p.B * p.H;
     const int qblk = p.n_blocks - 1 - (int)(blockIdx.x / n_bh);  // longest first
     const int bh = (int)(blockIdx.x % n_bh);
@@ -617,38 +628,40 @@ __global__ __launch_bounds__(DQ_THREADS) void bwd_dq_kernel(BwdArgs p) {
     const int N = p.N;
     const size_t base = (size_t)bh * N * HEAD_DIM;
     T* __restrict__ dQ = reinterpret_cast<T*>(p.dq) + base;
-
-    const int tid = threadIdx.x;
-    const int w = tid >> 6;
-    const int lane = tid & 63;
-    const int c = lane & 31;
-    const int hf = lane >> 5;
-    const int m0 = qblk * DQ_BM;
-    const int q0 = m0 + 32 * w;
-    const int qq = q0 + c;
+    DqLane L;
+    L.tid = threadIdx.x;
+    L.w = L.tid >> 6;
+    L.lane = L.tid & 63;
+    L.c = L.tid & 31;
+    L.hf = (L.tid >> 5) & 1;
+    L.m0 = qblk * DQ_BM;
+    L.q0 = L.m0 + 32 * L.w;
+    L.qq = L.q0 + L.c;
+    L.N = N;
 
     if (fixed) {  // the whole workgroup takes this branch
-        for (int id = tid; id < DQ_BM * (HEAD_DIM / 8); id += DQ_THREADS) {
-            const int row = m0 + id / (HEAD_DIM / 8);
+        for (int id = L.tid; id < DQ_BM * (HEAD_DIM / 8); id += DQ_THREADS) {
+            const int row = L.m0 + id / (HEAD_DIM / 8);
             if (row < N) st8<T>(dQ + (size_t)row * HEAD_DIM + (id % (HEAD_DIM / 8)) * 8, zero8<T>());
         }
         return;
     }
 
+    // Tiles: K in t0 / t1, V in t2 / t3.
     const T* __restrict__ Q = reinterpret_cast<const T*>(p.q) + base;
-    const T* __restrict__ K = reinterpret_cast<const T*>(p.k) + base;
-    const T* __restrict__ V = reinterpret_cast<const T*>(p.v) + base;
     const T* __restrict__ dO = reinterpret_cast<const T*>(p.dO) + base;
+    const __amdgpu_buffer_rsrc_t rk = slice_rsrc<T>(reinterpret_cast<const T*>(p.k) + base, N);
+    const __amdgpu_buffer_rsrc_t rv = slice_rsrc<T>(reinterpret_cast<const T*>(p.v) + base, N);
 
     typedef typename Vec<T>::x8 frag;
     frag qf[4], gf[4];
 #pragma unroll
     for (int dc = 0; dc < 4; ++dc) {
-        qf[dc] = qq < N ? ld8<T>(Q + (size_t)qq * HEAD_DIM + 16 * dc + 8 * hf) : zero8<T>();
-        gf[dc] = qq < N ? ld8<T>(dO + (size_t)qq * HEAD_DIM + 16 * dc + 8 * hf) : zero8<T>();
+        qf[dc] = L.qq < N ? ld8<T>(Q + (size_t)L.qq * HEAD_DIM + 16 * dc + 8 * L.hf) : zero8<T>();
+        gf[dc] = L.qq < N ? ld8<T>(dO + (size_t)L.qq * HEAD_DIM + 16 * dc + 8 * L.hf) : zero8<T>();
     }
-    const float lse2 = qq < N ? p.lse[(size_t)bh * N + qq] * LOG2E : INFINITY;
-    const float dq_row = qq < N ? p.dsum[(size_t)bh * N + qq] : 0.0f;
+    const float lse2 = L.qq < N ? p.lse[(size_t)bh * N + L.qq] * LOG2E : INFINITY;
+    const float dsum = L.qq < N ? p.dsum[(size_t)bh * N + L.qq] : 0.0f;
 
     f32x16 dq[2];
 #pragma unroll
@@ -656,76 +669,37 @@ __global__ __launch_bounds__(DQ_THREADS) void bwd_dq_kernel(BwdArgs p) {
 #pragma unroll
         for (int v = 0; v < 16; ++v) dq[db][v] = 0.0f;
 
-    const int n_end = min(m0 + DQ_BM, N);
-    for (int n0 = 0; n0 < n_end; n0 += DQ_BN) {
+    const int n_tiles = (min(L.m0 + DQ_BM, N) + DQ_BN - 1) / DQ_BN;
+    const int n_full = L.m0 / DQ_BN;
+    auto load = [&](T* kd, T* vd, int t) {
+        tile_load_lds<T>(kd, rk, t * DQ_BN, L.w, L.lane);
+        tile_load_lds<T>(vd, rv, t * DQ_BN, L.w, L.lane);
+    };
+    auto compute = [&](const T* kt, const T* vt, int t) {
+        if (t < n_full)
+            dq_tile<T, false>(kt, vt, t * DQ_BN, L, qf, gf, lse2, dsum, dq, p.scale_log2);
+        else
+            dq_tile<T, true>(kt, vt, t * DQ_BN, L, qf, gf, lse2, dsum, dq, p.scale_log2);
+    };
+    load(t0, t2, 0);
+    __syncthreads();
+    for (int t = 0; t < n_tiles; t += 2) {
+        if (t + 1 < n_tiles) load(t1, t3, t + 1);
+        compute(t0, t2, t);
         __syncthreads();
-        {
-            const int k2 = (tid >> 3) * 2;
-            const int d8 = (tid & 7) * 8;
-            const bool v0 = n0 + k2 < N, v1 = n0 + k2 + 1 < N;
-            frag x0 = v0 ? ld8<T>(K + (size_t)(n0 + k2) * HEAD_DIM + d8) : zero8<T>();
-            frag x1 = v1 ? ld8<T>(K + (size_t)(n0 + k2 + 1) * HEAD_DIM + d8) : zero8<T>();
-            st8<T>(&sm.k[k2][d8], x0);
-            st8<T>(&sm.k[k2 + 1][d8], x1);
-            const int pos = tpos(k2);
-#pragma unroll
-            for (int t = 0; t < 8; ++t) st2<T>(&sm.kt[d8 + t][pos], x0[t], x1[t]);
-            frag y0 = v0 ? ld8<T>(V + (size_t)(n0 + k2) * HEAD_DIM + d8) : zero8<T>();
-            frag y1 = v1 ? ld8<T>(V + (size_t)(n0 + k2 + 1) * HEAD_DIM + d8) : zero8<T>();
-            st8<T>(&sm.v[k2][d8], y0);
-            st8<T>(&sm.v[k2 + 1][d8], y1);
-        }
+        if (t + 1 >= n_tiles) break;
+        if (t + 2 < n_tiles) load(t0, t2, t + 2);
+        compute(t1, t3, t + 1);
         __syncthreads();
-
-        bool act[2];
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-            const int k0 = n0 + 32 * kb;
-            act[kb] = (k0 < q0 + 32) && (k0 < N);
-        }
-        if (!act[0]) continue;
-
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-            if (!act[kb]) continue;
-            const int k0 = n0 + 32 * kb;
-            f32x16 s, dp;
-#pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                s[v] = 0.0f;
-                dp[v] = 0.0f;
-            }
-#pragma unroll
-            for (int dc = 0; dc < 4; ++dc) {
-                mma(s, ld8<T>(&sm.k[32 * kb + c][16 * dc + 8 * hf]), qf[dc]);
-                mma(dp, ld8<T>(&sm.v[32 * kb + c][16 * dc + 8 * hf]), gf[dc]);
-            }
-#pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                float pv = fast_exp2(s[v] * p.scale_log2 - lse2);
-                if (k0 == q0) {
-                    const int kidx = k0 + 8 * (v >> 2) + 4 * hf + (v & 3);
-                    if (kidx > qq) pv = 0.0f;
-                }
-                s[v] = pv * (dp[v] - dq_row);  // dS^T
-            }
-#pragma unroll
-            for (int kc = 0; kc < 2; ++kc) {
-                const frag sb = to_operand<T>(s, 8 * kc);
-#pragma unroll
-                for (int db = 0; db < 2; ++db)
-                    mma(dq[db], ld8<T>(&sm.kt[32 * db + c][32 * kb + 16 * kc + 8 * hf]), sb);
-            }
-        }
     }
 
-    if (qq < N) {
-        T* row = dQ + (size_t)qq * HEAD_DIM;
+    if (L.qq < N) {
+        T* row = dQ + (size_t)L.qq * HEAD_DIM;
 #pragma unroll
         for (int db = 0; db < 2; ++db)
 #pragma unroll
             for (int g = 0; g < 4; ++g)
-                st4<T>(row + 32 * db + 8 * g + 4 * hf, dq[db][4 * g] * p.scale, dq[db][4 * g + 1] * p.scale,
+                st4<T>(row + 32 * db + 8 * g + 4 * L.hf, dq[db][4 * g] * p.scale, dq[db][4 * g + 1] * p.scale,
                        dq[db][4 * g + 2] * p.scale, dq[db][4 * g + 3] * p.scale);
     }
 }

@@ -135,6 +135,197 @@ __device__ __forceinline__ unsigned int pack_bf16(float lo, float hi) {
     return __builtin_bit_cast(unsigned int, v);
 }
 
+// ---------------------------------------------------------------------------
+// Column-slab LDS tiles.  A 64-row tile of a [rows, 64] matrix is split into
+// slabs of 32 bytes of columns (16 bf16 or 8 float); each slab stores its 64
+// rows 32 bytes apart, and slabs are SLAB_BYTES apart, 128 bytes more than
+// 2 KB so that neighbouring slabs sit in opposite halves of the LDS banks.
+// In this layout the two operand reads of the kernels are linear and free of
+// bank conflicts: a row operand (eight consecutive columns of row c, lanes
+// c = 0..31 in each lane half) is one 1 KB run, and each 16-lane group of a
+// transposed read (four rows x 32 bytes) is one 128-byte run.  It is also the
+// order in which a buffer load to LDS writes 64 lanes x 16 bytes.
+// ---------------------------------------------------------------------------
+constexpr int SLAB_BYTES = 32 * 64 + 128;
+constexpr int TILE_ROWS = 64;
+
+template <typename T> __host__ __device__ constexpr int slab_cols() { return 32 / (int)sizeof(T); }
+template <typename T> __host__ __device__ constexpr int tile_slabs() { return HEAD_DIM / slab_cols<T>(); }
+template <typename T> __host__ __device__ constexpr int tile_elems() {
+    return tile_slabs<T>() * SLAB_BYTES / (int)sizeof(T);
+}
+// Element offset of (row, col) inside a tile.
+template <typename T> __device__ __forceinline__ int toff(int row, int col) {
+    return (col / slab_cols<T>()) * (SLAB_BYTES / (int)sizeof(T)) + row * slab_cols<T>() + (col % slab_cols<T>());
+}
+
+// The 16-byte units of a tile are split over the 4 wavefronts: unit k of lane
+// `lane` in wavefront w holds row 32*(w & 1) + lane/2, slab (w >> 1) + 2*k,
+// byte half lane & 1.  One wavefront's unit k covers 1 KB of LDS contiguously.
+template <typename T> __device__ __forceinline__ int unit_row(int w, int lane) { return 32 * (w & 1) + (lane >> 1); }
+template <typename T> __device__ __forceinline__ int unit_col(int w, int lane, int k) {
+    return ((w >> 1) + 2 * k) * slab_cols<T>() + (lane & 1) * (16 / (int)sizeof(T));
+}
+template <typename T> __host__ __device__ constexpr int tile_units() { return tile_slabs<T>() / 2; }
+
+// Buffer resource over one [rows, 64] slice of T; reads past `rows` return 0.
+template <typename T>
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t slice_rsrc(const T* base, int rows) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(base), (short)0, rows * HEAD_DIM * (int)sizeof(T),
+                                             0x00020000);
+}
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+// Asynchronous copy of rows [row0, row0 + 64) of a slice into a tile: each
+// wavefront issues tile_units() buffer loads that write LDS directly (no
+// registers).  Rows past the end of the slice arrive as zeros.  The data is
+// visible after the next __syncthreads().
+template <typename T>
+__device__ __forceinline__ void tile_load_lds(T* tile, __amdgpu_buffer_rsrc_t rsrc, int row0, int w, int lane) {
+#pragma unroll
+    for (int k = 0; k < tile_units<T>(); ++k) {
+        const int s = (w >> 1) + 2 * k;
+        T* dst = tile + s * (SLAB_BYTES / (int)sizeof(T)) + (w & 1) * (1024 / (int)sizeof(T));
+        const int row = row0 + unit_row<T>(w, lane);
+        const int voff = row * HEAD_DIM * (int)sizeof(T) + s * 32 + (lane & 1) * 16;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void*)dst, 16, voff, 0, 0, 0);
+    }
+}
+
+// The LDS of a workgroup: four tiles, each its own __shared__ array, so that
+// the compiler can tell a tile being filled by in-flight buffer loads from the
+// one being read (and skips waiting for those loads before the reads); two
+// small per-buffer float arrays; a few floats for reductions.  Each program
+// gives the tiles its own roles.
+template <typename T>
+struct Tiles {
+    T* t[4];
+    float* aux[2];
+    float* red;
+};
+
+// Row operand: eight consecutive columns col .. col+7 of tile row `row`.
+template <typename T>
+__device__ __forceinline__ typename Vec<T>::x8 ld_row(const T* tile, int row, int col) {
+    return ld8<T>(tile + toff<T>(row, col));
+}
+
+// Transposed operand from a column-slab tile: the A operand whose row m is
+// tile column col0 + m and whose k-slot t of lane half hf is tile row
+//   row0 + 8*(t/4) + 4*hf + (t%4)   (ACC_ORDER: the order in which an MFMA
+//                                     accumulator holds its rows), or
+//   row0 + 8*hf + t                 (natural order).
+// bf16: two ds_read_b64_tr_b16.  Within each 16-lane group that instruction
+// hands lane 4a+b element b of the 8-byte chunks addressed by lanes a, a+4,
+// a+8 and a+12, so lane i of a group addresses tile row (slot base + i/4) at
+// column col0 + 16*(group parity) + 4*(i%4) and receives four k-slots of its
+// own column.  float32: eight scalar LDS reads.
+typedef __attribute__((ext_vector_type(4))) short s16x4;
+typedef __attribute__((ext_vector_type(8))) short s16x8;
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+
+template <bool ACC_ORDER>
+__device__ __forceinline__ bf16x8 ld_tile_t(const bf16* tile, int row0, int col0) {
+    const int l = threadIdx.x & 63;
+    const int i = l & 15;
+    const int hf = l >> 5;
+    const int gp = (l >> 4) & 1;
+    const int r = row0 + (ACC_ORDER ? 4 * hf : 8 * hf) + (i >> 2);
+    const int col = col0 + 16 * gp + 4 * (i & 3);
+    const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(tile + toff<bf16>(r, col)));
+    const s16x4 hi =
+        __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(tile + toff<bf16>(r + (ACC_ORDER ? 8 : 4), col)));
+    const s16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    return __builtin_bit_cast(bf16x8, v);
+}
+template <bool ACC_ORDER>
+__device__ __forceinline__ f32x8 ld_tile_t(const float* tile, int row0, int col0) {
+    const int l = threadIdx.x & 63;
+    const int c = l & 31;
+    const int hf = l >> 5;
+    f32x8 v;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+        const int r = row0 + (ACC_ORDER ? 8 * (t >> 2) + 4 * hf + (t & 3) : 8 * hf + t);
+        v[t] = tile[toff<float>(r, col0 + c)];
+    }
+    return v;
+}
+
+// A 16-byte unit of a row, as it moves through registers when the kernel
+// scales rows while staging them (fixed heads).
+__device__ __forceinline__ u32x4 ld_unit(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
+// Store a 16-byte unit scaled by e (rounded once to the element type).
+__device__ __forceinline__ void st_unit_scaled(bf16* dst, const u32x4& a, float e) {
+    u32x4 o;
+#pragma unroll
+    for (int m = 0; m < 4; ++m)
+        o[m] = pack_bf16(__uint_as_float(a[m] << 16) * e, __uint_as_float(a[m] & 0xffff0000u) * e);
+    *reinterpret_cast<u32x4*>(dst) = o;
+}
+__device__ __forceinline__ void st_unit_scaled(float* dst, const u32x4& a, float e) {
+    u32x4 o;
+#pragma unroll
+    for (int m = 0; m < 4; ++m) o[m] = __float_as_uint(__uint_as_float(a[m]) * e);
+    *reinterpret_cast<u32x4*>(dst) = o;
+}
+
+// Transposed operand from a row-major LDS tile (element stride ld): the A
+// operand whose row m is tile column col0 + m and whose k-slot t of lane half
+// hf is tile row
+//   row0 + 8*(t/4) + 4*hf + (t%4)   (ACC_ORDER: the order in which an MFMA
+//                                     accumulator holds its rows), or
+//   row0 + 8*hf + t                 (natural order).
+// bf16: two ds_read_b64_tr_b16.  Within each 16-lane group that instruction
+// hands lane 4a+b element b of the 8-byte chunks addressed by lanes a, a+4,
+// a+8 and a+12, so lane i of a group addresses tile row (slot base + i/4) at
+// column col0 + 16*(group parity) + 4*(i%4) and receives four k-slots of its
+// own column.  float32: eight scalar LDS reads.
+typedef __attribute__((ext_vector_type(4))) short s16x4;
+typedef __attribute__((ext_vector_type(8))) short s16x8;
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+
+template <bool ACC_ORDER>
+__device__ __forceinline__ bf16x8 ld_t(const bf16* tile, int ld, int row0, int col0) {
+    const int l = threadIdx.x & 63;
+    const int i = l & 15;
+    const int hf = l >> 5;
+    const int gp = (l >> 4) & 1;
+    const int r = row0 + (ACC_ORDER ? 4 * hf : 8 * hf) + (i >> 2);
+    const bf16* p = tile + r * ld + col0 + 16 * gp + 4 * (i & 3);
+    const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p));
+    const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p + (ACC_ORDER ? 8 : 4) * ld));
+    const s16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    return __builtin_bit_cast(bf16x8, v);
+}
+template <bool ACC_ORDER>
+__device__ __forceinline__ f32x8 ld_t(const float* tile, int ld, int row0, int col0) {
+    const int l = threadIdx.x & 63;
+    const int c = l & 31;
+    const int hf = l >> 5;
+    f32x8 v;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+        const int r = row0 + (ACC_ORDER ? 8 * (t >> 2) + 4 * hf + (t & 3) : 8 * hf + t);
+        v[t] = tile[r * ld + col0 + c];
+    }
+    return v;
+}
+
+// Row-major store of eight consecutive values scaled by e (rounded once).
+__device__ __forceinline__ void st8_scaled(bf16* dst, const bf16x8& x, float e) {
+    const u32x4 a = __builtin_bit_cast(u32x4, x);
+    u32x4 o;
+#pragma unroll
+    for (int m = 0; m < 4; ++m)
+        o[m] = pack_bf16(__uint_as_float(a[m] << 16) * e, __uint_as_float(a[m] & 0xffff0000u) * e);
+    *reinterpret_cast<u32x4*>(dst) = o;
+}
+__device__ __forceinline__ void st8_scaled(float* dst, const f32x8& x, float e) {
+    *reinterpret_cast<f32x8*>(dst) = x * e;
+}
+
 // Transposed store of two consecutive rows x0, x1 (eight consecutive columns
 // each): dst[t * ld] = (x0[t], x1[t]) as an adjacent pair, t = 0..7.  The bf16
 // version packs the halves of 32-bit words with v_perm_b32 (no per-element

@@ -12,11 +12,12 @@
 // one query (l % 32) and 16 of its keys: the running maximum and sum stay in
 // the lane (one exchange with the other lane half per tile), the
 // exponentials go straight into the B operand of O^T += V^T P^T, and O^T
-// again holds one query per lane.  Key tiles of 64 stream through a double
-// buffer in LDS while the next tile's global loads are in flight; the tiles
-// below the block's diagonal run a mask-free body.  The running maximum is
-// only raised when a tile exceeds it by more than 2^8, so most tiles skip the
-// rescale of the accumulator.
+// again holds one query per lane.  K and V tiles of 64 keys are copied from
+// memory straight into column-slab LDS tiles by buffer loads (rows past N
+// arrive as zeros), double-buffered so the next tile is in flight while this
+// one is used; V^T comes from transposing LDS reads.  Tiles below the block's
+// diagonal run a mask-free body.  The running maximum is only raised when a
+// tile exceeds it by more than 2^8, so most tiles skip the accumulator rescale.
 //
 // Fixed heads (Eq. compact-prior): P(i,j) = exp(a[j] + r[i-j]) / Z(i) factors
 // as ea(j) * er(i-j) / Z'(i) with ea = exp(a - A*), er = exp(r - R*) and
@@ -40,38 +41,11 @@ namespace saf {
 constexpr int FWD_BM = 128;  // queries per workgroup
 constexpr int FWD_BN = 64;   // keys per tile
 constexpr int FWD_THREADS = 256;
-constexpr int LDS_PAD = 8;   // elements appended to each LDS row
-constexpr float RESCALE_TAU = 8.0f;   // log2 units
-constexpr int FWD_BAND = FWD_BM + FWD_BN;    // 191 offsets used per tile
+constexpr float RESCALE_TAU = 8.0f;            // log2 units
+constexpr int FWD_BAND = FWD_BM + FWD_BN;      // 191 offsets used per tile
 constexpr int FWD_BAND_STRIDE = FWD_BAND + 8;  // spreads the copies over banks
-
-template <typename T>
-struct FwdOrdSmem {
-    T k[2][FWD_BN][HEAD_DIM + LDS_PAD];   // K tile, [key][d]
-    T vt[2][HEAD_DIM][FWD_BN + LDS_PAD];  // V tile transposed, [d][tpos(key)]
-};
-
-template <typename T>
-struct FwdFixSmem {
-    T vt[2][HEAD_DIM][FWD_BN + LDS_PAD];                // (ea * V) transposed, [d][key]
-    T band[2][BAND_COPIES][FWD_BAND_STRIDE];            // er, reversed, 8 shifted copies
-    float red[4];
-};
-
-template <typename T>
-struct FwdExactSmem {
-    T vt[HEAD_DIM][FWD_BN + LDS_PAD];  // V tile transposed, [d][tpos(key)]
-    float a[FWD_BN];
-    float rb[FWD_BAND];
-};
-
-template <typename T>
-constexpr size_t fwd_smem_bytes() {
-    size_t x = sizeof(FwdOrdSmem<T>);
-    if (sizeof(FwdFixSmem<T>) > x) x = sizeof(FwdFixSmem<T>);
-    if (sizeof(FwdExactSmem<T>) > x) x = sizeof(FwdExactSmem<T>);
-    return x;
-}
+static_assert(BAND_COPIES * FWD_BAND_STRIDE * 2 <= tile_elems<bf16>() * 2, "band copies fit in a tile");
+static_assert((FWD_BN + FWD_BAND) * 4 <= tile_elems<bf16>() * 2, "exact-program a and r fit in a tile");
 
 struct FwdArgs {
     const void* q;
@@ -88,12 +62,12 @@ struct FwdArgs {
 
 // Per-lane geometry of one workgroup.
 struct FwdLane {
-    int tid, w, c, hf, m0, q0, qq, N;
+    int tid, w, lane, c, hf, m0, q0, qq, N;
 };
 
 template <typename T>
 __device__ __forceinline__ void store_output(T* O, float* LSE, const FwdLane& L, const f32x16 (&oacc)[2],
-                                             float inv, float lse, bool write_lse = true) {
+                                             float inv, float lse, bool write_lse) {
     if (L.qq >= L.N) return;
     T* orow = O + (size_t)L.qq * HEAD_DIM;
 #pragma unroll
@@ -109,40 +83,8 @@ __device__ __forceinline__ void store_output(T* O, float* LSE, const FwdLane& L,
 // Ordinary heads
 // ---------------------------------------------------------------------------
 
-template <typename T>
-struct KVStage {
-    typename Vec<T>::x8 k[2], v[2];
-};
-
-template <typename T>
-__device__ __forceinline__ void ord_load(KVStage<T>& st, const T* K, const T* V, int n0, int N, int tid) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-        const int id = tid + FWD_THREADS * i;
-        const int row = id >> 3;
-        const int col = (id & 7) * 8;
-        st.k[i] = (n0 + row < N) ? ld8<T>(K + (size_t)(n0 + row) * HEAD_DIM + col) : zero8<T>();
-    }
-    const int k2 = (tid >> 3) * 2;
-    const int d8 = (tid & 7) * 8;
-    st.v[0] = (n0 + k2 < N) ? ld8<T>(V + (size_t)(n0 + k2) * HEAD_DIM + d8) : zero8<T>();
-    st.v[1] = (n0 + k2 + 1 < N) ? ld8<T>(V + (size_t)(n0 + k2 + 1) * HEAD_DIM + d8) : zero8<T>();
-}
-
-template <typename T>
-__device__ __forceinline__ void ord_store(FwdOrdSmem<T>& sm, int buf, const KVStage<T>& st, int tid) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-        const int id = tid + FWD_THREADS * i;
-        st8<T>(&sm.k[buf][id >> 3][(id & 7) * 8], st.k[i]);
-    }
-    const int k2 = (tid >> 3) * 2;
-    const int d8 = (tid & 7) * 8;
-    st_pair_t(&sm.vt[buf][d8][tpos(k2)], FWD_BN + LDS_PAD, st.v[0], st.v[1]);
-}
-
 template <typename T, bool MASK>
-__device__ __forceinline__ void ord_tile(const FwdOrdSmem<T>& sm, int buf, int n0, const FwdLane& L,
+__device__ __forceinline__ void ord_tile(const T* kt, const T* vt, int n0, const FwdLane& L,
                                          const typename Vec<T>::x8 (&qf)[4], f32x16 (&oacc)[2], float& m_run,
                                          float& l_run, float scale_log2) {
     typedef typename Vec<T>::x8 frag;
@@ -158,7 +100,7 @@ __device__ __forceinline__ void ord_tile(const FwdOrdSmem<T>& sm, int buf, int n
         for (int v = 0; v < 16; ++v) s[kb][v] = 0.0f;
         if (kb == 1 && !act1) continue;
 #pragma unroll
-        for (int dc = 0; dc < 4; ++dc) mma(s[kb], ld8<T>(&sm.k[buf][32 * kb + L.c][16 * dc + 8 * L.hf]), qf[dc]);
+        for (int dc = 0; dc < 4; ++dc) mma(s[kb], ld_row<T>(kt, 32 * kb + L.c, 16 * dc + 8 * L.hf), qf[dc]);
     }
     if (MASK) {
 #pragma unroll
@@ -205,18 +147,18 @@ __device__ __forceinline__ void ord_tile(const FwdOrdSmem<T>& sm, int buf, int n
         for (int kc = 0; kc < 2; ++kc) {
             const frag pb = to_operand<T>(s[kb], 8 * kc);
 #pragma unroll
-            for (int db = 0; db < 2; ++db)
-                mma(oacc[db], ld8<T>(&sm.vt[buf][32 * db + L.c][32 * kb + 16 * kc + 8 * L.hf]), pb);
+            for (int db = 0; db < 2; ++db) mma(oacc[db], ld_tile_t<true>(vt, 32 * kb + 16 * kc, 32 * db), pb);
         }
     }
 }
 
 template <typename T>
-__device__ void fwd_ordinary(void* smem, const FwdArgs& p, const FwdLane& L, size_t base, size_t row_base) {
-    FwdOrdSmem<T>& sm = *reinterpret_cast<FwdOrdSmem<T>*>(smem);
+__device__ __forceinline__ void fwd_ordinary(const Tiles<T>& sm, const FwdArgs& p, const FwdLane& L, size_t base,
+                                             size_t row_base) {
+    // Tiles: K in t[0] / t[1], V in t[2] / t[3] (two buffers each).
     const T* __restrict__ Q = reinterpret_cast<const T*>(p.q) + base;
-    const T* __restrict__ K = reinterpret_cast<const T*>(p.k) + base;
-    const T* __restrict__ V = reinterpret_cast<const T*>(p.v) + base;
+    const __amdgpu_buffer_rsrc_t rk = slice_rsrc<T>(reinterpret_cast<const T*>(p.k) + base, L.N);
+    const __amdgpu_buffer_rsrc_t rv = slice_rsrc<T>(reinterpret_cast<const T*>(p.v) + base, L.N);
     typedef typename Vec<T>::x8 frag;
     frag qf[4];
 #pragma unroll
@@ -233,23 +175,30 @@ __device__ void fwd_ordinary(void* smem, const FwdArgs& p, const FwdLane& L, siz
 
     const int n_tiles = (min(L.m0 + FWD_BM, L.N) + FWD_BN - 1) / FWD_BN;
     const int n_full = L.m0 / FWD_BN;  // tiles wholly below the block's first query
-    KVStage<T> st;
-    ord_load<T>(st, K, V, 0, L.N, L.tid);
-    ord_store<T>(sm, 0, st, L.tid);
-    __syncthreads();
-    for (int t = 0; t < n_tiles; ++t) {
-        const bool more = t + 1 < n_tiles;
-        if (more) ord_load<T>(st, K, V, (t + 1) * FWD_BN, L.N, L.tid);
+    auto load = [&](T* kd, T* vd, int t) {
+        tile_load_lds<T>(kd, rk, t * FWD_BN, L.w, L.lane);
+        tile_load_lds<T>(vd, rv, t * FWD_BN, L.w, L.lane);
+    };
+    auto compute = [&](const T* kt, const T* vt, int t) {
         if (t < n_full)
-            ord_tile<T, false>(sm, t & 1, t * FWD_BN, L, qf, oacc, m_run, l_run, p.scale_log2);
+            ord_tile<T, false>(kt, vt, t * FWD_BN, L, qf, oacc, m_run, l_run, p.scale_log2);
         else
-            ord_tile<T, true>(sm, t & 1, t * FWD_BN, L, qf, oacc, m_run, l_run, p.scale_log2);
-        if (more) ord_store<T>(sm, (t + 1) & 1, st, L.tid);
+            ord_tile<T, true>(kt, vt, t * FWD_BN, L, qf, oacc, m_run, l_run, p.scale_log2);
+    };
+    load(sm.t[0], sm.t[2], 0);
+    __syncthreads();
+    for (int t = 0; t < n_tiles; t += 2) {
+        if (t + 1 < n_tiles) load(sm.t[1], sm.t[3], t + 1);
+        compute(sm.t[0], sm.t[2], t);
+        __syncthreads();
+        if (t + 1 >= n_tiles) break;
+        if (t + 2 < n_tiles) load(sm.t[0], sm.t[2], t + 2);
+        compute(sm.t[1], sm.t[3], t + 1);
         __syncthreads();
     }
     const float l_tot = l_run + xor32(l_run);
     store_output<T>(reinterpret_cast<T*>(p.o) + base, p.lse + row_base, L, oacc, 1.0f / l_tot,
-                    (m_run + __log2f(l_tot)) * LN2);
+                    (m_run + __log2f(l_tot)) * LN2, true);
 }
 
 // ---------------------------------------------------------------------------
@@ -257,9 +206,12 @@ __device__ void fwd_ordinary(void* smem, const FwdArgs& p, const FwdLane& L, siz
 // ---------------------------------------------------------------------------
 
 template <typename T>
-__device__ void fwd_fixed_exact(void* smem, const FwdArgs& p, const FwdLane& L, size_t base, size_t row_base,
-                                const float* arow, const float* rrow) {
-    FwdExactSmem<T>& sm = *reinterpret_cast<FwdExactSmem<T>*>(smem);
+__device__ __forceinline__ void fwd_fixed_exact(const Tiles<T>& sm, const FwdArgs& p, const FwdLane& L, size_t base,
+                                                size_t row_base, const float* arow, const float* rrow) {
+    // Tiles: V in t[0]; a of the tile's keys and r over its offsets in t[1].
+    T* vt = sm.t[0];
+    float* as = reinterpret_cast<float*>(sm.t[1]);
+    float* rb = as + FWD_BN;
     const T* __restrict__ V = reinterpret_cast<const T*>(p.v) + base;
     typedef typename Vec<T>::x8 frag;
     const int N = L.N;
@@ -271,19 +223,20 @@ __device__ void fwd_fixed_exact(void* smem, const FwdArgs& p, const FwdLane& L, 
     float m_run = NEG_BIG;
     float l_run = 0.0f;
     const int n_end = min(L.m0 + FWD_BM, N);
+    const int row = unit_row<T>(L.w, L.lane);
     for (int n0 = 0; n0 < n_end; n0 += FWD_BN) {
         __syncthreads();
-        {
-            const int k2 = (L.tid >> 3) * 2;
-            const int d8 = (L.tid & 7) * 8;
-            frag x0 = (n0 + k2 < N) ? ld8<T>(V + (size_t)(n0 + k2) * HEAD_DIM + d8) : zero8<T>();
-            frag x1 = (n0 + k2 + 1 < N) ? ld8<T>(V + (size_t)(n0 + k2 + 1) * HEAD_DIM + d8) : zero8<T>();
-            st_pair_t(&sm.vt[d8][tpos(k2)], FWD_BN + LDS_PAD, x0, x1);
+#pragma unroll
+        for (int k = 0; k < tile_units<T>(); ++k) {
+            const int col = unit_col<T>(L.w, L.lane, k);
+            const u32x4 z = {0u, 0u, 0u, 0u};
+            const u32x4 x = n0 + row < N ? ld_unit(V + (size_t)(n0 + row) * HEAD_DIM + col) : z;
+            *reinterpret_cast<u32x4*>(vt + toff<T>(row, col)) = x;
         }
-        if (L.tid < FWD_BN) sm.a[L.tid] = (n0 + L.tid < N) ? arow[n0 + L.tid] : -INFINITY;
+        if (L.tid < FWD_BN) as[L.tid] = (n0 + L.tid < N) ? arow[n0 + L.tid] : -INFINITY;
         for (int x = L.tid; x < FWD_BAND - 1; x += FWD_THREADS) {
             const int delta = L.m0 - n0 - (FWD_BN - 1) + x;  // offsets m0-n0-63 .. m0-n0+127
-            sm.rb[x] = (delta >= 0 && delta < N) ? rrow[delta] : -INFINITY;
+            rb[x] = (delta >= 0 && delta < N) ? rrow[delta] : -INFINITY;
         }
         __syncthreads();
         if (!(n0 < L.q0 + 32)) continue;
@@ -294,7 +247,7 @@ __device__ void fwd_fixed_exact(void* smem, const FwdArgs& p, const FwdLane& L, 
             for (int v = 0; v < 16; ++v) {
                 const int kl = 32 * kb + 8 * (v >> 2) + 4 * L.hf + (v & 3);
                 const int x = (L.qq - L.m0) - kl + (FWD_BN - 1);
-                s[kb][v] = (sm.a[kl] + sm.rb[x]) * LOG2E;
+                s[kb][v] = (as[kl] + rb[x]) * LOG2E;
             }
         float mx = -INFINITY;
 #pragma unroll
@@ -322,8 +275,7 @@ __device__ void fwd_fixed_exact(void* smem, const FwdArgs& p, const FwdLane& L, 
             for (int kc = 0; kc < 2; ++kc) {
                 const frag pb = to_operand<T>(s[kb], 8 * kc);
 #pragma unroll
-                for (int db = 0; db < 2; ++db)
-                    mma(oacc[db], ld8<T>(&sm.vt[32 * db + L.c][32 * kb + 16 * kc + 8 * L.hf]), pb);
+                for (int db = 0; db < 2; ++db) mma(oacc[db], ld_tile_t<true>(vt, 32 * kb + 16 * kc, 32 * db), pb);
             }
         }
     }
@@ -338,44 +290,45 @@ __device__ void fwd_fixed_exact(void* smem, const FwdArgs& p, const FwdLane& L, 
 
 template <typename T>
 struct FixStage {
-    typename Vec<T>::x8 v[2];
-    float a[2];
-    float rb;
+    u32x4 v[tile_units<T>()];  // this lane's 16-byte units of the V tile (one row)
+    float a;                   // a of that row's key
+    float rb;                  // one band entry
 };
 
 template <typename T>
 __device__ __forceinline__ void fix_load(FixStage<T>& st, const T* V, const float* arow, const float* rrow, int n0,
-                                         int m0, int N, int tid) {
-    const int k2 = (tid >> 3) * 2;
-    const int d8 = (tid & 7) * 8;
-    st.v[0] = (n0 + k2 < N) ? ld8<T>(V + (size_t)(n0 + k2) * HEAD_DIM + d8) : zero8<T>();
-    st.v[1] = (n0 + k2 + 1 < N) ? ld8<T>(V + (size_t)(n0 + k2 + 1) * HEAD_DIM + d8) : zero8<T>();
-    st.a[0] = (n0 + k2 < N) ? arow[n0 + k2] : -INFINITY;
-    st.a[1] = (n0 + k2 + 1 < N) ? arow[n0 + k2 + 1] : -INFINITY;
+                                         const FwdLane& L) {
+    const int key = n0 + unit_row<T>(L.w, L.lane);
+    const bool ok = key < L.N;
+#pragma unroll
+    for (int k = 0; k < tile_units<T>(); ++k) {
+        const u32x4 z = {0u, 0u, 0u, 0u};
+        st.v[k] = ok ? ld_unit(V + (size_t)key * HEAD_DIM + unit_col<T>(L.w, L.lane, k)) : z;
+    }
+    st.a = ok ? arow[key] : -INFINITY;
     // Band entry u holds offset (m0 - n0 + 127) - u.
-    const int delta = m0 - n0 + (FWD_BM - 1) - tid;
-    st.rb = (tid < FWD_BAND - 1 && delta >= 0 && delta < N) ? rrow[delta] : -INFINITY;
+    const int delta = L.m0 - n0 + (FWD_BM - 1) - L.tid;
+    st.rb = (L.tid < FWD_BAND - 1 && delta >= 0 && delta < L.N) ? rrow[delta] : -INFINITY;
 }
 
 template <typename T>
-__device__ __forceinline__ void fix_store(FwdFixSmem<T>& sm, int buf, const FixStage<T>& st, int tid, float a_sh,
+__device__ __forceinline__ void fix_store(T* vs, T* band, const FixStage<T>& st, const FwdLane& L, float a_sh,
                                           float r_sh) {
-    const int k2 = (tid >> 3) * 2;
-    const int d8 = (tid & 7) * 8;
-    const float e0 = fast_exp2(fmaf(st.a[0], LOG2E, -a_sh));
-    const float e1 = fast_exp2(fmaf(st.a[1], LOG2E, -a_sh));
-    st_pair_t_scaled(&sm.vt[buf][d8][k2], FWD_BN + LDS_PAD, st.v[0], st.v[1], e0, e1);
-    if (tid < FWD_BAND - 1) {
-        const T e = (T)fast_exp2(fmaf(st.rb, LOG2E, -r_sh));
+    const float e = fast_exp2(fmaf(st.a, LOG2E, -a_sh));
+    const int row = unit_row<T>(L.w, L.lane);
+#pragma unroll
+    for (int k = 0; k < tile_units<T>(); ++k)
+        st_unit_scaled(vs + toff<T>(row, unit_col<T>(L.w, L.lane, k)), st.v[k], e);
+    if (L.tid < FWD_BAND - 1) {
+        const T b = (T)fast_exp2(fmaf(st.rb, LOG2E, -r_sh));
 #pragma unroll
         for (int s = 0; s < BAND_COPIES; ++s)
-            if (tid >= s) sm.band[buf][s][tid - s] = e;
+            if (L.tid >= s) band[s * FWD_BAND_STRIDE + L.tid - s] = b;
     }
 }
 
 template <typename T, bool MASK>
-__device__ __forceinline__ void fix_tile(const FwdFixSmem<T>& sm, int buf, int n0, const FwdLane& L,
-                                         f32x16 (&oacc)[2]) {
+__device__ __forceinline__ void fix_tile(const T* vs, const T* band, int n0, const FwdLane& L, f32x16 (&oacc)[2]) {
     typedef typename Vec<T>::x8 frag;
     const int ql = 32 * L.w + L.c;  // query within the block
 #pragma unroll
@@ -383,15 +336,16 @@ __device__ __forceinline__ void fix_tile(const FwdFixSmem<T>& sm, int buf, int n
         if (MASK && n0 + 16 * G > L.q0 + 31) continue;  // chunk wholly after this wavefront's queries
         const int u0 = (FWD_BM - 1) - ql + 16 * G + 8 * L.hf;
         const int s = u0 & 7;
-        const frag b = ld8<T>(&sm.band[buf][s][u0 - s]);
+        const frag b = ld8<T>(band + s * FWD_BAND_STRIDE + u0 - s);
 #pragma unroll
-        for (int db = 0; db < 2; ++db) mma(oacc[db], ld8<T>(&sm.vt[buf][32 * db + L.c][16 * G + 8 * L.hf]), b);
+        for (int db = 0; db < 2; ++db) mma(oacc[db], ld_tile_t<false>(vs, 16 * G, 32 * db), b);
     }
 }
 
 template <typename T>
-__device__ void fwd_fixed(void* smem, const FwdArgs& p, const FwdLane& L, size_t base, size_t row_base, int h) {
-    FwdFixSmem<T>& sm = *reinterpret_cast<FwdFixSmem<T>*>(smem);
+__device__ __forceinline__ void fwd_fixed(const Tiles<T>& sm, const FwdArgs& p, const FwdLane& L, size_t base,
+                                          size_t row_base, int h) {
+    // Tiles: ea * V in t[0] / t[1], the band in t[2] / t[3].
     const T* __restrict__ V = reinterpret_cast<const T*>(p.v) + base;
     const float* __restrict__ arow = p.a + (size_t)h * p.ld_prior;
     const float* __restrict__ rrow = p.r + (size_t)h * p.ld_prior;
@@ -414,7 +368,7 @@ __device__ void fwd_fixed(void* smem, const FwdArgs& p, const FwdLane& L, size_t
         ok = fmaxf(arow[i] + rrow[0], arow[0] + rrow[i]) - A - R >= -FAST_GUARD;
     }
     if (!__syncthreads_and(ok)) {
-        fwd_fixed_exact<T>(smem, p, L, base, row_base, arow, rrow);
+        fwd_fixed_exact<T>(sm, p, L, base, row_base, arow, rrow);
         return;
     }
     const float a_sh = A * LOG2E, r_sh = R * LOG2E;
@@ -424,20 +378,28 @@ __device__ void fwd_fixed(void* smem, const FwdArgs& p, const FwdLane& L, size_t
     for (int db = 0; db < 2; ++db)
 #pragma unroll
         for (int v = 0; v < 16; ++v) oacc[db][v] = 0.0f;
+
     const int n_tiles = (m1 + FWD_BN - 1) / FWD_BN;
     const int n_full = L.m0 / FWD_BN;
-    FixStage<T> st;
-    fix_load<T>(st, V, arow, rrow, 0, L.m0, N, L.tid);
-    fix_store<T>(sm, 0, st, L.tid, a_sh, r_sh);
-    __syncthreads();
-    for (int t = 0; t < n_tiles; ++t) {
-        const bool more = t + 1 < n_tiles;
-        if (more) fix_load<T>(st, V, arow, rrow, (t + 1) * FWD_BN, L.m0, N, L.tid);
+    auto compute = [&](const T* vs, const T* band, int t) {
         if (t < n_full)
-            fix_tile<T, false>(sm, t & 1, t * FWD_BN, L, oacc);
+            fix_tile<T, false>(vs, band, t * FWD_BN, L, oacc);
         else
-            fix_tile<T, true>(sm, t & 1, t * FWD_BN, L, oacc);
-        if (more) fix_store<T>(sm, (t + 1) & 1, st, L.tid, a_sh, r_sh);
+            fix_tile<T, true>(vs, band, t * FWD_BN, L, oacc);
+    };
+    FixStage<T> st;
+    fix_load<T>(st, V, arow, rrow, 0, L);
+    fix_store<T>(sm.t[0], sm.t[2], st, L, a_sh, r_sh);
+    __syncthreads();
+    for (int t = 0; t < n_tiles; t += 2) {
+        if (t + 1 < n_tiles) fix_load<T>(st, V, arow, rrow, (t + 1) * FWD_BN, L);
+        compute(sm.t[0], sm.t[2], t);
+        if (t + 1 < n_tiles) fix_store<T>(sm.t[1], sm.t[3], st, L, a_sh, r_sh);
+        __syncthreads();
+        if (t + 1 >= n_tiles) break;
+        if (t + 2 < n_tiles) fix_load<T>(st, V, arow, rrow, (t + 2) * FWD_BN, L);
+        compute(sm.t[1], sm.t[3], t + 1);
+        if (t + 2 < n_tiles) fix_store<T>(sm.t[0], sm.t[2], st, L, a_sh, r_sh);
         __syncthreads();
     }
     // 1 / Z'(i) = exp(A + R - log Z(i)), with log Z from the normaliser pre-pass.
@@ -458,10 +420,10 @@ __device__ void fwd_fixed(void* smem, const FwdArgs& p, const FwdLane& L, size_t
 // ---------------------------------------------------------------------------
 constexpr int NORM_THREADS = 256;
 constexpr int NORM_ROWS = 32;
-constexpr int NORM_PARTS = NORM_THREADS / NORM_ROWS;     // threads per row
-constexpr int NORM_KT = 512;                             // keys per tile
-constexpr int NORM_PART_KEYS = NORM_KT / NORM_PARTS;     // 64
-constexpr int NORM_BAND = NORM_ROWS + NORM_KT - 1;       // offsets per tile
+constexpr int NORM_PARTS = NORM_THREADS / NORM_ROWS;  // threads per row
+constexpr int NORM_KT = 512;                          // keys per tile
+constexpr int NORM_PART_KEYS = NORM_KT / NORM_PARTS;  // 64
+constexpr int NORM_BAND = NORM_ROWS + NORM_KT - 1;    // offsets per tile
 
 struct NormArgs {
     const float* a;
@@ -571,8 +533,13 @@ __global__ __launch_bounds__(NORM_THREADS) void fixed_lse_kernel(NormArgs p) {
 // ---------------------------------------------------------------------------
 
 template <typename T>
-__global__ __launch_bounds__(FWD_THREADS) void fwd_kernel(FwdArgs p) {
-    __shared__ __attribute__((aligned(16))) char smem[fwd_smem_bytes<T>()];
+__global__ __launch_bounds__(FWD_THREADS) __attribute__((amdgpu_waves_per_eu(3))) void fwd_kernel(FwdArgs p) {
+    __shared__ __attribute__((aligned(16))) T t0[tile_elems<T>()];
+    __shared__ __attribute__((aligned(16))) T t1[tile_elems<T>()];
+    __shared__ __attribute__((aligned(16))) T t2[tile_elems<T>()];
+    __shared__ __attribute__((aligned(16))) T t3[tile_elems<T>()];
+    __shared__ float red[4];
+    const Tiles<T> sm = {{t0, t1, t2, t3}, {nullptr, nullptr}, red};
     const int n_bh = p.B * p.H;
     // Longest blocks first: block index -> query block in descending order.
     const int qblk = p.n_qblocks - 1 - (int)(blockIdx.x / n_bh);
@@ -582,6 +549,7 @@ __global__ __launch_bounds__(FWD_THREADS) void fwd_kernel(FwdArgs p) {
     FwdLane L;
     L.tid = threadIdx.x;
     L.w = L.tid >> 6;
+    L.lane = L.tid & 63;
     L.c = L.tid & 31;
     L.hf = (L.tid >> 5) & 1;
     L.m0 = qblk * FWD_BM;
@@ -591,9 +559,9 @@ __global__ __launch_bounds__(FWD_THREADS) void fwd_kernel(FwdArgs p) {
     const size_t base = (size_t)bh * p.N * HEAD_DIM;
     const size_t row_base = (size_t)bh * p.N;
     if (fixed)
-        fwd_fixed<T>(smem, p, L, base, row_base, h);
+        fwd_fixed<T>(sm, p, L, base, row_base, h);
     else
-        fwd_ordinary<T>(smem, p, L, base, row_base);
+        fwd_ordinary<T>(sm, p, L, base, row_base);
 }
 
 }  // namespace saf
