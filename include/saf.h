@@ -35,8 +35,10 @@
  * - Arguments are checked before anything is enqueued; on any error nothing
  *   is launched and nothing is written.  A kernel fault surfaces at the
  *   caller's next synchronisation, not here.
- * - Limits of this build: d == 64, 1 <= H <= 64, N <= 2^24.  B, H or N equal
- *   to 0 is an empty problem: SAF_OK, nothing launched.
+ * - Limits of this build: d == 64, 1 <= H <= 64, N <= 2^24 for bf16 and
+ *   N <= 2^23 for float32 (one (batch, head) slice stays below 2^31 bytes),
+ *   and B * H * ceil(N / 32) <= 2^31 - 1.  B, H or N equal to 0 is an empty
+ *   problem: SAF_OK, nothing launched.
  * - Numerics: products on MFMA in the element type with float32 accumulation;
  *   softmax statistics, LSE and the fixed-head normalisers in float32.  Results
  *   are rounded once to the element type (nearest even for bf16).
@@ -60,7 +62,7 @@ typedef enum {
 typedef enum {
     SAF_OK = 0,
     SAF_ERR_NULL = 1,          /* a required pointer is NULL */
-    SAF_ERR_SHAPE = 2,         /* negative size, N > 2^24, ld_prior < N, or workspace too small */
+    SAF_ERR_SHAPE = 2,         /* negative size, N or B*H*N above the limits, ld_prior < N, or workspace too small */
     SAF_ERR_UNSUPPORTED = 3,   /* unknown dtype, d != 64, H > 64 */
     SAF_ERR_MISSING_PRIOR = 4, /* a head is fixed but a or r is NULL */
     SAF_ERR_LAUNCH = 5,        /* the HIP runtime rejected a kernel launch */
@@ -71,9 +73,12 @@ typedef enum {
 /*
  * Forward of the hybrid layer (Section "Replacement schedules and fused
  * execution"; Appendix "Mixed-head execution and numerical checks"): one
- * kernel launch in which every workgroup takes one (batch, head, block of
- * queries) and the head's flag selects its path; outputs land in the original
- * head order.
+ * launch of the attention kernel for all heads, in which every workgroup
+ * takes one (batch, head, block of queries) and the head's flag selects its
+ * path; outputs land in the original head order.  When some head is fixed, a
+ * small normaliser launch runs first and writes log Z(i) of the fixed heads
+ * into LSE (the paper precomputes these normalisers; here they are recomputed
+ * from a and r on every call, in float32).
  *   Q, K : [B,H,N,d] `dt`; read for ordinary heads only (fixed-head slices may
  *          hold anything, NaN included).  May be NULL if every head is fixed.
  *   V    : [B,H,N,d] `dt`.

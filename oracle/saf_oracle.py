@@ -27,7 +27,7 @@ Everything here evaluates the plain dense definitions in float64, one
   zero gradients (Appendix "Mixed-head execution and numerical checks").
   For an ordinary head the gradients are the chain rule through softmax.
 
-Readings of points the paper leaves open (each is listed in the design doc):
+Readings of points the paper leaves open:
 
 * 0-based storage: ``a[j] = alpha(j + 1)`` and ``r[delta] = rho(delta)``.
 * The per-row log-normaliser is returned as ``LSE`` (natural log): for an

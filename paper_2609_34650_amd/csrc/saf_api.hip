@@ -13,7 +13,10 @@
 
 namespace {
 
-constexpr int kMaxN = 1 << 24;
+// Kernels address one (batch, head) slice of N x 64 elements through a buffer
+// resource with 32-bit byte offsets, so a slice must stay below 2^31 bytes.
+constexpr int kMaxN = 1 << 24;      // bf16: 2^24 rows x 128 B = 2^31 B
+constexpr int kMaxNF32 = 1 << 23;   // float32: 2^23 rows x 256 B = 2^31 B
 
 struct Problem {
     uint64_t fixed_mask = 0;
@@ -32,8 +35,9 @@ saf_status_t check_common(saf_dtype_t dt, const uint8_t* head_is_fixed, const fl
     if (B < 0 || H < 0 || N < 0 || d < 0) return SAF_ERR_SHAPE;
     if (d != saf::HEAD_DIM) return SAF_ERR_UNSUPPORTED;
     if (H > 64) return SAF_ERR_UNSUPPORTED;
-    if (N > kMaxN) return SAF_ERR_SHAPE;
-    if ((int64_t)B * H * ((N + 127) / 128) > INT32_MAX) return SAF_ERR_SHAPE;
+    if (N > (dt == SAF_DTYPE_F32 ? kMaxNF32 : kMaxN)) return SAF_ERR_SHAPE;
+    // The largest grid is the backward row pre-pass: one workgroup per 32 rows.
+    if ((int64_t)B * H * ((N + 31) / 32) > INT32_MAX) return SAF_ERR_SHAPE;
     if (B == 0 || H == 0 || N == 0) {
         pr->empty = true;
         return SAF_OK;
@@ -234,7 +238,7 @@ SAF_EXPORT const char* saf_status_str(saf_status_t s) {
     switch (s) {
         case SAF_OK: return "ok";
         case SAF_ERR_NULL: return "a required pointer is NULL";
-        case SAF_ERR_SHAPE: return "invalid size (negative, N > 2^24, ld_prior < N, or workspace too small)";
+        case SAF_ERR_SHAPE: return "invalid size (negative, N above the limit, grid too large, ld_prior < N, or workspace too small)";
         case SAF_ERR_UNSUPPORTED: return "unsupported dtype, head dimension (d must be 64) or head count (H <= 64)";
         case SAF_ERR_MISSING_PRIOR: return "a head is fixed but a or r is NULL";
         case SAF_ERR_LAUNCH: return "kernel launch failed";

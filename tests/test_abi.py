@@ -73,6 +73,8 @@ def test_forward_argument_errors(lib):
     assert _fwd(lib, N=-1) == 2
     assert _fwd(lib, B=-2) == 2
     assert _fwd(lib, N=(1 << 24) + 1) == 2
+    assert _fwd(lib, dt=0, N=(1 << 23) + 1) == 2      # float32 slice would pass 2^31 bytes
+    assert _fwd(lib, B=1 << 12, flags=[0] * 64, N=1 << 20) == 2   # grid above 2^31 - 1 workgroups
     assert _fwd(lib, a=None) == 4                     # a fixed head needs a and r
     assert _fwd(lib, r=None) == 4
     assert _fwd(lib, ld=7) == 2                       # prior shorter than N
