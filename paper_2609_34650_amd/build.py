@@ -28,6 +28,10 @@ HIPCC_FLAGS = [
     # MFMA accumulators in ordinary VGPRs: the softmax works on them directly,
     # with no copies between AGPRs and VGPRs.
     "-mllvm", "-amdgpu-mfma-vgpr-form",
+    # Schedule for instruction-level parallelism (LDS reads issued well ahead
+    # of the MFMAs that consume them) rather than for the smallest register
+    # count: every kernel runs at two wavefronts per SIMD either way.
+    "-mllvm", "-amdgpu-sched-strategy=max-ilp",
     "-Wall",
     "-Wno-unused-function",
 ]

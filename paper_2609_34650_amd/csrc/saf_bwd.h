@@ -254,35 +254,29 @@ __device__ __forceinline__ void kv_ordinary(const Tiles<T>& sm, const BwdArgs& p
                 dk[kb][db][v] = 0.0f;
             }
 
+    // Slots: the tiles that meet the diagonal first (masked), then the rest.
     const int n_tiles = (L.N - L.n0 + KV_BM - 1) / KV_BM;
-    auto load = [&](T* qd, T* gd, float* rows, int t) {
-        const int mq = L.n0 + t * KV_BM;
-        tile_load_lds<T>(qd, rq, mq, L.w, L.lane);
-        tile_load_lds<T>(gd, rg, mq, L.w, L.lane);
-        if (L.tid < KV_BM) {
-            const bool ok = mq + L.tid < L.N;
-            rows[L.tid] = ok ? LSE[mq + L.tid] * LOG2E : INFINITY;
-            rows[KV_BM + L.tid] = ok ? Dsum[mq + L.tid] : 0.0f;
-        }
-    };
-    auto compute = [&](const T* qt, const T* gt, const float* rows, int t) {
-        const int mq = L.n0 + t * KV_BM;
-        if (t < KV_MASK_TILES)
-            kv_tile<T, true>(qt, gt, rows, mq, L, kf, vf, dv, dk, p.scale_log2);
-        else
-            kv_tile<T, false>(qt, gt, rows, mq, L, kf, vf, dv, dk, p.scale_log2);
-    };
-    load(sm.t[0], sm.t[2], sm.aux[0], 0);
-    __syncthreads();
-    for (int t = 0; t < n_tiles; t += 2) {
-        if (t + 1 < n_tiles) load(sm.t[1], sm.t[3], sm.aux[1], t + 1);
-        compute(sm.t[0], sm.t[2], sm.aux[0], t);
-        __syncthreads();
-        if (t + 1 >= n_tiles) break;
-        if (t + 2 < n_tiles) load(sm.t[0], sm.t[2], sm.aux[0], t + 2);
-        compute(sm.t[1], sm.t[3], sm.aux[1], t + 1);
-        __syncthreads();
-    }
+    const int n_mask = min(KV_MASK_TILES, n_tiles);
+    const int P = (n_mask + 1) & ~1;
+    run_slots(
+        P, P + n_tiles - n_mask, [&](int i) { return i < P ? (i < n_mask ? i : -1) : n_mask + (i - P); },
+        [&](auto buf, int t) {
+            constexpr int b = decltype(buf)::value;
+            const int mq = L.n0 + t * KV_BM;
+            tile_load_lds<T>(sm.t[b], rq, mq, L.w, L.lane);
+            tile_load_lds<T>(sm.t[2 + b], rg, mq, L.w, L.lane);
+            if (L.tid < KV_BM) {
+                const bool ok = mq + L.tid < L.N;
+                sm.aux[b][L.tid] = ok ? LSE[mq + L.tid] * LOG2E : INFINITY;
+                sm.aux[b][KV_BM + L.tid] = ok ? Dsum[mq + L.tid] : 0.0f;
+            }
+        },
+        [&](auto) {},
+        [&](auto buf, int t, auto mask) {
+            constexpr int b = decltype(buf)::value;
+            kv_tile<T, decltype(mask)::value>(sm.t[b], sm.t[2 + b], sm.aux[b], L.n0 + t * KV_BM, L, kf, vf, dv, dk,
+                                              p.scale_log2);
+        });
     float one[KV_KB], ks[KV_KB];
 #pragma unroll
     for (int kb = 0; kb < KV_KB; ++kb) {
@@ -496,28 +490,17 @@ __device__ __forceinline__ void kv_fixed(const Tiles<T>& sm, const BwdArgs& p, c
             for (int v = 0; v < 16; ++v) dv[kb][db][v] = 0.0f;
 
     const int n_tiles = (N - L.n0 + KV_BM - 1) / KV_BM;
-    auto compute = [&](const T* dog, const T* band, int t) {
-        const int mq = L.n0 + t * KV_BM;
-        if (t < KV_MASK_TILES)
-            kvf_tile<T, true>(dog, band, mq, L, dv);
-        else
-            kvf_tile<T, false>(dog, band, mq, L, dv);
-    };
+    const int n_mask = min(KV_MASK_TILES, n_tiles);
+    const int P = (n_mask + 1) & ~1;
     KvFixStage<T> st;
-    kvf_load<T>(st, dO, LSE, rrow, L.n0, L);
-    kvf_store<T>(sm.t[0], sm.t[2], st, L, g_sh, r_sh);
-    __syncthreads();
-    for (int t = 0; t < n_tiles; t += 2) {
-        if (t + 1 < n_tiles) kvf_load<T>(st, dO, LSE, rrow, L.n0 + (t + 1) * KV_BM, L);
-        compute(sm.t[0], sm.t[2], t);
-        if (t + 1 < n_tiles) kvf_store<T>(sm.t[1], sm.t[3], st, L, g_sh, r_sh);
-        __syncthreads();
-        if (t + 1 >= n_tiles) break;
-        if (t + 2 < n_tiles) kvf_load<T>(st, dO, LSE, rrow, L.n0 + (t + 2) * KV_BM, L);
-        compute(sm.t[1], sm.t[3], t + 1);
-        if (t + 2 < n_tiles) kvf_store<T>(sm.t[0], sm.t[2], st, L, g_sh, r_sh);
-        __syncthreads();
-    }
+    run_slots(
+        P, P + n_tiles - n_mask, [&](int i) { return i < P ? (i < n_mask ? i : -1) : n_mask + (i - P); },
+        [&](auto, int t) { kvf_load<T>(st, dO, LSE, rrow, L.n0 + t * KV_BM, L); },
+        [&](auto buf) { kvf_store<T>(sm.t[decltype(buf)::value], sm.t[2 + decltype(buf)::value], st, L, g_sh, r_sh); },
+        [&](auto buf, int t, auto mask) {
+            kvf_tile<T, decltype(mask)::value>(sm.t[decltype(buf)::value], sm.t[2 + decltype(buf)::value],
+                                               L.n0 + t * KV_BM, L, dv);
+        });
     float ea[KV_KB];
 #pragma unroll
     for (int kb = 0; kb < KV_KB; ++kb) {
@@ -615,7 +598,7 @@ __device__ __forceinline__ void dq_tile(const T* kt, const T* vt, int n0, const 
 }
 
 template <typename T>
-__global__ __launch_bounds__(DQ_THREADS) void bwd_dq_kernel(BwdArgs p) {
+__global__ __launch_bounds__(DQ_THREADS) __attribute__((amdgpu_waves_per_eu(3))) void bwd_dq_kernel(BwdArgs p) {
     __shared__ __attribute__((aligned(16))) T t0[tile_elems<T>()];
     __shared__ __attribute__((aligned(16))) T t1[tile_elems<T>()];
     __shared__ __attribute__((aligned(16))) T t2[tile_elems<T>()];
@@ -669,29 +652,25 @@ __global__ __launch_bounds__(DQ_THREADS) void bwd_dq_kernel(BwdArgs p) {
 #pragma unroll
         for (int v = 0; v < 16; ++v) dq[db][v] = 0.0f;
 
+    // Slots: the tiles that meet the diagonal first (masked), then the tiles
+    // wholly below the block's first query.
     const int n_tiles = (min(L.m0 + DQ_BM, N) + DQ_BN - 1) / DQ_BN;
     const int n_full = L.m0 / DQ_BN;
-    auto load = [&](T* kd, T* vd, int t) {
-        tile_load_lds<T>(kd, rk, t * DQ_BN, L.w, L.lane);
-        tile_load_lds<T>(vd, rv, t * DQ_BN, L.w, L.lane);
-    };
-    auto compute = [&](const T* kt, const T* vt, int t) {
-        if (t < n_full)
-            dq_tile<T, false>(kt, vt, t * DQ_BN, L, qf, gf, lse2, dsum, dq, p.scale_log2);
-        else
-            dq_tile<T, true>(kt, vt, t * DQ_BN, L, qf, gf, lse2, dsum, dq, p.scale_log2);
-    };
-    load(t0, t2, 0);
-    __syncthreads();
-    for (int t = 0; t < n_tiles; t += 2) {
-        if (t + 1 < n_tiles) load(t1, t3, t + 1);
-        compute(t0, t2, t);
-        __syncthreads();
-        if (t + 1 >= n_tiles) break;
-        if (t + 2 < n_tiles) load(t0, t2, t + 2);
-        compute(t1, t3, t + 1);
-        __syncthreads();
-    }
+    const int n_mask = n_tiles - n_full;
+    const int P = (n_mask + 1) & ~1;
+    T* const kt[2] = {t0, t1};
+    T* const vt[2] = {t2, t3};
+    run_slots(
+        P, P + n_full, [&](int i) { return i < P ? (i < n_mask ? n_full + i : -1) : i - P; },
+        [&](auto buf, int t) {
+            tile_load_lds<T>(kt[decltype(buf)::value], rk, t * DQ_BN, L.w, L.lane);
+            tile_load_lds<T>(vt[decltype(buf)::value], rv, t * DQ_BN, L.w, L.lane);
+        },
+        [&](auto) {},
+        [&](auto buf, int t, auto mask) {
+            dq_tile<T, decltype(mask)::value>(kt[decltype(buf)::value], vt[decltype(buf)::value], t * DQ_BN, L, qf,
+                                              gf, lse2, dsum, dq, p.scale_log2);
+        });
 
     if (L.qq < N) {
         T* row = dQ + (size_t)L.qq * HEAD_DIM;

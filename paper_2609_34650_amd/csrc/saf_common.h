@@ -20,6 +20,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 namespace saf {
 
 typedef __bf16 bf16;
@@ -122,11 +124,21 @@ __device__ __forceinline__ int tpos(int k) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-__device__ __forceinline__ float xor32(float x) { return __shfl_xor(x, 32); }
-
 // IEEE maximum (NaN-propagating): lowers to v_maximum3_f32 chains with no
 // NaN-quieting of the inputs, unlike fmaxf.
 __device__ __forceinline__ float vmax(float a, float b) { return __builtin_elementwise_maximum(a, b); }
+
+// Reductions over the lane pair (l, l ^ 32) with one v_permlane32_swap (a
+// VALU exchange of the two wavefront halves, no LDS round trip).  Both lanes
+// of a pair get the same, bitwise identical result.
+__device__ __forceinline__ float pair_max(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return vmax(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float pair_sum(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
 
 typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
 
@@ -204,6 +216,61 @@ struct Tiles {
     float* aux[2];
     float* red;
 };
+
+// Double-buffered tile schedule shared by the programs.  Slots [0, P) hold
+// the tiles that need masking (P even; a slot whose tile_of is -1 is
+// padding), slots [P, total) the mask-free tiles.  Slot i works on buffer
+// i % 2 while the copy for slot i+1 goes to the other buffer:
+//   issue(buf, t)          starts copying tile t towards buffer buf (buffer
+//                          loads straight to LDS, or loads into registers);
+//   finish(buf)            completes a register-staged copy into LDS buffer
+//                          buf, after this slot's compute (a no-op for
+//                          direct loads);
+//   compute(buf, t, MASK)  works on tile t in buffer buf.
+// buf and MASK arrive as std::integral_constant, so every buffer access
+// names a fixed LDS array and the mask-free loop holds exactly one body per
+// buffer.  A __syncthreads() closes every slot; a buffer is refilled only
+// after the barrier that follows its last read.
+typedef std::integral_constant<int, 0> Buf0;
+typedef std::integral_constant<int, 1> Buf1;
+
+template <typename TileOf, typename Issue, typename Finish, typename Compute>
+__device__ __forceinline__ void run_slots(int P, int total, TileOf tile_of, Issue issue, Finish finish,
+                                          Compute compute) {
+    auto pre = [&](auto buf, int i) {
+        if (i < total) {
+            const int t = tile_of(i);
+            if (t >= 0) issue(buf, t);
+        }
+    };
+    auto fin = [&](auto buf, int i) {
+        if (i < total && tile_of(i) >= 0) finish(buf);
+    };
+    pre(Buf0{}, 0);
+    fin(Buf0{}, 0);
+    __syncthreads();
+    for (int i = 0; i < P; i += 2) {
+        pre(Buf1{}, i + 1);
+        if (tile_of(i) >= 0) compute(Buf0{}, tile_of(i), std::true_type{});
+        fin(Buf1{}, i + 1);
+        __syncthreads();
+        pre(Buf0{}, i + 2);
+        if (tile_of(i + 1) >= 0) compute(Buf1{}, tile_of(i + 1), std::true_type{});
+        fin(Buf0{}, i + 2);
+        __syncthreads();
+    }
+    for (int i = P; i < total; i += 2) {
+        pre(Buf1{}, i + 1);
+        compute(Buf0{}, tile_of(i), std::false_type{});
+        fin(Buf1{}, i + 1);
+        __syncthreads();
+        if (i + 1 >= total) break;
+        pre(Buf0{}, i + 2);
+        compute(Buf1{}, tile_of(i + 1), std::false_type{});
+        fin(Buf0{}, i + 2);
+        __syncthreads();
+    }
+}
 
 // Row operand: eight consecutive columns col .. col+7 of tile row `row`.
 template <typename T>

@@ -1,10 +1,17 @@
 // Forward of the hybrid causal-attention layer: one launch for all heads.
 //
-// Workgroup = (batch b, head h, block of 128 queries); 4 wavefronts, each
-// owning 32 consecutive queries.  The head's flag picks the program of the
-// whole workgroup (Appendix "Mixed-head execution and numerical checks": one
-// program per batch element, head and query block, a head-state flag selects
-// the computation, outputs keep the original head order).
+// Workgroup = (batch b, head h, block of 256 queries); 4 wavefronts, each
+// owning 64 consecutive queries as two 32-query column blocks.  The head's
+// flag picks the program of the whole workgroup (Appendix "Mixed-head
+// execution and numerical checks": one program per batch element, head and
+// query block, a head-state flag selects the computation, outputs keep the
+// original head order).
+//
+// Every product streams one operand from LDS and keeps the other in
+// registers.  A 32x32x16 MFMA takes 32 cycles and its LDS operand is 1 KB, so
+// with one 32-wide register block the four SIMDs would need all of the CU's
+// LDS bandwidth (128 bytes per clock); with two register blocks per wavefront
+// every LDS fragment feeds two MFMAs and LDS runs at half that.
 //
 // Ordinary heads (Eqs. standard-head): FlashAttention-2 tiling with online
 // softmax, the scheme the paper uses for ordinary heads.  Scores are formed
@@ -38,14 +45,17 @@
 
 namespace saf {
 
-constexpr int FWD_BM = 128;  // queries per workgroup
+constexpr int FWD_BM = 256;  // queries per workgroup
+constexpr int FWD_QW = 64;   // queries per wavefront (two 32-query blocks)
 constexpr int FWD_BN = 64;   // keys per tile
 constexpr int FWD_THREADS = 256;
-constexpr float RESCALE_TAU = 8.0f;            // log2 units
-constexpr int FWD_BAND = FWD_BM + FWD_BN;      // 191 offsets used per tile
-constexpr int FWD_BAND_STRIDE = FWD_BAND + 8;  // spreads the copies over banks
+constexpr float RESCALE_TAU = 8.0f;                      // log2 units
+constexpr int FWD_BAND = FWD_BM + FWD_BN - 1;            // offsets met by one tile
+constexpr int FWD_BAND_STRIDE = (FWD_BAND + 7) / 8 * 8 + 8;  // every copy 16-byte aligned
+static_assert(FWD_THREADS / 64 * FWD_QW == FWD_BM, "wavefronts cover the query block");
 static_assert(BAND_COPIES * FWD_BAND_STRIDE * 2 <= tile_elems<bf16>() * 2, "band copies fit in a tile");
 static_assert((FWD_BN + FWD_BAND) * 4 <= tile_elems<bf16>() * 2, "exact-program a and r fit in a tile");
+static_assert(FWD_BAND <= 2 * FWD_THREADS, "two band entries per thread");
 
 struct FwdArgs {
     const void* q;
@@ -60,95 +70,119 @@ struct FwdArgs {
     float scale_log2;  // log2(e) / sqrt(d)
 };
 
-// Per-lane geometry of one workgroup.
+// Per-lane geometry of one workgroup: the wavefront's queries are q0 .. q0+63,
+// query block qb covers q0 + 32*qb .. +31, and this lane's query in it is
+// q0 + 32*qb + c.
 struct FwdLane {
-    int tid, w, lane, c, hf, m0, q0, qq, N;
+    int tid, w, lane, c, hf, m0, q0, N;
 };
 
 template <typename T>
-__device__ __forceinline__ void store_output(T* O, float* LSE, const FwdLane& L, const f32x16 (&oacc)[2],
-                                             float inv, float lse, bool write_lse) {
-    if (L.qq >= L.N) return;
-    T* orow = O + (size_t)L.qq * HEAD_DIM;
+__device__ __forceinline__ void store_rows(T* O, float* LSE, const FwdLane& L, int qq, const f32x16 (&oacc)[2],
+                                           float inv, float lse, bool write_lse) {
+    if (qq >= L.N) return;
+    T* orow = O + (size_t)qq * HEAD_DIM;
 #pragma unroll
     for (int db = 0; db < 2; ++db)
 #pragma unroll
         for (int g = 0; g < 4; ++g)
             st4<T>(orow + 32 * db + 8 * g + 4 * L.hf, oacc[db][4 * g] * inv, oacc[db][4 * g + 1] * inv,
                    oacc[db][4 * g + 2] * inv, oacc[db][4 * g + 3] * inv);
-    if (write_lse && L.hf == 0) LSE[L.qq] = lse;
+    if (write_lse && L.hf == 0) LSE[qq] = lse;
 }
 
 // ---------------------------------------------------------------------------
 // Ordinary heads
 // ---------------------------------------------------------------------------
 
+// Lazy online-softmax rescale of both query blocks: the running maxima only
+// move when a tile exceeds one of them by more than 2^RESCALE_TAU
+// (wave-uniform decision), so most tiles leave the accumulators alone and
+// probabilities stay below 2^RESCALE_TAU.
+__device__ __forceinline__ void ord_rescale(const float (&mx)[2], float (&m_run)[2], float (&l_run)[2],
+                                            f32x16 (&oacc)[2][2]) {
+    if (__any(mx[0] > m_run[0] + RESCALE_TAU || mx[1] > m_run[1] + RESCALE_TAU)) {
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb) {
+            const float m_new = fmaxf(m_run[qb], mx[qb]);
+            const float alpha = fast_exp2(m_run[qb] - m_new);
+            m_run[qb] = m_new;
+            l_run[qb] *= alpha;
+#pragma unroll
+            for (int db = 0; db < 2; ++db)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) oacc[qb][db][v] *= alpha;
+        }
+    }
+}
+
+// One 64-key tile, as two 32-key sub-blocks kb processed one after the
+// other (a scheduling barrier keeps their live ranges apart).  s[qb]: scores
+// of the sub-block's 32 keys (rows) against query block qb (columns).  MASK:
+// the tile meets the diagonal; keys after a query are hidden by one compare
+// per score (no branches, so the masked body schedules like the plain one).
+// A sub-block wholly after the wavefront's queries is skipped.
 template <typename T, bool MASK>
 __device__ __forceinline__ void ord_tile(const T* kt, const T* vt, int n0, const FwdLane& L,
-                                         const typename Vec<T>::x8 (&qf)[4], f32x16 (&oacc)[2], float& m_run,
-                                         float& l_run, float scale_log2) {
+                                         const typename Vec<T>::x8 (&qf)[2][4], f32x16 (&oacc)[2][2],
+                                         float (&m_run)[2], float (&l_run)[2], float sl2) {
     typedef typename Vec<T>::x8 frag;
-    bool act1 = true;
-    if (MASK) {
-        if (!(n0 < L.q0 + 32 && n0 < L.N)) return;  // tile wholly after this wavefront's queries
-        act1 = (n0 + 32 < L.q0 + 32) && (n0 + 32 < L.N);
-    }
-    f32x16 s[2];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
+        const int k0 = n0 + 32 * kb;
+        if (MASK && k0 > L.q0 + FWD_QW - 1) break;
+        f32x16 s[2];
 #pragma unroll
-        for (int v = 0; v < 16; ++v) s[kb][v] = 0.0f;
-        if (kb == 1 && !act1) continue;
+        for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
-        for (int dc = 0; dc < 4; ++dc) mma(s[kb], ld_row<T>(kt, 32 * kb + L.c, 16 * dc + 8 * L.hf), qf[dc]);
-    }
-    if (MASK) {
+            for (int v = 0; v < 16; ++v) s[qb][v] = 0.0f;
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-            const int k0 = n0 + 32 * kb;
-            if (kb == 1 && !act1) {
+        for (int dc = 0; dc < 4; ++dc) {
+            const frag kf = ld_row<T>(kt, 32 * kb + L.c, 16 * dc + 8 * L.hf);
 #pragma unroll
-                for (int v = 0; v < 16; ++v) s[kb][v] = -INFINITY;
-            } else if (k0 == L.q0) {  // diagonal sub-block: hide keys after the query
+            for (int qb = 0; qb < 2; ++qb) mma(s[qb], kf, qf[qb][dc]);
+        }
+        if (MASK) {
+#pragma unroll
+            for (int qb = 0; qb < 2; ++qb) {
+                const int qq = L.q0 + 32 * qb + L.c;
 #pragma unroll
                 for (int v = 0; v < 16; ++v) {
                     const int kk = k0 + 8 * (v >> 2) + 4 * L.hf + (v & 3);
-                    if (kk > L.qq) s[kb][v] = -INFINITY;
+                    s[qb][v] = kk > qq ? -INFINITY : s[qb][v];
                 }
             }
         }
-    }
-    float mx = -INFINITY;
+        float mx[2];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+        for (int qb = 0; qb < 2; ++qb) {
+            float m = vmax(s[qb][0], s[qb][1]);
 #pragma unroll
-        for (int v = 0; v < 16; v += 2) mx = vmax(vmax(mx, s[kb][v]), s[kb][v + 1]);
-    mx = vmax(mx, xor32(mx)) * scale_log2;
-    if (__any(mx > m_run + RESCALE_TAU)) {
-        const float m_new = fmaxf(m_run, mx);
-        const float alpha = fast_exp2(m_run - m_new);
-        m_run = m_new;
-        l_run *= alpha;
+            for (int v = 2; v < 16; v += 2) m = vmax(vmax(m, s[qb][v]), s[qb][v + 1]);
+            mx[qb] = pair_max(m) * sl2;
+        }
+        ord_rescale(mx, m_run, l_run, oacc);
+        frag pb[2][2];  // [qb][kc]
 #pragma unroll
-        for (int db = 0; db < 2; ++db)
+        for (int qb = 0; qb < 2; ++qb) {
+            const float neg_m = -m_run[qb];
 #pragma unroll
-            for (int v = 0; v < 16; ++v) oacc[db][v] *= alpha;
-    }
-    const float neg_m = -m_run;
+            for (int v = 0; v < 16; ++v) {
+                s[qb][v] = fast_exp2(fmaf(s[qb][v], sl2, neg_m));
+                l_run[qb] += s[qb][v];  // float32 row sum, before rounding to the operand type
+            }
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-        if (MASK && kb == 1 && !act1) continue;
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-            s[kb][v] = fast_exp2(fmaf(s[kb][v], scale_log2, neg_m));
-            l_run += s[kb][v];  // float32 row sum, before rounding to the operand type
+            for (int kc = 0; kc < 2; ++kc) pb[qb][kc] = to_operand<T>(s[qb], 8 * kc);
         }
 #pragma unroll
-        for (int kc = 0; kc < 2; ++kc) {
-            const frag pb = to_operand<T>(s[kb], 8 * kc);
+        for (int kc = 0; kc < 2; ++kc)
 #pragma unroll
-            for (int db = 0; db < 2; ++db) mma(oacc[db], ld_tile_t<true>(vt, 32 * kb + 16 * kc, 32 * db), pb);
-        }
+            for (int db = 0; db < 2; ++db) {
+                const frag vf = ld_tile_t<true>(vt, 32 * kb + 16 * kc, 32 * db);
+#pragma unroll
+                for (int qb = 0; qb < 2; ++qb) mma(oacc[qb][db], vf, pb[qb][kc]);
+            }
+        __builtin_amdgcn_sched_barrier(0);
     }
 }
 
@@ -160,45 +194,47 @@ __device__ __forceinline__ void fwd_ordinary(const Tiles<T>& sm, const FwdArgs& 
     const __amdgpu_buffer_rsrc_t rk = slice_rsrc<T>(reinterpret_cast<const T*>(p.k) + base, L.N);
     const __amdgpu_buffer_rsrc_t rv = slice_rsrc<T>(reinterpret_cast<const T*>(p.v) + base, L.N);
     typedef typename Vec<T>::x8 frag;
-    frag qf[4];
+    frag qf[2][4];
 #pragma unroll
-    for (int dc = 0; dc < 4; ++dc)
-        qf[dc] = L.qq < L.N ? ld8<T>(Q + (size_t)L.qq * HEAD_DIM + 16 * dc + 8 * L.hf) : zero8<T>();
-
-    f32x16 oacc[2];
+    for (int qb = 0; qb < 2; ++qb) {
+        const int qq = L.q0 + 32 * qb + L.c;
 #pragma unroll
-    for (int db = 0; db < 2; ++db)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) oacc[db][v] = 0.0f;
-    float m_run = NEG_BIG;
-    float l_run = 0.0f;  // this lane's share of the row sum
-
-    const int n_tiles = (min(L.m0 + FWD_BM, L.N) + FWD_BN - 1) / FWD_BN;
-    const int n_full = L.m0 / FWD_BN;  // tiles wholly below the block's first query
-    auto load = [&](T* kd, T* vd, int t) {
-        tile_load_lds<T>(kd, rk, t * FWD_BN, L.w, L.lane);
-        tile_load_lds<T>(vd, rv, t * FWD_BN, L.w, L.lane);
-    };
-    auto compute = [&](const T* kt, const T* vt, int t) {
-        if (t < n_full)
-            ord_tile<T, false>(kt, vt, t * FWD_BN, L, qf, oacc, m_run, l_run, p.scale_log2);
-        else
-            ord_tile<T, true>(kt, vt, t * FWD_BN, L, qf, oacc, m_run, l_run, p.scale_log2);
-    };
-    load(sm.t[0], sm.t[2], 0);
-    __syncthreads();
-    for (int t = 0; t < n_tiles; t += 2) {
-        if (t + 1 < n_tiles) load(sm.t[1], sm.t[3], t + 1);
-        compute(sm.t[0], sm.t[2], t);
-        __syncthreads();
-        if (t + 1 >= n_tiles) break;
-        if (t + 2 < n_tiles) load(sm.t[0], sm.t[2], t + 2);
-        compute(sm.t[1], sm.t[3], t + 1);
-        __syncthreads();
+        for (int dc = 0; dc < 4; ++dc)
+            qf[qb][dc] = qq < L.N ? ld8<T>(Q + (size_t)qq * HEAD_DIM + 16 * dc + 8 * L.hf) : zero8<T>();
     }
-    const float l_tot = l_run + xor32(l_run);
-    store_output<T>(reinterpret_cast<T*>(p.o) + base, p.lse + row_base, L, oacc, 1.0f / l_tot,
-                    (m_run + __log2f(l_tot)) * LN2, true);
+    f32x16 oacc[2][2];
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+        for (int db = 0; db < 2; ++db)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) oacc[qb][db][v] = 0.0f;
+    float m_run[2] = {NEG_BIG, NEG_BIG};
+    float l_run[2] = {0.0f, 0.0f};  // this lane's share of each row sum
+
+    // Slots: first the tiles that meet the diagonal (masked), then the tiles
+    // wholly below the block's first query (mask-free).
+    const int n_tiles = (min(L.m0 + FWD_BM, L.N) + FWD_BN - 1) / FWD_BN;
+    const int n_full = L.m0 / FWD_BN;
+    const int n_mask = n_tiles - n_full;  // 1 .. 4
+    const int P = (n_mask + 1) & ~1;
+    run_slots(
+        P, P + n_full, [&](int i) { return i < P ? (i < n_mask ? n_full + i : -1) : i - P; },
+        [&](auto buf, int t) {
+            tile_load_lds<T>(sm.t[decltype(buf)::value], rk, t * FWD_BN, L.w, L.lane);
+            tile_load_lds<T>(sm.t[2 + decltype(buf)::value], rv, t * FWD_BN, L.w, L.lane);
+        },
+        [&](auto) {},
+        [&](auto buf, int t, auto mask) {
+            ord_tile<T, decltype(mask)::value>(sm.t[decltype(buf)::value], sm.t[2 + decltype(buf)::value],
+                                               t * FWD_BN, L, qf, oacc, m_run, l_run, p.scale_log2);
+        });
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+        const float l_tot = pair_sum(l_run[qb]);
+        store_rows<T>(reinterpret_cast<T*>(p.o) + base, p.lse + row_base, L, L.q0 + 32 * qb + L.c, oacc[qb],
+                      1.0f / l_tot, (m_run[qb] + __log2f(l_tot)) * LN2, true);
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -211,17 +247,19 @@ __device__ __forceinline__ void fwd_fixed_exact(const Tiles<T>& sm, const FwdArg
     // Tiles: V in t[0]; a of the tile's keys and r over its offsets in t[1].
     T* vt = sm.t[0];
     float* as = reinterpret_cast<float*>(sm.t[1]);
-    float* rb = as + FWD_BN;
+    float* rb = as + FWD_BN;  // rb[x] = r(m0 - n0 - 63 + x)
     const T* __restrict__ V = reinterpret_cast<const T*>(p.v) + base;
     typedef typename Vec<T>::x8 frag;
     const int N = L.N;
-    f32x16 oacc[2];
+    f32x16 oacc[2][2];
 #pragma unroll
-    for (int db = 0; db < 2; ++db)
+    for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) oacc[db][v] = 0.0f;
-    float m_run = NEG_BIG;
-    float l_run = 0.0f;
+        for (int db = 0; db < 2; ++db)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) oacc[qb][db][v] = 0.0f;
+    float m_run[2] = {NEG_BIG, NEG_BIG};
+    float l_run[2] = {0.0f, 0.0f};
     const int n_end = min(L.m0 + FWD_BM, N);
     const int row = unit_row<T>(L.w, L.lane);
     for (int n0 = 0; n0 < n_end; n0 += FWD_BN) {
@@ -234,54 +272,63 @@ __device__ __forceinline__ void fwd_fixed_exact(const Tiles<T>& sm, const FwdArg
             *reinterpret_cast<u32x4*>(vt + toff<T>(row, col)) = x;
         }
         if (L.tid < FWD_BN) as[L.tid] = (n0 + L.tid < N) ? arow[n0 + L.tid] : -INFINITY;
-        for (int x = L.tid; x < FWD_BAND - 1; x += FWD_THREADS) {
-            const int delta = L.m0 - n0 - (FWD_BN - 1) + x;  // offsets m0-n0-63 .. m0-n0+127
+        for (int x = L.tid; x < FWD_BAND; x += FWD_THREADS) {
+            const int delta = L.m0 - n0 - (FWD_BN - 1) + x;
             rb[x] = (delta >= 0 && delta < N) ? rrow[delta] : -INFINITY;
         }
         __syncthreads();
-        if (!(n0 < L.q0 + 32)) continue;
-        f32x16 s[2];
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
+        for (int qb = 0; qb < 2; ++qb) {
+            const int qs = L.q0 + 32 * qb;
+            if (!(n0 <= qs + 31)) continue;  // tile wholly after this query block
+            const int ql = qs + L.c - L.m0;  // query within the block
+            f32x16 s[2];
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int kl = 32 * kb + 8 * (v >> 2) + 4 * L.hf + (v & 3);
-                const int x = (L.qq - L.m0) - kl + (FWD_BN - 1);
-                s[kb][v] = (as[kl] + rb[x]) * LOG2E;
-            }
-        float mx = -INFINITY;
+            for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
+                for (int v = 0; v < 16; ++v) {
+                    const int kl = 32 * kb + 8 * (v >> 2) + 4 * L.hf + (v & 3);
+                    s[kb][v] = (as[kl] + rb[ql - kl + (FWD_BN - 1)]) * LOG2E;
+                }
+            float mx = -INFINITY;
 #pragma unroll
-            for (int v = 0; v < 16; ++v) mx = fmaxf(mx, s[kb][v]);
-        mx = fmaxf(mx, xor32(mx));
-        const float m_new = fmaxf(m_run, mx);
-        const float alpha = fast_exp2(m_run - m_new);
-        m_run = m_new;
-        l_run *= alpha;
+            for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int db = 0; db < 2; ++db)
+                for (int v = 0; v < 16; ++v) mx = fmaxf(mx, s[kb][v]);
+            mx = pair_max(mx);
+            const float m_new = fmaxf(m_run[qb], mx);
+            const float alpha = fast_exp2(m_run[qb] - m_new);
+            m_run[qb] = m_new;
+            l_run[qb] *= alpha;
 #pragma unroll
-            for (int v = 0; v < 16; ++v) oacc[db][v] *= alpha;
+            for (int db = 0; db < 2; ++db)
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
+                for (int v = 0; v < 16; ++v) oacc[qb][db][v] *= alpha;
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const float e = fast_exp2(s[kb][v] - m_new);
-                s[kb][v] = e;
-                l_run += e;
-            }
+            for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
-            for (int kc = 0; kc < 2; ++kc) {
-                const frag pb = to_operand<T>(s[kb], 8 * kc);
+                for (int v = 0; v < 16; ++v) {
+                    const float e = fast_exp2(s[kb][v] - m_new);
+                    s[kb][v] = e;
+                    l_run[qb] += e;
+                }
 #pragma unroll
-                for (int db = 0; db < 2; ++db) mma(oacc[db], ld_tile_t<true>(vt, 32 * kb + 16 * kc, 32 * db), pb);
+                for (int kc = 0; kc < 2; ++kc) {
+                    const frag pb = to_operand<T>(s[kb], 8 * kc);
+#pragma unroll
+                    for (int db = 0; db < 2; ++db)
+                        mma(oacc[qb][db], ld_tile_t<true>(vt, 32 * kb + 16 * kc, 32 * db), pb);
+                }
             }
         }
     }
     // LSE of fixed heads comes from the normaliser pre-pass.
-    const float l_tot = l_run + xor32(l_run);
-    store_output<T>(reinterpret_cast<T*>(p.o) + base, p.lse + row_base, L, oacc, 1.0f / l_tot, 0.0f, false);
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+        const float l_tot = pair_sum(l_run[qb]);
+        store_rows<T>(reinterpret_cast<T*>(p.o) + base, p.lse + row_base, L, L.q0 + 32 * qb + L.c, oacc[qb],
+                      1.0f / l_tot, 0.0f, false);
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -292,9 +339,10 @@ template <typename T>
 struct FixStage {
     u32x4 v[tile_units<T>()];  // this lane's 16-byte units of the V tile (one row)
     float a;                   // a of that row's key
-    float rb;                  // one band entry
+    float rb[2];               // two band entries
 };
 
+// Band entry u of the tile at n0 holds offset (m0 - n0 + FWD_BM - 1) - u.
 template <typename T>
 __device__ __forceinline__ void fix_load(FixStage<T>& st, const T* V, const float* arow, const float* rrow, int n0,
                                          const FwdLane& L) {
@@ -306,9 +354,12 @@ __device__ __forceinline__ void fix_load(FixStage<T>& st, const T* V, const floa
         st.v[k] = ok ? ld_unit(V + (size_t)key * HEAD_DIM + unit_col<T>(L.w, L.lane, k)) : z;
     }
     st.a = ok ? arow[key] : -INFINITY;
-    // Band entry u holds offset (m0 - n0 + 127) - u.
-    const int delta = L.m0 - n0 + (FWD_BM - 1) - L.tid;
-    st.rb = (L.tid < FWD_BAND - 1 && delta >= 0 && delta < L.N) ? rrow[delta] : -INFINITY;
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+        const int u = L.tid + FWD_THREADS * k;
+        const int delta = L.m0 - n0 + (FWD_BM - 1) - u;
+        st.rb[k] = (u < FWD_BAND && delta >= 0 && delta < L.N) ? rrow[delta] : -INFINITY;
+    }
 }
 
 template <typename T>
@@ -319,26 +370,38 @@ __device__ __forceinline__ void fix_store(T* vs, T* band, const FixStage<T>& st,
 #pragma unroll
     for (int k = 0; k < tile_units<T>(); ++k)
         st_unit_scaled(vs + toff<T>(row, unit_col<T>(L.w, L.lane, k)), st.v[k], e);
-    if (L.tid < FWD_BAND - 1) {
-        const T b = (T)fast_exp2(fmaf(st.rb, LOG2E, -r_sh));
 #pragma unroll
-        for (int s = 0; s < BAND_COPIES; ++s)
-            if (L.tid >= s) band[s * FWD_BAND_STRIDE + L.tid - s] = b;
+    for (int k = 0; k < 2; ++k) {
+        const int u = L.tid + FWD_THREADS * k;
+        if (u < FWD_BAND) {
+            const T b = (T)fast_exp2(fmaf(st.rb[k], LOG2E, -r_sh));
+#pragma unroll
+            for (int s = 0; s < BAND_COPIES; ++s)
+                if (u >= s) band[s * FWD_BAND_STRIDE + u - s] = b;
+        }
     }
 }
 
 template <typename T, bool MASK>
-__device__ __forceinline__ void fix_tile(const T* vs, const T* band, int n0, const FwdLane& L, f32x16 (&oacc)[2]) {
+__device__ __forceinline__ void fix_tile(const T* vs, const T* band, int n0, const FwdLane& L,
+                                         f32x16 (&oacc)[2][2]) {
     typedef typename Vec<T>::x8 frag;
-    const int ql = 32 * L.w + L.c;  // query within the block
 #pragma unroll
     for (int G = 0; G < 4; ++G) {
-        if (MASK && n0 + 16 * G > L.q0 + 31) continue;  // chunk wholly after this wavefront's queries
-        const int u0 = (FWD_BM - 1) - ql + 16 * G + 8 * L.hf;
-        const int s = u0 & 7;
-        const frag b = ld8<T>(band + s * FWD_BAND_STRIDE + u0 - s);
+        if (MASK && n0 + 16 * G > L.q0 + FWD_QW - 1) continue;  // chunk wholly after this wavefront's queries
+        frag vf[2];
 #pragma unroll
-        for (int db = 0; db < 2; ++db) mma(oacc[db], ld_tile_t<false>(vs, 16 * G, 32 * db), b);
+        for (int db = 0; db < 2; ++db) vf[db] = ld_tile_t<false>(vs, 16 * G, 32 * db);
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb) {
+            if (MASK && n0 + 16 * G > L.q0 + 32 * qb + 31) continue;
+            const int ql = L.q0 - L.m0 + 32 * qb + L.c;  // query within the block
+            const int u0 = (FWD_BM - 1) - ql + 16 * G + 8 * L.hf;
+            const int s = u0 & 7;
+            const frag b = ld8<T>(band + s * FWD_BAND_STRIDE + u0 - s);
+#pragma unroll
+            for (int db = 0; db < 2; ++db) mma(oacc[qb][db], vf[db], b);
+        }
     }
 }
 
@@ -373,39 +436,35 @@ __device__ __forceinline__ void fwd_fixed(const Tiles<T>& sm, const FwdArgs& p, 
     }
     const float a_sh = A * LOG2E, r_sh = R * LOG2E;
 
-    f32x16 oacc[2];
+    f32x16 oacc[2][2];
 #pragma unroll
-    for (int db = 0; db < 2; ++db)
+    for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) oacc[db][v] = 0.0f;
+        for (int db = 0; db < 2; ++db)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) oacc[qb][db][v] = 0.0f;
 
     const int n_tiles = (m1 + FWD_BN - 1) / FWD_BN;
     const int n_full = L.m0 / FWD_BN;
-    auto compute = [&](const T* vs, const T* band, int t) {
-        if (t < n_full)
-            fix_tile<T, false>(vs, band, t * FWD_BN, L, oacc);
-        else
-            fix_tile<T, true>(vs, band, t * FWD_BN, L, oacc);
-    };
+    const int n_mask = n_tiles - n_full;
+    const int P = (n_mask + 1) & ~1;
     FixStage<T> st;
-    fix_load<T>(st, V, arow, rrow, 0, L);
-    fix_store<T>(sm.t[0], sm.t[2], st, L, a_sh, r_sh);
-    __syncthreads();
-    for (int t = 0; t < n_tiles; t += 2) {
-        if (t + 1 < n_tiles) fix_load<T>(st, V, arow, rrow, (t + 1) * FWD_BN, L);
-        compute(sm.t[0], sm.t[2], t);
-        if (t + 1 < n_tiles) fix_store<T>(sm.t[1], sm.t[3], st, L, a_sh, r_sh);
-        __syncthreads();
-        if (t + 1 >= n_tiles) break;
-        if (t + 2 < n_tiles) fix_load<T>(st, V, arow, rrow, (t + 2) * FWD_BN, L);
-        compute(sm.t[1], sm.t[3], t + 1);
-        if (t + 2 < n_tiles) fix_store<T>(sm.t[0], sm.t[2], st, L, a_sh, r_sh);
-        __syncthreads();
-    }
+    run_slots(
+        P, P + n_full, [&](int i) { return i < P ? (i < n_mask ? n_full + i : -1) : i - P; },
+        [&](auto, int t) { fix_load<T>(st, V, arow, rrow, t * FWD_BN, L); },
+        [&](auto buf) { fix_store<T>(sm.t[decltype(buf)::value], sm.t[2 + decltype(buf)::value], st, L, a_sh, r_sh); },
+        [&](auto buf, int t, auto mask) {
+            fix_tile<T, decltype(mask)::value>(sm.t[decltype(buf)::value], sm.t[2 + decltype(buf)::value],
+                                               t * FWD_BN, L, oacc);
+        });
     // 1 / Z'(i) = exp(A + R - log Z(i)), with log Z from the normaliser pre-pass.
-    const float lse = L.qq < N ? p.lse[row_base + L.qq] : 0.0f;
-    const float inv = fast_exp2((A + R - lse) * LOG2E);
-    store_output<T>(reinterpret_cast<T*>(p.o) + base, p.lse + row_base, L, oacc, inv, 0.0f, false);
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+        const int qq = L.q0 + 32 * qb + L.c;
+        const float lse = qq < N ? p.lse[row_base + qq] : 0.0f;
+        const float inv = fast_exp2((A + R - lse) * LOG2E);
+        store_rows<T>(reinterpret_cast<T*>(p.o) + base, p.lse + row_base, L, qq, oacc[qb], inv, 0.0f, false);
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -533,7 +592,7 @@ __global__ __launch_bounds__(NORM_THREADS) void fixed_lse_kernel(NormArgs p) {
 // ---------------------------------------------------------------------------
 
 template <typename T>
-__global__ __launch_bounds__(FWD_THREADS) __attribute__((amdgpu_waves_per_eu(3))) void fwd_kernel(FwdArgs p) {
+__global__ __launch_bounds__(FWD_THREADS) __attribute__((amdgpu_waves_per_eu(2))) void fwd_kernel(FwdArgs p) {
     __shared__ __attribute__((aligned(16))) T t0[tile_elems<T>()];
     __shared__ __attribute__((aligned(16))) T t1[tile_elems<T>()];
     __shared__ __attribute__((aligned(16))) T t2[tile_elems<T>()];
@@ -553,8 +612,7 @@ __global__ __launch_bounds__(FWD_THREADS) __attribute__((amdgpu_waves_per_eu(3))
     L.c = L.tid & 31;
     L.hf = (L.tid >> 5) & 1;
     L.m0 = qblk * FWD_BM;
-    L.q0 = L.m0 + 32 * L.w;
-    L.qq = L.q0 + L.c;
+    L.q0 = L.m0 + FWD_QW * L.w;
     L.N = p.N;
     const size_t base = (size_t)bh * p.N * HEAD_DIM;
     const size_t row_base = (size_t)bh * p.N;
