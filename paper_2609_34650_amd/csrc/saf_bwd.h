@@ -146,7 +146,7 @@ __device__ __forceinline__ void kv_store_zero(T* base, const KvLane& L) {
 // --- ordinary heads ---------------------------------------------------------
 
 // One query tile: qt / gt are the Q / dO tiles, rows holds LSE * log2(e)
-// (first KV_BM floats) and D (next KV_BM).
+// (first KV_BM floats) and -D (next KV_BM).
 template <typename T, bool MASK>
 __device__ __forceinline__ void kv_tile(const T* qt, const T* gt, const float* rows, int mq, const KvLane& L,
                                         const typename Vec<T>::x8 (&kf)[KV_KB][4],
@@ -171,13 +171,18 @@ __device__ __forceinline__ void kv_tile(const T* qt, const T* gt, const float* r
             }
         }
         {
+            // dP - D in one go: the accumulator starts at -D of its rows.
             frag ga[4];
 #pragma unroll
             for (int dc = 0; dc < 4; ++dc) ga[dc] = ld_row<T>(gt, 32 * qb + L.c, 16 * dc + 8 * L.hf);
 #pragma unroll
             for (int kb = 0; kb < KV_KB; ++kb) {
 #pragma unroll
-                for (int v = 0; v < 16; ++v) dp[kb][v] = 0.0f;
+                for (int g = 0; g < 4; ++g) {
+                    const f32x4 nd4 = *reinterpret_cast<const f32x4*>(rows + KV_BM + 32 * qb + 8 * g + 4 * L.hf);
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) dp[kb][4 * g + u] = nd4[u];
+                }
 #pragma unroll
                 for (int dc = 0; dc < 4; ++dc) mma(dp[kb], ga[dc], vf[kb][dc]);
             }
@@ -185,7 +190,6 @@ __device__ __forceinline__ void kv_tile(const T* qt, const T* gt, const float* r
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
             const f32x4 l4 = *reinterpret_cast<const f32x4*>(rows + 32 * qb + 8 * g + 4 * L.hf);
-            const f32x4 d4 = *reinterpret_cast<const f32x4*>(rows + KV_BM + 32 * qb + 8 * g + 4 * L.hf);
 #pragma unroll
             for (int kb = 0; kb < KV_KB; ++kb)
 #pragma unroll
@@ -197,7 +201,7 @@ __device__ __forceinline__ void kv_tile(const T* qt, const T* gt, const float* r
                         if (row < L.kw + 32 * kb + L.c) pv = 0.0f;
                     }
                     s[kb][v] = pv;
-                    dp[kb][v] = pv * (dp[kb][v] - d4[u]);
+                    dp[kb][v] = pv * dp[kb][v];
                 }
         }
 #pragma unroll
@@ -268,7 +272,7 @@ __device__ __forceinline__ void kv_ordinary(const Tiles<T>& sm, const BwdArgs& p
             if (L.tid < KV_BM) {
                 const bool ok = mq + L.tid < L.N;
                 sm.aux[b][L.tid] = ok ? LSE[mq + L.tid] * LOG2E : INFINITY;
-                sm.aux[b][KV_BM + L.tid] = ok ? Dsum[mq + L.tid] : 0.0f;
+                sm.aux[b][KV_BM + L.tid] = ok ? -Dsum[mq + L.tid] : 0.0f;
             }
         },
         [&](auto) {},

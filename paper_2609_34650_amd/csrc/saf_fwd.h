@@ -23,8 +23,10 @@
 // memory straight into column-slab LDS tiles by buffer loads (rows past N
 // arrive as zeros), double-buffered so the next tile is in flight while this
 // one is used; V^T comes from transposing LDS reads.  Tiles below the block's
-// diagonal run a mask-free body.  The running maximum is only raised when a
-// tile exceeds it by more than 2^8, so most tiles skip the accumulator rescale.
+// diagonal run a mask-free body.  Probabilities are formed against the
+// running maximum as it stands; only when a sub-block's partial sum shows
+// that its scores exceed that maximum by a wide margin is the maximum
+// recomputed and the accumulator rescaled, so most tiles do neither.
 //
 // Fixed heads (Eq. compact-prior): P(i,j) = exp(a[j] + r[i-j]) / Z(i) factors
 // as ea(j) * er(i-j) / Z'(i) with ea = exp(a - A*), er = exp(r - R*) and
@@ -49,7 +51,12 @@ constexpr int FWD_BM = 256;  // queries per workgroup
 constexpr int FWD_QW = 64;   // queries per wavefront (two 32-query blocks)
 constexpr int FWD_BN = 64;   // keys per tile
 constexpr int FWD_THREADS = 256;
-constexpr float RESCALE_TAU = 8.0f;                      // log2 units
+// A sub-block's probabilities are taken against the running maximum as it
+// stands; the maximum is only raised (and the accumulators rescaled) when a
+// lane's partial sum over the sub-block exceeds this bound, so no
+// probability exceeds it either.  Values up to 2^20 are harmless in float32
+// sums and in bf16 operands (same exponent range).
+constexpr float RESCALE_SUM = 1048576.0f;
 constexpr int FWD_BAND = FWD_BM + FWD_BN - 1;            // offsets met by one tile
 constexpr int FWD_BAND_STRIDE = (FWD_BAND + 7) / 8 * 8 + 8;  // every copy 16-byte aligned
 static_assert(FWD_THREADS / 64 * FWD_QW == FWD_BM, "wavefronts cover the query block");
@@ -95,24 +102,38 @@ __device__ __forceinline__ void store_rows(T* O, float* LSE, const FwdLane& L, i
 // Ordinary heads
 // ---------------------------------------------------------------------------
 
-// Lazy online-softmax rescale of both query blocks: the running maxima only
-// move when a tile exceeds one of them by more than 2^RESCALE_TAU
-// (wave-uniform decision), so most tiles leave the accumulators alone and
-// probabilities stay below 2^RESCALE_TAU.
+// Raise the running maxima of both query blocks to at least mx (log2
+// units) and rescale the row sums and accumulators to match.
 __device__ __forceinline__ void ord_rescale(const float (&mx)[2], float (&m_run)[2], float (&l_run)[2],
                                             f32x16 (&oacc)[2][2]) {
-    if (__any(mx[0] > m_run[0] + RESCALE_TAU || mx[1] > m_run[1] + RESCALE_TAU)) {
 #pragma unroll
-        for (int qb = 0; qb < 2; ++qb) {
-            const float m_new = fmaxf(m_run[qb], mx[qb]);
-            const float alpha = fast_exp2(m_run[qb] - m_new);
-            m_run[qb] = m_new;
-            l_run[qb] *= alpha;
+    for (int qb = 0; qb < 2; ++qb) {
+        const float m_new = fmaxf(m_run[qb], mx[qb]);
+        const float alpha = fast_exp2(m_run[qb] - m_new);
+        m_run[qb] = m_new;
+        l_run[qb] *= alpha;
 #pragma unroll
-            for (int db = 0; db < 2; ++db)
+        for (int db = 0; db < 2; ++db)
 #pragma unroll
-                for (int v = 0; v < 16; ++v) oacc[qb][db][v] *= alpha;
+            for (int v = 0; v < 16; ++v) oacc[qb][db][v] *= alpha;
+    }
+}
+
+// exp2(s * sl2 - m) for both query blocks, with this lane's partial sums.
+__device__ __forceinline__ void ord_probs(const f32x16 (&s)[2], const float (&m_run)[2], float sl2, f32x16 (&pr)[2],
+                                          float (&ts)[2]) {
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+        const float neg_m = -m_run[qb];
+        float t0 = 0.0f, t1 = 0.0f;
+#pragma unroll
+        for (int v = 0; v < 16; v += 2) {
+            pr[qb][v] = fast_exp2(fmaf(s[qb][v], sl2, neg_m));
+            pr[qb][v + 1] = fast_exp2(fmaf(s[qb][v + 1], sl2, neg_m));
+            t0 += pr[qb][v];
+            t1 += pr[qb][v + 1];
         }
+        ts[qb] = t0 + t1;
     }
 }
 
@@ -153,26 +174,31 @@ __device__ __forceinline__ void ord_tile(const T* kt, const T* vt, int n0, const
                 }
             }
         }
-        float mx[2];
+        // Probabilities against the running maximum; the maximum itself is
+        // only recomputed when some lane's partial sum shows that this
+        // sub-block exceeds it by a wide margin (or on the first visible
+        // sub-block, where the maximum is still NEG_BIG and the sums are inf).
+        f32x16 pr[2];
+        float ts[2];
+        ord_probs(s, m_run, sl2, pr, ts);
+        if (__any(ts[0] > RESCALE_SUM || ts[1] > RESCALE_SUM)) {
+            float mx[2];
 #pragma unroll
-        for (int qb = 0; qb < 2; ++qb) {
-            float m = vmax(s[qb][0], s[qb][1]);
+            for (int qb = 0; qb < 2; ++qb) {
+                float m = vmax(s[qb][0], s[qb][1]);
 #pragma unroll
-            for (int v = 2; v < 16; v += 2) m = vmax(vmax(m, s[qb][v]), s[qb][v + 1]);
-            mx[qb] = pair_max(m) * sl2;
+                for (int v = 2; v < 16; v += 2) m = vmax(vmax(m, s[qb][v]), s[qb][v + 1]);
+                mx[qb] = pair_max(m) * sl2;
+            }
+            ord_rescale(mx, m_run, l_run, oacc);
+            ord_probs(s, m_run, sl2, pr, ts);
         }
-        ord_rescale(mx, m_run, l_run, oacc);
         frag pb[2][2];  // [qb][kc]
 #pragma unroll
         for (int qb = 0; qb < 2; ++qb) {
-            const float neg_m = -m_run[qb];
+            l_run[qb] += ts[qb];  // float32 row sum, before rounding to the operand type
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                s[qb][v] = fast_exp2(fmaf(s[qb][v], sl2, neg_m));
-                l_run[qb] += s[qb][v];  // float32 row sum, before rounding to the operand type
-            }
-#pragma unroll
-            for (int kc = 0; kc < 2; ++kc) pb[qb][kc] = to_operand<T>(s[qb], 8 * kc);
+            for (int kc = 0; kc < 2; ++kc) pb[qb][kc] = to_operand<T>(pr[qb], 8 * kc);
         }
 #pragma unroll
         for (int kc = 0; kc < 2; ++kc)
