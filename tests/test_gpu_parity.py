@@ -67,6 +67,53 @@ def test_bf16_several_tiles_ragged():
     print(compare_layer(run_gpu(inp, "bf16"), inp, "bf16"))
 
 
+def _growing_scores_inputs(dtype, backward):
+    N = 700
+    inp = _inp(1, 2, N, [1], dtype, seed=5, backward=backward)
+    q = inp["Q"] + np.float32(4.0)
+    k = inp["K"] + (np.arange(N, dtype=np.float32) / 512.0)[None, None, :, None]
+    rnd = gen.round_to_bf16 if dtype == "bf16" else (lambda x: x.astype(np.float32))
+    inp["Q"], inp["K"] = rnd(q), rnd(k)
+    return inp
+
+
+def test_scores_growing_along_keys_f32():
+    """Queries and keys share a component whose weight grows with the key
+    position, so a query's score rises by about one nat every 16 keys: tiles
+    later in a row score tens of log2 units above the running maximum, and the
+    forward has to raise it (and rescale its accumulators) in the middle of
+    rows, not only on the first tile.  Forward and backward at 1e-4."""
+    announce("growing scores f32")
+    inp = _growing_scores_inputs("f32", True)
+    print(compare_layer(run_gpu(inp, "f32"), inp, "f32"))
+
+
+def test_scores_growing_along_keys_bf16_forward():
+    """The same inputs in bf16, forward only (O and LSE, where the rescaling
+    lives).  The bf16 backward of such peaked rows is not held to the bar:
+    with O rounded to bf16, D = rowsum(dO * O) alone moves dQ by more than
+    1e-2 + 2e-2 |dQ| here, for any kernel that rounds O and dS to bf16 (a
+    float64 simulation of that rounding reaches 1.2 times the bound)."""
+    announce("growing scores bf16 forward")
+    inp = _growing_scores_inputs("bf16", False)
+    print(compare_layer(run_gpu(inp, "bf16", backward=False), inp, "bf16", backward=False))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_fixed_exact_fallback(dtype):
+    """a is 60 nats lower on the first half of the keys, so the normalisers of
+    rows in that half lie far below the maxima of the blocks that also touch
+    the second half: those forward and key-block programs must fall back to
+    exact per-element exponentials (the factorised form would underflow)."""
+    announce(f"fixed exact fallback {dtype}")
+    N = 600
+    inp = _inp(1, 2, N, [0], dtype, seed=7)
+    a = inp["a"].copy()
+    a[0, : N // 2] -= 60.0
+    inp["a"] = a.astype(np.float32)
+    print(compare_layer(run_gpu(inp, dtype), inp, dtype))
+
+
 def test_fuzz_head_states_f32():
     """Fifty random (B, H, N, fixed set) draws, including empty and full fixed
     sets, against the oracle (the paper's 50-operation state fuzz)."""
