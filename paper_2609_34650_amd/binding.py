@@ -1,4 +1,5 @@
-"""Thin ctypes binding to libsaf.so (C ABI in ``include/saf.h``).
+"""Thin ctypes binding to libsaf.so (C ABI in ``include/saf.h`` and
+``include/saf_calib.h``).
 
 Only argument marshalling happens here: tensor checks, pointers, the head
 flags and the caller's current HIP stream.  Every step of the layer runs in
@@ -42,6 +43,9 @@ EXPORTS = (
     "saf_hybrid_attn_bwd",
     "saf_hybrid_attn_bwd_stage",
     "saf_status_str",
+    "saf_calib_accumulate",
+    "saf_calib_finalize_workspace_bytes",
+    "saf_calib_finalize",
 )
 
 
@@ -78,6 +82,12 @@ def load() -> ctypes.CDLL:
     lib.saf_hybrid_attn_bwd.argtypes = bwd_args
     lib.saf_hybrid_attn_bwd_stage.restype = ctypes.c_int
     lib.saf_hybrid_attn_bwd_stage.argtypes = [i] + bwd_args
+    lib.saf_calib_accumulate.restype = ctypes.c_int
+    lib.saf_calib_accumulate.argtypes = [i, vp, vp, vp, i, i, i, i, i, vp, vp, vp, vp]
+    lib.saf_calib_finalize_workspace_bytes.restype = ctypes.c_size_t
+    lib.saf_calib_finalize_workspace_bytes.argtypes = [i, i]
+    lib.saf_calib_finalize.restype = ctypes.c_int
+    lib.saf_calib_finalize.argtypes = [i, i, i, vp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
     lib.saf_status_str.restype = ctypes.c_char_p
     lib.saf_status_str.argtypes = [i]
     del f32p
@@ -255,3 +265,63 @@ class HybridAttention(torch.autograd.Function):
         Q, K, V, O, LSE, a, r = ctx.saved_tensors
         dQ, dK, dV = saf_hybrid_attn_bwd(Q, K, V, O, dO.contiguous(), LSE, ctx.flags, a, r)
         return dQ, dK, dV, None, None, None
+
+
+# ---------------------------------------------------------------------------
+# Calibration statistics
+# ---------------------------------------------------------------------------
+
+class CalibState:
+    """Running calibration statistics of one layer on one device: ``mean`` and
+    ``m2`` ``[H, T, T]`` float32, ``ent`` ``[H]`` float64, and the number of
+    inputs folded in so far."""
+
+    def __init__(self, H: int, T: int, device):
+        self.mean = torch.empty((H, T, T), dtype=torch.float32, device=device)
+        self.m2 = torch.empty((H, T, T), dtype=torch.float32, device=device)
+        self.ent = torch.empty((H,), dtype=torch.float64, device=device)
+        self.n_seen = 0
+
+
+def saf_calib_accumulate(Q: torch.Tensor, K: torch.Tensor, LSE: torch.Tensor, state: CalibState) -> CalibState:
+    """Fold one micro-batch (``Q, K`` ``[B, H, T, d]``, ``LSE`` ``[B, H, T]``
+    from the all-ordinary forward) into ``state`` on the current stream."""
+    lib = load()
+    B, H, T, d = Q.shape
+    dev = Q.device
+    _check_act("Q", Q, Q.shape, Q.dtype, dev)
+    _check_act("K", K, Q.shape, Q.dtype, dev)
+    _check_act("LSE", LSE, (B, H, T), torch.float32, dev)
+    _check_act("mean", state.mean, (H, T, T), torch.float32, dev)
+    _check_act("m2", state.m2, (H, T, T), torch.float32, dev)
+    _check_act("ent", state.ent, (H,), torch.float64, dev)
+    code = lib.saf_calib_accumulate(_dtype_code(Q), _ptr(Q), _ptr(K), _ptr(LSE), B, H, T, d, state.n_seen,
+                                    _ptr(state.mean), _ptr(state.m2), _ptr(state.ent), _stream(dev))
+    _raise(code, "saf_calib_accumulate")
+    state.n_seen += B
+    return state
+
+
+def saf_calib_finalize_workspace_bytes(H: int, T: int) -> int:
+    return int(load().saf_calib_finalize_workspace_bytes(H, T))
+
+
+def saf_calib_finalize(state: CalibState, workspace: Optional[torch.Tensor] = None):
+    """Scores and marginals of ``state`` on the current stream.  Returns a dict
+    with ``A_mean`` (the state's ``mean``), ``eta_abs``, ``eta_rel`` ``[H, T]``
+    and ``s_var``, ``s_kl`` ``[H]`` (float32)."""
+    lib = load()
+    H, T, _ = state.mean.shape
+    dev = state.mean.device
+    out = {name: torch.empty(shape, dtype=torch.float32, device=dev)
+           for name, shape in (("eta_abs", (H, T)), ("eta_rel", (H, T)), ("s_var", (H,)), ("s_kl", (H,)))}
+    nbytes = saf_calib_finalize_workspace_bytes(H, T)
+    if workspace is None:
+        workspace = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=dev)
+    code = lib.saf_calib_finalize(H, T, state.n_seen, _ptr(state.mean), _ptr(state.m2), _ptr(state.ent),
+                                  _ptr(out["eta_abs"]), _ptr(out["eta_rel"]), _ptr(out["s_var"]),
+                                  _ptr(out["s_kl"]), workspace.data_ptr(),
+                                  workspace.numel() * workspace.element_size(), _stream(dev))
+    _raise(code, "saf_calib_finalize")
+    out["A_mean"] = state.mean
+    return out

@@ -128,3 +128,56 @@ def make_inputs(B: int, H: int, N: int, d: int, fixed: Sequence[int], dtype: str
 def workload_inputs(w: Workload, seed: int = SEED) -> dict:
     fixed = list(w.fixed) if w.fixed is not None else fixed_heads(w.H, w.n_fixed, seed, w.stream_id)
     return make_inputs(w.B, w.H, w.N, w.d, fixed, w.dtype, seed, w.stream_id, w.backward)
+
+
+# ---------------------------------------------------------------------------
+# Calibration inputs (the statistics pass that precedes head replacement)
+# ---------------------------------------------------------------------------
+
+@dataclass(frozen=True)
+class CalibWorkload:
+    """Queries and keys of one layer on ``n_cal`` calibration inputs of length
+    ``T``, folded in micro-batches of ``micro`` inputs."""
+    name: str
+    n_cal: int
+    micro: int
+    H: int
+    T: int
+    d: int
+    dtype: str
+    stream_id: int = 0
+
+
+# The 124M-style layer at 4K: 32 calibration sequences in micro-batches of two.
+CALIB_WORKLOADS: Dict[str, CalibWorkload] = {
+    "calib124m_4k": CalibWorkload("calib124m_4k", 32, 2, 12, 4096, 64, "bf16", stream_id=11),
+}
+
+# Calibration queries and keys share a per-head component across inputs, so
+# the attention patterns have an input-independent part and an input-dependent
+# part: X_n = SHARED * X_common + NOISE * eps_n with SHARED^2 + NOISE^2 = 1.
+CALIB_SHARED = 0.8
+CALIB_NOISE = 0.6
+
+
+def calib_inputs(n_cal: int, H: int, T: int, d: int, dtype: str, seed: int = SEED, stream_id: int = 0,
+                 first: int = 0, count: Optional[int] = None) -> dict:
+    """Draw ``Q, K`` ``[count, H, T, d]`` float32 (bf16-representable for
+    ``dtype == "bf16"``) for calibration inputs ``first .. first+count-1`` of
+    ``n_cal``.  Input n always gets the same values, whichever slice asks."""
+    if dtype not in ("f32", "bf16"):
+        raise ValueError(dtype)
+    count = n_cal - first if count is None else count
+    if first < 0 or count < 0 or first + count > n_cal:
+        raise ValueError("input range outside the calibration set")
+    gq, gk = _streams(seed, stream_id, 2)
+    common_q = gq.standard_normal((H, T, d), dtype=np.float32)
+    common_k = gk.standard_normal((H, T, d), dtype=np.float32)
+    out = {}
+    for name, common, sid in (("Q", common_q, 0), ("K", common_k, 1)):
+        x = np.empty((count, H, T, d), dtype=np.float32)
+        for i in range(count):
+            g = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, stream_id, 100 + sid, first + i])))
+            x[i] = CALIB_SHARED * common + CALIB_NOISE * g.standard_normal((H, T, d), dtype=np.float32)
+        out[name] = round_to_bf16(x) if dtype == "bf16" else x
+    return out

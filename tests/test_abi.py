@@ -1,5 +1,5 @@
 """C ABI checks that need no GPU: libsaf.so loads, exports exactly the entry
-points include/saf.h declares, and rejects bad arguments with the documented
+points include/*.h declare, and rejects bad arguments with the documented
 status before anything is launched.  Device pointers here are fake (aligned
 integers that are never dereferenced: every call below fails validation)."""
 
@@ -12,7 +12,8 @@ import numpy as np
 import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "saf.h")
+HEADERS = sorted(os.path.join(ROOT, "include", f) for f in os.listdir(os.path.join(ROOT, "include"))
+                 if f.endswith(".h"))
 
 
 @pytest.fixture(scope="module")
@@ -22,7 +23,7 @@ def lib():
 
 
 def _declared():
-    text = open(HEADER).read()
+    text = "".join(open(h).read() for h in HEADERS)
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"\b(saf_\w+)\s*\(", text)))
 
@@ -123,3 +124,51 @@ def test_status_strings(lib):
     for code in range(8):
         assert binding.status_str(code) and binding.status_str(code) != "unknown status"
     assert binding.status_str(99) == "unknown status"
+
+
+# ---------------------------------------------------------------------------
+# Calibration statistics (include/saf_calib.h)
+# ---------------------------------------------------------------------------
+
+def _acc(lib, dt=1, Q=FAKE, K=FAKE, LSE=FAKE, B=2, H=3, T=16, d=64, n_seen=0, mean=FAKE, m2=FAKE, ent=FAKE):
+    return lib.saf_calib_accumulate(dt, Q, K, LSE, B, H, T, d, n_seen, mean, m2, ent, None)
+
+
+def _fin(lib, H=3, T=16, n=4, mean=FAKE, m2=FAKE, ent=FAKE, ea=FAKE, er=FAKE, sv=FAKE, sk=FAKE, ws=FAKE,
+         ws_bytes=None):
+    if ws_bytes is None:
+        ws_bytes = lib.saf_calib_finalize_workspace_bytes(max(H, 1), max(T, 1))
+    return lib.saf_calib_finalize(H, T, n, mean, m2, ent, ea, er, sv, sk, ws, ws_bytes, None)
+
+
+def test_calib_accumulate_rejects_bad_arguments(lib):
+    assert _acc(lib, dt=7) == 3
+    assert _acc(lib, d=128) == 3
+    assert _acc(lib, H=65) == 3
+    assert _acc(lib, B=-1) == 2
+    assert _acc(lib, n_seen=-1) == 2
+    assert _acc(lib, T=(1 << 16) + 1) == 2
+    assert _acc(lib, n_seen=(1 << 24) - 1, B=2) == 2
+    assert _acc(lib, Q=None) == 1
+    assert _acc(lib, LSE=None) == 1
+    assert _acc(lib, ent=None) == 1
+    assert _acc(lib, mean=FAKE + 4) == 6
+    assert _acc(lib, ent=FAKE + 4) == 6
+    # Empty problems launch nothing.
+    assert _acc(lib, B=0, Q=None, K=None, LSE=None, mean=None, m2=None, ent=None) == 0
+    assert _acc(lib, T=0, Q=None, K=None, LSE=None, mean=None, m2=None, ent=None) == 0
+
+
+def test_calib_finalize_rejects_bad_arguments(lib):
+    assert lib.saf_calib_finalize_workspace_bytes(3, 16) % 256 == 0
+    assert lib.saf_calib_finalize_workspace_bytes(3, 16) >= 3 * 2 * 8
+    assert lib.saf_calib_finalize_workspace_bytes(0, 16) == 0
+    assert lib.saf_calib_finalize_workspace_bytes(65, 16) == 0
+    assert _fin(lib, n=0) == 2
+    assert _fin(lib, H=65) == 3
+    assert _fin(lib, T=-1) == 2
+    assert _fin(lib, mean=None) == 1
+    assert _fin(lib, sk=None) == 1
+    assert _fin(lib, ws=FAKE + 16) == 6
+    assert _fin(lib, ws_bytes=8) == 2
+    assert _fin(lib, H=0, mean=None) == 0
