@@ -23,6 +23,15 @@ Prints one JSON line with:
 FLOP rule: one causal N x N x d contraction counts 2*d*N(N+1)/2.  An ordinary
 head counts 7 (2 forward, 5 backward: S recompute, dP, dV, dK, dQ); a fixed
 head counts 2 (P V forward, P^T dO backward).
+
+``--calib`` times the calibration statistics instead (include/saf_calib.h):
+one step = folding 32 calibration inputs of one 12-head layer (T = 4096) into
+the running statistics (mean attention, scalar sums; no per-entry squared
+deviations) in micro-batches of two, then the finalisation.  The
+queries, keys and forward LSE of all inputs are resident in HBM before the
+timed region (the model's forward produces them anyway).  Its roofline is the
+accumulation launch's algorithmic HBM bytes (state read and write, Q, K, LSE)
+over its duration.
 """
 
 from __future__ import annotations
@@ -79,15 +88,22 @@ def stage_bytes(B: int, H: int, N: int, d: int, n_fixed: int, elem: int):
     }
 
 
-def kernel_source_digest() -> str:
-    """sha256 over the HIP sources (headers and .hip files, sorted by name)."""
+# Device sources behind each workload's kernels: a change to any of them
+# makes the committed counter summary of that workload stale.
+KERNEL_SOURCES = {
+    "layer": ("saf_common.h", "saf_fwd.h", "saf_bwd.h"),
+    "calib": ("saf_common.h", "saf_calib_kernels.h"),
+}
+
+
+def kernel_source_digest(group: str = "layer") -> str:
+    """sha256 over the device sources of one kernel group (in the listed order)."""
     csrc = os.path.join(ROOT, "paper_2609_34650_amd", "csrc")
     h = hashlib.sha256()
-    for name in sorted(os.listdir(csrc)):
-        if name.endswith((".h", ".hip")):
-            h.update(name.encode())
-            with open(os.path.join(csrc, name), "rb") as f:
-                h.update(f.read())
+    for name in KERNEL_SOURCES[group]:
+        h.update(name.encode())
+        with open(os.path.join(csrc, name), "rb") as f:
+            h.update(f.read())
     return h.hexdigest()
 
 
@@ -107,7 +123,8 @@ def measured_traffic(workload: str, stage: str):
                 digest = parts[1]
             elif len(parts) >= 3 and parts[0] == "traffic_bytes:" and parts[1] == stage:
                 found = float(parts[2])
-    if digest != kernel_source_digest():
+    group = "calib" if workload in gen.CALIB_WORKLOADS else "layer"
+    if digest != kernel_source_digest(group):
         return None
     return found
 
@@ -124,6 +141,8 @@ def parse():
                     help="(batch, head) slices the oracle baseline runs (0: all, at most eight per worker)")
     ap.add_argument("--compare-ordinary", dest="compare", action="store_true", default=True)
     ap.add_argument("--no-compare-ordinary", dest="compare", action="store_false")
+    ap.add_argument("--calib", action="store_true",
+                    help="time the calibration statistics (workload calib124m_4k) instead of the layer")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run one plain 64 MiB read + 64 MiB write elementwise kernel (torch.neg) before the "
                          "timed steps: a known-size reference for HBM byte counters in a profiler run")
@@ -226,6 +245,139 @@ def cpu_baseline(inp, w, slices_req):
     }
 
 
+# ---------------------------------------------------------------------------
+# Calibration statistics
+# ---------------------------------------------------------------------------
+
+CALIB_METRIC = "calibration statistics ms/layer (32 inputs, T=4096, 12 heads, micro-batches of 2)"
+
+
+def calib_call_bytes(B: int, H: int, T: int, d: int, elem: int, first: bool) -> float:
+    """Algorithmic HBM bytes of one accumulation call without per-entry
+    squared deviations: Q, K and LSE of its inputs, plus the float32 mean:
+    the first call writes the whole [H, T, T] plane, later calls read and
+    write its lower triangle."""
+    inputs = 2.0 * B * H * T * d * elem + 4.0 * B * H * T
+    state = 4.0 * H * T * T if first else 2 * 4.0 * H * T * (T + 1) / 2
+    return inputs + state
+
+
+def calib_cpu_baseline(inp, w, rows_per_head: int):
+    """The calibration oracle (as it stands) on an evenly spaced sample of
+    query rows of every head, one head per process; scaled to the layer."""
+    import multiprocessing as mp
+    try:
+        from threadpoolctl import threadpool_limits
+    except ImportError:  # pragma: no cover
+        threadpool_limits = None
+    rows = np.linspace(0, w.T - 1, rows_per_head).round().astype(np.int64)
+    workers = max(1, min(MAX_HOST_WORKERS, len(os.sched_getaffinity(0)), w.H))
+    jobs = [(np.ascontiguousarray(inp["Q"][:, h:h + 1]), np.ascontiguousarray(inp["K"][:, h:h + 1]), rows)
+            for h in range(w.H)]
+    ctx = threadpool_limits(limits=1) if threadpool_limits else None
+    t0 = time.perf_counter()
+    try:
+        with mp.get_context("fork").Pool(workers) as pool:
+            pool.map(_calib_job, jobs, chunksize=1)
+    finally:
+        if ctx is not None and hasattr(ctx, "unregister"):
+            ctx.unregister()
+    wall = time.perf_counter() - t0
+    return {
+        "value": round(wall * 1e3 * w.T / len(rows), 1),
+        "unit": "ms/layer",
+        "cores": workers,
+        "kind": "oracle",
+        "sample": (f"{len(rows)} of {w.T} query rows of each of the {w.H} heads, all {w.n_cal} inputs, fp64 "
+                   f"dense, {wall:.1f} s wall on {workers} processes, scaled by {w.T}/{len(rows)}"),
+    }
+
+
+def _calib_job(job):
+    from oracle import calib_oracle as co
+    q, k, rows = job
+    co.calibration_stats(q, k, rows=rows)
+    return rows.shape[0]
+
+
+def main_calib(args, torch):
+    from paper_2609_34650_amd import binding
+    w = gen.CALIB_WORKLOADS["calib124m_4k"]
+    inp = gen.calib_inputs(w.n_cal, w.H, w.T, w.d, w.dtype, stream_id=w.stream_id)
+    dev = torch.device("cuda", 0)
+    tdt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    Q = torch.from_numpy(inp["Q"]).to(dev).to(tdt)
+    K = torch.from_numpy(inp["K"]).to(dev).to(tdt)
+    flags = np.zeros(w.H, np.uint8)
+    LSE = torch.empty((w.n_cal, w.H, w.T), dtype=torch.float32, device=dev)
+    O = torch.empty_like(Q)
+    binding.saf_hybrid_attn_fwd(Q, K, Q, flags, O=O, LSE=LSE)
+    del O
+    state = binding.CalibState(w.H, w.T, dev)
+    ws = torch.empty(max(binding.saf_calib_finalize_workspace_bytes(w.H, w.T), 256), dtype=torch.uint8, device=dev)
+    n_calls = w.n_cal // w.micro
+
+    def step(evs=None):
+        state.n_seen = 0
+        for c in range(n_calls):
+            sl = slice(c * w.micro, (c + 1) * w.micro)
+            if evs is not None:
+                evs[c].record()
+            binding.saf_calib_accumulate(Q[sl], K[sl], LSE[sl], state)
+        if evs is not None:
+            evs[n_calls].record()
+        out = binding.saf_calib_finalize(state, ws)
+        if evs is not None:
+            evs[n_calls + 1].record()
+        return out
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    steps = args.steps
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(n_calls + 2)] for _ in range(steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s_ in range(steps):
+        step(evs[s_])
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    first = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    later = float(np.mean([e[c].elapsed_time(e[c + 1]) for e in evs for c in range(1, n_calls)]))
+    fin = float(np.mean([e[n_calls].elapsed_time(e[n_calls + 1]) for e in evs]))
+    elem = 2 if w.dtype == "bf16" else 4
+    b_first = calib_call_bytes(w.micro, w.H, w.T, w.d, elem, True)
+    b_later = calib_call_bytes(w.micro, w.H, w.T, w.d, elem, False)
+    gbs = b_later / (later * 1e-3) / 1e9
+    result = {
+        "metric": CALIB_METRIC,
+        "value": round(ms, 4),
+        "unit": "ms/layer",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": f"{w.name}: calibration statistics of one layer", "n_cal": w.n_cal,
+                   "micro_batch": w.micro, "H": w.H, "T": w.T, "d": w.d, "parallelism": "single GPU"},
+        "kernels": {
+            "calib_accumulate_first": {"ms": round(first, 4), "min_hbm_gbs": round(b_first / (first * 1e-3) / 1e9, 1)},
+            "calib_accumulate": {"ms": round(later, 4), "min_hbm_gbs": round(gbs, 1)},
+            "calib_finalize": {"ms": round(fin, 4)},
+        },
+        "roofline": {"bound": "hbm", "kernel": "calib_accumulate", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
+                     "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
+                     "traffic": measured_traffic(w.name, "calib_accumulate")},
+    }
+    if args.cpu_baseline:
+        result["cpu_baseline"] = calib_cpu_baseline(inp, w, 128)
+    print(json.dumps(result), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -238,6 +390,17 @@ def main():
         sys.exit(1)
     from paper_2609_34650_amd import binding
     binding.load()
+    if args.copy_calibration:
+        # A known-size copy for scaling the HBM counters: 64 MiB read, 64 MiB written.
+        src = torch.empty(COPY_CALIBRATION_BYTES // 4, dtype=torch.float32, device="cuda").fill_(1.0)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
+    if args.calib:
+        main_calib(args, torch)
+        return
 
     w = gen.WORKLOADS[args.workload]
     inp = gen.workload_inputs(w)
@@ -246,14 +409,6 @@ def main():
     hybrid_flags = inp["is_fixed"].copy()
     ordinary_flags = np.zeros_like(hybrid_flags)
     layer = Layer(torch, inp, w.dtype, w.backward)
-
-    if args.copy_calibration:
-        src = torch.empty(COPY_CALIBRATION_BYTES // 4, dtype=torch.float32, device="cuda").fill_(1.0)
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        torch.neg(src, out=dst)
-        torch.cuda.synchronize()
-        del src, dst
 
     for _ in range(args.warmup):
         layer.step(hybrid_flags)

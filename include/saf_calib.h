@@ -28,12 +28,17 @@
  * key j, offset delta = i - j.
  *
  * Running state of one layer (caller-owned DEVICE buffers):
- *   mean : [H, T, T] float32, row-major (query, key): the mean of A over the
- *          inputs folded in so far; entries above the diagonal are 0.
- *   m2   : [H, T, T] float32: per entry, the sum over those inputs of the
- *          squared deviation from their mean (Welford's running form).
- *   ent  : [H] float64: sum over those inputs and all query rows of
- *          sum_j A(i, j) ln A(i, j) (0 ln 0 = 0).
+ *   mean  : [H, T, T] float32, row-major (query, key): the mean of A over the
+ *           inputs folded in so far; entries above the diagonal are 0.
+ *   m2    : optional [H, T, T] float32: per entry, the sum over those inputs
+ *           of the squared deviation from their mean (the per-entry sample
+ *           variance is m2 / (n - 1)).  Pass NULL to skip it: the scores do
+ *           not need it, and keeping it doubles the memory traffic.
+ *   stats : saf_calib_stats_bytes(H, T) bytes of float64 partial sums, per
+ *           head and 128 x 128 tile of the attention matrix: the sum over
+ *           those inputs of A ln A over the tile (0 ln 0 = 0) and the tile's
+ *           sum of squared deviations.  Its layout is private to the library;
+ *           saf_calib_finalize reads it.
  * Limits: d == 64, 1 <= H <= 64, T <= 65536, n_seen + B <= 2^24.
  */
 #ifndef SAF_CALIB_H
@@ -53,18 +58,25 @@ extern "C" {
  *           same attention, as saf_hybrid_attn_fwd writes them with every head
  *           ordinary.  The weights are recomputed as exp(S - LSE).
  *   n_seen: inputs already folded into the state.  0 starts a new state:
- *           mean, m2 and ent are then written in full and their previous
- *           contents ignored.
- *   mean, m2 (16-byte aligned), ent (8-byte aligned): the state, updated.
- * Each micro-batch costs one launch (two when n_seen == 0: ent is zeroed
- * first).  ent is accumulated with float64 atomic adds, so its last bits may
- * depend on the order in which workgroups finish.
+ *           mean, m2 (if kept) and stats are then written in full and their
+ *           previous contents ignored.
+ *   mean, m2 (16-byte aligned; m2 may be NULL), stats (8-byte aligned): the
+ *           state, updated.  Whether m2 is kept must not change between the
+ *           calls of one state.
+ * Per entry the mean follows Welford's recurrence over the inputs in order,
+ * so the mean after several calls is bitwise the mean after one call over the
+ * same inputs.  One launch per micro-batch; no atomics, so the state does not
+ * depend on the order in which workgroups run.
  */
 saf_status_t saf_calib_accumulate(saf_dtype_t dt,
                                   const void* Q, const void* K, const float* LSE,
                                   int B, int H, int T, int d, int n_seen,
-                                  float* mean, float* m2, double* ent,
+                                  float* mean, float* m2, double* stats,
                                   hipStream_t stream);
+
+/* Bytes of the stats buffer of a state (a multiple of 256); 0 for an invalid
+ * problem. */
+size_t saf_calib_stats_bytes(int H, int T);
 
 /* Bytes of device workspace saf_calib_finalize needs (a multiple of 256);
  * 0 for an invalid problem. */
@@ -77,13 +89,14 @@ size_t saf_calib_finalize_workspace_bytes(int H, int T);
  *                      n_total == 1 (the sample variance needs two inputs).
  *   workspace        : DEVICE, >= saf_calib_finalize_workspace_bytes(),
  *                      256-byte aligned, contents on entry ignored.
- * Four launches: zero fills, one pass over the lower triangle of mean and m2,
- * and a per-head reduction.  The sums are gathered with atomic adds (float32
- * for the marginals, float64 for the scores), so their last bits may depend
- * on the order in which workgroups finish.
+ * Four launches: two zero fills, one pass over the lower triangle of the
+ * mean, and a per-head reduction.  The marginals gather partial sums over
+ * 256-row chunks with float32 atomic adds, so their last bits may depend on
+ * the order in which workgroups finish; the scores are reduced in float64
+ * without atomics.
  */
 saf_status_t saf_calib_finalize(int H, int T, int n_total,
-                                const float* mean, const float* m2, const double* ent,
+                                const float* mean, const double* stats,
                                 float* eta_abs, float* eta_rel, float* s_var, float* s_kl,
                                 void* workspace, size_t workspace_bytes,
                                 hipStream_t stream);

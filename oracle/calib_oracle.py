@@ -73,6 +73,8 @@ def calibration_stats(Q, K, rows: Optional[np.ndarray] = None,
 
     * ``A_mean`` ``[H, R, T]``: rows ``rows`` of ``A_hat`` (``R = T`` rows by
       default);
+    * ``sq_dev`` ``[H, R, T]``: per entry, ``sum_n (A^(n) - A_hat)^2`` (the
+      sample variance of the entry times ``N - 1``);
     * ``s_var`` ``[H]``, ``s_kl`` ``[H]``: the two scores, summed over the
       evaluated rows only (the full scores when every row is evaluated);
     * ``eta_abs`` ``[H, T]``, ``eta_rel`` ``[H, T]``: the marginals, summed over
@@ -84,6 +86,7 @@ def calibration_stats(Q, K, rows: Optional[np.ndarray] = None,
     rows = np.arange(T) if rows is None else np.asarray(rows, dtype=np.int64).reshape(-1)
     R = rows.shape[0]
     A_mean = np.zeros((H, R, T))
+    sq_ent = np.zeros((H, R, T))
     sq_dev = np.zeros(H)       # sum_n ||A^(n) - A_hat||^2 over the rows
     kl_sum = np.zeros(H)       # sum_n sum_i KL(A^(n)[i] || A_hat[i]) over the rows
     eta_abs = np.zeros((H, T))
@@ -95,7 +98,8 @@ def calibration_stats(Q, K, rows: Optional[np.ndarray] = None,
             A = np.stack([attention_matrix(Q[n, h], K[n, h], r_blk) for n in range(N)])  # [N, rb, T]
             mean = A.mean(axis=0)
             A_mean[h, sel] = mean
-            sq_dev[h] += np.sum((A - mean[None]) ** 2)
+            sq_ent[h, sel] = np.sum((A - mean[None]) ** 2, axis=0)
+            sq_dev[h] += np.sum(sq_ent[h, sel])
             # KL(p || q) = sum p log p - sum p log q, with 0 log 0 = 0.
             kl_sum[h] += np.sum(xlogy(A, A)) - np.sum(xlogy(A, np.broadcast_to(mean, A.shape)))
             eta_abs[h] += mean.sum(axis=0)
@@ -104,4 +108,5 @@ def calibration_stats(Q, K, rows: Optional[np.ndarray] = None,
                 eta_rel[h, : i + 1] += mean[li, i::-1]
     s_var = sq_dev / ((N - 1) * T * T) if N > 1 else np.full(H, np.nan)
     s_kl = kl_sum / (N * T)
-    return {"A_mean": A_mean, "s_var": s_var, "s_kl": s_kl, "eta_abs": eta_abs, "eta_rel": eta_rel}
+    return {"A_mean": A_mean, "sq_dev": sq_ent, "s_var": s_var, "s_kl": s_kl, "eta_abs": eta_abs,
+            "eta_rel": eta_rel}

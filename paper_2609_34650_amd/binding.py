@@ -44,6 +44,7 @@ EXPORTS = (
     "saf_hybrid_attn_bwd_stage",
     "saf_status_str",
     "saf_calib_accumulate",
+    "saf_calib_stats_bytes",
     "saf_calib_finalize_workspace_bytes",
     "saf_calib_finalize",
 )
@@ -84,10 +85,12 @@ def load() -> ctypes.CDLL:
     lib.saf_hybrid_attn_bwd_stage.argtypes = [i] + bwd_args
     lib.saf_calib_accumulate.restype = ctypes.c_int
     lib.saf_calib_accumulate.argtypes = [i, vp, vp, vp, i, i, i, i, i, vp, vp, vp, vp]
+    lib.saf_calib_stats_bytes.restype = ctypes.c_size_t
+    lib.saf_calib_stats_bytes.argtypes = [i, i]
     lib.saf_calib_finalize_workspace_bytes.restype = ctypes.c_size_t
     lib.saf_calib_finalize_workspace_bytes.argtypes = [i, i]
     lib.saf_calib_finalize.restype = ctypes.c_int
-    lib.saf_calib_finalize.argtypes = [i, i, i, vp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+    lib.saf_calib_finalize.argtypes = [i, i, i, vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
     lib.saf_status_str.restype = ctypes.c_char_p
     lib.saf_status_str.argtypes = [i]
     del f32p
@@ -272,14 +275,18 @@ class HybridAttention(torch.autograd.Function):
 # ---------------------------------------------------------------------------
 
 class CalibState:
-    """Running calibration statistics of one layer on one device: ``mean`` and
-    ``m2`` ``[H, T, T]`` float32, ``ent`` ``[H]`` float64, and the number of
-    inputs folded in so far."""
+    """Running calibration statistics of one layer on one device: ``mean``
+    ``[H, T, T]`` float32, optionally ``m2`` ``[H, T, T]`` float32 (per-entry
+    squared deviations), the library's float64 partial sums ``stats``, and the
+    number of inputs folded in so far."""
 
-    def __init__(self, H: int, T: int, device):
+    def __init__(self, H: int, T: int, device, keep_m2: bool = False):
         self.mean = torch.empty((H, T, T), dtype=torch.float32, device=device)
-        self.m2 = torch.empty((H, T, T), dtype=torch.float32, device=device)
-        self.ent = torch.empty((H,), dtype=torch.float64, device=device)
+        self.m2 = torch.empty((H, T, T), dtype=torch.float32, device=device) if keep_m2 else None
+        nbytes = int(load().saf_calib_stats_bytes(H, T))
+        if nbytes == 0:
+            raise ValueError(f"unsupported calibration shape H={H} T={T}")
+        self.stats = torch.empty((nbytes // 8,), dtype=torch.float64, device=device)
         self.n_seen = 0
 
 
@@ -293,10 +300,10 @@ def saf_calib_accumulate(Q: torch.Tensor, K: torch.Tensor, LSE: torch.Tensor, st
     _check_act("K", K, Q.shape, Q.dtype, dev)
     _check_act("LSE", LSE, (B, H, T), torch.float32, dev)
     _check_act("mean", state.mean, (H, T, T), torch.float32, dev)
-    _check_act("m2", state.m2, (H, T, T), torch.float32, dev)
-    _check_act("ent", state.ent, (H,), torch.float64, dev)
+    _check_act("m2", state.m2, (H, T, T), torch.float32, dev, allow_none=True)
+    _check_act("stats", state.stats, (int(lib.saf_calib_stats_bytes(H, T)) // 8,), torch.float64, dev)
     code = lib.saf_calib_accumulate(_dtype_code(Q), _ptr(Q), _ptr(K), _ptr(LSE), B, H, T, d, state.n_seen,
-                                    _ptr(state.mean), _ptr(state.m2), _ptr(state.ent), _stream(dev))
+                                    _ptr(state.mean), _ptr(state.m2), _ptr(state.stats), _stream(dev))
     _raise(code, "saf_calib_accumulate")
     state.n_seen += B
     return state
@@ -318,7 +325,7 @@ def saf_calib_finalize(state: CalibState, workspace: Optional[torch.Tensor] = No
     nbytes = saf_calib_finalize_workspace_bytes(H, T)
     if workspace is None:
         workspace = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=dev)
-    code = lib.saf_calib_finalize(H, T, state.n_seen, _ptr(state.mean), _ptr(state.m2), _ptr(state.ent),
+    code = lib.saf_calib_finalize(H, T, state.n_seen, _ptr(state.mean), _ptr(state.stats),
                                   _ptr(out["eta_abs"]), _ptr(out["eta_rel"]), _ptr(out["s_var"]),
                                   _ptr(out["s_kl"]), workspace.data_ptr(),
                                   workspace.numel() * workspace.element_size(), _stream(dev))

@@ -174,14 +174,19 @@ unsigned fill_grid(size_t n) {
     return (unsigned)(blocks < 4096 ? (blocks > 0 ? blocks : 1) : 4096);
 }
 
-size_t calib_workspace_bytes(int H) { return ((size_t)H * 2 * sizeof(double) + 255) & ~(size_t)255; }
+int calib_tiles(int T) { return (T + saf::CAL_TILE - 1) / saf::CAL_TILE; }
+size_t calib_stats_bytes(int H, int T) {
+    const size_t nt = (size_t)calib_tiles(T);
+    return ((size_t)H * nt * nt * 2 * sizeof(double) + 255) & ~(size_t)255;
+}
+size_t calib_workspace_bytes(int H, int T) {
+    const size_t nr = (size_t)((T + saf::CAL_FIN_ROWS - 1) / saf::CAL_FIN_ROWS);
+    const size_t nc = (size_t)((T + saf::CAL_FIN_COLS - 1) / saf::CAL_FIN_COLS);
+    return ((size_t)H * nr * nc * sizeof(double) + 255) & ~(size_t)255;
+}
 
 template <typename T>
 saf_status_t launch_calib_accum(const saf::CalibArgs& args, hipStream_t stream) {
-    if (args.n_seen == 0) {
-        hipLaunchKernelGGL(saf::calib_fill_kernel, dim3(1), dim3(256), 0, stream, args.ent, (size_t)args.H);
-        if (launched() != SAF_OK) return SAF_ERR_LAUNCH;
-    }
     const unsigned grid = (unsigned)((size_t)args.H * args.n_tiles * args.n_tiles);
     hipLaunchKernelGGL(saf::calib_accum_kernel<T>, dim3(grid), dim3(saf::CAL_THREADS), 0, stream, args);
     return launched();
@@ -261,16 +266,16 @@ SAF_EXPORT saf_status_t saf_hybrid_attn_bwd(saf_dtype_t dt, const void* Q, const
 }
 
 SAF_EXPORT saf_status_t saf_calib_accumulate(saf_dtype_t dt, const void* Q, const void* K, const float* LSE, int B,
-                                             int H, int T, int d, int n_seen, float* mean, float* m2, double* ent,
+                                             int H, int T, int d, int n_seen, float* mean, float* m2, double* stats,
                                              hipStream_t stream) {
     if (dt != SAF_DTYPE_F32 && dt != SAF_DTYPE_BF16) return SAF_ERR_UNSUPPORTED;
     if (B < 0 || H < 0 || T < 0 || d < 0 || n_seen < 0) return SAF_ERR_SHAPE;
     if (d != saf::HEAD_DIM || H > 64) return SAF_ERR_UNSUPPORTED;
     if (T > kMaxCalibT || (int64_t)n_seen + B > kMaxCalibInputs) return SAF_ERR_SHAPE;
     if (B == 0 || H == 0 || T == 0) return SAF_OK;
-    if (Q == nullptr || K == nullptr || LSE == nullptr || mean == nullptr || m2 == nullptr || ent == nullptr)
-        return SAF_ERR_NULL;
-    if (!aligned16(Q) || !aligned16(K) || !aligned16(LSE) || !aligned16(mean) || !aligned16(m2) || !aligned8(ent))
+    if (Q == nullptr || K == nullptr || LSE == nullptr || mean == nullptr || stats == nullptr) return SAF_ERR_NULL;
+    if (!aligned16(Q) || !aligned16(K) || !aligned16(LSE) || !aligned16(mean) || (m2 && !aligned16(m2)) ||
+        !aligned8(stats))
         return SAF_ERR_ALIGNMENT;
     saf::CalibArgs args;
     args.q = Q;
@@ -278,59 +283,62 @@ SAF_EXPORT saf_status_t saf_calib_accumulate(saf_dtype_t dt, const void* Q, cons
     args.lse = LSE;
     args.mean = mean;
     args.m2 = m2;
-    args.ent = ent;
+    args.stats = stats;
     args.B = B;
     args.H = H;
     args.T = T;
     args.n_seen = n_seen;
-    args.n_tiles = (T + saf::CAL_TILE - 1) / saf::CAL_TILE;
-    args.scale_log2 = saf::LOG2E / sqrtf((float)saf::HEAD_DIM);
+    args.n_tiles = calib_tiles(T);
+    args.scale = 1.0f / sqrtf((float)saf::HEAD_DIM);
     return dt == SAF_DTYPE_BF16 ? launch_calib_accum<saf::bf16>(args, stream) : launch_calib_accum<float>(args, stream);
+}
+
+SAF_EXPORT size_t saf_calib_stats_bytes(int H, int T) {
+    if (H <= 0 || H > 64 || T <= 0 || T > kMaxCalibT) return 0;
+    return calib_stats_bytes(H, T);
 }
 
 SAF_EXPORT size_t saf_calib_finalize_workspace_bytes(int H, int T) {
     if (H <= 0 || H > 64 || T <= 0 || T > kMaxCalibT) return 0;
-    return calib_workspace_bytes(H);
+    return calib_workspace_bytes(H, T);
 }
 
-SAF_EXPORT saf_status_t saf_calib_finalize(int H, int T, int n_total, const float* mean, const float* m2,
-                                           const double* ent, float* eta_abs, float* eta_rel, float* s_var,
-                                           float* s_kl, void* workspace, size_t workspace_bytes_given,
-                                           hipStream_t stream) {
+SAF_EXPORT saf_status_t saf_calib_finalize(int H, int T, int n_total, const float* mean, const double* stats,
+                                           float* eta_abs, float* eta_rel, float* s_var, float* s_kl,
+                                           void* workspace, size_t workspace_bytes_given, hipStream_t stream) {
     if (H < 0 || T < 0 || n_total < 0) return SAF_ERR_SHAPE;
     if (H > 64) return SAF_ERR_UNSUPPORTED;
     if (T > kMaxCalibT || n_total > kMaxCalibInputs) return SAF_ERR_SHAPE;
     if (H == 0 || T == 0) return SAF_OK;
     if (n_total < 1) return SAF_ERR_SHAPE;
-    if (mean == nullptr || m2 == nullptr || ent == nullptr || eta_abs == nullptr || eta_rel == nullptr ||
-        s_var == nullptr || s_kl == nullptr || workspace == nullptr)
+    if (mean == nullptr || stats == nullptr || eta_abs == nullptr || eta_rel == nullptr || s_var == nullptr ||
+        s_kl == nullptr || workspace == nullptr)
         return SAF_ERR_NULL;
-    if (!aligned16(mean) || !aligned16(m2) || !aligned8(ent) || (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
+    if (!aligned16(mean) || !aligned8(stats) || (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
         return SAF_ERR_ALIGNMENT;
-    if (workspace_bytes_given < calib_workspace_bytes(H)) return SAF_ERR_SHAPE;
+    if (workspace_bytes_given < calib_workspace_bytes(H, T)) return SAF_ERR_SHAPE;
     saf::CalibFinalArgs args;
     args.mean = mean;
-    args.m2 = m2;
-    args.ent = ent;
+    args.stats = stats;
     args.eta_abs = eta_abs;
     args.eta_rel = eta_rel;
     args.s_var = s_var;
     args.s_kl = s_kl;
-    args.acc = reinterpret_cast<double*>(workspace);
+    args.part = reinterpret_cast<double*>(workspace);
     args.H = H;
     args.T = T;
     args.n_total = n_total;
+    args.n_tiles = calib_tiles(T);
     args.n_cgroups = (T + saf::CAL_FIN_COLS - 1) / saf::CAL_FIN_COLS;
     args.n_rchunks = (T + saf::CAL_FIN_ROWS - 1) / saf::CAL_FIN_ROWS;
     const size_t n_eta = (size_t)H * T;
     hipLaunchKernelGGL(saf::calib_fill_kernel, dim3(fill_grid(n_eta)), dim3(256), 0, stream, eta_abs, n_eta);
     hipLaunchKernelGGL(saf::calib_fill_kernel, dim3(fill_grid(n_eta)), dim3(256), 0, stream, eta_rel, n_eta);
-    hipLaunchKernelGGL(saf::calib_fill_kernel, dim3(1), dim3(256), 0, stream, args.acc, (size_t)2 * H);
     if (launched() != SAF_OK) return SAF_ERR_LAUNCH;
     const unsigned grid = (unsigned)((size_t)H * args.n_rchunks * args.n_cgroups);
     hipLaunchKernelGGL(saf::calib_final_kernel, dim3(grid), dim3(saf::CAL_FIN_COLS), 0, stream, args);
     if (launched() != SAF_OK) return SAF_ERR_LAUNCH;
-    hipLaunchKernelGGL(saf::calib_scores_kernel, dim3(1), dim3(64), 0, stream, args);
+    hipLaunchKernelGGL(saf::calib_scores_kernel, dim3(H), dim3(256), 0, stream, args);
     return launched();
 }
 

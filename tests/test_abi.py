@@ -130,15 +130,14 @@ def test_status_strings(lib):
 # Calibration statistics (include/saf_calib.h)
 # ---------------------------------------------------------------------------
 
-def _acc(lib, dt=1, Q=FAKE, K=FAKE, LSE=FAKE, B=2, H=3, T=16, d=64, n_seen=0, mean=FAKE, m2=FAKE, ent=FAKE):
-    return lib.saf_calib_accumulate(dt, Q, K, LSE, B, H, T, d, n_seen, mean, m2, ent, None)
+def _acc(lib, dt=1, Q=FAKE, K=FAKE, LSE=FAKE, B=2, H=3, T=16, d=64, n_seen=0, mean=FAKE, m2=FAKE, stats=FAKE):
+    return lib.saf_calib_accumulate(dt, Q, K, LSE, B, H, T, d, n_seen, mean, m2, stats, None)
 
 
-def _fin(lib, H=3, T=16, n=4, mean=FAKE, m2=FAKE, ent=FAKE, ea=FAKE, er=FAKE, sv=FAKE, sk=FAKE, ws=FAKE,
-         ws_bytes=None):
+def _fin(lib, H=3, T=16, n=4, mean=FAKE, stats=FAKE, ea=FAKE, er=FAKE, sv=FAKE, sk=FAKE, ws=FAKE, ws_bytes=None):
     if ws_bytes is None:
         ws_bytes = lib.saf_calib_finalize_workspace_bytes(max(H, 1), max(T, 1))
-    return lib.saf_calib_finalize(H, T, n, mean, m2, ent, ea, er, sv, sk, ws, ws_bytes, None)
+    return lib.saf_calib_finalize(H, T, n, mean, stats, ea, er, sv, sk, ws, ws_bytes, None)
 
 
 def test_calib_accumulate_rejects_bad_arguments(lib):
@@ -151,17 +150,25 @@ def test_calib_accumulate_rejects_bad_arguments(lib):
     assert _acc(lib, n_seen=(1 << 24) - 1, B=2) == 2
     assert _acc(lib, Q=None) == 1
     assert _acc(lib, LSE=None) == 1
-    assert _acc(lib, ent=None) == 1
+    assert _acc(lib, stats=None) == 1
+    assert _acc(lib, mean=None) == 1
     assert _acc(lib, mean=FAKE + 4) == 6
-    assert _acc(lib, ent=FAKE + 4) == 6
+    assert _acc(lib, m2=FAKE + 4) == 6
+    assert _acc(lib, stats=FAKE + 4) == 6
     # Empty problems launch nothing.
-    assert _acc(lib, B=0, Q=None, K=None, LSE=None, mean=None, m2=None, ent=None) == 0
-    assert _acc(lib, T=0, Q=None, K=None, LSE=None, mean=None, m2=None, ent=None) == 0
+    assert _acc(lib, B=0, Q=None, K=None, LSE=None, mean=None, m2=None, stats=None) == 0
+    assert _acc(lib, T=0, Q=None, K=None, LSE=None, mean=None, m2=None, stats=None) == 0
 
 
 def test_calib_finalize_rejects_bad_arguments(lib):
     assert lib.saf_calib_finalize_workspace_bytes(3, 16) % 256 == 0
-    assert lib.saf_calib_finalize_workspace_bytes(3, 16) >= 3 * 2 * 8
+    assert lib.saf_calib_finalize_workspace_bytes(3, 16) >= 3 * 8
+    assert lib.saf_calib_finalize_workspace_bytes(2, 1000) >= 2 * 4 * 4 * 8
+    assert lib.saf_calib_stats_bytes(3, 16) >= 3 * 2 * 8
+    assert lib.saf_calib_stats_bytes(2, 300) >= 2 * 3 * 3 * 2 * 8
+    assert lib.saf_calib_stats_bytes(2, 300) % 256 == 0
+    assert lib.saf_calib_stats_bytes(0, 16) == 0
+    assert lib.saf_calib_stats_bytes(2, (1 << 16) + 1) == 0
     assert lib.saf_calib_finalize_workspace_bytes(0, 16) == 0
     assert lib.saf_calib_finalize_workspace_bytes(65, 16) == 0
     assert _fin(lib, n=0) == 2

@@ -54,6 +54,7 @@ def test_scores_and_mean_against_library_routines():
         # Eq. variance-score: (1/T^2) * sum over entries of the sample variance.
         s_var = np.var(A, axis=0, ddof=1).sum() / (T * T)
         np.testing.assert_allclose(st["s_var"][h], s_var, rtol=1e-10)
+        np.testing.assert_allclose(st["sq_dev"][h], np.var(A, axis=0, ddof=0) * N, rtol=1e-10, atol=1e-18)
         # Eq. forward-kl-score with scipy's KL of each causal row.
         Ahat = A.mean(axis=0)
         kl = sum(entropy(A[n, i, : i + 1], Ahat[i, : i + 1]) for n in range(N) for i in range(T))
@@ -124,7 +125,9 @@ def test_row_subsets_add_up():
     a, b = co.calibration_stats(Q, K, rows=even), co.calibration_stats(Q, K, rows=odd)
     for key in ("s_var", "s_kl", "eta_abs", "eta_rel"):
         np.testing.assert_allclose(a[key] + b[key], full[key], rtol=1e-12, atol=1e-16)
-    np.testing.assert_allclose(a["A_mean"][0], full["A_mean"][0][even], rtol=0, atol=0)
+    for key in ("A_mean", "sq_dev"):
+        np.testing.assert_allclose(a[key][0], full[key][0][even], rtol=0, atol=0)
+        np.testing.assert_allclose(b[key][0], full[key][0][odd], rtol=0, atol=0)
 
 
 def test_single_input_variance_is_undefined():

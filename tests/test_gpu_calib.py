@@ -25,7 +25,7 @@ SVAR_RTOL = 1e-3
 SKL_ATOL = 1e-4
 
 
-def _gpu_stats(Q, K, dtype, micro, state=None, reuse_garbage=False):
+def _gpu_stats(Q, K, dtype, micro, state=None, reuse_garbage=False, keep_m2=False):
     """Run the forward for LSE and fold the inputs in micro-batches of the
     listed sizes.  Returns (numpy dict, state)."""
     torch = torch_cuda()
@@ -34,11 +34,12 @@ def _gpu_stats(Q, K, dtype, micro, state=None, reuse_garbage=False):
     dev = torch.device("cuda", 0)
     N, H, T, d = Q.shape
     if state is None:
-        state = binding.CalibState(H, T, dev)
+        state = binding.CalibState(H, T, dev, keep_m2=keep_m2)
         if reuse_garbage:
             state.mean.fill_(float("nan"))
-            state.m2.fill_(float("nan"))
-            state.ent.fill_(float("nan"))
+            if state.m2 is not None:
+                state.m2.fill_(float("nan"))
+            state.stats.fill_(float("nan"))
     start = 0
     for m in micro:
         q = torch.from_numpy(np.ascontiguousarray(Q[start:start + m])).to(dev).to(tdt).contiguous()
@@ -50,7 +51,8 @@ def _gpu_stats(Q, K, dtype, micro, state=None, reuse_garbage=False):
     out = binding.saf_calib_finalize(state)
     torch.cuda.synchronize()
     res = {k: v.double().cpu().numpy() for k, v in out.items()}
-    res["m2"] = state.m2.double().cpu().numpy()
+    if state.m2 is not None:
+        res["m2"] = state.m2.double().cpu().numpy()
     return res, state
 
 
@@ -61,6 +63,8 @@ def _inputs(N, H, T, dtype, stream_id):
 
 def _compare(g, o, T):
     np.testing.assert_allclose(g["A_mean"], o["A_mean"], rtol=A_RTOL, atol=A_ATOL)
+    if "m2" in g:
+        np.testing.assert_allclose(g["m2"], o["sq_dev"], rtol=SVAR_RTOL, atol=1e-9)
     assert np.all(np.triu(g["A_mean"], 1) == 0)
     np.testing.assert_allclose(g["eta_abs"], o["eta_abs"], rtol=A_RTOL, atol=A_ATOL * T)
     np.testing.assert_allclose(g["eta_rel"], o["eta_rel"], rtol=A_RTOL, atol=A_ATOL * T)
@@ -68,31 +72,40 @@ def _compare(g, o, T):
     np.testing.assert_allclose(g["s_kl"], o["s_kl"], rtol=0, atol=SKL_ATOL)
 
 
-@pytest.mark.parametrize("dtype,N,H,T,micro", [
-    ("f32", 5, 2, 200, (2, 3)),          # two tiles, ragged tail
-    ("bf16", 4, 3, 300, (1, 2, 1)),      # three tiles, odd micro-batches
-    ("bf16", 3, 1, 128, (3,)),           # exactly one tile
-    ("bf16", 2, 2, 37, (2,)),            # one partial tile
+@pytest.mark.parametrize("dtype,N,H,T,micro,keep_m2", [
+    ("f32", 5, 2, 200, (2, 3), True),          # two tiles, ragged tail
+    ("f32", 3, 1, 130, (1, 2), False),
+    ("bf16", 4, 3, 300, (1, 2, 1), True),      # three tiles, odd micro-batches
+    ("bf16", 4, 2, 260, (3, 1), False),
+    ("bf16", 3, 1, 128, (3,), False),          # exactly one tile
+    ("bf16", 2, 2, 37, (2,), True),            # one partial tile
 ])
-def test_calib_matches_oracle(dtype, N, H, T, micro):
+def test_calib_matches_oracle(dtype, N, H, T, micro, keep_m2):
     from oracle import calib_oracle as co
-    announce(f"calib parity {dtype} N={N} H={H} T={T} micro={micro}")
+    announce(f"calib parity {dtype} N={N} H={H} T={T} micro={micro} keep_m2={keep_m2}")
     inp = _inputs(N, H, T, dtype, stream_id=21)
-    g, _ = _gpu_stats(inp["Q"], inp["K"], dtype, micro)
+    g, _ = _gpu_stats(inp["Q"], inp["K"], dtype, micro, keep_m2=keep_m2)
     o = co.calibration_stats(inp["Q"], inp["K"])
     _compare(g, o, T)
 
 
 def test_calib_split_equals_single_call_and_ignores_old_state():
-    """Welford's recurrence runs in input order either way, so the state after
-    micro-batches (1, 2, 1) is bitwise the state after one call of 4; and
+    """Welford's recurrence runs in input order either way, so the mean after
+    micro-batches (1, 2, 1) is bitwise the mean after one call of 4 (the
+    squared deviations are added per call, so they agree to rounding); and
     n_seen = 0 ignores whatever the state buffers held."""
     announce("calib split vs single call")
     inp = _inputs(4, 2, 260, "bf16", stream_id=22)
-    a, _ = _gpu_stats(inp["Q"], inp["K"], "bf16", (4,), reuse_garbage=True)
-    b, _ = _gpu_stats(inp["Q"], inp["K"], "bf16", (1, 2, 1))
+    a, _ = _gpu_stats(inp["Q"], inp["K"], "bf16", (4,), reuse_garbage=True, keep_m2=True)
+    b, _ = _gpu_stats(inp["Q"], inp["K"], "bf16", (1, 2, 1), keep_m2=True)
+    c, _ = _gpu_stats(inp["Q"], inp["K"], "bf16", (2, 2), keep_m2=False)
     np.testing.assert_array_equal(a["A_mean"], b["A_mean"])
-    np.testing.assert_array_equal(a["m2"], b["m2"])
+    np.testing.assert_array_equal(a["A_mean"], c["A_mean"])
+    np.testing.assert_allclose(a["m2"], b["m2"], rtol=1e-5, atol=1e-12)
+    np.testing.assert_allclose(a["s_var"], c["s_var"], rtol=1e-5)
+    # The variance score's sum of squared deviations is the sum of the
+    # per-entry ones.
+    np.testing.assert_allclose(b["s_var"], b["m2"].sum(axis=(1, 2)) / (3 * 260 * 260), rtol=1e-5)
     # ent gathers float32 per-lane partials per call: equal to rounding only.
     np.testing.assert_allclose(a["s_kl"], b["s_kl"], rtol=0, atol=1e-6)
     assert np.all(np.isfinite(a["A_mean"]))
@@ -128,7 +141,7 @@ def test_calib_full_size_sampled_rows():
     w = inputs.CALIB_WORKLOADS["calib124m_4k"]
     announce(f"calib full size {w.name}")
     inp = inputs.calib_inputs(w.n_cal, w.H, w.T, w.d, w.dtype, stream_id=w.stream_id)
-    g, _ = _gpu_stats(inp["Q"], inp["K"], w.dtype, (w.micro,) * (w.n_cal // w.micro))
+    g, _ = _gpu_stats(inp["Q"], inp["K"], w.dtype, (w.micro,) * (w.n_cal // w.micro), keep_m2=True)
     rows = np.array([0, 1, 127, 128, 2049, 4000, w.T - 1])
     o = co.calibration_stats(inp["Q"], inp["K"], rows=rows)
     np.testing.assert_allclose(g["A_mean"][:, rows], o["A_mean"], rtol=A_RTOL, atol=A_ATOL)
