@@ -26,6 +26,13 @@ Everything here evaluates the plain dense definitions in float64, one
   execution", paragraph "Fused computation"); its query and key slots get
   zero gradients (Appendix "Mixed-head execution and numerical checks").
   For an ordinary head the gradients are the chain rule through softmax.
+* Trainable patterns (Appendix "Pattern content and trainability": the
+  variant that keeps optimising alpha and rho): the gradients of the same loss
+  with respect to a fixed head's preference vectors.  With logits
+  ``L(i, j) = a[j] + r[i - j]`` and ``P = softmax_causal(L)``,
+  ``dP = dO V^T``, ``D_i = sum_j P_ij dP_ij``, ``dL = P * (dP - D)``, and
+  ``da[j] = sum_i dL(i, j)``, ``dr[delta] = sum_{i - j = delta} dL(i, j)``,
+  each summed over the batch (a and r are shared by every batch element).
 
 Readings of points the paper leaves open:
 
@@ -59,6 +66,8 @@ __all__ = [
     "layer_forward",
     "layer_backward",
     "layer_forward_backward_parallel",
+    "fixed_pattern_grad",
+    "layer_pattern_grad",
 ]
 
 _F64 = np.float64
@@ -268,6 +277,51 @@ def layer_backward(Q, K, V, dO, is_fixed, a=None, r=None, row_block: int = 512,
         dK[b, h] = dk
         dV[b, h] = dv
     return dQ, dK, dV
+
+
+# ---------------------------------------------------------------------------
+# Gradients of trainable patterns
+# ---------------------------------------------------------------------------
+
+def fixed_pattern_grad(v, do, a, r, row_block: int = 512) -> Tuple[np.ndarray, np.ndarray]:
+    """Gradients ``(da, dr)`` ``[n]`` of ``sum(O * dO)`` with respect to one
+    fixed head's ``a`` and ``r`` for one batch element, where ``O = P V``.
+    ``D`` is taken from its definition ``sum_j P_ij dP_ij``."""
+    v = _as64(v)
+    do = _as64(do)
+    n = v.shape[0]
+    a = _as64(a)[:n]
+    r = _as64(r)[:n]
+    da = np.zeros(n)
+    dr = np.zeros(n)
+    for start in range(0, n, row_block):
+        rows = np.arange(start, min(n, start + row_block))
+        p, _ = _probs_block(None, None, True, a, r, rows, n)
+        dp = do[rows] @ v.T
+        D = np.sum(p * dp, axis=1)
+        dl = p * (dp - D[:, None])
+        da += dl.sum(axis=0)
+        for li, i in enumerate(rows):
+            dr[: i + 1] += dl[li, i::-1]        # offsets 0..i of row i
+    return da, dr
+
+
+def layer_pattern_grad(V, dO, is_fixed, a, r, row_block: int = 512) -> Tuple[np.ndarray, np.ndarray]:
+    """``da, dr`` ``[H, N]`` (float64) of ``sum(O * dO)`` for the fixed heads of
+    a layer, summed over the batch; rows of ordinary heads are zero."""
+    V = np.asarray(V)
+    B, H, N, _ = V.shape
+    is_fixed = np.asarray(is_fixed).astype(bool).reshape(-1)
+    da = np.zeros((H, N))
+    dr = np.zeros((H, N))
+    for h in range(H):
+        if not is_fixed[h]:
+            continue
+        for b in range(B):
+            ga, gr = fixed_pattern_grad(V[b, h], dO[b, h], a[h], r[h], row_block)
+            da[h] += ga
+            dr[h] += gr
+    return da, dr
 
 
 # ---------------------------------------------------------------------------

@@ -271,6 +271,61 @@ def test_delta_identity():
                                rtol=1e-12, atol=1e-13)
 
 
+def test_pattern_gradient_matches_central_finite_differences():
+    """Gradients of the trainable-pattern variant: da and dr of sum(O * dO),
+    summed over the batch, against central differences of the loss in a and r."""
+    B, H, N, d = 2, 2, 7, 3
+    Q, K, V, dO = (_rand(B, H, N, d) for _ in range(4))
+    a, r = _rand(H, N), _rand(H, N)
+    is_fixed = np.array([1, 0], dtype=np.uint8)
+    da, dr = orc.layer_pattern_grad(V, dO, is_fixed, a, r, row_block=3)
+    eps = 1e-6
+    for X, G in ((a, da), (r, dr)):
+        num = np.zeros_like(X)
+        for idx in np.ndindex(X.shape):
+            old = X[idx]
+            X[idx] = old + eps
+            fp = _loss(Q, K, V, dO, is_fixed, a, r)
+            X[idx] = old - eps
+            fm = _loss(Q, K, V, dO, is_fixed, a, r)
+            X[idx] = old
+            num[idx] = (fp - fm) / (2 * eps)
+        err = np.linalg.norm(G - num) / np.linalg.norm(num)
+        assert err < 1e-7, err
+    assert not da[1].any() and not dr[1].any()          # ordinary head: no pattern
+    # A row's logits all shift with a common constant: the gradients sum to 0.
+    np.testing.assert_allclose(da.sum(axis=1), 0.0, atol=1e-12)
+    np.testing.assert_allclose(dr.sum(axis=1), 0.0, atol=1e-12)
+
+
+def test_pattern_gradient_matches_autograd():
+    """Autograd through a dense torch float64 build of Eq. compact-prior."""
+    torch = pytest.importorskip("torch")
+    n, d = 21, 4
+    a0, r0 = _rand(n) * 2, _rand(n) * 2
+    V, dO = _rand(n, d), _rand(n, d)
+    a = torch.tensor(a0, requires_grad=True)
+    r = torch.tensor(r0, requires_grad=True)
+    i = torch.arange(n)
+    off = i[:, None] - i[None, :]
+    logits = a[None, :] + r[off.clamp(min=0)]
+    logits = logits.masked_fill(off < 0, float("-inf"))
+    P = torch.softmax(logits, dim=1)
+    (P @ torch.tensor(V)).backward(torch.tensor(dO))
+    da, dr = orc.fixed_pattern_grad(V, dO, a0, r0, row_block=5)
+    np.testing.assert_allclose(da, a.grad.numpy(), rtol=1e-11, atol=1e-13)
+    np.testing.assert_allclose(dr, r.grad.numpy(), rtol=1e-11, atol=1e-13)
+
+
+def test_pattern_gradient_of_uniform_values_is_zero():
+    """V with identical rows gives O independent of the pattern: no gradient."""
+    n, d = 15, 3
+    V = np.tile(_rand(1, d), (n, 1))
+    da, dr = orc.fixed_pattern_grad(V, _rand(n, d), _rand(n), _rand(n))
+    np.testing.assert_allclose(da, 0.0, atol=1e-13)
+    np.testing.assert_allclose(dr, 0.0, atol=1e-13)
+
+
 def test_fixed_heads_never_read_queries_or_keys():
     B, H, N, d = 2, 3, 16, 4
     Q, K, V, dO = (_rand(B, H, N, d) for _ in range(4))
