@@ -142,6 +142,37 @@ saf_status_t saf_hybrid_attn_bwd_stage(saf_bwd_stage_t stage, saf_dtype_t dt,
                                        void* workspace, size_t workspace_bytes,
                                        hipStream_t stream);
 
+/*
+ * Gradients of trainable fixed patterns (Appendix "Pattern content and
+ * trainability": the variant that keeps optimising alpha and rho after
+ * replacement).  For every fixed head, with L(i, j) = a[j] + r[i - j],
+ * P = softmax_causal(L) and the loss sum(O * dO):
+ *     dP = dO V^T,  D_i = rowsum(dO * O)_i,  dL = P * (dP - D),
+ *     da[h][j] = sum_b sum_i dL(i, j),   dr[h][delta] = sum_b sum_{i-j=delta} dL(i, j).
+ * The frozen layer never needs this call; it adds one N x N x d product per
+ * fixed head and batch element.  Call it beside saf_hybrid_attn_bwd (which
+ * still gives dV, and zeros in the fixed heads' dQ and dK).
+ *   V, O, dO  : [B,H,N,d] `dt` (O and LSE as written by the forward).
+ *   LSE       : [B,H,N] float32 from the forward (log Z for fixed heads).
+ *   da, dr    : DEVICE [H, N] float32, written; rows of ordinary heads are 0.
+ *               Sums over batch elements and key blocks are gathered with
+ *               float32 atomic adds, so their last bits may depend on the
+ *               order in which workgroups finish.
+ *   workspace : DEVICE, >= saf_hybrid_attn_bwd_workspace_bytes(), 256-byte
+ *               aligned, contents on entry ignored.
+ * Four launches: two zero fills, the row pre-pass D for the fixed heads, and
+ * one workgroup per (batch element, fixed head, block of 128 keys).
+ */
+saf_status_t saf_hybrid_attn_bwd_pattern(saf_dtype_t dt,
+                                         const void* V, const void* O, const void* dO,
+                                         const float* LSE,
+                                         const uint8_t* head_is_fixed,
+                                         const float* a, const float* r, int ld_prior,
+                                         int B, int H, int N, int d,
+                                         float* da, float* dr,
+                                         void* workspace, size_t workspace_bytes,
+                                         hipStream_t stream);
+
 /* Static text for a status code ("unknown status" for anything else). */
 const char* saf_status_str(saf_status_t s);
 

@@ -42,6 +42,7 @@ EXPORTS = (
     "saf_hybrid_attn_bwd_workspace_bytes",
     "saf_hybrid_attn_bwd",
     "saf_hybrid_attn_bwd_stage",
+    "saf_hybrid_attn_bwd_pattern",
     "saf_status_str",
     "saf_calib_accumulate",
     "saf_calib_stats_bytes",
@@ -83,6 +84,9 @@ def load() -> ctypes.CDLL:
     lib.saf_hybrid_attn_bwd.argtypes = bwd_args
     lib.saf_hybrid_attn_bwd_stage.restype = ctypes.c_int
     lib.saf_hybrid_attn_bwd_stage.argtypes = [i] + bwd_args
+    lib.saf_hybrid_attn_bwd_pattern.restype = ctypes.c_int
+    lib.saf_hybrid_attn_bwd_pattern.argtypes = [i, vp, vp, vp, vp, u8p, vp, vp, i, i, i, i, i, vp, vp, vp,
+                                                ctypes.c_size_t, vp]
     lib.saf_calib_accumulate.restype = ctypes.c_int
     lib.saf_calib_accumulate.argtypes = [i, vp, vp, vp, i, i, i, i, i, vp, vp, vp, vp]
     lib.saf_calib_stats_bytes.restype = ctypes.c_size_t
@@ -250,6 +254,36 @@ def saf_hybrid_attn_bwd_stage(stage: int, Q, K, V, O, dO, LSE, head_is_fixed, a=
                                                     workspace)
     _raise(lib.saf_hybrid_attn_bwd_stage(int(stage), *args), "saf_hybrid_attn_bwd_stage")
     return outs
+
+
+def saf_hybrid_attn_bwd_pattern(V, O, dO, LSE, head_is_fixed, a, r, da=None, dr=None,
+                                workspace: Optional[torch.Tensor] = None):
+    """Gradients ``(da, dr)`` ``[H, N]`` float32 of ``sum(O * dO)`` with
+    respect to the fixed heads' ``a`` and ``r`` (summed over the batch); rows
+    of ordinary heads are zero."""
+    lib = load()
+    B, H, N, d = V.shape
+    dev = V.device
+    for name, t in (("V", V), ("O", O), ("dO", dO)):
+        _check_act(name, t, V.shape, V.dtype, dev)
+    _check_act("LSE", LSE, (B, H, N), torch.float32, dev)
+    da = torch.empty((H, N), dtype=torch.float32, device=dev) if da is None else da
+    dr = torch.empty((H, N), dtype=torch.float32, device=dev) if dr is None else dr
+    _check_act("da", da, (H, N), torch.float32, dev)
+    _check_act("dr", dr, (H, N), torch.float32, dev)
+    nbytes = saf_hybrid_attn_bwd_workspace_bytes(V.dtype, B, H, N, d)
+    if workspace is None:
+        workspace = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=dev)
+    flags = _flags(head_is_fixed, H)
+    pa, lda = _prior("a", a, H, N, dev)
+    pr, ldr = _prior("r", r, H, N, dev)
+    if pa is not None and pr is not None and lda != ldr:
+        raise ValueError("a and r must share one row stride")
+    code = lib.saf_hybrid_attn_bwd_pattern(
+        _dtype_code(V), _ptr(V), _ptr(O), _ptr(dO), _ptr(LSE), flags.ctypes.data, pa, pr, lda, B, H, N, d,
+        _ptr(da), _ptr(dr), workspace.data_ptr(), workspace.numel() * workspace.element_size(), _stream(dev))
+    _raise(code, "saf_hybrid_attn_bwd_pattern")
+    return da, dr
 
 
 class HybridAttention(torch.autograd.Function):

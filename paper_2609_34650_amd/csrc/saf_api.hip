@@ -10,6 +10,7 @@
 #include "saf_bwd.h"
 #include "saf_calib_kernels.h"
 #include "saf_fwd.h"
+#include "saf_pattern.h"
 
 #define SAF_EXPORT extern "C" __attribute__((visibility("default")))
 
@@ -263,6 +264,59 @@ SAF_EXPORT saf_status_t saf_hybrid_attn_bwd(saf_dtype_t dt, const void* Q, const
         if (st != SAF_OK) return st;
     }
     return SAF_OK;
+}
+
+SAF_EXPORT saf_status_t saf_hybrid_attn_bwd_pattern(saf_dtype_t dt, const void* V, const void* O, const void* dO,
+                                                    const float* LSE, const uint8_t* head_is_fixed, const float* a,
+                                                    const float* r, int ld_prior, int B, int H, int N, int d,
+                                                    float* da, float* dr, void* workspace,
+                                                    size_t workspace_bytes_given, hipStream_t stream) {
+    Problem pr;
+    saf_status_t st = check_common(dt, head_is_fixed, a, r, ld_prior, B, H, N, d, &pr);
+    if (st != SAF_OK || pr.empty) return st;
+    if (V == nullptr || O == nullptr || dO == nullptr || LSE == nullptr || da == nullptr || dr == nullptr ||
+        workspace == nullptr)
+        return SAF_ERR_NULL;
+    if (!aligned16(V) || !aligned16(O) || !aligned16(dO) || !aligned16(LSE) ||
+        (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
+        return SAF_ERR_ALIGNMENT;
+    if (workspace_bytes_given < workspace_bytes(B, H, N)) return SAF_ERR_SHAPE;
+    const size_t n_out = (size_t)H * N;
+    hipLaunchKernelGGL(saf::pat_fill_kernel, dim3(fill_grid(n_out)), dim3(256), 0, stream, da, n_out);
+    hipLaunchKernelGGL(saf::pat_fill_kernel, dim3(fill_grid(n_out)), dim3(256), 0, stream, dr, n_out);
+    if (launched() != SAF_OK) return SAF_ERR_LAUNCH;
+    if (!pr.any_fixed) return SAF_OK;
+    // D for the fixed heads: the row pre-pass with the ordinary heads masked out.
+    const uint64_t all = H == 64 ? ~0ull : ((1ull << H) - 1);
+    Problem inv = pr;
+    inv.fixed_mask = all & ~pr.fixed_mask;
+    saf::BwdArgs ba = make_bwd_args(nullptr, nullptr, V, O, dO, LSE, a, r, ld_prior, B, H, N, nullptr, nullptr,
+                                    nullptr, workspace, inv);
+    st = run_bwd_stage(SAF_BWD_PREPROCESS, dt, ba, stream);
+    if (st != SAF_OK) return st;
+    saf::PatArgs pa;
+    pa.v = V;
+    pa.dO = dO;
+    pa.lse = LSE;
+    pa.dsum = reinterpret_cast<const float*>(workspace);
+    pa.a = a;
+    pa.r = r;
+    pa.da = da;
+    pa.dr = dr;
+    pa.B = B;
+    pa.H = H;
+    pa.N = N;
+    pa.ld_prior = ld_prior;
+    pa.n_fixed = 0;
+    for (int h = 0; h < H; ++h)
+        if ((pr.fixed_mask >> h) & 1ull) pa.heads[pa.n_fixed++] = (unsigned char)h;
+    pa.n_kblocks = (N + saf::PAT_BN - 1) / saf::PAT_BN;
+    const unsigned grid = (unsigned)((size_t)pa.n_kblocks * B * pa.n_fixed);
+    if (dt == SAF_DTYPE_BF16)
+        hipLaunchKernelGGL(saf::bwd_pattern_kernel<saf::bf16>, dim3(grid), dim3(saf::PAT_THREADS), 0, stream, pa);
+    else
+        hipLaunchKernelGGL(saf::bwd_pattern_kernel<float>, dim3(grid), dim3(saf::PAT_THREADS), 0, stream, pa);
+    return launched();
 }
 
 SAF_EXPORT saf_status_t saf_calib_accumulate(saf_dtype_t dt, const void* Q, const void* K, const float* LSE, int B,

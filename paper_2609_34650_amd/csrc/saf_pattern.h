@@ -1,0 +1,198 @@
+// Gradients of trainable fixed patterns (Appendix "Pattern content and
+// trainability": the variant that keeps optimising alpha and rho after
+// replacement).  For a fixed head, with logits L(i, j) = a[j] + r[i - j],
+// P = softmax_causal(L), O = P V and the loss sum(O * dO):
+//     dP = dO V^T,  D_i = rowsum(dO * O)_i,  dL = P * (dP - D),
+//     da[j] = sum_i dL(i, j),  dr[delta] = sum_{i - j = delta} dL(i, j),
+// each summed over the batch (a and r are shared by every batch element).
+//
+// Workgroup = (batch b, fixed head, block of 128 keys), 4 wavefronts of 32
+// keys (one per lane column c), streaming query tiles of 64 rows from the
+// block's first key to N.  dP comes from the MFMA with dO rows as the A
+// operand (from LDS) and the wavefront's V rows as the B operand (registers),
+// so a lane's accumulator entries are 16 queries of its key: dL summed down
+// the lane is the key's share of da.  P is recomputed per entry as
+// exp(a[j] + r[i - j] - log Z(i)) with log Z from the forward's LSE and the
+// offsets' r values from an LDS band copied per tile.  dr gathers dL by
+// offset in an LDS ring of 256 floats indexed by delta mod 256 (LDS atomic
+// adds): tile t touches offsets 64t - 127 .. 64t + 63, so once tile t is done
+// the offsets below 64(t+1) - 127 are final; the next tile flushes them to
+// dr with global atomic adds and clears their slots, which the tile after it
+// is the first to reuse.  The dO tile, the tile's LSE and D rows and the r
+// band are copied by buffer loads straight to LDS (rows or offsets outside
+// 0 .. N-1 arrive as 0 and are masked), double-buffered over tiles.
+#pragma once
+
+#include "saf_common.h"
+
+namespace saf {
+
+constexpr int PAT_BN = 128;      // keys per workgroup
+constexpr int PAT_BM = TILE_ROWS;  // queries per tile
+constexpr int PAT_THREADS = 256;
+constexpr int PAT_BAND = 192;    // r entries per tile (offsets 64t - 127 .. 64t + 64)
+constexpr int PAT_RING = 256;    // dr ring slots
+static_assert(PAT_BM + PAT_BN - 1 <= PAT_BAND, "a tile's offsets fit in the band");
+static_assert(PAT_BAND + PAT_BM <= PAT_RING, "live offsets never share a ring slot");
+
+struct PatArgs {
+    const void* v;
+    const void* dO;
+    const float* lse;
+    const float* dsum;   // D, [B, H, N]
+    const float* a;
+    const float* r;
+    float* da;           // [H, N]
+    float* dr;           // [H, N]
+    int B, H, N, ld_prior, n_fixed, n_kblocks;
+    unsigned char heads[64];  // the fixed heads
+};
+
+// One query tile t (queries q0 .. q0+63, q0 = k0 + 64 t) against the
+// wavefront's 32 keys.  MASK: the tile meets the diagonal or runs past N.
+template <typename T, bool MASK>
+__device__ __forceinline__ void pat_tile(const T* gt, const float* rows, const float* band, float* ring, int t,
+                                         int q0, int k0, int w, int c, int hf, int N,
+                                         const typename Vec<T>::x8 (&vf)[4], float a_key, float& da_acc) {
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb) {
+        // Rows of this block all precede the wavefront's first key.
+        if (MASK && 2 * t + rb < w) continue;
+        f32x16 dp;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) dp[v] = 0.0f;
+#pragma unroll
+        for (int dc = 0; dc < 4; ++dc) mma(dp, ld_row<T>(gt, 32 * rb + c, 16 * dc + 8 * hf), vf[dc]);
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            const f32x4 l4 = *reinterpret_cast<const f32x4*>(rows + 32 * rb + 8 * g + 4 * hf);
+            const f32x4 d4 = *reinterpret_cast<const f32x4*>(rows + PAT_BM + 32 * rb + 8 * g + 4 * hf);
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int v = 4 * g + u;
+                const int ql = 32 * rb + 8 * g + 4 * hf + u;        // query - q0
+                const int bi = ql - 32 * w - c + (PAT_BN - 1);       // band index of i - j
+                float pv = fast_exp2((a_key + band[bi] - l4[u]) * LOG2E);
+                if (MASK && (ql < 32 * w + c - 64 * t || q0 + ql >= N)) pv = 0.0f;
+                const float dl = pv * (dp[v] - d4[u]);
+                da_acc += dl;
+                const int delta = 64 * t + ql - 32 * w - c;
+                atomicAdd(ring + (delta & (PAT_RING - 1)), dl);
+            }
+        }
+    }
+}
+
+template <typename T>
+__global__ __launch_bounds__(PAT_THREADS) void bwd_pattern_kernel(PatArgs p) {
+    __shared__ __attribute__((aligned(16))) T g0[tile_elems<T>()];
+    __shared__ __attribute__((aligned(16))) T g1[tile_elems<T>()];
+    __shared__ __attribute__((aligned(16))) float rows0[2 * PAT_BM];  // LSE, then D
+    __shared__ __attribute__((aligned(16))) float rows1[2 * PAT_BM];
+    __shared__ __attribute__((aligned(16))) float band0[PAT_BAND];
+    __shared__ __attribute__((aligned(16))) float band1[PAT_BAND];
+    __shared__ float ring[PAT_RING];
+
+    const int per_block = p.B * p.n_fixed;
+    const int kblk = (int)(blockIdx.x / per_block);  // ascending: longest first
+    const int rem = (int)(blockIdx.x % per_block);
+    const int b = rem / p.n_fixed;
+    const int h = p.heads[rem % p.n_fixed];
+    const int tid = threadIdx.x;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int lane = tid & 63;
+    const int c = tid & 31;
+    const int hf = (tid >> 5) & 1;
+    const int N = p.N;
+    const int k0 = kblk * PAT_BN;
+    const int key = k0 + 32 * w + c;
+    const size_t slice = (size_t)(b * p.H + h) * N;
+    const T* V = reinterpret_cast<const T*>(p.v) + slice * HEAD_DIM;
+    const float* arow = p.a + (size_t)h * p.ld_prior;
+    const float* rrow = p.r + (size_t)h * p.ld_prior;
+
+    for (int i = tid; i < PAT_RING; i += PAT_THREADS) ring[i] = 0.0f;
+    typedef typename Vec<T>::x8 frag;
+    frag vf[4];
+#pragma unroll
+    for (int dc = 0; dc < 4; ++dc) vf[dc] = key < N ? ld8<T>(V + (size_t)key * HEAD_DIM + 16 * dc + 8 * hf) : zero8<T>();
+    const float a_key = key < N ? arow[key] : -INFINITY;
+
+    const __amdgpu_buffer_rsrc_t rg = slice_rsrc<T>(reinterpret_cast<const T*>(p.dO) + slice * HEAD_DIM, N);
+    const __amdgpu_buffer_rsrc_t rl =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(p.lse + slice), (short)0, N * 4, 0x00020000);
+    const __amdgpu_buffer_rsrc_t rd =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(p.dsum + slice), (short)0, N * 4, 0x00020000);
+    const __amdgpu_buffer_rsrc_t rr =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(rrow), (short)0, N * 4, 0x00020000);
+
+    const int n_tiles = (N - k0 + PAT_BM - 1) / PAT_BM;
+    const int n_mask = min(PAT_BN / PAT_BM, n_tiles);
+    const bool ragged_end = (N - k0) % PAT_BM != 0;  // the last tile runs past N
+    // Slots: masked tiles (the diagonal ones, then the last one if ragged)
+    // come first in tile order except that a ragged last tile keeps its place
+    // at the end; see tile_of below.
+    float da_acc = 0.0f;
+    auto issue = [&](auto buf, int t) {
+        constexpr int B_ = decltype(buf)::value;
+        const int q0 = k0 + PAT_BM * t;
+        tile_load_lds<T>(B_ ? g1 : g0, rg, q0, w, lane);
+        // Five 64-entry copies: LSE rows, D rows, three parts of the r band
+        // (offsets q0 - k0 - 127 .. q0 - k0 + 64; negative ones arrive as 0).
+        float* rows = B_ ? rows1 : rows0;
+        float* band = B_ ? band1 : band0;
+        if (w == 0) {
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rl, (lds_void*)rows, 4, (q0 + lane) * 4, 0, 0, 0);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rd, (lds_void*)(rows + PAT_BM), 4, (q0 + lane) * 4, 0, 0, 0);
+        } else {
+            const int off = q0 - k0 - (PAT_BN - 1) + 64 * (w - 1) + lane;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rr, (lds_void*)(band + 64 * (w - 1)), 4, off * 4, 0, 0, 0);
+        }
+    };
+    auto flush = [&](int lo, int count) {
+        // Offsets lo .. lo+count-1 are final: add them to dr and clear them.
+        if (tid < count) {
+            const int delta = lo + tid;
+            if (delta >= 0 && delta < N) {
+                const int s = delta & (PAT_RING - 1);
+                const float v = ring[s];
+                if (v != 0.0f) atomicAdd(p.dr + (size_t)h * N + delta, v);
+                ring[s] = 0.0f;
+            }
+        }
+    };
+    auto compute = [&](auto buf, int t, auto mask) {
+        constexpr int B_ = decltype(buf)::value;
+        if (t >= 1) flush(PAT_BM * t - (PAT_BM + PAT_BN - 1), PAT_BM);  // final after tile t-1
+        pat_tile<T, decltype(mask)::value>(B_ ? g1 : g0, B_ ? rows1 : rows0, B_ ? band1 : band0, ring, t,
+                                           k0 + PAT_BM * t, k0, w, c, hf, N, vf, a_key, da_acc);
+    };
+    // Tiles in order; the masked ones are the first n_mask and, if ragged, the
+    // last.  run_slots wants the masked slots first, so a ragged tail is given
+    // its own masked pass after the others.
+    const int n_plain_end = ragged_end && n_tiles > n_mask ? n_tiles - 1 : n_tiles;
+    const int P = (n_mask + 1) & ~1;
+    run_slots(
+        P, P + (n_plain_end - n_mask), [&](int i) { return i < P ? (i < n_mask ? i : -1) : n_mask + (i - P); },
+        issue, [&](auto) {}, compute);
+    int t_last = n_plain_end - 1;
+    if (n_plain_end < n_tiles) {
+        // The ragged last tile, masked, in a pass of its own (buffer 0 is free
+        // after the barrier that closed the last slot).
+        issue(Buf0{}, n_tiles - 1);
+        __syncthreads();
+        compute(Buf0{}, n_tiles - 1, std::true_type{});
+        __syncthreads();
+        t_last = n_tiles - 1;
+    }
+    flush(PAT_BM * t_last - (PAT_BN - 1), PAT_BM + PAT_BN - 1);
+    const float da_key = pair_sum(da_acc);
+    if (hf == 0 && key < N) atomicAdd(p.da + (size_t)h * N + key, da_key);
+}
+
+__global__ void pat_fill_kernel(float* p, size_t n) {
+    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+        p[i] = 0.0f;
+}
+
+}  // namespace saf

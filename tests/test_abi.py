@@ -179,3 +179,34 @@ def test_calib_finalize_rejects_bad_arguments(lib):
     assert _fin(lib, ws=FAKE + 16) == 6
     assert _fin(lib, ws_bytes=8) == 2
     assert _fin(lib, H=0, mean=None) == 0
+
+
+# ---------------------------------------------------------------------------
+# Trainable-pattern gradients (saf_hybrid_attn_bwd_pattern)
+# ---------------------------------------------------------------------------
+
+def _pat(lib, dt=1, V=FAKE, O=FAKE, dO=FAKE, LSE=FAKE, flags=(0, 1), a=FAKE, r=FAKE, ld=None, B=1, N=8, d=64,
+         da=FAKE, dr=FAKE, ws=FAKE, ws_bytes=None):
+    f = np.asarray(flags, dtype=np.uint8)
+    H = f.shape[0]
+    ld = N if ld is None else ld
+    if ws_bytes is None:
+        ws_bytes = lib.saf_hybrid_attn_bwd_workspace_bytes(dt, max(B, 1), max(H, 1), max(N, 1), 64)
+    return lib.saf_hybrid_attn_bwd_pattern(dt, V, O, dO, LSE, f.ctypes.data if H else None, a, r, ld, B, H, N, d,
+                                           da, dr, ws, ws_bytes, None)
+
+
+def test_pattern_gradient_rejects_bad_arguments(lib):
+    assert _pat(lib, dt=5) == 3
+    assert _pat(lib, d=32) == 3
+    assert _pat(lib, flags=(0, 2)) == 7
+    assert _pat(lib, a=None) == 4
+    assert _pat(lib, ld=4) == 2
+    assert _pat(lib, V=None) == 1
+    assert _pat(lib, da=None) == 1
+    assert _pat(lib, dr=None) == 1
+    assert _pat(lib, ws=None) == 1
+    assert _pat(lib, O=FAKE + 8) == 6
+    assert _pat(lib, ws=FAKE + 64) == 6
+    assert _pat(lib, ws_bytes=16) == 2
+    assert _pat(lib, B=0, V=None, O=None, dO=None, LSE=None, da=None, dr=None, ws=None) == 0
