@@ -155,14 +155,18 @@ saf_status_t saf_hybrid_attn_bwd_stage(saf_bwd_stage_t stage, saf_dtype_t dt,
  *   V, O, dO  : [B,H,N,d] `dt` (O and LSE as written by the forward).
  *   LSE       : [B,H,N] float32 from the forward (log Z for fixed heads).
  *   da, dr    : DEVICE [H, N] float32, written; rows of ordinary heads are 0.
- *               Sums over batch elements and key blocks are gathered with
- *               float32 atomic adds, so their last bits may depend on the
- *               order in which workgroups finish.
- *   workspace : DEVICE, >= saf_hybrid_attn_bwd_workspace_bytes(), 256-byte
- *               aligned, contents on entry ignored.
- * Four launches: two zero fills, the row pre-pass D for the fixed heads, and
- * one workgroup per (batch element, fixed head, block of 128 keys).
+ *               Partial sums per batch element and block of 128 keys go to
+ *               the workspace and are added in a fixed order: the result does
+ *               not depend on scheduling.
+ *   workspace : DEVICE, >= saf_hybrid_attn_bwd_pattern_workspace_bytes(),
+ *               256-byte aligned, contents on entry ignored (about
+ *               B * H * N^2 / 64 bytes: 25 MB at B = 8, H = 12, N = 4096).
+ * Five launches: two zero fills, the row pre-pass D for the fixed heads, one
+ * workgroup per (batch element, fixed head, block of 128 keys), and the
+ * reduction of the partial sums.
  */
+size_t saf_hybrid_attn_bwd_pattern_workspace_bytes(saf_dtype_t dt, int B, int H, int N, int d);
+
 saf_status_t saf_hybrid_attn_bwd_pattern(saf_dtype_t dt,
                                          const void* V, const void* O, const void* dO,
                                          const float* LSE,

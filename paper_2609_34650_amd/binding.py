@@ -42,6 +42,7 @@ EXPORTS = (
     "saf_hybrid_attn_bwd_workspace_bytes",
     "saf_hybrid_attn_bwd",
     "saf_hybrid_attn_bwd_stage",
+    "saf_hybrid_attn_bwd_pattern_workspace_bytes",
     "saf_hybrid_attn_bwd_pattern",
     "saf_status_str",
     "saf_calib_accumulate",
@@ -84,6 +85,8 @@ def load() -> ctypes.CDLL:
     lib.saf_hybrid_attn_bwd.argtypes = bwd_args
     lib.saf_hybrid_attn_bwd_stage.restype = ctypes.c_int
     lib.saf_hybrid_attn_bwd_stage.argtypes = [i] + bwd_args
+    lib.saf_hybrid_attn_bwd_pattern_workspace_bytes.restype = ctypes.c_size_t
+    lib.saf_hybrid_attn_bwd_pattern_workspace_bytes.argtypes = [i, i, i, i, i]
     lib.saf_hybrid_attn_bwd_pattern.restype = ctypes.c_int
     lib.saf_hybrid_attn_bwd_pattern.argtypes = [i, vp, vp, vp, vp, u8p, vp, vp, i, i, i, i, i, vp, vp, vp,
                                                 ctypes.c_size_t, vp]
@@ -271,7 +274,8 @@ def saf_hybrid_attn_bwd_pattern(V, O, dO, LSE, head_is_fixed, a, r, da=None, dr=
     dr = torch.empty((H, N), dtype=torch.float32, device=dev) if dr is None else dr
     _check_act("da", da, (H, N), torch.float32, dev)
     _check_act("dr", dr, (H, N), torch.float32, dev)
-    nbytes = saf_hybrid_attn_bwd_workspace_bytes(V.dtype, B, H, N, d)
+    code = SAF_DTYPE_BF16 if V.dtype == torch.bfloat16 else SAF_DTYPE_F32
+    nbytes = int(lib.saf_hybrid_attn_bwd_pattern_workspace_bytes(code, B, H, N, d))
     if workspace is None:
         workspace = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=dev)
     flags = _flags(head_is_fixed, H)

@@ -64,6 +64,19 @@ saf_status_t check_common(saf_dtype_t dt, const uint8_t* head_is_fixed, const fl
 
 saf_status_t launched() { return hipGetLastError() == hipSuccess ? SAF_OK : SAF_ERR_LAUNCH; }
 
+// Pattern gradients: D [B,H,N], then da partials [B,H,N], then dr partials
+// [B,H,R] with R = sum over key blocks of (N - 128 J) (H bounds the number of
+// fixed heads), each part 256-byte aligned.
+size_t pattern_rows_total(int N) {
+    const size_t nj = (size_t)((N + saf::PAT_BN - 1) / saf::PAT_BN);
+    return nj * (size_t)N - (size_t)saf::PAT_BN * (nj * (nj - 1) / 2);
+}
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+size_t pattern_workspace_bytes(int B, int H, int N) {
+    const size_t bh = (size_t)B * H;
+    return align256(bh * N * 4) + align256(bh * N * 4) + align256(bh * pattern_rows_total(N) * 4);
+}
+
 template <typename T>
 saf_status_t launch_fwd(const saf::FwdArgs& args, hipStream_t stream) {
     if (args.fixed_mask) {
@@ -266,6 +279,12 @@ SAF_EXPORT saf_status_t saf_hybrid_attn_bwd(saf_dtype_t dt, const void* Q, const
     return SAF_OK;
 }
 
+SAF_EXPORT size_t saf_hybrid_attn_bwd_pattern_workspace_bytes(saf_dtype_t dt, int B, int H, int N, int d) {
+    if (dt != SAF_DTYPE_F32 && dt != SAF_DTYPE_BF16) return 0;
+    if (B <= 0 || H <= 0 || N <= 0 || d != saf::HEAD_DIM || H > 64 || N > kMaxN) return 0;
+    return pattern_workspace_bytes(B, H, N);
+}
+
 SAF_EXPORT saf_status_t saf_hybrid_attn_bwd_pattern(saf_dtype_t dt, const void* V, const void* O, const void* dO,
                                                     const float* LSE, const uint8_t* head_is_fixed, const float* a,
                                                     const float* r, int ld_prior, int B, int H, int N, int d,
@@ -280,7 +299,7 @@ SAF_EXPORT saf_status_t saf_hybrid_attn_bwd_pattern(saf_dtype_t dt, const void* 
     if (!aligned16(V) || !aligned16(O) || !aligned16(dO) || !aligned16(LSE) ||
         (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
         return SAF_ERR_ALIGNMENT;
-    if (workspace_bytes_given < workspace_bytes(B, H, N)) return SAF_ERR_SHAPE;
+    if ((size_t)H * N > INT32_MAX || workspace_bytes_given < pattern_workspace_bytes(B, H, N)) return SAF_ERR_SHAPE;
     const size_t n_out = (size_t)H * N;
     hipLaunchKernelGGL(saf::pat_fill_kernel, dim3(fill_grid(n_out)), dim3(256), 0, stream, da, n_out);
     hipLaunchKernelGGL(saf::pat_fill_kernel, dim3(fill_grid(n_out)), dim3(256), 0, stream, dr, n_out);
@@ -298,7 +317,12 @@ SAF_EXPORT saf_status_t saf_hybrid_attn_bwd_pattern(saf_dtype_t dt, const void* 
     pa.v = V;
     pa.dO = dO;
     pa.lse = LSE;
-    pa.dsum = reinterpret_cast<const float*>(workspace);
+    char* wsb = reinterpret_cast<char*>(workspace);
+    const size_t bhn = align256((size_t)B * H * N * 4);
+    pa.dsum = reinterpret_cast<const float*>(wsb);
+    pa.da_part = reinterpret_cast<float*>(wsb + bhn);
+    pa.dr_part = reinterpret_cast<float*>(wsb + 2 * bhn);
+    pa.dr_row_total = pattern_rows_total(N);
     pa.a = a;
     pa.r = r;
     pa.da = da;
@@ -316,6 +340,9 @@ SAF_EXPORT saf_status_t saf_hybrid_attn_bwd_pattern(saf_dtype_t dt, const void* 
         hipLaunchKernelGGL(saf::bwd_pattern_kernel<saf::bf16>, dim3(grid), dim3(saf::PAT_THREADS), 0, stream, pa);
     else
         hipLaunchKernelGGL(saf::bwd_pattern_kernel<float>, dim3(grid), dim3(saf::PAT_THREADS), 0, stream, pa);
+    if (launched() != SAF_OK) return SAF_ERR_LAUNCH;
+    const unsigned rgrid = (unsigned)((size_t)pa.n_fixed * ((N + 255) / 256));
+    hipLaunchKernelGGL(saf::pat_reduce_kernel, dim3(rgrid), dim3(256), 0, stream, pa);
     return launched();
 }
 

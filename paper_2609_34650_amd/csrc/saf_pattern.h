@@ -13,14 +13,23 @@
 // so a lane's accumulator entries are 16 queries of its key: dL summed down
 // the lane is the key's share of da.  P is recomputed per entry as
 // exp(a[j] + r[i - j] - log Z(i)) with log Z from the forward's LSE and the
-// offsets' r values from an LDS band copied per tile.  dr gathers dL by
-// offset in an LDS ring of 256 floats indexed by delta mod 256 (LDS atomic
-// adds): tile t touches offsets 64t - 127 .. 64t + 63, so once tile t is done
-// the offsets below 64(t+1) - 127 are final; the next tile flushes them to
-// dr with global atomic adds and clears their slots, which the tile after it
-// is the first to reuse.  The dO tile, the tile's LSE and D rows and the r
-// band are copied by buffer loads straight to LDS (rows or offsets outside
-// 0 .. N-1 arrive as 0 and are masked), double-buffered over tiles.
+// offsets' r values from an LDS band copied per tile.  dr needs sums along
+// the diagonals of each 32 x 32 block of dL: a wavefront writes the block
+// into its own LDS scratch (column-major, rows padded to 36 floats), then lane
+// d (0..62) walks diagonal d - 31 (address stride 37, so the 64 lanes hit 64
+// different banks) and adds the sum into the wavefront's ring of 256 floats
+// indexed by offset mod 256 (distinct lanes, distinct slots: no atomics; LDS
+// atomic adds per entry were six times slower than the whole rest of the
+// kernel).  Tile t touches offsets 64t - 127 .. 64t + 63, so once tile t is
+// done the offsets below 64(t+1) - 127 are final; the next tile stores their
+// sum over the four rings into the workgroup's own row of partial sums and
+// clears the slots, which the tile after it is the first to reuse.  Plain stores, no global atomics:
+// every workgroup of a head reaches the same offsets at about the same time,
+// and atomic adds on one address serialise.  A second kernel sums the partial
+// rows over batch elements and key blocks (and the da partials over batch
+// elements).  The dO tile, the tile's LSE and D rows and the r band are
+// copied by buffer loads straight to LDS (rows or offsets outside 0 .. N-1
+// arrive as 0 and are masked), double-buffered over tiles.
 #pragma once
 
 #include "saf_common.h"
@@ -32,6 +41,7 @@ constexpr int PAT_BM = TILE_ROWS;  // queries per tile
 constexpr int PAT_THREADS = 256;
 constexpr int PAT_BAND = 192;    // r entries per tile (offsets 64t - 127 .. 64t + 64)
 constexpr int PAT_RING = 256;    // dr ring slots
+constexpr int PAT_SCR = 36;      // scratch column stride (floats): 16-byte aligned columns
 static_assert(PAT_BM + PAT_BN - 1 <= PAT_BAND, "a tile's offsets fit in the band");
 static_assert(PAT_BAND + PAT_BM <= PAT_RING, "live offsets never share a ring slot");
 
@@ -44,15 +54,24 @@ struct PatArgs {
     const float* r;
     float* da;           // [H, N]
     float* dr;           // [H, N]
+    float* da_part;      // [B, n_fixed, N]
+    float* dr_part;      // [B, n_fixed, R]: per key block J a row of N - 128 J offsets
+    size_t dr_row_total; // R = sum over key blocks of (N - 128 J)
     int B, H, N, ld_prior, n_fixed, n_kblocks;
     unsigned char heads[64];  // the fixed heads
 };
 
+// First entry of key block J's row in one (batch, fixed head) part of dr_part.
+__host__ __device__ inline size_t pat_row_base(int J, int N) {
+    return (size_t)J * N - (size_t)PAT_BN * ((size_t)J * (J - 1) / 2);
+}
+
 // One query tile t (queries q0 .. q0+63, q0 = k0 + 64 t) against the
 // wavefront's 32 keys.  MASK: the tile meets the diagonal or runs past N.
+// scr: the wavefront's 32 x PAT_SCR scratch; ring: its 256 offset slots.
 template <typename T, bool MASK>
-__device__ __forceinline__ void pat_tile(const T* gt, const float* rows, const float* band, float* ring, int t,
-                                         int q0, int k0, int w, int c, int hf, int N,
+__device__ __forceinline__ void pat_tile(const T* gt, const float* rows, const float* band, float* scr, float* ring,
+                                         int t, int q0, int k0, int w, int c, int hf, int lane, int N,
                                          const typename Vec<T>::x8 (&vf)[4], float a_key, float& da_acc) {
 #pragma unroll
     for (int rb = 0; rb < 2; ++rb) {
@@ -67,6 +86,7 @@ __device__ __forceinline__ void pat_tile(const T* gt, const float* rows, const f
         for (int g = 0; g < 4; ++g) {
             const f32x4 l4 = *reinterpret_cast<const f32x4*>(rows + 32 * rb + 8 * g + 4 * hf);
             const f32x4 d4 = *reinterpret_cast<const f32x4*>(rows + PAT_BM + 32 * rb + 8 * g + 4 * hf);
+            f32x4 dl4;
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
                 const int v = 4 * g + u;
@@ -76,10 +96,22 @@ __device__ __forceinline__ void pat_tile(const T* gt, const float* rows, const f
                 if (MASK && (ql < 32 * w + c - 64 * t || q0 + ql >= N)) pv = 0.0f;
                 const float dl = pv * (dp[v] - d4[u]);
                 da_acc += dl;
-                const int delta = 64 * t + ql - 32 * w - c;
-                atomicAdd(ring + (delta & (PAT_RING - 1)), dl);
+                dl4[u] = dl;
             }
+            // Block row 8g + 4hf + u of column c.
+            *reinterpret_cast<f32x4*>(scr + c * PAT_SCR + 8 * g + 4 * hf) = dl4;
         }
+        // Lane d sums block diagonal d - 31 (row - column); the wavefront's
+        // own LDS writes above are visible to its later reads.
+        const int d = lane - 31;
+        float sum = 0.0f;
+#pragma unroll
+        for (int k = 0; k < 32; ++k) {
+            const int row = k + d;  // entry (row, column k)
+            if (row >= 0 && row < 32) sum += scr[k * PAT_SCR + row];
+        }
+        const int delta = 64 * t + 32 * rb - 32 * w + d;
+        if (lane < 63 && delta >= 0) ring[delta & (PAT_RING - 1)] += sum;
     }
 }
 
@@ -91,13 +123,15 @@ __global__ __launch_bounds__(PAT_THREADS) void bwd_pattern_kernel(PatArgs p) {
     __shared__ __attribute__((aligned(16))) float rows1[2 * PAT_BM];
     __shared__ __attribute__((aligned(16))) float band0[PAT_BAND];
     __shared__ __attribute__((aligned(16))) float band1[PAT_BAND];
-    __shared__ float ring[PAT_RING];
+    __shared__ __attribute__((aligned(16))) float scratch[4][32 * PAT_SCR];
+    __shared__ float ring[4][PAT_RING];
 
     const int per_block = p.B * p.n_fixed;
     const int kblk = (int)(blockIdx.x / per_block);  // ascending: longest first
     const int rem = (int)(blockIdx.x % per_block);
     const int b = rem / p.n_fixed;
-    const int h = p.heads[rem % p.n_fixed];
+    const int hidx = rem % p.n_fixed;
+    const int h = p.heads[hidx];
     const int tid = threadIdx.x;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int lane = tid & 63;
@@ -111,7 +145,7 @@ __global__ __launch_bounds__(PAT_THREADS) void bwd_pattern_kernel(PatArgs p) {
     const float* arow = p.a + (size_t)h * p.ld_prior;
     const float* rrow = p.r + (size_t)h * p.ld_prior;
 
-    for (int i = tid; i < PAT_RING; i += PAT_THREADS) ring[i] = 0.0f;
+    for (int i = tid; i < 4 * PAT_RING; i += PAT_THREADS) ring[i / PAT_RING][i % PAT_RING] = 0.0f;
     typedef typename Vec<T>::x8 frag;
     frag vf[4];
 #pragma unroll
@@ -129,9 +163,6 @@ __global__ __launch_bounds__(PAT_THREADS) void bwd_pattern_kernel(PatArgs p) {
     const int n_tiles = (N - k0 + PAT_BM - 1) / PAT_BM;
     const int n_mask = min(PAT_BN / PAT_BM, n_tiles);
     const bool ragged_end = (N - k0) % PAT_BM != 0;  // the last tile runs past N
-    // Slots: masked tiles (the diagonal ones, then the last one if ragged)
-    // come first in tile order except that a ragged last tile keeps its place
-    // at the end; see tile_of below.
     float da_acc = 0.0f;
     auto issue = [&](auto buf, int t) {
         constexpr int B_ = decltype(buf)::value;
@@ -149,23 +180,27 @@ __global__ __launch_bounds__(PAT_THREADS) void bwd_pattern_kernel(PatArgs p) {
             __builtin_amdgcn_raw_ptr_buffer_load_lds(rr, (lds_void*)(band + 64 * (w - 1)), 4, off * 4, 0, 0, 0);
         }
     };
+    float* dr_row = p.dr_part + (size_t)(b * p.n_fixed + hidx) * p.dr_row_total + pat_row_base(kblk, N);
+    const int max_delta = N - 1 - k0;
     auto flush = [&](int lo, int count) {
-        // Offsets lo .. lo+count-1 are final: add them to dr and clear them.
+        // Offsets lo .. lo+count-1 are final: store them and clear their slots.
         if (tid < count) {
             const int delta = lo + tid;
-            if (delta >= 0 && delta < N) {
+            if (delta >= 0 && delta <= max_delta) {
                 const int s = delta & (PAT_RING - 1);
-                const float v = ring[s];
-                if (v != 0.0f) atomicAdd(p.dr + (size_t)h * N + delta, v);
-                ring[s] = 0.0f;
+                dr_row[delta] = (ring[0][s] + ring[1][s]) + (ring[2][s] + ring[3][s]);
+                ring[0][s] = 0.0f;
+                ring[1][s] = 0.0f;
+                ring[2][s] = 0.0f;
+                ring[3][s] = 0.0f;
             }
         }
     };
     auto compute = [&](auto buf, int t, auto mask) {
         constexpr int B_ = decltype(buf)::value;
         if (t >= 1) flush(PAT_BM * t - (PAT_BM + PAT_BN - 1), PAT_BM);  // final after tile t-1
-        pat_tile<T, decltype(mask)::value>(B_ ? g1 : g0, B_ ? rows1 : rows0, B_ ? band1 : band0, ring, t,
-                                           k0 + PAT_BM * t, k0, w, c, hf, N, vf, a_key, da_acc);
+        pat_tile<T, decltype(mask)::value>(B_ ? g1 : g0, B_ ? rows1 : rows0, B_ ? band1 : band0, scratch[w],
+                                           ring[w], t, k0 + PAT_BM * t, k0, w, c, hf, lane, N, vf, a_key, da_acc);
     };
     // Tiles in order; the masked ones are the first n_mask and, if ragged, the
     // last.  run_slots wants the masked slots first, so a ragged tail is given
@@ -187,7 +222,29 @@ __global__ __launch_bounds__(PAT_THREADS) void bwd_pattern_kernel(PatArgs p) {
     }
     flush(PAT_BM * t_last - (PAT_BN - 1), PAT_BM + PAT_BN - 1);
     const float da_key = pair_sum(da_acc);
-    if (hf == 0 && key < N) atomicAdd(p.da + (size_t)h * N + key, da_key);
+    if (hf == 0 && key < N) p.da_part[(size_t)(b * p.n_fixed + hidx) * N + key] = da_key;
+}
+
+// da[h][j] = sum_b da_part, dr[h][delta] = sum over b and the key blocks J
+// with 128 J <= N - 1 - delta of dr_part.  One thread per (fixed head,
+// position); consecutive threads read consecutive addresses.
+__global__ __launch_bounds__(256) void pat_reduce_kernel(PatArgs p) {
+    const int per_head = (p.N + 255) / 256;
+    const int hidx = (int)(blockIdx.x / per_head);
+    const int x = (int)(blockIdx.x % per_head) * 256 + (int)threadIdx.x;
+    if (x >= p.N) return;
+    const int h = p.heads[hidx];
+    const int N = p.N;
+    float sa = 0.0f, sr = 0.0f;
+    const int j_max = (N - 1 - x) / PAT_BN;  // key blocks that reach offset x
+    for (int b = 0; b < p.B; ++b) {
+        const size_t part = (size_t)(b * p.n_fixed + hidx);
+        sa += p.da_part[part * N + x];
+        const float* rows = p.dr_part + part * p.dr_row_total;
+        for (int J = 0; J <= j_max; ++J) sr += rows[pat_row_base(J, N) + x];
+    }
+    p.da[(size_t)h * N + x] = sa;
+    p.dr[(size_t)h * N + x] = sr;
 }
 
 __global__ void pat_fill_kernel(float* p, size_t n) {

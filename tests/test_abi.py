@@ -191,7 +191,7 @@ def _pat(lib, dt=1, V=FAKE, O=FAKE, dO=FAKE, LSE=FAKE, flags=(0, 1), a=FAKE, r=F
     H = f.shape[0]
     ld = N if ld is None else ld
     if ws_bytes is None:
-        ws_bytes = lib.saf_hybrid_attn_bwd_workspace_bytes(dt, max(B, 1), max(H, 1), max(N, 1), 64)
+        ws_bytes = lib.saf_hybrid_attn_bwd_pattern_workspace_bytes(dt, max(B, 1), max(H, 1), max(N, 1), 64)
     return lib.saf_hybrid_attn_bwd_pattern(dt, V, O, dO, LSE, f.ctypes.data if H else None, a, r, ld, B, H, N, d,
                                            da, dr, ws, ws_bytes, None)
 
@@ -209,4 +209,9 @@ def test_pattern_gradient_rejects_bad_arguments(lib):
     assert _pat(lib, O=FAKE + 8) == 6
     assert _pat(lib, ws=FAKE + 64) == 6
     assert _pat(lib, ws_bytes=16) == 2
+    # D, da partials and one partial row per key block (lengths N, N-128, ...).
+    need = lib.saf_hybrid_attn_bwd_pattern_workspace_bytes(1, 2, 3, 300, 64)
+    rows = 300 + 172 + 44
+    assert need >= 2 * 3 * 300 * 4 * 2 + 2 * 3 * rows * 4 and need % 256 == 0
+    assert _pat(lib, ws_bytes=lib.saf_hybrid_attn_bwd_pattern_workspace_bytes(1, 1, 2, 8, 64) - 1) == 2
     assert _pat(lib, B=0, V=None, O=None, dO=None, LSE=None, da=None, dr=None, ws=None) == 0
