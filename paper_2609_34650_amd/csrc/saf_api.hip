@@ -64,17 +64,28 @@ saf_status_t check_common(saf_dtype_t dt, const uint8_t* head_is_fixed, const fl
 
 saf_status_t launched() { return hipGetLastError() == hipSuccess ? SAF_OK : SAF_ERR_LAUNCH; }
 
-// Pattern gradients: D [B,H,N], then da partials [B,H,N], then dr partials
-// [B,H,R] with R = sum over key blocks of (N - 128 J) (H bounds the number of
-// fixed heads), each part 256-byte aligned.
-size_t pattern_rows_total(int N) {
-    const size_t nj = (size_t)((N + saf::PAT_BN - 1) / saf::PAT_BN);
-    return nj * (size_t)N - (size_t)saf::PAT_BN * (nj * (nj - 1) / 2);
+// Pattern gradients: D [B,H,N], then da partials [B,H,chunks,N], then dr
+// partials [B,H,key blocks,chunks,64*chunk_tiles+127] (H bounds the number of
+// fixed heads), each part 256-byte aligned.  Chunks of 16 query tiles, more
+// when N is so long that the grid's y extent would pass 1024.
+struct PatGeom {
+    int n_kblocks, chunk_tiles, n_chunks, part_len;
+};
+PatGeom pattern_geometry(int N) {
+    PatGeom g;
+    g.n_kblocks = (N + saf::PAT_BN - 1) / saf::PAT_BN;
+    const int tiles = (N + saf::PAT_BM - 1) / saf::PAT_BM;
+    g.chunk_tiles = tiles > 16 * 1024 ? (tiles + 1023) / 1024 : 16;
+    g.n_chunks = (tiles + g.chunk_tiles - 1) / g.chunk_tiles;
+    g.part_len = saf::PAT_BM * g.chunk_tiles + saf::PAT_BN - 1;
+    return g;
 }
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 size_t pattern_workspace_bytes(int B, int H, int N) {
+    const PatGeom g = pattern_geometry(N);
     const size_t bh = (size_t)B * H;
-    return align256(bh * N * 4) + align256(bh * N * 4) + align256(bh * pattern_rows_total(N) * 4);
+    return align256(bh * N * 4) + align256(bh * g.n_chunks * N * 4) +
+           align256(bh * g.n_kblocks * g.n_chunks * (size_t)g.part_len * 4);
 }
 
 template <typename T>
@@ -299,7 +310,8 @@ SAF_EXPORT saf_status_t saf_hybrid_attn_bwd_pattern(saf_dtype_t dt, const void* 
     if (!aligned16(V) || !aligned16(O) || !aligned16(dO) || !aligned16(LSE) ||
         (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
         return SAF_ERR_ALIGNMENT;
-    if ((size_t)H * N > INT32_MAX || workspace_bytes_given < pattern_workspace_bytes(B, H, N)) return SAF_ERR_SHAPE;
+    if ((size_t)H * N > INT32_MAX || B > 65535 || workspace_bytes_given < pattern_workspace_bytes(B, H, N))
+        return SAF_ERR_SHAPE;
     const size_t n_out = (size_t)H * N;
     hipLaunchKernelGGL(saf::pat_fill_kernel, dim3(fill_grid(n_out)), dim3(256), 0, stream, da, n_out);
     hipLaunchKernelGGL(saf::pat_fill_kernel, dim3(fill_grid(n_out)), dim3(256), 0, stream, dr, n_out);
@@ -317,12 +329,16 @@ SAF_EXPORT saf_status_t saf_hybrid_attn_bwd_pattern(saf_dtype_t dt, const void* 
     pa.v = V;
     pa.dO = dO;
     pa.lse = LSE;
+    const PatGeom geo = pattern_geometry(N);
     char* wsb = reinterpret_cast<char*>(workspace);
     const size_t bhn = align256((size_t)B * H * N * 4);
+    const size_t dab = align256((size_t)B * H * geo.n_chunks * N * 4);
     pa.dsum = reinterpret_cast<const float*>(wsb);
     pa.da_part = reinterpret_cast<float*>(wsb + bhn);
-    pa.dr_part = reinterpret_cast<float*>(wsb + 2 * bhn);
-    pa.dr_row_total = pattern_rows_total(N);
+    pa.dr_part = reinterpret_cast<float*>(wsb + bhn + dab);
+    pa.chunk_tiles = geo.chunk_tiles;
+    pa.n_chunks = geo.n_chunks;
+    pa.part_len = geo.part_len;
     pa.a = a;
     pa.r = r;
     pa.da = da;
@@ -334,15 +350,15 @@ SAF_EXPORT saf_status_t saf_hybrid_attn_bwd_pattern(saf_dtype_t dt, const void* 
     pa.n_fixed = 0;
     for (int h = 0; h < H; ++h)
         if ((pr.fixed_mask >> h) & 1ull) pa.heads[pa.n_fixed++] = (unsigned char)h;
-    pa.n_kblocks = (N + saf::PAT_BN - 1) / saf::PAT_BN;
-    const unsigned grid = (unsigned)((size_t)pa.n_kblocks * B * pa.n_fixed);
+    pa.n_kblocks = geo.n_kblocks;
+    const dim3 grid((unsigned)((size_t)pa.n_kblocks * B * pa.n_fixed), (unsigned)geo.n_chunks);
     if (dt == SAF_DTYPE_BF16)
-        hipLaunchKernelGGL(saf::bwd_pattern_kernel<saf::bf16>, dim3(grid), dim3(saf::PAT_THREADS), 0, stream, pa);
+        hipLaunchKernelGGL(saf::bwd_pattern_kernel<saf::bf16>, grid, dim3(saf::PAT_THREADS), 0, stream, pa);
     else
-        hipLaunchKernelGGL(saf::bwd_pattern_kernel<float>, dim3(grid), dim3(saf::PAT_THREADS), 0, stream, pa);
+        hipLaunchKernelGGL(saf::bwd_pattern_kernel<float>, grid, dim3(saf::PAT_THREADS), 0, stream, pa);
     if (launched() != SAF_OK) return SAF_ERR_LAUNCH;
-    const unsigned rgrid = (unsigned)((size_t)pa.n_fixed * ((N + 255) / 256));
-    hipLaunchKernelGGL(saf::pat_reduce_kernel, dim3(rgrid), dim3(256), 0, stream, pa);
+    const dim3 rgrid((unsigned)((size_t)pa.n_fixed * ((N + 255) / 256)), (unsigned)B);
+    hipLaunchKernelGGL(saf::pat_reduce_kernel, rgrid, dim3(256), 0, stream, pa);
     return launched();
 }
 

@@ -6,9 +6,11 @@
 //     da[j] = sum_i dL(i, j),  dr[delta] = sum_{i - j = delta} dL(i, j),
 // each summed over the batch (a and r are shared by every batch element).
 //
-// Workgroup = (batch b, fixed head, block of 128 keys), 4 wavefronts of 32
-// keys (one per lane column c), streaming query tiles of 64 rows from the
-// block's first key to N.  dP comes from the MFMA with dO rows as the A
+// Workgroup = (batch b, fixed head, block of 128 keys, chunk of query
+// tiles), 4 wavefronts of 32 keys (one per lane column c), streaming the
+// chunk's query tiles of 64 rows (the block's tiles run from its first key to
+// N; cutting them into chunks of at most 16 tiles keeps the workgroups of the
+// first key blocks from setting the kernel's duration alone).  dP comes from the MFMA with dO rows as the A
 // operand (from LDS) and the wavefront's V rows as the B operand (registers),
 // so a lane's accumulator entries are 16 queries of its key: dL summed down
 // the lane is the key's share of da.  P is recomputed per entry as
@@ -54,16 +56,19 @@ struct PatArgs {
     const float* r;
     float* da;           // [H, N]
     float* dr;           // [H, N]
-    float* da_part;      // [B, n_fixed, N]
-    float* dr_part;      // [B, n_fixed, R]: per key block J a row of N - 128 J offsets
-    size_t dr_row_total; // R = sum over key blocks of (N - 128 J)
+    float* da_part;      // [B, n_fixed, n_chunks, N]: per chunk, its key block's keys
+    float* dr_part;      // [B, n_fixed, n_kblocks, n_chunks, part_len]: per chunk, its offsets
     int B, H, N, ld_prior, n_fixed, n_kblocks;
+    int chunk_tiles;     // query tiles per chunk
+    int n_chunks;        // chunks of the longest key block (the grid's y extent)
+    int part_len;        // 64 * chunk_tiles + 127: offsets one chunk touches
     unsigned char heads[64];  // the fixed heads
 };
 
-// First entry of key block J's row in one (batch, fixed head) part of dr_part.
-__host__ __device__ inline size_t pat_row_base(int J, int N) {
-    return (size_t)J * N - (size_t)PAT_BN * ((size_t)J * (J - 1) / 2);
+// Query tiles of key block J, and its chunks.
+__host__ __device__ inline int pat_tiles(int J, int N) { return (N - J * PAT_BN + PAT_BM - 1) / PAT_BM; }
+__host__ __device__ inline int pat_chunks(int J, int N, int chunk_tiles) {
+    return (pat_tiles(J, N) + chunk_tiles - 1) / chunk_tiles;
 }
 
 // One query tile t (queries q0 .. q0+63, q0 = k0 + 64 t) against the
@@ -129,6 +134,12 @@ __global__ __launch_bounds__(PAT_THREADS) void bwd_pattern_kernel(PatArgs p) {
     const int per_block = p.B * p.n_fixed;
     const int kblk = (int)(blockIdx.x / per_block);  // ascending: longest first
     const int rem = (int)(blockIdx.x % per_block);
+    const int chunk = (int)blockIdx.y;
+    const int N = p.N;
+    const int n_tiles = pat_tiles(kblk, N);
+    const int t0 = chunk * p.chunk_tiles;  // this chunk's tiles: t0 .. t1-1
+    if (t0 >= n_tiles) return;             // the key block ends before this chunk
+    const int t1 = min(t0 + p.chunk_tiles, n_tiles);
     const int b = rem / p.n_fixed;
     const int hidx = rem % p.n_fixed;
     const int h = p.heads[hidx];
@@ -137,7 +148,6 @@ __global__ __launch_bounds__(PAT_THREADS) void bwd_pattern_kernel(PatArgs p) {
     const int lane = tid & 63;
     const int c = tid & 31;
     const int hf = (tid >> 5) & 1;
-    const int N = p.N;
     const int k0 = kblk * PAT_BN;
     const int key = k0 + 32 * w + c;
     const size_t slice = (size_t)(b * p.H + h) * N;
@@ -160,9 +170,10 @@ __global__ __launch_bounds__(PAT_THREADS) void bwd_pattern_kernel(PatArgs p) {
     const __amdgpu_buffer_rsrc_t rr =
         __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(rrow), (short)0, N * 4, 0x00020000);
 
-    const int n_tiles = (N - k0 + PAT_BM - 1) / PAT_BM;
-    const int n_mask = min(PAT_BN / PAT_BM, n_tiles);
-    const bool ragged_end = (N - k0) % PAT_BM != 0;  // the last tile runs past N
+    // Masked tiles: the two that meet the diagonal (first chunk only) and a
+    // last tile that runs past N (last chunk only).
+    const int m_lo = t0 == 0 ? min(PAT_BN / PAT_BM, t1) : 0;
+    const bool ragged_end = t1 == n_tiles && (N - k0) % PAT_BM != 0 && t1 - 1 >= t0 + m_lo;
     float da_acc = 0.0f;
     auto issue = [&](auto buf, int t) {
         constexpr int B_ = decltype(buf)::value;
@@ -180,7 +191,10 @@ __global__ __launch_bounds__(PAT_THREADS) void bwd_pattern_kernel(PatArgs p) {
             __builtin_amdgcn_raw_ptr_buffer_load_lds(rr, (lds_void*)(band + 64 * (w - 1)), 4, off * 4, 0, 0, 0);
         }
     };
-    float* dr_row = p.dr_part + (size_t)(b * p.n_fixed + hidx) * p.dr_row_total + pat_row_base(kblk, N);
+    const size_t part = (size_t)(b * p.n_fixed + hidx);
+    // This chunk's offsets start at 64 t0 - 127 (entry 0 of its row).
+    const int delta0 = PAT_BM * t0 - (PAT_BN - 1);
+    float* dr_row = p.dr_part + ((part * p.n_kblocks + kblk) * p.n_chunks + chunk) * (size_t)p.part_len;
     const int max_delta = N - 1 - k0;
     auto flush = [&](int lo, int count) {
         // Offsets lo .. lo+count-1 are final: store them and clear their slots.
@@ -188,7 +202,7 @@ __global__ __launch_bounds__(PAT_THREADS) void bwd_pattern_kernel(PatArgs p) {
             const int delta = lo + tid;
             if (delta >= 0 && delta <= max_delta) {
                 const int s = delta & (PAT_RING - 1);
-                dr_row[delta] = (ring[0][s] + ring[1][s]) + (ring[2][s] + ring[3][s]);
+                dr_row[delta - delta0] = (ring[0][s] + ring[1][s]) + (ring[2][s] + ring[3][s]);
                 ring[0][s] = 0.0f;
                 ring[1][s] = 0.0f;
                 ring[2][s] = 0.0f;
@@ -198,53 +212,62 @@ __global__ __launch_bounds__(PAT_THREADS) void bwd_pattern_kernel(PatArgs p) {
     };
     auto compute = [&](auto buf, int t, auto mask) {
         constexpr int B_ = decltype(buf)::value;
-        if (t >= 1) flush(PAT_BM * t - (PAT_BM + PAT_BN - 1), PAT_BM);  // final after tile t-1
+        if (t > t0) flush(PAT_BM * t - (PAT_BM + PAT_BN - 1), PAT_BM);  // final after tile t-1
         pat_tile<T, decltype(mask)::value>(B_ ? g1 : g0, B_ ? rows1 : rows0, B_ ? band1 : band0, scratch[w],
                                            ring[w], t, k0 + PAT_BM * t, k0, w, c, hf, lane, N, vf, a_key, da_acc);
     };
-    // Tiles in order; the masked ones are the first n_mask and, if ragged, the
-    // last.  run_slots wants the masked slots first, so a ragged tail is given
-    // its own masked pass after the others.
-    const int n_plain_end = ragged_end && n_tiles > n_mask ? n_tiles - 1 : n_tiles;
-    const int P = (n_mask + 1) & ~1;
+    // Tiles in order.  run_slots wants the masked slots first, so a ragged
+    // last tile gets a masked pass of its own after the others.
+    const int plain_end = ragged_end ? t1 - 1 : t1;
+    const int P = (m_lo + 1) & ~1;
     run_slots(
-        P, P + (n_plain_end - n_mask), [&](int i) { return i < P ? (i < n_mask ? i : -1) : n_mask + (i - P); },
-        issue, [&](auto) {}, compute);
-    int t_last = n_plain_end - 1;
-    if (n_plain_end < n_tiles) {
-        // The ragged last tile, masked, in a pass of its own (buffer 0 is free
-        // after the barrier that closed the last slot).
-        issue(Buf0{}, n_tiles - 1);
+        P, P + (plain_end - t0 - m_lo),
+        [&](int i) { return i < P ? (i < m_lo ? t0 + i : -1) : t0 + m_lo + (i - P); }, issue, [&](auto) {},
+        compute);
+    int t_last = plain_end - 1;
+    if (ragged_end) {
+        // Buffer 0 is free after the barrier that closed the last slot.
+        issue(Buf0{}, t1 - 1);
         __syncthreads();
-        compute(Buf0{}, n_tiles - 1, std::true_type{});
+        compute(Buf0{}, t1 - 1, std::true_type{});
         __syncthreads();
-        t_last = n_tiles - 1;
+        t_last = t1 - 1;
     }
     flush(PAT_BM * t_last - (PAT_BN - 1), PAT_BM + PAT_BN - 1);
     const float da_key = pair_sum(da_acc);
-    if (hf == 0 && key < N) p.da_part[(size_t)(b * p.n_fixed + hidx) * N + key] = da_key;
+    if (hf == 0 && key < N) p.da_part[(part * p.n_chunks + chunk) * N + key] = da_key;
 }
 
-// da[h][j] = sum_b da_part, dr[h][delta] = sum over b and the key blocks J
-// with 128 J <= N - 1 - delta of dr_part.  One thread per (fixed head,
-// position); consecutive threads read consecutive addresses.
+// da[h][j] += sum over the chunks of j's key block of da_part, and
+// dr[h][delta] += sum over the key blocks J with 128 J <= N - 1 - delta, and
+// over the (one or two) chunks of J whose offsets include delta, of dr_part;
+// for one batch element (blockIdx.y) per thread, added atomically into the
+// zeroed outputs.  Consecutive threads read consecutive addresses.
 __global__ __launch_bounds__(256) void pat_reduce_kernel(PatArgs p) {
     const int per_head = (p.N + 255) / 256;
     const int hidx = (int)(blockIdx.x / per_head);
     const int x = (int)(blockIdx.x % per_head) * 256 + (int)threadIdx.x;
     if (x >= p.N) return;
+    const int b = (int)blockIdx.y;
     const int h = p.heads[hidx];
     const int N = p.N;
-    float sa = 0.0f, sr = 0.0f;
+    const int cq = PAT_BM * p.chunk_tiles;  // queries per chunk
+    const size_t part = (size_t)(b * p.n_fixed + hidx);
+    float sa = 0.0f;
+    const int nc_key = pat_chunks(x / PAT_BN, N, p.chunk_tiles);
+    for (int ch = 0; ch < nc_key; ++ch) sa += p.da_part[(part * p.n_chunks + ch) * N + x];
+    float sr = 0.0f;
     const int j_max = (N - 1 - x) / PAT_BN;  // key blocks that reach offset x
-    for (int b = 0; b < p.B; ++b) {
-        const size_t part = (size_t)(b * p.n_fixed + hidx);
-        sa += p.da_part[part * N + x];
-        const float* rows = p.dr_part + part * p.dr_row_total;
-        for (int J = 0; J <= j_max; ++J) sr += rows[pat_row_base(J, N) + x];
+    const int ca = x / cq;                  // the chunk whose own queries give offset x
+    for (int J = 0; J <= j_max; ++J) {
+        const int nc = pat_chunks(J, N, p.chunk_tiles);
+        const float* rows = p.dr_part + (part * p.n_kblocks + J) * p.n_chunks * (size_t)p.part_len;
+        if (ca < nc) sr += rows[(size_t)ca * p.part_len + (x - (cq * ca - (PAT_BN - 1)))];
+        if (ca + 1 < nc && x >= cq * (ca + 1) - (PAT_BN - 1))
+            sr += rows[(size_t)(ca + 1) * p.part_len + (x - (cq * (ca + 1) - (PAT_BN - 1)))];
     }
-    p.da[(size_t)h * N + x] = sa;
-    p.dr[(size_t)h * N + x] = sr;
+    atomicAdd(p.da + (size_t)h * N + x, sa);
+    atomicAdd(p.dr + (size_t)h * N + x, sr);
 }
 
 __global__ void pat_fill_kernel(float* p, size_t n) {

@@ -209,9 +209,9 @@ def test_pattern_gradient_rejects_bad_arguments(lib):
     assert _pat(lib, O=FAKE + 8) == 6
     assert _pat(lib, ws=FAKE + 64) == 6
     assert _pat(lib, ws_bytes=16) == 2
-    # D, da partials and one partial row per key block (lengths N, N-128, ...).
+    # D, da partials, and per key block and chunk of query tiles a row of the
+    # offsets it touches (16 tiles of 64 queries + 127).
     need = lib.saf_hybrid_attn_bwd_pattern_workspace_bytes(1, 2, 3, 300, 64)
-    rows = 300 + 172 + 44
-    assert need >= 2 * 3 * 300 * 4 * 2 + 2 * 3 * rows * 4 and need % 256 == 0
+    assert need >= 2 * 3 * 300 * 4 * 2 + 2 * 3 * 3 * (16 * 64 + 127) * 4 and need % 256 == 0
     assert _pat(lib, ws_bytes=lib.saf_hybrid_attn_bwd_pattern_workspace_bytes(1, 1, 2, 8, 64) - 1) == 2
     assert _pat(lib, B=0, V=None, O=None, dO=None, LSE=None, da=None, dr=None, ws=None) == 0

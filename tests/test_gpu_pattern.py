@@ -57,6 +57,7 @@ def _check(dtype, g, o, is_fixed):
     ("bf16", 1, 2, 129, (0,)),        # last key block holds one key
     ("bf16", 1, 1, 1, (0,)),          # a single position: no gradient
     ("bf16", 3, 2, 1000, (0, 1)),     # several key blocks, every head fixed
+    ("f32", 1, 2, 2200, (1,)),        # key blocks cut into up to three chunks
 ])
 def test_pattern_gradient_matches_oracle(dtype, B, H, N, fixed):
     announce(f"pattern grad {dtype} B={B} H={H} N={N} fixed={fixed}")
