@@ -24,6 +24,14 @@ FLOP rule: one causal N x N x d contraction counts 2*d*N(N+1)/2.  An ordinary
 head counts 7 (2 forward, 5 backward: S recompute, dP, dV, dK, dQ); a fixed
 head counts 2 (P V forward, P^T dO backward).
 
+``--pattern`` times the gradients of trainable fixed patterns
+(saf_hybrid_attn_bwd_pattern: da, dr of the fixed heads) at the layer
+workload, next to the frozen layer; its roofline is the ALU bound of the
+per-entry work (7 float32 operations per causal entry of each fixed head and
+batch element: the three of the weight's exponent and exp, dP - D, the
+product, and the two sums) against the chip's float32 vector rate
+(256 CUs x 4 SIMDs x 32 lanes per clock x 2.4 GHz = 78.6 Tops/s).
+
 ``--calib`` times the calibration statistics instead (include/saf_calib.h):
 one step = folding 32 calibration inputs of one 12-head layer (T = 4096) into
 the running statistics (mean attention, scalar sums; no per-entry squared
@@ -55,6 +63,8 @@ METRIC = "hybrid-attn fwd+bwd ms/layer + MFMA util, H=12 (25% fixed), N=4096, d=
 PEAK_BF16_TFLOPS = 2500.0
 PEAK_F32_TFLOPS = 157.3
 PEAK_HBM_GBS = 8000.0
+PEAK_F32_VALU_TOPS = 78.6   # float32 vector operations per second (an FMA counts once)
+PATTERN_OPS_PER_ENTRY = 7
 MAX_HOST_WORKERS = 16
 COPY_CALIBRATION_BYTES = 64 << 20
 
@@ -93,6 +103,7 @@ def stage_bytes(B: int, H: int, N: int, d: int, n_fixed: int, elem: int):
 KERNEL_SOURCES = {
     "layer": ("saf_common.h", "saf_fwd.h", "saf_bwd.h"),
     "calib": ("saf_common.h", "saf_calib_kernels.h"),
+    "pattern": ("saf_common.h", "saf_pattern.h"),
 }
 
 
@@ -123,7 +134,7 @@ def measured_traffic(workload: str, stage: str):
                 digest = parts[1]
             elif len(parts) >= 3 and parts[0] == "traffic_bytes:" and parts[1] == stage:
                 found = float(parts[2])
-    group = "calib" if workload in gen.CALIB_WORKLOADS else "layer"
+    group = "calib" if workload in gen.CALIB_WORKLOADS else ("pattern" if workload.startswith("pattern_") else "layer")
     if digest != kernel_source_digest(group):
         return None
     return found
@@ -141,6 +152,8 @@ def parse():
                     help="(batch, head) slices the oracle baseline runs (0: all, at most eight per worker)")
     ap.add_argument("--compare-ordinary", dest="compare", action="store_true", default=True)
     ap.add_argument("--no-compare-ordinary", dest="compare", action="store_false")
+    ap.add_argument("--pattern", action="store_true",
+                    help="time the trainable-pattern gradients (da, dr) at the layer workload instead")
     ap.add_argument("--calib", action="store_true",
                     help="time the calibration statistics (workload calib124m_4k) instead of the layer")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -378,6 +391,103 @@ def main_calib(args, torch):
     print(json.dumps(result), flush=True)
 
 
+# ---------------------------------------------------------------------------
+# Trainable-pattern gradients
+# ---------------------------------------------------------------------------
+
+def main_pattern(args, torch):
+    from paper_2609_34650_amd import binding
+    w = gen.WORKLOADS[args.workload]
+    inp = gen.workload_inputs(w)
+    flags = inp["is_fixed"].copy()
+    n_fixed = int(flags.sum())
+    layer = Layer(torch, inp, w.dtype, True)
+    dev = torch.device("cuda", 0)
+    da = torch.empty((w.H, w.N), dtype=torch.float32, device=dev)
+    dr = torch.empty_like(da)
+    code = binding.SAF_DTYPE_BF16 if w.dtype == "bf16" else binding.SAF_DTYPE_F32
+    nbytes = int(binding.load().saf_hybrid_attn_bwd_pattern_workspace_bytes(code, w.B, w.H, w.N, w.d))
+    ws = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+
+    def pattern():
+        binding.saf_hybrid_attn_bwd_pattern(layer.V, layer.O, layer.dO, layer.LSE, flags, layer.a, layer.r, da, dr,
+                                            ws)
+
+    for _ in range(args.warmup):
+        layer.step(flags)
+        pattern()
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for e in ev:
+        layer.step(flags)
+        e[0].record()
+        pattern()
+        e[1].record()
+    torch.cuda.synchronize()
+    ms_trainable = (time.perf_counter() - t0) * 1e3 / args.steps
+    ms_pat = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    ms_frozen, _ = timed_block(torch, layer, flags, args.steps, with_events=False)
+    entries = w.B * n_fixed * w.N * (w.N + 1) / 2
+    tops = PATTERN_OPS_PER_ENTRY * entries / (ms_pat * 1e-3) / 1e12
+    result = {
+        "metric": "trainable-pattern gradients ms/layer (da, dr of the fixed heads), H=12 (25% fixed), N=4096, d=64",
+        "value": round(ms_pat, 4),
+        "unit": "ms/layer",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_pat, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": f"{w.name}: trainable-pattern gradients", "B": w.B, "H": w.H, "n_fixed": n_fixed,
+                   "N": w.N, "d": w.d, "parallelism": "single GPU"},
+        "layer_ms_frozen": round(ms_frozen, 4),
+        "layer_ms_trainable": round(ms_trainable, 4),
+        "trainable_overhead": round(ms_trainable / ms_frozen - 1.0, 4),
+        "roofline": {"bound": "alu", "kernel": "bwd_pattern", "achieved": round(tops, 2),
+                     "peak": PEAK_F32_VALU_TOPS, "unit": "Tops/s", "frac": round(tops / PEAK_F32_VALU_TOPS, 4),
+                     "traffic": measured_traffic(f"pattern_{w.name}", "bwd_pattern")},
+    }
+    if args.cpu_baseline:
+        result["cpu_baseline"] = pattern_cpu_baseline(inp, w)
+    print(json.dumps(result), flush=True)
+
+
+def _pattern_job(job):
+    from oracle import saf_oracle as orc
+    v, do, a, r = job
+    orc.fixed_pattern_grad(v, do, a, r)
+    return 1
+
+
+def pattern_cpu_baseline(inp, w):
+    """The oracle's pattern gradients on every (batch, fixed head) slice, one
+    slice per process."""
+    import multiprocessing as mp
+    try:
+        from threadpoolctl import threadpool_limits
+    except ImportError:  # pragma: no cover
+        threadpool_limits = None
+    fixed = [h for h in range(w.H) if inp["is_fixed"][h]]
+    jobs = [(inp["V"][b, h], inp["dO"][b, h], inp["a"][h], inp["r"][h]) for b in range(w.B) for h in fixed]
+    workers = max(1, min(MAX_HOST_WORKERS, len(os.sched_getaffinity(0)), len(jobs)))
+    ctx = threadpool_limits(limits=1) if threadpool_limits else None
+    t0 = time.perf_counter()
+    try:
+        with mp.get_context("fork").Pool(workers) as pool:
+            pool.map(_pattern_job, jobs, chunksize=1)
+    finally:
+        if ctx is not None and hasattr(ctx, "unregister"):
+            ctx.unregister()
+    wall = time.perf_counter() - t0
+    return {"value": round(wall * 1e3, 1), "unit": "ms/layer", "cores": workers, "kind": "oracle",
+            "sample": f"all {len(jobs)} (batch, fixed head) slices, fp64 dense, {wall:.1f} s wall on {workers} processes"}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -400,6 +510,9 @@ def main():
         del src, dst
     if args.calib:
         main_calib(args, torch)
+        return
+    if args.pattern:
+        main_pattern(args, torch)
         return
 
     w = gen.WORKLOADS[args.workload]
