@@ -1,5 +1,5 @@
-"""Thin ctypes binding to libsaf.so (C ABI in ``include/saf.h`` and
-``include/saf_calib.h``).
+"""Thin ctypes binding to libsaf.so (C ABI in ``include/saf.h``,
+``include/saf_calib.h`` and ``include/saf_fit.h``).
 
 Only argument marshalling happens here: tensor checks, pointers, the head
 flags and the caller's current HIP stream.  Every step of the layer runs in
@@ -49,6 +49,9 @@ EXPORTS = (
     "saf_calib_stats_bytes",
     "saf_calib_finalize_workspace_bytes",
     "saf_calib_finalize",
+    "saf_fit_workspace_bytes",
+    "saf_fit_targets",
+    "saf_compact_fit",
 )
 
 
@@ -98,6 +101,13 @@ def load() -> ctypes.CDLL:
     lib.saf_calib_finalize_workspace_bytes.argtypes = [i, i]
     lib.saf_calib_finalize.restype = ctypes.c_int
     lib.saf_calib_finalize.argtypes = [i, i, i, vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+    lib.saf_fit_workspace_bytes.restype = ctypes.c_size_t
+    lib.saf_fit_workspace_bytes.argtypes = [i, i]
+    lib.saf_fit_targets.restype = ctypes.c_int
+    lib.saf_fit_targets.argtypes = [i, i, vp, ctypes.c_float, vp, vp, vp, vp, ctypes.c_size_t, vp]
+    lib.saf_compact_fit.restype = ctypes.c_int
+    lib.saf_compact_fit.argtypes = [i, i, vp, vp, vp, i, ctypes.c_float, ctypes.c_float, vp, vp, vp, vp, vp,
+                                    ctypes.c_size_t, vp]
     lib.saf_status_str.restype = ctypes.c_char_p
     lib.saf_status_str.argtypes = [i]
     del f32p
@@ -370,3 +380,62 @@ def saf_calib_finalize(state: CalibState, workspace: Optional[torch.Tensor] = No
     _raise(code, "saf_calib_finalize")
     out["A_mean"] = state.mean
     return out
+
+
+# ---------------------------------------------------------------------------
+# Compact fit
+# ---------------------------------------------------------------------------
+
+FIT_FLOOR = 1e-9
+FIT_STEPS = 400
+FIT_LR = 0.05
+FIT_ACCEPT_KL = 0.2
+
+
+def _fit_workspace(H: int, T: int, dev, workspace):
+    nbytes = int(load().saf_fit_workspace_bytes(H, T))
+    if nbytes == 0:
+        raise ValueError(f"unsupported fit shape H={H} T={T}")
+    if workspace is None:
+        workspace = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    return workspace
+
+
+def saf_fit_targets(mean: torch.Tensor, floor_value: float = FIT_FLOOR, workspace: Optional[torch.Tensor] = None):
+    """Target marginals of the compact fit from the calibration mean
+    ``[H, T, T]``: returns ``(eta_abs, eta_rel, neg_entropy)``."""
+    lib = load()
+    H, T, _ = mean.shape
+    dev = mean.device
+    _check_act("mean", mean, (H, T, T), torch.float32, dev)
+    eta_abs = torch.empty((H, T), dtype=torch.float32, device=dev)
+    eta_rel = torch.empty_like(eta_abs)
+    neg_entropy = torch.empty((H,), dtype=torch.float64, device=dev)
+    workspace = _fit_workspace(H, T, dev, workspace)
+    code = lib.saf_fit_targets(H, T, _ptr(mean), float(floor_value), _ptr(eta_abs), _ptr(eta_rel), _ptr(neg_entropy),
+                               workspace.data_ptr(), workspace.numel() * workspace.element_size(), _stream(dev))
+    _raise(code, "saf_fit_targets")
+    return eta_abs, eta_rel, neg_entropy
+
+
+def saf_compact_fit(eta_abs: torch.Tensor, eta_rel: torch.Tensor, neg_entropy: torch.Tensor,
+                    steps: int = FIT_STEPS, lr: float = FIT_LR, floor_value: float = FIT_FLOOR,
+                    workspace: Optional[torch.Tensor] = None):
+    """Fit every head: returns ``(a, r, log_z, kl)`` (``[H, T]``, ``[H, T]``,
+    ``[H, T]``, ``[H]`` float32); a head passes when ``kl <= 0.2``."""
+    lib = load()
+    H, T = eta_abs.shape
+    dev = eta_abs.device
+    _check_act("eta_abs", eta_abs, (H, T), torch.float32, dev)
+    _check_act("eta_rel", eta_rel, (H, T), torch.float32, dev)
+    _check_act("neg_entropy", neg_entropy, (H,), torch.float64, dev)
+    a = torch.empty((H, T), dtype=torch.float32, device=dev)
+    r = torch.empty_like(a)
+    log_z = torch.empty_like(a)
+    kl = torch.empty((H,), dtype=torch.float32, device=dev)
+    workspace = _fit_workspace(H, T, dev, workspace)
+    code = lib.saf_compact_fit(H, T, _ptr(eta_abs), _ptr(eta_rel), _ptr(neg_entropy), int(steps), float(lr),
+                               float(floor_value), _ptr(a), _ptr(r), _ptr(log_z), _ptr(kl), workspace.data_ptr(),
+                               workspace.numel() * workspace.element_size(), _stream(dev))
+    _raise(code, "saf_compact_fit")
+    return a, r, log_z, kl

@@ -1,14 +1,16 @@
 // Host side of libsaf.so: argument checks and kernel launches for the C ABI
-// declared in include/saf.h and include/saf_calib.h.  No allocation, no
-// synchronisation, no global mutable state.
+// declared in include/saf.h, include/saf_calib.h and include/saf_fit.h.  No
+// allocation, no synchronisation, no global mutable state.
 #include "saf.h"
 #include "saf_calib.h"
+#include "saf_fit.h"
 
 #include <math.h>
 #include <stdint.h>
 
 #include "saf_bwd.h"
 #include "saf_calib_kernels.h"
+#include "saf_fit_kernels.h"
 #include "saf_fwd.h"
 #include "saf_pattern.h"
 
@@ -436,6 +438,147 @@ SAF_EXPORT saf_status_t saf_calib_finalize(int H, int T, int n_total, const floa
     hipLaunchKernelGGL(saf::calib_final_kernel, dim3(grid), dim3(saf::CAL_FIN_COLS), 0, stream, args);
     if (launched() != SAF_OK) return SAF_ERR_LAUNCH;
     hipLaunchKernelGGL(saf::calib_scores_kernel, dim3(H), dim3(256), 0, stream, args);
+    return launched();
+}
+
+// ---------------------------------------------------------------------------
+// Compact fit
+// ---------------------------------------------------------------------------
+namespace {
+
+struct FitLayout {
+    size_t rowsum, part, m, v, col, diag, logz, total;
+};
+FitLayout fit_layout(int H, int T) {
+    const size_t ht = (size_t)H * T;
+    const size_t nr = (size_t)((T + saf::FIT_ROWS - 1) / saf::FIT_ROWS);
+    const size_t nc = (size_t)((T + saf::FIT_COLS - 1) / saf::FIT_COLS);
+    FitLayout l;
+    size_t off = 0;
+    l.rowsum = off; off += align256(ht * 4);
+    l.part = off;   off += align256((size_t)H * nr * nc * 8);
+    l.m = off;      off += align256(2 * ht * 4);
+    l.v = off;      off += align256(2 * ht * 4);
+    l.col = off;    off += align256(ht * 4);
+    l.diag = off;   off += align256(ht * 4);
+    l.logz = off;   off += align256(ht * 4);
+    l.total = off;
+    return l;
+}
+
+saf::FitArgs fit_args(int H, int T, void* workspace) {
+    const FitLayout l = fit_layout(H, T);
+    char* w = reinterpret_cast<char*>(workspace);
+    saf::FitArgs f = {};
+    f.rowsum = reinterpret_cast<float*>(w + l.rowsum);
+    f.part = reinterpret_cast<double*>(w + l.part);
+    f.m = reinterpret_cast<float*>(w + l.m);
+    f.v = reinterpret_cast<float*>(w + l.v);
+    f.col = reinterpret_cast<float*>(w + l.col);
+    f.diag = reinterpret_cast<float*>(w + l.diag);
+    f.logz = reinterpret_cast<float*>(w + l.logz);
+    f.H = H;
+    f.T = T;
+    f.n_cgroups = (T + saf::FIT_COLS - 1) / saf::FIT_COLS;
+    f.n_rchunks = (T + saf::FIT_ROWS - 1) / saf::FIT_ROWS;
+    return f;
+}
+
+saf_status_t check_fit_shape(int H, int T) {
+    if (H < 0 || T < 0) return SAF_ERR_SHAPE;
+    if (H > 64) return SAF_ERR_UNSUPPORTED;
+    if (T > kMaxCalibT) return SAF_ERR_SHAPE;
+    return SAF_OK;
+}
+
+}  // namespace
+
+SAF_EXPORT size_t saf_fit_workspace_bytes(int H, int T) {
+    if (H <= 0 || T <= 0 || check_fit_shape(H, T) != SAF_OK) return 0;
+    return fit_layout(H, T).total;
+}
+
+SAF_EXPORT saf_status_t saf_fit_targets(int H, int T, const float* mean, float floor_value, float* eta_abs,
+                                        float* eta_rel, double* neg_entropy, void* workspace,
+                                        size_t workspace_bytes_given, hipStream_t stream) {
+    saf_status_t st = check_fit_shape(H, T);
+    if (st != SAF_OK) return st;
+    if (H == 0 || T == 0) return SAF_OK;
+    if (!(floor_value > 0.0f) || !(floor_value < 1.0f)) return SAF_ERR_SHAPE;
+    if (mean == nullptr || eta_abs == nullptr || eta_rel == nullptr || neg_entropy == nullptr || workspace == nullptr)
+        return SAF_ERR_NULL;
+    if (!aligned16(mean) || !aligned8(neg_entropy) || (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
+        return SAF_ERR_ALIGNMENT;
+    if (workspace_bytes_given < fit_layout(H, T).total) return SAF_ERR_SHAPE;
+    saf::FitArgs f = fit_args(H, T, workspace);
+    f.mean = mean;
+    f.eta_abs = eta_abs;
+    f.eta_rel = eta_rel;
+    f.neg_entropy = neg_entropy;
+    f.floor_value = floor_value;
+    const size_t ht = (size_t)H * T;
+    hipLaunchKernelGGL(saf::fit_fill_kernel, dim3(fill_grid(ht)), dim3(256), 0, stream, eta_abs, ht);
+    hipLaunchKernelGGL(saf::fit_fill_kernel, dim3(fill_grid(ht)), dim3(256), 0, stream, eta_rel, ht);
+    hipLaunchKernelGGL(saf::fit_rowsum_kernel, dim3((unsigned)(H * ((T + 3) / 4))), dim3(256), 0, stream, f);
+    const unsigned grid = (unsigned)((size_t)H * f.n_rchunks * f.n_cgroups);
+    hipLaunchKernelGGL(saf::fit_target_kernel, dim3(grid), dim3(saf::FIT_COLS), 0, stream, f);
+    hipLaunchKernelGGL(saf::fit_entropy_kernel, dim3(H), dim3(256), 0, stream, f);
+    return launched();
+}
+
+SAF_EXPORT saf_status_t saf_compact_fit(int H, int T, const float* eta_abs, const float* eta_rel,
+                                        const double* neg_entropy, int steps, float lr, float floor_value, float* a,
+                                        float* r, float* log_z, float* kl, void* workspace,
+                                        size_t workspace_bytes_given, hipStream_t stream) {
+    saf_status_t st = check_fit_shape(H, T);
+    if (st != SAF_OK) return st;
+    if (H == 0 || T == 0) return SAF_OK;
+    if (steps < 0 || !(lr >= 0.0f) || !(floor_value > 0.0f) || !(floor_value < 1.0f)) return SAF_ERR_SHAPE;
+    if (eta_abs == nullptr || eta_rel == nullptr || neg_entropy == nullptr || a == nullptr || r == nullptr ||
+        kl == nullptr || workspace == nullptr)
+        return SAF_ERR_NULL;
+    if (!aligned8(neg_entropy) || (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0) return SAF_ERR_ALIGNMENT;
+    if (workspace_bytes_given < fit_layout(H, T).total) return SAF_ERR_SHAPE;
+    saf::FitArgs f = fit_args(H, T, workspace);
+    f.eta_abs = const_cast<float*>(eta_abs);
+    f.eta_rel = const_cast<float*>(eta_rel);
+    f.neg_entropy = const_cast<double*>(neg_entropy);
+    f.alpha = a;
+    f.rho = r;
+    f.kl = kl;
+    f.floor_value = floor_value;
+    f.lr = lr;
+    if (log_z != nullptr) f.logz = log_z;
+    saf::NormArgs na = {};
+    na.a = a;
+    na.r = r;
+    na.lse = f.logz;
+    na.B = 1;
+    na.H = H;
+    na.N = T;
+    na.ld_prior = T;
+    na.n_rblocks = (T + saf::NORM_ROWS - 1) / saf::NORM_ROWS;
+    na.n_fixed = H;
+    for (int h = 0; h < H; ++h) na.heads[h] = (unsigned char)h;
+    const size_t ht = (size_t)H * T;
+    const unsigned elem_grid = fill_grid(ht);
+    const unsigned lse_grid = (unsigned)((size_t)na.n_rblocks * H);
+    const unsigned marg_grid = (unsigned)((size_t)H * f.n_rchunks * f.n_cgroups);
+    hipLaunchKernelGGL(saf::fit_init_kernel, dim3(elem_grid), dim3(256), 0, stream, f);
+    if (launched() != SAF_OK) return SAF_ERR_LAUNCH;
+    double p1 = 1.0, p2 = 1.0;
+    for (int t = 1; t <= steps; ++t) {
+        p1 *= (double)saf::FIT_ADAM_BETA1;
+        p2 *= (double)saf::FIT_ADAM_BETA2;
+        f.bc1 = (float)(1.0 - p1);
+        f.bc2 = (float)(1.0 - p2);
+        hipLaunchKernelGGL(saf::fixed_lse_kernel, dim3(lse_grid), dim3(saf::NORM_THREADS), 0, stream, na);
+        hipLaunchKernelGGL(saf::fit_marginals_kernel, dim3(marg_grid), dim3(saf::FIT_COLS), 0, stream, f);
+        hipLaunchKernelGGL(saf::fit_adam_kernel, dim3(elem_grid), dim3(256), 0, stream, f);
+        if (launched() != SAF_OK) return SAF_ERR_LAUNCH;
+    }
+    hipLaunchKernelGGL(saf::fixed_lse_kernel, dim3(lse_grid), dim3(saf::NORM_THREADS), 0, stream, na);
+    hipLaunchKernelGGL(saf::fit_kl_kernel, dim3(H), dim3(256), 0, stream, f);
     return launched();
 }
 

@@ -181,3 +181,29 @@ def calib_inputs(n_cal: int, H: int, T: int, d: int, dtype: str, seed: int = SEE
             x[i] = CALIB_SHARED * common + CALIB_NOISE * g.standard_normal((H, T, d), dtype=np.float32)
         out[name] = round_to_bf16(x) if dtype == "bf16" else x
     return out
+
+
+# ---------------------------------------------------------------------------
+# Target patterns for the compact fit (stand-ins for calibration means)
+# ---------------------------------------------------------------------------
+
+def fit_target_means(H: int, T: int, seed: int = SEED, stream_id: int = 0) -> np.ndarray:
+    """Draw ``[H, T, T]`` float32 causal row-stochastic patterns shaped like
+    mean attention: per head a sink weight on key 0, a recency decay and
+    Gaussian noise, ``s(i, j) = sink [j == 0] - decay ln(1 + i - j) + noise``,
+    then a softmax over ``j <= i`` in float64, rounded to float32 (zeros
+    above the diagonal)."""
+    g = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, stream_id, 13])))
+    out = np.zeros((H, T, T), dtype=np.float32)
+    i = np.arange(T)
+    off = i[:, None] - i[None, :]
+    causal = off >= 0
+    for h in range(H):
+        sink, decay, noise = g.uniform(0.0, 4.0), g.uniform(0.2, 1.5), g.uniform(0.2, 1.5)
+        s = -decay * np.log1p(np.clip(off, 0, None)) + noise * g.standard_normal((T, T))
+        s[:, 0] += sink
+        s = np.where(causal, s, -np.inf)
+        s -= s.max(axis=1, keepdims=True)
+        e = np.exp(s)
+        out[h] = (e / e.sum(axis=1, keepdims=True)).astype(np.float32)
+    return out

@@ -215,3 +215,33 @@ def test_pattern_gradient_rejects_bad_arguments(lib):
     assert need >= 2 * 3 * 300 * 4 * 2 + 2 * 3 * 3 * (16 * 64 + 127) * 4 and need % 256 == 0
     assert _pat(lib, ws_bytes=lib.saf_hybrid_attn_bwd_pattern_workspace_bytes(1, 1, 2, 8, 64) - 1) == 2
     assert _pat(lib, B=0, V=None, O=None, dO=None, LSE=None, da=None, dr=None, ws=None) == 0
+
+
+# ---------------------------------------------------------------------------
+# Compact fit (include/saf_fit.h)
+# ---------------------------------------------------------------------------
+
+def test_fit_entry_points_reject_bad_arguments(lib):
+    import ctypes
+    ws_bytes = lib.saf_fit_workspace_bytes(3, 100)
+    assert ws_bytes % 256 == 0 and ws_bytes >= 3 * 100 * 4 * 8  # rowsum, moments (4), marginals (2), log Z
+    assert lib.saf_fit_workspace_bytes(0, 100) == 0 and lib.saf_fit_workspace_bytes(65, 100) == 0
+    assert lib.saf_fit_workspace_bytes(3, (1 << 16) + 1) == 0
+    f = ctypes.c_float
+    tg = lambda H=3, T=100, mean=FAKE, fl=1e-9, ea=FAKE, er=FAKE, ne=FAKE, ws=FAKE, wb=ws_bytes: \
+        lib.saf_fit_targets(H, T, mean, f(fl), ea, er, ne, ws, wb, None)
+    assert tg(H=65) == 3
+    assert tg(T=-1) == 2
+    assert tg(fl=0.0) == 2 and tg(fl=1.5) == 2
+    assert tg(mean=None) == 1 and tg(ne=None) == 1
+    assert tg(mean=FAKE + 4) == 6 and tg(ne=FAKE + 4) == 6 and tg(ws=FAKE + 64) == 6
+    assert tg(wb=ws_bytes - 1) == 2
+    assert tg(H=0, mean=None) == 0
+    cf = lambda H=3, T=100, ea=FAKE, er=FAKE, ne=FAKE, steps=400, lr=0.05, fl=1e-9, a=FAKE, r=FAKE, lz=None, \
+        kl=FAKE, ws=FAKE, wb=ws_bytes: lib.saf_compact_fit(H, T, ea, er, ne, steps, f(lr), f(fl), a, r, lz, kl, ws, wb,
+                                                           None)
+    assert cf(steps=-1) == 2 and cf(lr=-1.0) == 2 and cf(fl=0.0) == 2
+    assert cf(ea=None) == 1 and cf(a=None) == 1 and cf(kl=None) == 1
+    assert cf(ne=FAKE + 4) == 6 and cf(ws=FAKE + 8) == 6
+    assert cf(wb=16) == 2
+    assert cf(T=0, ea=None) == 0

@@ -1,0 +1,94 @@
+"""GPU parity of the compact fit (include/saf_fit.h) against the fp64 oracle
+(``oracle.fit_oracle``).
+
+Both sides start from the same seeded float32 target means
+(``paper_2609_34650_amd.inputs.fit_target_means``, causal row-stochastic
+patterns with a sink, a recency decay and noise).  Each side computes its own
+targets and runs its own fitter.
+
+Bars.  Targets: the marginals are float32 sums of up to T terms each below 1,
+``|g - o| <= 1e-6 + 1e-5 |o|``; ``sum Pi ln Pi`` relative 1e-5.  Fit: the
+float32 fitter follows the oracle's Adam trajectory closely for the first
+steps (alpha and rho to 1e-4) and ends at the same optimum region: the
+acceptance KL agrees to ``1e-4 + 1e-3 KL`` and the fitted log Z(i) (unique for
+given parameters, and the gauge of the parameters cancels in it only with
+both vectors) is compared through the fitted pattern's row normalisers.
+"""
+
+import numpy as np
+import pytest
+
+from gpu_helpers import announce, torch_cuda
+
+pytestmark = pytest.mark.gpu
+
+
+def _targets_gpu(mean):
+    torch = torch_cuda()
+    from paper_2609_34650_amd import binding
+    m = torch.from_numpy(mean).to("cuda")
+    ea, er, ne = binding.saf_fit_targets(m)
+    torch.cuda.synchronize()
+    return ea, er, ne
+
+
+@pytest.mark.parametrize("H,T", [(2, 1), (3, 37), (2, 256), (2, 300)])
+def test_fit_targets_match_oracle(H, T):
+    from oracle import fit_oracle as fo
+    from paper_2609_34650_amd import inputs
+    announce(f"fit targets H={H} T={T}")
+    mean = inputs.fit_target_means(H, T, stream_id=41)
+    ea, er, ne = _targets_gpu(mean)
+    for h in range(H):
+        o = fo.fit_targets(mean[h].astype(np.float64))
+        np.testing.assert_allclose(ea[h].double().cpu().numpy(), o["eta_abs"], rtol=1e-5, atol=1e-6)
+        np.testing.assert_allclose(er[h].double().cpu().numpy(), o["eta_rel"], rtol=1e-5, atol=1e-6)
+        np.testing.assert_allclose(float(ne[h]), o["neg_entropy"], rtol=1e-5, atol=1e-9)
+
+
+@pytest.mark.parametrize("H,T,steps", [(2, 64, 5), (3, 200, 5), (2, 130, 400), (1, 1, 3)])
+def test_compact_fit_matches_oracle(H, T, steps):
+    torch = torch_cuda()
+    from oracle import fit_oracle as fo
+    from paper_2609_34650_amd import binding, inputs
+    announce(f"compact fit H={H} T={T} steps={steps}")
+    mean = inputs.fit_target_means(H, T, stream_id=42)
+    ea, er, ne = _targets_gpu(mean)
+    a, r, log_z, kl = binding.saf_compact_fit(ea, er, ne, steps=steps)
+    torch.cuda.synchronize()
+    for h in range(H):
+        t = fo.fit_targets(mean[h].astype(np.float64))
+        oa, orr = fo.fit(t["eta_abs"], t["eta_rel"], steps=steps)
+        okl = fo.fit_kl(oa, orr, t["eta_abs"], t["eta_rel"], t["neg_entropy"])
+        _, _, _, olz = fo.fit_objective(oa, orr, t["eta_abs"], t["eta_rel"])
+        ga, gr = a[h].double().cpu().numpy(), r[h].double().cpu().numpy()
+        if steps <= 5:
+            np.testing.assert_allclose(ga, oa, rtol=0, atol=1e-4)
+            np.testing.assert_allclose(gr, orr, rtol=0, atol=1e-4)
+        np.testing.assert_allclose(float(kl[h]), okl, rtol=1e-3, atol=1e-4)
+        # The GPU's log Z of its own parameters, recomputed by the oracle's
+        # definition, and its acceptance KL from the oracle's formula.
+        _, _, _, glz_def = fo.fit_objective(ga, gr, t["eta_abs"], t["eta_rel"])
+        np.testing.assert_allclose(log_z[h].double().cpu().numpy(), glz_def, rtol=0, atol=2e-5)
+        gkl_def = fo.fit_kl(ga, gr, t["eta_abs"], t["eta_rel"], t["neg_entropy"])
+        np.testing.assert_allclose(float(kl[h]), gkl_def, rtol=1e-4, atol=1e-5)
+        assert np.isfinite(olz).all()
+
+
+@pytest.mark.slow
+def test_compact_fit_long_context():
+    """400 steps at T = 1024 (the oracle is dense float64): both fits land at
+    the same acceptance KL, below the 0.2-nat threshold for these targets."""
+    torch = torch_cuda()
+    from oracle import fit_oracle as fo
+    from paper_2609_34650_amd import binding, inputs
+    announce("compact fit H=2 T=1024 steps=400")
+    mean = inputs.fit_target_means(2, 1024, stream_id=43)
+    ea, er, ne = _targets_gpu(mean)
+    a, r, log_z, kl = binding.saf_compact_fit(ea, er, ne)
+    torch.cuda.synchronize()
+    for h in range(2):
+        t = fo.fit_targets(mean[h].astype(np.float64))
+        oa, orr = fo.fit(t["eta_abs"], t["eta_rel"])
+        okl = fo.fit_kl(oa, orr, t["eta_abs"], t["eta_rel"], t["neg_entropy"])
+        np.testing.assert_allclose(float(kl[h]), okl, rtol=1e-3, atol=1e-4)
