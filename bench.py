@@ -32,6 +32,14 @@ batch element: the three of the weight's exponent and exp, dP - D, the
 product, and the two sums) against the chip's float32 vector rate
 (256 CUs x 4 SIMDs x 32 lanes per clock x 2.4 GHz = 78.6 Tops/s).
 
+``--fit`` times the compact fit of one 12-head layer at T = 4096: the
+targets from the calibration mean (floor, renormalise, marginals), then the
+fitter's 400 Adam steps and the acceptance KL, for all heads at once; its
+roofline is the ALU bound of the fitted pattern's marginals (per Adam step
+and causal entry, one exponential and three operations for the column sum
+and again for the diagonal sum: 8 operations) against the float32 vector
+rate.
+
 ``--calib`` times the calibration statistics instead (include/saf_calib.h):
 one step = folding 32 calibration inputs of one 12-head layer (T = 4096) into
 the running statistics (mean attention, scalar sums; no per-entry squared
@@ -154,6 +162,8 @@ def parse():
     ap.add_argument("--no-compare-ordinary", dest="compare", action="store_false")
     ap.add_argument("--pattern", action="store_true",
                     help="time the trainable-pattern gradients (da, dr) at the layer workload instead")
+    ap.add_argument("--fit", action="store_true",
+                    help="time the compact fit (targets + 400 Adam steps) of a 12-head layer at T=4096 instead")
     ap.add_argument("--calib", action="store_true",
                     help="time the calibration statistics (workload calib124m_4k) instead of the layer")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -488,6 +498,88 @@ def pattern_cpu_baseline(inp, w):
             "sample": f"all {len(jobs)} (batch, fixed head) slices, fp64 dense, {wall:.1f} s wall on {workers} processes"}
 
 
+# ---------------------------------------------------------------------------
+# Compact fit
+# ---------------------------------------------------------------------------
+
+FIT_OPS_PER_ENTRY = 8
+
+
+def _fit_job(job):
+    from oracle import fit_oracle as fo
+    mean, steps = job
+    t = fo.fit_targets(mean)
+    fo.fit(t["eta_abs"], t["eta_rel"], steps=steps)
+    return steps
+
+
+def main_fit(args, torch):
+    from paper_2609_34650_amd import binding
+    H, T, steps = 12, 4096, binding.FIT_STEPS
+    means = gen.fit_target_means(H, T, stream_id=44)
+    dev = torch.device("cuda", 0)
+    mean = torch.from_numpy(means).to(dev)
+    ws = torch.empty(int(binding.load().saf_fit_workspace_bytes(H, T)), dtype=torch.uint8, device=dev)
+
+    def step():
+        ea, er, ne = binding.saf_fit_targets(mean, workspace=ws)
+        return binding.saf_compact_fit(ea, er, ne, steps=steps, workspace=ws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    n_timed = max(1, min(args.steps, 10))
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record()
+    for _ in range(n_timed):
+        a, r, log_z, kl = step()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / n_timed
+    ms_ev = e0.elapsed_time(e1) / n_timed
+    entries = H * T * (T + 1) / 2
+    tops = FIT_OPS_PER_ENTRY * entries * steps / (ms_ev * 1e-3) / 1e12
+    kl_h = kl.cpu().numpy()
+    result = {
+        "metric": "compact fit ms/layer (targets + 400 Adam steps + KL check), H=12, T=4096",
+        "value": round(ms, 3),
+        "unit": "ms/layer",
+        "n_gpus": 1,
+        "steps": n_timed,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 3),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": "fit124m_4k: compact fit of one layer's 12 heads", "H": H, "T": T,
+                   "adam_steps": steps, "lr": binding.FIT_LR, "parallelism": "single GPU"},
+        "fit_kl": [round(float(x), 4) for x in kl_h],
+        "accepted": int((kl_h <= binding.FIT_ACCEPT_KL).sum()),
+        "roofline": {"bound": "alu", "kernel": "fit (all launches)", "achieved": round(tops, 2),
+                     "peak": PEAK_F32_VALU_TOPS, "unit": "Tops/s", "frac": round(tops / PEAK_F32_VALU_TOPS, 4),
+                     "traffic": None},
+    }
+    if args.cpu_baseline:
+        import multiprocessing as mp
+        sample_steps = 4
+        workers = max(1, min(MAX_HOST_WORKERS, len(os.sched_getaffinity(0)), H))
+        jobs = [(means[h].astype(np.float64), sample_steps) for h in range(H)]
+        t0 = time.perf_counter()
+        with mp.get_context("fork").Pool(workers) as pool:
+            pool.map(_fit_job, jobs, chunksize=1)
+        wall = time.perf_counter() - t0
+        result["cpu_baseline"] = {
+            "value": round(wall * 1e3 * steps / sample_steps, 1), "unit": "ms/layer", "cores": workers,
+            "kind": "oracle",
+            "sample": (f"targets + {sample_steps} of {steps} Adam steps for all {H} heads, fp64 dense, {wall:.1f} s "
+                       f"wall on {workers} processes, scaled by {steps}/{sample_steps} (targets counted in every "
+                       f"scaled step: an upper bound)")}
+    print(json.dumps(result), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -513,6 +605,9 @@ def main():
         return
     if args.pattern:
         main_pattern(args, torch)
+        return
+    if args.fit:
+        main_fit(args, torch)
         return
 
     w = gen.WORKLOADS[args.workload]
