@@ -153,32 +153,61 @@ __global__ void fit_init_kernel(FitArgs p) {
 }
 
 // Column and diagonal sums of P(i, j) = exp(alpha(j) + rho(i - j) - log Z(i)).
+// The block's rho and alpha values (offsets and keys i - j for its rows and
+// columns: 511 of each) and its rows' log Z are staged in LDS first, so the
+// walk reads consecutive LDS words across a wavefront.
 __global__ __launch_bounds__(FIT_COLS) void fit_marginals_kernel(FitArgs p) {
+    __shared__ float rs[2 * FIT_COLS];
+    __shared__ float as[2 * FIT_COLS];
+    __shared__ float zs[FIT_ROWS];
     const int per_head = p.n_rchunks * p.n_cgroups;
     const int h = (int)(blockIdx.x / per_head);
     const int rem = (int)(blockIdx.x % per_head);
     const int i0 = (rem / p.n_cgroups) * FIT_ROWS;
     const int j_first = (rem % p.n_cgroups) * FIT_COLS;
-    const int j = j_first + (int)threadIdx.x;
-    if (j_first > i0 + FIT_ROWS - 1) return;
+    if (j_first > i0 + FIT_ROWS - 1) return;  // the whole block lies above the diagonal
     const int T = p.T;
-    if (j >= T) return;
+    const int tid = (int)threadIdx.x;
+    const int j = j_first + tid;
     const float* __restrict__ al = p.alpha + (size_t)h * T;
     const float* __restrict__ rh = p.rho + (size_t)h * T;
     const float* __restrict__ lz = p.logz + (size_t)h * T;
-    const int i_end = min(i0 + FIT_ROWS, T);
-    const int i_beg = max(i0, j);
-    if (i_beg >= i_end) return;
-    const float aj = al[j];   // column j's alpha
-    const float rj = rh[j];   // diagonal j's rho
-    float colsum = 0.0f, dg = 0.0f;
-    for (int i = i_beg; i < i_end; ++i) {
-        const float z = lz[i];
-        colsum += fast_exp2((aj + rh[i - j] - z) * LOG2E);
-        dg += fast_exp2((al[i - j] + rj - z) * LOG2E);
+    // Staged index x holds position base + x, base = i0 - j_first - (FIT_COLS - 1).
+    const int base = i0 - j_first - (FIT_COLS - 1);
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+        const int x = tid + FIT_COLS * k;
+        const int q = base + x;
+        const bool in = q >= 0 && q < T;
+        rs[x] = in ? rh[q] : 0.0f;
+        as[x] = in ? al[q] : 0.0f;
     }
-    atomicAdd(p.col + (size_t)h * T + j, colsum);
-    atomicAdd(p.diag + (size_t)h * T + j, dg);
+    zs[tid] = i0 + tid < T ? lz[i0 + tid] : 0.0f;
+    __syncthreads();
+    if (j >= T) return;
+    const int n_rows = min(FIT_ROWS, T - i0);
+    const float aj = al[j] * LOG2E;  // column j's alpha
+    const float rj = rh[j] * LOG2E;  // diagonal j's rho
+    const int off = j_first - j + (FIT_COLS - 1);  // staged index of position i - j is (i - i0) + off
+    const int r_beg = max(0, j - i0);               // rows i >= j
+    float c0 = 0.0f, c1 = 0.0f, d0 = 0.0f, d1 = 0.0f;
+    int r = r_beg;
+    for (; r + 2 <= n_rows; r += 2) {
+        const float z0 = zs[r] * LOG2E, z1 = zs[r + 1] * LOG2E;
+        c0 += fast_exp2(fmaf(rs[r + off], LOG2E, aj - z0));
+        c1 += fast_exp2(fmaf(rs[r + 1 + off], LOG2E, aj - z1));
+        d0 += fast_exp2(fmaf(as[r + off], LOG2E, rj - z0));
+        d1 += fast_exp2(fmaf(as[r + 1 + off], LOG2E, rj - z1));
+    }
+    if (r < n_rows) {
+        const float z0 = zs[r] * LOG2E;
+        c0 += fast_exp2(fmaf(rs[r + off], LOG2E, aj - z0));
+        d0 += fast_exp2(fmaf(as[r + off], LOG2E, rj - z0));
+    }
+    if (r_beg < n_rows) {
+        atomicAdd(p.col + (size_t)h * T + j, c0 + c1);
+        atomicAdd(p.diag + (size_t)h * T + j, d0 + d1);
+    }
 }
 
 // One Adam step on alpha and rho; clears the marginal sums it read.
