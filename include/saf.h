@@ -94,6 +94,30 @@ saf_status_t saf_hybrid_attn_fwd(saf_dtype_t dt,
                                  void* O, float* LSE,
                                  hipStream_t stream);
 
+/*
+ * Forward of the hybrid layer with grouped-query attention and head
+ * dimension 64, 96 or 128 (the paper's grouped-query prefill layout --
+ * Section "Pretrained grouped-query models" -- and its 1B model's head
+ * width).  Query head h uses key/value head h / (Hq / Hkv); a fixed query
+ * head reads only V of its group (the grouped-query implementation keeps the
+ * shared key and value heads, Appendix "Mixed-head execution and numerical
+ * checks").  Same conventions and outputs as saf_hybrid_attn_fwd, with
+ *   Q, O : [B, Hq, N, d] `dt`;  K, V : [B, Hkv, N, d] `dt`;
+ *   LSE  : [B, Hq, N] float32;  head_is_fixed, a, r : per query head (Hq).
+ * Limits: d in {64, 96, 128}, Hq <= 64, Hq a multiple of Hkv, one slice
+ * N * d * sizeof(dt) < 2^31 bytes.  With Hkv == Hq and d == 64 it computes
+ * what saf_hybrid_attn_fwd computes (a separate, simpler kernel: one 32-query
+ * block per wavefront, a normaliser launch first when a head is fixed).
+ * There is no backward for this layout in this build.
+ */
+saf_status_t saf_hybrid_attn_fwd_gqa(saf_dtype_t dt,
+                                     const void* Q, const void* K, const void* V,
+                                     const uint8_t* head_is_fixed,
+                                     const float* a, const float* r, int ld_prior,
+                                     int B, int Hq, int Hkv, int N, int d,
+                                     void* O, float* LSE,
+                                     hipStream_t stream);
+
 /* Bytes of device workspace saf_hybrid_attn_bwd needs (a multiple of 256).
  * Returns 0 for an empty or invalid problem. */
 size_t saf_hybrid_attn_bwd_workspace_bytes(saf_dtype_t dt, int B, int H, int N, int d);

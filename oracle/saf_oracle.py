@@ -68,6 +68,7 @@ __all__ = [
     "layer_forward_backward_parallel",
     "fixed_pattern_grad",
     "layer_pattern_grad",
+    "layer_forward_gqa",
 ]
 
 _F64 = np.float64
@@ -277,6 +278,33 @@ def layer_backward(Q, K, V, dO, is_fixed, a=None, r=None, row_block: int = 512,
         dK[b, h] = dk
         dV[b, h] = dv
     return dQ, dK, dV
+
+
+def layer_forward_gqa(Q, K, V, is_fixed, a=None, r=None, row_block: int = 512,
+                      heads: Optional[Sequence[Tuple[int, int]]] = None):
+    """Grouped-query forward: ``Q`` ``[B, Hq, N, d]``, ``K``, ``V``
+    ``[B, Hkv, N, d]``; query head ``h`` attends with key/value head
+    ``h // (Hq // Hkv)`` (a fixed head uses only that V).  Returns ``O``
+    ``[B, Hq, N, d]`` and ``LSE`` ``[B, Hq, N]`` (float64; NaN outside the
+    listed ``(b, h)`` pairs when ``heads`` is given)."""
+    V = np.asarray(V)
+    B, Hkv, N, d = V.shape
+    is_fixed = np.asarray(is_fixed).astype(bool).reshape(-1)
+    Hq = is_fixed.shape[0]
+    if Hq % Hkv:
+        raise ValueError("query heads must be a multiple of key/value heads")
+    group = Hq // Hkv
+    O = np.full((B, Hq, N, d), np.nan)
+    LSE = np.full((B, Hq, N), np.nan)
+    todo = heads if heads is not None else [(b, h) for b in range(B) for h in range(Hq)]
+    for b, h in todo:
+        g = h // group
+        fx = bool(is_fixed[h])
+        o, lse = head_forward(None if fx else Q[b, h], None if fx else K[b, g], V[b, g], fx,
+                              a[h] if fx else None, r[h] if fx else None, row_block)
+        O[b, h] = o
+        LSE[b, h] = lse
+    return O, LSE
 
 
 # ---------------------------------------------------------------------------

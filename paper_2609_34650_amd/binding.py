@@ -39,6 +39,7 @@ STATUS = {
 
 EXPORTS = (
     "saf_hybrid_attn_fwd",
+    "saf_hybrid_attn_fwd_gqa",
     "saf_hybrid_attn_bwd_workspace_bytes",
     "saf_hybrid_attn_bwd",
     "saf_hybrid_attn_bwd_stage",
@@ -81,6 +82,8 @@ def load() -> ctypes.CDLL:
     vp, i, f32p, u8p = ctypes.c_void_p, ctypes.c_int, ctypes.POINTER(ctypes.c_float), ctypes.c_void_p
     lib.saf_hybrid_attn_fwd.restype = ctypes.c_int
     lib.saf_hybrid_attn_fwd.argtypes = [i, vp, vp, vp, u8p, vp, vp, i, i, i, i, i, vp, vp, vp]
+    lib.saf_hybrid_attn_fwd_gqa.restype = ctypes.c_int
+    lib.saf_hybrid_attn_fwd_gqa.argtypes = [i, vp, vp, vp, u8p, vp, vp, i, i, i, i, i, i, vp, vp, vp]
     lib.saf_hybrid_attn_bwd_workspace_bytes.restype = ctypes.c_size_t
     lib.saf_hybrid_attn_bwd_workspace_bytes.argtypes = [i, i, i, i, i]
     bwd_args = [i, vp, vp, vp, vp, vp, vp, u8p, vp, vp, i, i, i, i, i, vp, vp, vp, vp, ctypes.c_size_t, vp]
@@ -211,6 +214,38 @@ def saf_hybrid_attn_fwd(Q: Optional[torch.Tensor], K: Optional[torch.Tensor], V:
         _dtype_code(V), _ptr(Q), _ptr(K), _ptr(V), flags.ctypes.data, pa, pr, lda,
         B, H, N, d, _ptr(O), _ptr(LSE), _stream(dev))
     _raise(code, "saf_hybrid_attn_fwd")
+    return O, LSE
+
+
+def saf_hybrid_attn_fwd_gqa(Q: Optional[torch.Tensor], K: Optional[torch.Tensor], V: torch.Tensor,
+                            head_is_fixed: Sequence[int], a: Optional[torch.Tensor] = None,
+                            r: Optional[torch.Tensor] = None, O: Optional[torch.Tensor] = None,
+                            LSE: Optional[torch.Tensor] = None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Grouped-query forward: ``Q`` ``[B, Hq, N, d]``, ``K``, ``V``
+    ``[B, Hkv, N, d]`` (d in 64, 96, 128).  Returns ``(O, LSE)``."""
+    lib = load()
+    B, Hkv, N, d = V.shape
+    dev = V.device
+    _check_act("V", V, V.shape, V.dtype, dev)
+    _check_act("K", K, V.shape, V.dtype, dev, allow_none=True)
+    flags = np.ascontiguousarray(np.asarray(
+        head_is_fixed.detach().cpu().numpy() if isinstance(head_is_fixed, torch.Tensor) else head_is_fixed,
+        dtype=np.uint8).reshape(-1))
+    Hq = flags.shape[0]
+    _check_act("Q", Q, (B, Hq, N, d), V.dtype, dev, allow_none=True)
+    if O is None:
+        O = torch.empty((B, Hq, N, d), dtype=V.dtype, device=dev)
+    if LSE is None:
+        LSE = torch.empty((B, Hq, N), dtype=torch.float32, device=dev)
+    _check_act("O", O, (B, Hq, N, d), V.dtype, dev)
+    _check_act("LSE", LSE, (B, Hq, N), torch.float32, dev)
+    pa, lda = _prior("a", a, Hq, N, dev)
+    pr, ldr = _prior("r", r, Hq, N, dev)
+    if pa is not None and pr is not None and lda != ldr:
+        raise ValueError("a and r must share one row stride")
+    code = lib.saf_hybrid_attn_fwd_gqa(_dtype_code(V), _ptr(Q), _ptr(K), _ptr(V), flags.ctypes.data, pa, pr, lda,
+                                       B, Hq, Hkv, N, d, _ptr(O), _ptr(LSE), _stream(dev))
+    _raise(code, "saf_hybrid_attn_fwd_gqa")
     return O, LSE
 
 

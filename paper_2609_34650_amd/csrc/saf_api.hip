@@ -12,6 +12,7 @@
 #include "saf_calib_kernels.h"
 #include "saf_fit_kernels.h"
 #include "saf_fwd.h"
+#include "saf_gqa.h"
 #include "saf_pattern.h"
 
 #define SAF_EXPORT extern "C" __attribute__((visibility("default")))
@@ -249,6 +250,83 @@ SAF_EXPORT saf_status_t saf_hybrid_attn_fwd(saf_dtype_t dt, const void* Q, const
     args.n_qblocks = (N + saf::FWD_BM - 1) / saf::FWD_BM;
     args.scale_log2 = saf::LOG2E / sqrtf((float)saf::HEAD_DIM);
     return dt == SAF_DTYPE_BF16 ? launch_fwd<saf::bf16>(args, stream) : launch_fwd<float>(args, stream);
+}
+
+namespace {
+
+template <typename T, int D>
+void launch_gqa(const saf::GqaArgs& args, hipStream_t stream) {
+    const unsigned grid = (unsigned)((size_t)args.n_qblocks * args.B * args.Hq);
+    hipLaunchKernelGGL((saf::gqa_fwd_kernel<T, D>), dim3(grid), dim3(saf::GQA_THREADS), 0, stream, args);
+}
+
+}  // namespace
+
+SAF_EXPORT saf_status_t saf_hybrid_attn_fwd_gqa(saf_dtype_t dt, const void* Q, const void* K, const void* V,
+                                                const uint8_t* head_is_fixed, const float* a, const float* r,
+                                                int ld_prior, int B, int Hq, int Hkv, int N, int d, void* O,
+                                                float* LSE, hipStream_t stream) {
+    if (dt != SAF_DTYPE_F32 && dt != SAF_DTYPE_BF16) return SAF_ERR_UNSUPPORTED;
+    if (B < 0 || Hq < 0 || Hkv < 0 || N < 0 || d < 0) return SAF_ERR_SHAPE;
+    if (d != 64 && d != 96 && d != 128) return SAF_ERR_UNSUPPORTED;
+    if (Hq > 64) return SAF_ERR_UNSUPPORTED;
+    // One (batch, head) slice stays below 2^31 bytes for 32-bit buffer offsets.
+    if ((int64_t)N * d * (dt == SAF_DTYPE_F32 ? 4 : 2) > INT32_MAX) return SAF_ERR_SHAPE;
+    if ((int64_t)B * Hq * ((N + saf::GQA_BM - 1) / saf::GQA_BM) > INT32_MAX) return SAF_ERR_SHAPE;
+    if (B == 0 || Hq == 0 || N == 0) return SAF_OK;
+    if (Hkv == 0 || Hq % Hkv != 0) return SAF_ERR_SHAPE;
+    if (head_is_fixed == nullptr) return SAF_ERR_NULL;
+    uint64_t mask = 0;
+    bool any_ordinary = false;
+    for (int h = 0; h < Hq; ++h) {
+        if (head_is_fixed[h] > 1) return SAF_ERR_FLAG;
+        if (head_is_fixed[h]) mask |= 1ull << h;
+        else any_ordinary = true;
+    }
+    if (mask && (a == nullptr || r == nullptr)) return SAF_ERR_MISSING_PRIOR;
+    if (mask && ld_prior < N) return SAF_ERR_SHAPE;
+    if (V == nullptr || O == nullptr || LSE == nullptr) return SAF_ERR_NULL;
+    if (any_ordinary && (Q == nullptr || K == nullptr)) return SAF_ERR_NULL;
+    if (!aligned16(V) || !aligned16(O) || !aligned16(LSE) || (Q && !aligned16(Q)) || (K && !aligned16(K)))
+        return SAF_ERR_ALIGNMENT;
+    if (mask) {
+        saf::NormArgs na = {};
+        na.a = a;
+        na.r = r;
+        na.lse = LSE;
+        na.B = B;
+        na.H = Hq;
+        na.N = N;
+        na.ld_prior = ld_prior;
+        na.n_rblocks = (N + saf::NORM_ROWS - 1) / saf::NORM_ROWS;
+        na.n_fixed = 0;
+        for (int h = 0; h < Hq; ++h)
+            if ((mask >> h) & 1ull) na.heads[na.n_fixed++] = (unsigned char)h;
+        const unsigned ngrid = (unsigned)((size_t)na.n_rblocks * na.n_fixed);
+        hipLaunchKernelGGL(saf::fixed_lse_kernel, dim3(ngrid), dim3(saf::NORM_THREADS), 0, stream, na);
+        if (launched() != SAF_OK) return SAF_ERR_LAUNCH;
+    }
+    saf::GqaArgs args;
+    args.q = Q;
+    args.k = K;
+    args.v = V;
+    args.a = a;
+    args.r = r;
+    args.o = O;
+    args.lse = LSE;
+    args.fixed_mask = mask;
+    args.B = B;
+    args.Hq = Hq;
+    args.Hkv = Hkv;
+    args.N = N;
+    args.ld_prior = ld_prior;
+    args.n_qblocks = (N + saf::GQA_BM - 1) / saf::GQA_BM;
+    args.scale_log2 = saf::LOG2E / sqrtf((float)d);
+    const bool bf = dt == SAF_DTYPE_BF16;
+    if (d == 64) bf ? launch_gqa<saf::bf16, 64>(args, stream) : launch_gqa<float, 64>(args, stream);
+    else if (d == 96) bf ? launch_gqa<saf::bf16, 96>(args, stream) : launch_gqa<float, 96>(args, stream);
+    else bf ? launch_gqa<saf::bf16, 128>(args, stream) : launch_gqa<float, 128>(args, stream);
+    return launched();
 }
 
 SAF_EXPORT size_t saf_hybrid_attn_bwd_workspace_bytes(saf_dtype_t dt, int B, int H, int N, int d) {

@@ -162,9 +162,10 @@ constexpr int SLAB_BYTES = 32 * 64 + 128;
 constexpr int TILE_ROWS = 64;
 
 template <typename T> __host__ __device__ constexpr int slab_cols() { return 32 / (int)sizeof(T); }
-template <typename T> __host__ __device__ constexpr int tile_slabs() { return HEAD_DIM / slab_cols<T>(); }
-template <typename T> __host__ __device__ constexpr int tile_elems() {
-    return tile_slabs<T>() * SLAB_BYTES / (int)sizeof(T);
+// D: the row width (head dimension) of the matrix the tile comes from.
+template <typename T, int D = HEAD_DIM> __host__ __device__ constexpr int tile_slabs() { return D / slab_cols<T>(); }
+template <typename T, int D = HEAD_DIM> __host__ __device__ constexpr int tile_elems() {
+    return tile_slabs<T, D>() * SLAB_BYTES / (int)sizeof(T);
 }
 // Element offset of (row, col) inside a tile.
 template <typename T> __device__ __forceinline__ int toff(int row, int col) {
@@ -178,13 +179,14 @@ template <typename T> __device__ __forceinline__ int unit_row(int w, int lane) {
 template <typename T> __device__ __forceinline__ int unit_col(int w, int lane, int k) {
     return ((w >> 1) + 2 * k) * slab_cols<T>() + (lane & 1) * (16 / (int)sizeof(T));
 }
-template <typename T> __host__ __device__ constexpr int tile_units() { return tile_slabs<T>() / 2; }
+template <typename T, int D = HEAD_DIM> __host__ __device__ constexpr int tile_units() {
+    return tile_slabs<T, D>() / 2;
+}
 
-// Buffer resource over one [rows, 64] slice of T; reads past `rows` return 0.
-template <typename T>
+// Buffer resource over one [rows, D] slice of T; reads past `rows` return 0.
+template <typename T, int D = HEAD_DIM>
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t slice_rsrc(const T* base, int rows) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(base), (short)0, rows * HEAD_DIM * (int)sizeof(T),
-                                             0x00020000);
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(base), (short)0, rows * D * (int)sizeof(T), 0x00020000);
 }
 
 typedef __attribute__((address_space(3))) void lds_void;
@@ -193,14 +195,14 @@ typedef __attribute__((address_space(3))) void lds_void;
 // wavefront issues tile_units() buffer loads that write LDS directly (no
 // registers).  Rows past the end of the slice arrive as zeros.  The data is
 // visible after the next __syncthreads().
-template <typename T>
+template <typename T, int D = HEAD_DIM>
 __device__ __forceinline__ void tile_load_lds(T* tile, __amdgpu_buffer_rsrc_t rsrc, int row0, int w, int lane) {
 #pragma unroll
-    for (int k = 0; k < tile_units<T>(); ++k) {
+    for (int k = 0; k < tile_units<T, D>(); ++k) {
         const int s = (w >> 1) + 2 * k;
         T* dst = tile + s * (SLAB_BYTES / (int)sizeof(T)) + (w & 1) * (1024 / (int)sizeof(T));
         const int row = row0 + unit_row<T>(w, lane);
-        const int voff = row * HEAD_DIM * (int)sizeof(T) + s * 32 + (lane & 1) * 16;
+        const int voff = row * D * (int)sizeof(T) + s * 32 + (lane & 1) * 16;
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void*)dst, 16, voff, 0, 0, 0);
     }
 }

@@ -1,0 +1,246 @@
+// Forward of the hybrid layer with grouped-query attention and head
+// dimensions 64, 96 or 128 (the layouts of the paper's grouped-query prefill
+// measurement and of its 1B model's head width: Section "Pretrained
+// grouped-query models" and Appendix "Mixed-head execution and numerical
+// checks", where the grouped-query implementation drops the replaced heads'
+// query projections but keeps every shared key and value head).
+//
+// Q, O: [B, Hq, N, D]; K, V: [B, Hkv, N, D]; query head h reads key/value
+// head h / (Hq / Hkv).  A fixed query head reads only V of its group.
+//
+// Workgroup = (batch b, query head h, block of 128 queries), 4 wavefronts of
+// 32 queries (one query per lane column c, as in the layer's forward: scores
+// are formed transposed, S^T = K Q^T, keys in accumulator rows).  K and V
+// tiles of 64 keys go to column-slab LDS tiles D wide by buffer loads straight
+// to LDS, double-buffered; the tiles that meet the diagonal come first with a
+// per-score causal compare.
+//   Ordinary head: online softmax (running maximum raised when a sub-block
+//   exceeds it, accumulator and sum rescaled), O^T += V^T P^T on MFMA, LSE =
+//   m + ln l.
+//   Fixed head: P(i, j) = exp(a[j] + r[i - j] - log Z(i)) per entry, with
+//   log Z from the normaliser pre-pass (the layer forward's fixed_lse_kernel)
+//   and the tile's a values and r band staged in LDS; O^T += V^T P^T.  The
+//   rows are already normalised, so no running maximum is needed.
+#pragma once
+
+#include "saf_common.h"
+
+namespace saf {
+
+constexpr int GQA_BM = 128;  // queries per workgroup
+constexpr int GQA_BN = 64;   // keys per tile
+constexpr int GQA_THREADS = 256;
+constexpr int GQA_BAND = GQA_BM + GQA_BN - 1;  // offsets met by one tile
+
+struct GqaArgs {
+    const void* q;
+    const void* k;
+    const void* v;
+    const float* a;
+    const float* r;
+    void* o;
+    float* lse;
+    uint64_t fixed_mask;
+    int B, Hq, Hkv, N, ld_prior, n_qblocks;
+    float scale_log2;  // log2(e) / sqrt(D)
+};
+
+struct GqaLane {
+    int tid, w, lane, c, hf, m0, q0, N;
+};
+
+// One 64-key tile (two 32-key sub-blocks) of an ordinary head.
+template <typename T, int D, bool MASK>
+__device__ __forceinline__ void gqa_ord_tile(const T* kt, const T* vt, int n0, const GqaLane& L,
+                                             const typename Vec<T>::x8 (&qf)[D / 16], f32x16 (&oacc)[D / 32],
+                                             float& m_run, float& l_run, float sl2) {
+    typedef typename Vec<T>::x8 frag;
+    const int qq = L.q0 + L.c;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+        const int k0 = n0 + 32 * kb;
+        if (MASK && k0 > L.q0 + 31) break;  // sub-block wholly after the wavefront's queries
+        f32x16 s;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) s[v] = 0.0f;
+#pragma unroll
+        for (int dc = 0; dc < D / 16; ++dc) mma(s, ld_row<T>(kt, 32 * kb + L.c, 16 * dc + 8 * L.hf), qf[dc]);
+        float mx = -INFINITY;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            if (MASK) {
+                const int kk = k0 + 8 * (v >> 2) + 4 * L.hf + (v & 3);
+                s[v] = kk > qq ? -INFINITY : s[v];
+            }
+            mx = vmax(mx, s[v]);
+        }
+        mx = pair_max(mx) * sl2;
+        if (mx > m_run) {  // raise the running maximum, rescale (per lane; both halves agree)
+            const float alpha = fast_exp2(m_run - mx);
+            m_run = mx;
+            l_run *= alpha;
+#pragma unroll
+            for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) oacc[db][v] *= alpha;
+        }
+        f32x16 pr;
+        float t = 0.0f;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            pr[v] = fast_exp2(fmaf(s[v], sl2, -m_run));
+            t += pr[v];
+        }
+        l_run += t;
+        frag pb[2];
+#pragma unroll
+        for (int kc = 0; kc < 2; ++kc) pb[kc] = to_operand<T>(pr, 8 * kc);
+#pragma unroll
+        for (int kc = 0; kc < 2; ++kc)
+#pragma unroll
+            for (int db = 0; db < D / 32; ++db) mma(oacc[db], ld_tile_t<true>(vt, 32 * kb + 16 * kc, 32 * db), pb[kc]);
+    }
+}
+
+// One 64-key tile of a fixed head.  as[k]: a of the tile's key k; rb[x]:
+// r(m0 - n0 - 63 + x); lz: log Z of this lane's query.
+template <typename T, int D, bool MASK>
+__device__ __forceinline__ void gqa_fix_tile(const T* vt, const float* as, const float* rb, int n0, const GqaLane& L,
+                                             float lz, f32x16 (&oacc)[D / 32]) {
+    typedef typename Vec<T>::x8 frag;
+    const int qq = L.q0 + L.c;
+    const int ql = qq - L.m0;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+        const int k0 = n0 + 32 * kb;
+        if (MASK && k0 > L.q0 + 31) break;
+        f32x16 pr;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            const int kl = 32 * kb + 8 * (v >> 2) + 4 * L.hf + (v & 3);  // key within the tile
+            float x = fast_exp2((as[kl] + rb[ql - kl + (GQA_BN - 1)] - lz) * LOG2E);
+            if (MASK && n0 + kl > qq) x = 0.0f;
+            pr[v] = x;
+        }
+        frag pb[2];
+#pragma unroll
+        for (int kc = 0; kc < 2; ++kc) pb[kc] = to_operand<T>(pr, 8 * kc);
+#pragma unroll
+        for (int kc = 0; kc < 2; ++kc)
+#pragma unroll
+            for (int db = 0; db < D / 32; ++db) mma(oacc[db], ld_tile_t<true>(vt, 32 * kb + 16 * kc, 32 * db), pb[kc]);
+    }
+}
+
+template <typename T, int D>
+__global__ __launch_bounds__(GQA_THREADS) __attribute__((amdgpu_waves_per_eu(2))) void gqa_fwd_kernel(GqaArgs p) {
+    __shared__ __attribute__((aligned(16))) T k0s[tile_elems<T, D>()];
+    __shared__ __attribute__((aligned(16))) T k1s[tile_elems<T, D>()];
+    __shared__ __attribute__((aligned(16))) T v0s[tile_elems<T, D>()];
+    __shared__ __attribute__((aligned(16))) T v1s[tile_elems<T, D>()];
+    __shared__ float ab0[GQA_BN + GQA_BAND + 1];
+    __shared__ float ab1[GQA_BN + GQA_BAND + 1];
+    const int n_bh = p.B * p.Hq;
+    const int qblk = p.n_qblocks - 1 - (int)(blockIdx.x / n_bh);  // longest first
+    const int bh = (int)(blockIdx.x % n_bh);
+    const int b = bh / p.Hq;
+    const int h = bh % p.Hq;
+    const int hkv = h / (p.Hq / p.Hkv);
+    const bool fixed = (p.fixed_mask >> h) & 1ull;
+    GqaLane L;
+    L.tid = threadIdx.x;
+    L.w = __builtin_amdgcn_readfirstlane(L.tid >> 6);
+    L.lane = L.tid & 63;
+    L.c = L.tid & 31;
+    L.hf = (L.tid >> 5) & 1;
+    L.m0 = qblk * GQA_BM;
+    L.q0 = L.m0 + 32 * L.w;
+    L.N = p.N;
+    const int N = p.N;
+    const size_t qbase = (size_t)bh * N * D;
+    const size_t kvbase = ((size_t)b * p.Hkv + hkv) * N * D;
+    const size_t row_base = (size_t)bh * N;
+    const __amdgpu_buffer_rsrc_t rk = slice_rsrc<T, D>(reinterpret_cast<const T*>(p.k) + kvbase, N);
+    const __amdgpu_buffer_rsrc_t rv = slice_rsrc<T, D>(reinterpret_cast<const T*>(p.v) + kvbase, N);
+    typedef typename Vec<T>::x8 frag;
+    const int qq = L.q0 + L.c;
+
+    f32x16 oacc[D / 32];
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) oacc[db][v] = 0.0f;
+
+    const int n_tiles = (min(L.m0 + GQA_BM, N) + GQA_BN - 1) / GQA_BN;
+    const int n_full = L.m0 / GQA_BN;
+    const int n_mask = n_tiles - n_full;  // 1 or 2
+    const int P = (n_mask + 1) & ~1;
+    auto tile_of = [&](int i) { return i < P ? (i < n_mask ? n_full + i : -1) : i - P; };
+    float row_scale = 1.0f, lse_out = 0.0f;
+    if (!fixed) {
+        const T* __restrict__ Q = reinterpret_cast<const T*>(p.q) + qbase;
+        frag qf[D / 16];
+#pragma unroll
+        for (int dc = 0; dc < D / 16; ++dc)
+            qf[dc] = qq < N ? ld8<T>(Q + (size_t)qq * D + 16 * dc + 8 * L.hf) : zero8<T>();
+        float m_run = NEG_BIG, l_run = 0.0f;
+        run_slots(
+            P, P + n_full, tile_of,
+            [&](auto buf, int t) {
+                constexpr int B_ = decltype(buf)::value;
+                tile_load_lds<T, D>(B_ ? k1s : k0s, rk, t * GQA_BN, L.w, L.lane);
+                tile_load_lds<T, D>(B_ ? v1s : v0s, rv, t * GQA_BN, L.w, L.lane);
+            },
+            [&](auto) {},
+            [&](auto buf, int t, auto mask) {
+                constexpr int B_ = decltype(buf)::value;
+                gqa_ord_tile<T, D, decltype(mask)::value>(B_ ? k1s : k0s, B_ ? v1s : v0s, t * GQA_BN, L, qf, oacc,
+                                                          m_run, l_run, p.scale_log2);
+            });
+        const float l_tot = pair_sum(l_run);
+        row_scale = 1.0f / l_tot;
+        lse_out = (m_run + __log2f(l_tot)) * LN2;
+    } else {
+        const float* arow = p.a + (size_t)h * p.ld_prior;
+        const float* rrow = p.r + (size_t)h * p.ld_prior;
+        const float lz = qq < N ? p.lse[row_base + qq] : 0.0f;
+        run_slots(
+            P, P + n_full, tile_of,
+            [&](auto buf, int t) {
+                constexpr int B_ = decltype(buf)::value;
+                tile_load_lds<T, D>(B_ ? v1s : v0s, rv, t * GQA_BN, L.w, L.lane);
+                // The tile's a values, then r over offsets m0 - n0 - 63 .. m0 - n0 + 127.
+                float* ab = B_ ? ab1 : ab0;
+                const int n0 = t * GQA_BN;
+                for (int x = L.tid; x < GQA_BN + GQA_BAND; x += GQA_THREADS) {
+                    float val;
+                    if (x < GQA_BN) {
+                        val = n0 + x < N ? arow[n0 + x] : -INFINITY;
+                    } else {
+                        const int delta = L.m0 - n0 - (GQA_BN - 1) + (x - GQA_BN);
+                        val = (delta >= 0 && delta < N) ? rrow[delta] : -INFINITY;
+                    }
+                    ab[x] = val;
+                }
+            },
+            [&](auto) {},
+            [&](auto buf, int t, auto mask) {
+                constexpr int B_ = decltype(buf)::value;
+                const float* ab = B_ ? ab1 : ab0;
+                gqa_fix_tile<T, D, decltype(mask)::value>(B_ ? v1s : v0s, ab, ab + GQA_BN, t * GQA_BN, L, lz, oacc);
+            });
+    }
+    if (qq < N) {
+        T* orow = reinterpret_cast<T*>(p.o) + qbase + (size_t)qq * D;
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+                st4<T>(orow + 32 * db + 8 * g + 4 * L.hf, oacc[db][4 * g] * row_scale,
+                       oacc[db][4 * g + 1] * row_scale, oacc[db][4 * g + 2] * row_scale,
+                       oacc[db][4 * g + 3] * row_scale);
+        if (!fixed && L.hf == 0) p.lse[row_base + qq] = lse_out;
+    }
+}
+
+}  // namespace saf

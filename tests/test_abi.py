@@ -245,3 +245,33 @@ def test_fit_entry_points_reject_bad_arguments(lib):
     assert cf(ne=FAKE + 4) == 6 and cf(ws=FAKE + 8) == 6
     assert cf(wb=16) == 2
     assert cf(T=0, ea=None) == 0
+
+
+# ---------------------------------------------------------------------------
+# Grouped-query forward (saf_hybrid_attn_fwd_gqa)
+# ---------------------------------------------------------------------------
+
+def _gqa(lib, dt=1, Q=FAKE, K=FAKE, V=FAKE, flags=(0, 1, 0, 0), a=FAKE, r=FAKE, ld=None, B=1, Hkv=2, N=8, d=128,
+         O=FAKE, LSE=FAKE):
+    f = np.asarray(flags, dtype=np.uint8)
+    Hq = f.shape[0]
+    ld = N if ld is None else ld
+    return lib.saf_hybrid_attn_fwd_gqa(dt, Q, K, V, f.ctypes.data if Hq else None, a, r, ld, B, Hq, Hkv, N, d, O,
+                                       LSE, None)
+
+
+def test_gqa_forward_rejects_bad_arguments(lib):
+    assert _gqa(lib, d=80) == 3
+    assert _gqa(lib, dt=9) == 3
+    assert _gqa(lib, Hkv=3) == 2          # 4 query heads are not a multiple of 3
+    assert _gqa(lib, Hkv=0) == 2
+    assert _gqa(lib, flags=(0, 2, 0, 0)) == 7
+    assert _gqa(lib, a=None) == 4
+    assert _gqa(lib, ld=4) == 2
+    assert _gqa(lib, V=None) == 1
+    assert _gqa(lib, Q=None) == 1         # an ordinary head needs Q and K
+    assert _gqa(lib, Q=None, K=None, flags=(1, 1, 1, 1)) != 1
+    assert _gqa(lib, O=FAKE + 2) == 6
+    assert _gqa(lib, N=(1 << 23), d=128) == 2   # 2^23 rows x 256 B reaches 2^31
+    assert _gqa(lib, flags=[0] * 65, Hkv=5) == 3
+    assert _gqa(lib, N=0, Q=None, K=None, V=None, O=None, LSE=None) == 0

@@ -1,0 +1,101 @@
+"""GPU parity of the grouped-query forward (saf_hybrid_attn_fwd_gqa) for head
+dimensions 64, 96 and 128 against the fp64 oracle
+(``oracle.saf_oracle.layer_forward_gqa``).
+
+Inputs come from the seeded generator (query heads as drawn; key/value heads
+are the first Hkv heads of the drawn K and V).  Bars are the layer's:
+float32 ``max |gpu - oracle| <= 1e-4``; bf16 ``|gpu - oracle| <= 1e-2 +
+2e-2 |oracle|`` on O and LSE.
+"""
+
+import numpy as np
+import pytest
+
+from gpu_helpers import BF16_ATOL, BF16_RTOL, F32_ATOL, announce, torch_cuda
+
+pytestmark = pytest.mark.gpu
+
+
+def _inputs(dtype, B, Hq, Hkv, N, d, fixed, stream_id):
+    from paper_2609_34650_amd import inputs
+    inp = inputs.make_inputs(B, Hq, N, d, fixed, dtype, stream_id=stream_id, backward=False)
+    inp["K"] = np.ascontiguousarray(inp["K"][:, :Hkv])
+    inp["V"] = np.ascontiguousarray(inp["V"][:, :Hkv])
+    return inp
+
+
+def _run_gpu(inp, dtype):
+    torch = torch_cuda()
+    from paper_2609_34650_amd import binding
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    dev = torch.device("cuda", 0)
+    Q, K, V = (torch.from_numpy(inp[k]).to(dev).to(tdt).contiguous() for k in ("Q", "K", "V"))
+    a = torch.from_numpy(np.ascontiguousarray(inp["a"])).to(dev)
+    r = torch.from_numpy(np.ascontiguousarray(inp["r"])).to(dev)
+    O, LSE = binding.saf_hybrid_attn_fwd_gqa(Q, K, V, inp["is_fixed"], a, r)
+    torch.cuda.synchronize()
+    return O.double().cpu().numpy(), LSE.double().cpu().numpy()
+
+
+def _check(dtype, g, o):
+    if dtype == "f32":
+        assert np.max(np.abs(g - o)) <= F32_ATOL
+    else:
+        excess = np.abs(g - o) - (BF16_ATOL + BF16_RTOL * np.abs(o))
+        assert np.max(excess) <= 0, float(np.max(excess))
+
+
+@pytest.mark.parametrize("dtype,B,Hq,Hkv,N,d,fixed", [
+    ("f32", 1, 4, 4, 200, 64, (1,)),
+    ("bf16", 2, 8, 2, 300, 128, (0, 5)),
+    ("bf16", 1, 6, 1, 77, 96, (2, 3)),
+    ("f32", 1, 4, 2, 130, 96, (0,)),
+    ("f32", 1, 2, 1, 129, 128, ()),
+    ("bf16", 1, 4, 2, 1, 128, (1,)),
+    ("bf16", 1, 4, 4, 257, 64, (0, 1, 2, 3)),
+])
+def test_gqa_forward_matches_oracle(dtype, B, Hq, Hkv, N, d, fixed):
+    from oracle import saf_oracle as orc
+    announce(f"gqa fwd {dtype} B={B} Hq={Hq} Hkv={Hkv} N={N} d={d} fixed={fixed}")
+    inp = _inputs(dtype, B, Hq, Hkv, N, d, list(fixed), stream_id=51)
+    O, LSE = _run_gpu(inp, dtype)
+    Oo, LSEo = orc.layer_forward_gqa(inp["Q"], inp["K"], inp["V"], inp["is_fixed"], inp["a"], inp["r"])
+    _check(dtype, O, Oo)
+    _check(dtype, LSE, LSEo)
+
+
+def test_gqa_forward_equals_layer_forward_at_d64():
+    """With one query head per key/value head and d = 64 the grouped-query
+    kernel and the layer's own forward compute the same function."""
+    torch = torch_cuda()
+    from paper_2609_34650_amd import binding
+    announce("gqa vs layer forward d=64")
+    inp = _inputs("f32", 2, 4, 4, 333, 64, [1, 2], stream_id=52)
+    O, LSE = _run_gpu(inp, "f32")
+    dev = torch.device("cuda", 0)
+    t = {k: torch.from_numpy(inp[k]).to(dev) for k in ("Q", "K", "V", "a", "r")}
+    O2, LSE2 = binding.saf_hybrid_attn_fwd(t["Q"], t["K"], t["V"], inp["is_fixed"], t["a"], t["r"])
+    torch.cuda.synchronize()
+    np.testing.assert_allclose(O, O2.double().cpu().numpy(), rtol=0, atol=2e-5)
+    np.testing.assert_allclose(LSE, LSE2.double().cpu().numpy(), rtol=0, atol=2e-5)
+
+
+@pytest.mark.slow
+def test_gqa_prefill_shape_sampled():
+    """The grouped-query prefill layout (32 query heads, 8 key/value heads,
+    d = 128, 8 fixed heads, N = 4096, bf16): every head of one batch element,
+    sampled rows against the oracle."""
+    from oracle import saf_oracle as orc
+    from paper_2609_34650_amd import inputs
+    fixed = inputs.fixed_heads(32, 8, stream_id=53)
+    announce(f"gqa prefill shape fixed={fixed}")
+    inp = _inputs("bf16", 1, 32, 8, 4096, 128, fixed, stream_id=53)
+    O, LSE = _run_gpu(inp, "bf16")
+    rows = np.array([0, 1, 63, 64, 127, 128, 1000, 2047, 4095])
+    for h in range(32):
+        g = h // 4
+        fx = bool(inp["is_fixed"][h])
+        o, lse = orc.head_forward(None if fx else inp["Q"][0, h], None if fx else inp["K"][0, g], inp["V"][0, g], fx,
+                                  inp["a"][h] if fx else None, inp["r"][h] if fx else None, rows=rows)
+        _check("bf16", O[0, h, rows], o)
+        _check("bf16", LSE[0, h, rows], lse)

@@ -326,6 +326,27 @@ def test_pattern_gradient_of_uniform_values_is_zero():
     np.testing.assert_allclose(dr, 0.0, atol=1e-13)
 
 
+def test_gqa_forward_equals_expanded_heads():
+    """Grouped-query forward = the multi-head forward with each key/value head
+    repeated for its group; with one query head per group it is the layer
+    forward itself (and d = 96 uses 1/sqrt(96))."""
+    B, Hq, Hkv, N, d = 2, 6, 2, 11, 96
+    Q = _rand(B, Hq, N, d)
+    K, V = _rand(B, Hkv, N, d), _rand(B, Hkv, N, d)
+    a, r = _rand(Hq, N), _rand(Hq, N)
+    is_fixed = np.array([0, 1, 0, 0, 1, 1], dtype=np.uint8)
+    O, LSE = orc.layer_forward_gqa(Q, K, V, is_fixed, a, r)
+    Ke, Ve = np.repeat(K, Hq // Hkv, axis=1), np.repeat(V, Hq // Hkv, axis=1)
+    O2, LSE2 = orc.layer_forward(Q, Ke, Ve, is_fixed, a, r)
+    np.testing.assert_allclose(O, O2, rtol=0, atol=0)
+    np.testing.assert_allclose(LSE, LSE2, rtol=0, atol=0)
+    # An ordinary head against torch's scaled_dot_product_attention at d = 96.
+    torch = pytest.importorskip("torch")
+    ref = torch.nn.functional.scaled_dot_product_attention(
+        torch.tensor(Q[:, 0:1]), torch.tensor(K[:, 0:1]), torch.tensor(V[:, 0:1]), is_causal=True)
+    np.testing.assert_allclose(O[:, 0:1], ref.numpy(), rtol=1e-12, atol=1e-13)
+
+
 def test_fixed_heads_never_read_queries_or_keys():
     B, H, N, d = 2, 3, 16, 4
     Q, K, V, dO = (_rand(B, H, N, d) for _ in range(4))
