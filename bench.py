@@ -32,6 +32,14 @@ batch element: the three of the weight's exponent and exp, dP - D, the
 product, and the two sums) against the chip's float32 vector rate
 (256 CUs x 4 SIMDs x 32 lanes per clock x 2.4 GHz = 78.6 Tops/s).
 
+``--gqa`` times the grouped-query prefill forward (saf_hybrid_attn_fwd_gqa)
+in the layout of the paper's grouped-query prefill measurement: B = 4,
+T = 4096, 32 query heads sharing 8 key/value heads, d = 128, bf16, at 30 %
+fixed heads (and a sweep over 0-75 %), against the same kernel with every
+head ordinary; torch's flash SDPA (forced, no fallback) is timed beside it
+for reference when available.  MFMA roofline: an ordinary head counts 2
+contractions (QK^T, PV), a fixed head 1 (PV).
+
 ``--fit`` times the compact fit of one 12-head layer at T = 4096: the
 targets from the calibration mean (floor, renormalise, marginals), then the
 fitter's 400 Adam steps and the acceptance KL, for all heads at once; its
@@ -112,6 +120,7 @@ KERNEL_SOURCES = {
     "layer": ("saf_common.h", "saf_fwd.h", "saf_bwd.h"),
     "calib": ("saf_common.h", "saf_calib_kernels.h"),
     "pattern": ("saf_common.h", "saf_pattern.h"),
+    "gqa": ("saf_common.h", "saf_gqa.h"),
 }
 
 
@@ -142,7 +151,12 @@ def measured_traffic(workload: str, stage: str):
                 digest = parts[1]
             elif len(parts) >= 3 and parts[0] == "traffic_bytes:" and parts[1] == stage:
                 found = float(parts[2])
-    group = "calib" if workload in gen.CALIB_WORKLOADS else ("pattern" if workload.startswith("pattern_") else "layer")
+    if workload in gen.CALIB_WORKLOADS:
+        group = "calib"
+    elif workload.startswith(("pattern_", "gqa_")):
+        group = workload.split("_")[0]
+    else:
+        group = "layer"
     if digest != kernel_source_digest(group):
         return None
     return found
@@ -162,6 +176,8 @@ def parse():
     ap.add_argument("--no-compare-ordinary", dest="compare", action="store_false")
     ap.add_argument("--pattern", action="store_true",
                     help="time the trainable-pattern gradients (da, dr) at the layer workload instead")
+    ap.add_argument("--gqa", action="store_true",
+                    help="time the grouped-query prefill forward (B=4, T=4096, 32/8 heads, d=128) instead")
     ap.add_argument("--fit", action="store_true",
                     help="time the compact fit (targets + 400 Adam steps) of a 12-head layer at T=4096 instead")
     ap.add_argument("--calib", action="store_true",
@@ -580,6 +596,143 @@ def main_fit(args, torch):
     print(json.dumps(result), flush=True)
 
 
+# ---------------------------------------------------------------------------
+# Grouped-query prefill forward
+# ---------------------------------------------------------------------------
+
+def _gqa_job(job):
+    from oracle import saf_oracle as orc
+    q, k, v, fx, a, r = job
+    orc.head_forward(q, k, v, fx, a, r, 512)
+    return 1
+
+
+def gqa_cpu_baseline(inp, Hkv, flags):
+    """The oracle's dense fp64 forward on every query head of batch element 0
+    (one head per process), scaled by B to the whole prefill call."""
+    import multiprocessing as mp
+    try:
+        from threadpoolctl import threadpool_limits
+    except ImportError:  # pragma: no cover
+        threadpool_limits = None
+    B, Hq = inp["Q"].shape[:2]
+    group = Hq // Hkv
+    jobs = []
+    for h in range(Hq):
+        fx = bool(flags[h])
+        g = h // group
+        jobs.append((None if fx else inp["Q"][0, h], None if fx else inp["K"][0, g], inp["V"][0, g], fx,
+                     inp["a"][h] if fx else None, inp["r"][h] if fx else None))
+    workers = max(1, min(MAX_HOST_WORKERS, len(os.sched_getaffinity(0)), len(jobs)))
+    ctx = threadpool_limits(limits=1) if threadpool_limits else None
+    t0 = time.perf_counter()
+    try:
+        with mp.get_context("fork").Pool(workers) as pool:
+            pool.map(_gqa_job, jobs, chunksize=1)
+    finally:
+        if ctx is not None and hasattr(ctx, "unregister"):
+            ctx.unregister()
+    wall = time.perf_counter() - t0
+    scale = B * Hq / len(jobs)
+    return {"value": round(wall * 1e3 * scale, 1), "unit": "ms", "cores": workers, "kind": "oracle",
+            "sample": f"all {Hq} query heads of batch element 0 ({int(sum(flags))} fixed), fp64 dense, "
+                      f"{wall:.1f} s wall on {workers} processes, scaled by {scale:g} to all {B * Hq} head slices"}
+
+
+def main_gqa(args, torch):
+    from paper_2609_34650_amd import binding
+    B, Hq, Hkv, N, d = 4, 32, 8, 4096, 128
+    inp = gen.make_inputs(B, Hq, N, d, [], "bf16", stream_id=61, backward=False)
+    dev = torch.device("cuda", 0)
+    Q = torch.from_numpy(inp["Q"]).to(dev).to(torch.bfloat16)
+    K = torch.from_numpy(np.ascontiguousarray(inp["K"][:, :Hkv])).to(dev).to(torch.bfloat16)
+    V = torch.from_numpy(np.ascontiguousarray(inp["V"][:, :Hkv])).to(dev).to(torch.bfloat16)
+    a = torch.from_numpy(inp["a"]).to(dev)
+    r = torch.from_numpy(inp["r"]).to(dev)
+    O = torch.empty_like(Q)
+    LSE = torch.empty((B, Hq, N), dtype=torch.float32, device=dev)
+    C = contraction_flop(N, d)
+
+    def flags_for(n_fixed):
+        f = np.zeros(Hq, np.uint8)
+        f[gen.fixed_heads(Hq, n_fixed, stream_id=61)] = 1
+        return f
+
+    def timed(flags, steps):
+        for _ in range(args.warmup):
+            binding.saf_hybrid_attn_fwd_gqa(Q, K, V, flags, a, r, O=O, LSE=LSE)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            binding.saf_hybrid_attn_fwd_gqa(Q, K, V, flags, a, r, O=O, LSE=LSE)
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps
+
+    main_fixed = round(0.3 * Hq)
+    fl = flags_for(main_fixed)
+    for _ in range(args.warmup):
+        binding.saf_hybrid_attn_fwd_gqa(Q, K, V, fl, a, r, O=O, LSE=LSE)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        binding.saf_hybrid_attn_fwd_gqa(Q, K, V, fl, a, r, O=O, LSE=LSE)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    ms_ev = timed(fl, args.steps)
+    flop = B * C * (2 * (Hq - main_fixed) + main_fixed)
+    tflops = flop / (ms_ev * 1e-3) / 1e12
+    ms_ord = timed(flags_for(0), args.steps)
+    sweep = {}
+    for rate in (0.1, 0.2, 0.3, 0.5, 0.75, 1.0):
+        nf = round(rate * Hq)
+        t = timed(flags_for(nf), args.steps)
+        sweep[f"{int(rate * 100)}%"] = {"n_fixed": nf, "ms": round(t, 4), "speedup_vs_all_ordinary": round(ms_ord / t, 3)}
+    sdpa = None
+    try:
+        from torch.nn.attention import SDPBackend, sdpa_kernel
+        with sdpa_kernel([SDPBackend.FLASH_ATTENTION]):
+            for _ in range(args.warmup):
+                torch.nn.functional.scaled_dot_product_attention(Q, K, V, is_causal=True, enable_gqa=True)
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(args.steps):
+                torch.nn.functional.scaled_dot_product_attention(Q, K, V, is_causal=True, enable_gqa=True)
+            e1.record()
+            torch.cuda.synchronize()
+            sdpa = round(e0.elapsed_time(e1) / args.steps, 4)
+    except Exception as exc:  # no flash kernel for this build or shape: report none
+        sdpa = f"unavailable: {type(exc).__name__}"
+    result = {
+        "metric": "GQA prefill attention forward ms (B=4, T=4096, 32 query / 8 kv heads, d=128, 30% fixed)",
+        "value": round(ms, 4),
+        "unit": "ms",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "gqa_prefill_4k: grouped-query hybrid attention forward", "B": B, "Hq": Hq,
+                   "Hkv": Hkv, "N": N, "d": d, "n_fixed": main_fixed, "parallelism": "single GPU"},
+        "tflops": round(tflops, 1),
+        "all_ordinary_ms": round(ms_ord, 4),
+        "speedup_vs_all_ordinary": round(ms_ord / ms_ev, 3),
+        "sweep": sweep,
+        "torch_flash_sdpa_all_ordinary_ms": sdpa,
+        "cpu_baseline": gqa_cpu_baseline(inp, Hkv, fl) if args.cpu_baseline else None,
+        "roofline": {"bound": "mfma", "kernel": "gqa_fwd", "achieved": round(tflops, 1), "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(tflops / PEAK_BF16_TFLOPS, 4),
+                     "traffic": measured_traffic("gqa_prefill_4k", "gqa_fwd")},
+    }
+    print(json.dumps(result), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -608,6 +761,9 @@ def main():
         return
     if args.fit:
         main_fit(args, torch)
+        return
+    if args.gqa:
+        main_gqa(args, torch)
         return
 
     w = gen.WORKLOADS[args.workload]

@@ -6,6 +6,7 @@
 #include "saf_fit.h"
 
 #include <math.h>
+#include <algorithm>
 #include <stdint.h>
 
 #include "saf_bwd.h"
@@ -116,6 +117,14 @@ saf_status_t launch_fwd(const saf::FwdArgs& args, hipStream_t stream) {
     return launched();
 }
 
+// Heads in order of decreasing work for slice_of: ordinary heads, then fixed.
+void fill_head_order(unsigned char* order, uint64_t fixed_mask, int H) {
+    int n = 0;
+    for (int pass = 0; pass < 2; ++pass)
+        for (int h = 0; h < H; ++h)
+            if ((int)((fixed_mask >> h) & 1ull) == pass) order[n++] = (unsigned char)h;
+}
+
 size_t workspace_bytes(int B, int H, int N) {
     const size_t d_bytes = (size_t)B * H * N * sizeof(float);
     return (d_bytes + 255) & ~(size_t)255;
@@ -176,6 +185,7 @@ saf::BwdArgs make_bwd_args(const void* Q, const void* K, const void* V, const vo
     args.dv = dV;
     args.dsum = reinterpret_cast<float*>(workspace);
     args.fixed_mask = pr.fixed_mask;
+    fill_head_order(args.head_order, pr.fixed_mask, H);
     args.B = B;
     args.H = H;
     args.N = N;
@@ -247,6 +257,7 @@ SAF_EXPORT saf_status_t saf_hybrid_attn_fwd(saf_dtype_t dt, const void* Q, const
     args.H = H;
     args.N = N;
     args.ld_prior = ld_prior;
+    fill_head_order(args.head_order, pr.fixed_mask, H);
     args.n_qblocks = (N + saf::FWD_BM - 1) / saf::FWD_BM;
     args.scale_log2 = saf::LOG2E / sqrtf((float)saf::HEAD_DIM);
     return dt == SAF_DTYPE_BF16 ? launch_fwd<saf::bf16>(args, stream) : launch_fwd<float>(args, stream);
@@ -322,6 +333,17 @@ SAF_EXPORT saf_status_t saf_hybrid_attn_fwd_gqa(saf_dtype_t dt, const void* Q, c
     args.ld_prior = ld_prior;
     args.n_qblocks = (N + saf::GQA_BM - 1) / saf::GQA_BM;
     args.scale_log2 = saf::LOG2E / sqrtf((float)d);
+    {
+        const int group = Hq / Hkv;
+        int work[64];
+        for (int g = 0; g < Hkv; ++g) {
+            work[g] = 0;
+            for (int i = 0; i < group; ++i) work[g] += ((mask >> (g * group + i)) & 1ull) ? 1 : 2;
+            args.kv_order[g] = (unsigned char)g;
+        }
+        std::stable_sort(args.kv_order, args.kv_order + Hkv,
+                         [&](unsigned char x, unsigned char y) { return work[x] > work[y]; });
+    }
     const bool bf = dt == SAF_DTYPE_BF16;
     if (d == 64) bf ? launch_gqa<saf::bf16, 64>(args, stream) : launch_gqa<float, 64>(args, stream);
     else if (d == 96) bf ? launch_gqa<saf::bf16, 96>(args, stream) : launch_gqa<float, 96>(args, stream);

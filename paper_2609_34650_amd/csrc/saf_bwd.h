@@ -33,6 +33,7 @@ struct BwdArgs {
     int B, H, N, ld_prior, n_blocks;
     float scale;       // 1 / sqrt(d)
     float scale_log2;  // log2(e) / sqrt(d)
+    unsigned char head_order[64];  // ordinary heads, then fixed heads (slice_of)
 };
 
 // ---------------------------------------------------------------------------
@@ -525,10 +526,10 @@ __global__ __launch_bounds__(KV_THREADS) __attribute__((amdgpu_waves_per_eu(size
     __shared__ __attribute__((aligned(16))) float x1[2 * KV_BM];
     __shared__ float red[4];
     const Tiles<T> sm = {{t0, t1, t2, t3}, {x0, x1}, red};
-    const int n_bh = p.B * p.H;
-    const int kblk = (int)(blockIdx.x / n_bh);  // ascending: longest first
-    const int bh = (int)(blockIdx.x % n_bh);
-    const int h = bh % p.H;
+    const SliceOf sl = slice_of(blockIdx.x, p.B, p.H, 1, [&](int k) { return (int)p.head_order[k]; });
+    const int kblk = sl.level;  // ascending: longest first
+    const int h = sl.h;
+    const int bh = sl.b * p.H + h;
     KvLane L;
     L.tid = threadIdx.x;
     L.w = L.tid >> 6;
@@ -607,10 +608,10 @@ __global__ __launch_bounds__(DQ_THREADS) __attribute__((amdgpu_waves_per_eu(3)))
     __shared__ __attribute__((aligned(16))) T t1[tile_elems<T>()];
     __shared__ __attribute__((aligned(16))) T t2[tile_elems<T>()];
     __shared__ __attribute__((aligned(16))) T t3[tile_elems<T>()];
-    const int n_bh = p.B * p.H;
-    const int qblk = p.n_blocks - 1 - (int)(blockIdx.x / n_bh);  // longest first
-    const int bh = (int)(blockIdx.x % n_bh);
-    const int h = bh % p.H;
+    const SliceOf sl = slice_of(blockIdx.x, p.B, p.H, 1, [&](int k) { return (int)p.head_order[k]; });
+    const int qblk = p.n_blocks - 1 - sl.level;  // longest first
+    const int h = sl.h;
+    const int bh = sl.b * p.H + h;
     const bool fixed = (p.fixed_mask >> h) & 1ull;
     const int N = p.N;
     const size_t base = (size_t)bh * N * HEAD_DIM;

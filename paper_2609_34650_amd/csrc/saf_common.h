@@ -471,6 +471,52 @@ __device__ __forceinline__ float dot8(const f32x8& x, const f32x8& y, float acc)
     return acc;
 }
 
+// ---------------------------------------------------------------------------
+// Workgroup -> (level, batch b, query head h) for grids of n_levels x B x Hs
+// x group workgroups, where a slice (b, s) of the B x Hs slices carries
+// `group` query heads h = s * group + i that share its data (group = 1: one
+// head per slice; grouped-query attention: the query heads of one key/value
+// head).  Workgroups are dealt to the 8 XCDs in turn (workgroup i to XCD
+// i mod 8), so when the slices split evenly over the XCDs:
+//   * every workgroup of a slice runs on one XCD (the slice's K and V come
+//     into one L2 only);
+//   * slices are dealt to the XCDs in order of decreasing work, back and
+//     forth (XCD 0..7, then 7..0, ...): order(k) is the k-th heaviest head
+//     (or key/value head), and the slice of rank m is (b = m % B,
+//     order(m / B)), so every XCD gets an equal share of ordinary and fixed
+//     heads;
+//   * an XCD works through its slices level by level.
+// Otherwise workgroups go level by level with the slices in plain order.
+// Level 0 is dispatched first; kernels map it to their longest blocks.
+// ---------------------------------------------------------------------------
+struct SliceOf {
+    int level, b, h;
+};
+
+template <typename Order>
+__device__ __forceinline__ SliceOf slice_of(unsigned blk, int B, int Hs, int group, Order order) {
+    const int n_slices = B * Hs;
+    SliceOf s;
+    if ((n_slices & 7) == 0) {
+        const int x = (int)(blk & 7);
+        const int j = (int)(blk >> 3);
+        const int per_level = (n_slices >> 3) * group;  // workgroups of one level on one XCD
+        s.level = j / per_level;
+        const int within = j % per_level;
+        const int li = within / group;  // this XCD's li-th slice
+        const int m = li * 8 + ((li & 1) ? 7 - x : x);
+        s.b = m % B;
+        s.h = order(m / B) * group + within % group;
+    } else {
+        const int n_bh = n_slices * group;
+        s.level = (int)(blk / n_bh);
+        const int bh = (int)(blk % n_bh);
+        s.b = bh / (Hs * group);
+        s.h = bh % (Hs * group);
+    }
+    return s;
+}
+
 // Maximum / minimum over the 256 threads of a workgroup (4 wavefronts);
 // `red` is 4 floats of LDS.  Contains barriers: call from uniform code.
 __device__ __forceinline__ float wave_max(float x) {

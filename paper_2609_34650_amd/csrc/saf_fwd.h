@@ -75,6 +75,7 @@ struct FwdArgs {
     uint64_t fixed_mask;
     int B, H, N, ld_prior, n_qblocks;
     float scale_log2;  // log2(e) / sqrt(d)
+    unsigned char head_order[64];  // ordinary heads, then fixed heads (slice_of)
 };
 
 // Per-lane geometry of one workgroup: the wavefront's queries are q0 .. q0+63,
@@ -625,11 +626,11 @@ __global__ __launch_bounds__(FWD_THREADS) __attribute__((amdgpu_waves_per_eu(2))
     __shared__ __attribute__((aligned(16))) T t3[tile_elems<T>()];
     __shared__ float red[4];
     const Tiles<T> sm = {{t0, t1, t2, t3}, {nullptr, nullptr}, red};
-    const int n_bh = p.B * p.H;
-    // Longest blocks first: block index -> query block in descending order.
-    const int qblk = p.n_qblocks - 1 - (int)(blockIdx.x / n_bh);
-    const int bh = (int)(blockIdx.x % n_bh);
-    const int h = bh % p.H;
+    // Longest blocks first: level -> query block in descending order.
+    const SliceOf sl = slice_of(blockIdx.x, p.B, p.H, 1, [&](int k) { return (int)p.head_order[k]; });
+    const int qblk = p.n_qblocks - 1 - sl.level;
+    const int h = sl.h;
+    const int bh = sl.b * p.H + h;
     const bool fixed = (p.fixed_mask >> h) & 1ull;
     FwdLane L;
     L.tid = threadIdx.x;

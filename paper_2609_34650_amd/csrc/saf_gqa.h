@@ -17,10 +17,17 @@
 //   Ordinary head: online softmax (running maximum raised when a sub-block
 //   exceeds it, accumulator and sum rescaled), O^T += V^T P^T on MFMA, LSE =
 //   m + ln l.
-//   Fixed head: P(i, j) = exp(a[j] + r[i - j] - log Z(i)) per entry, with
-//   log Z from the normaliser pre-pass (the layer forward's fixed_lse_kernel)
-//   and the tile's a values and r band staged in LDS; O^T += V^T P^T.  The
-//   rows are already normalised, so no running maximum is needed.
+//   Fixed head, factorised (as in the layer forward): P(i, j) =
+//   ea(j) er(i - j) exp(A + R - log Z(i)) with ea = exp(a - A), er =
+//   exp(r - R) and A, R the maxima of a and r over the block's positions.  V
+//   rows are scaled by ea while they are staged through registers into LDS,
+//   and the weight operand is the Toeplitz band er read from LDS (eight
+//   shifted copies keep every 8-entry read aligned): no exponential per
+//   entry.  log Z comes from the normaliser pre-pass (the layer forward's
+//   fixed_lse_kernel).  A block where some row's diagonal and sink terms both
+//   lie more than FAST_GUARD below A + R takes the exact per-entry program:
+//   P(i, j) = exp(a[j] + r[i - j] - log Z(i)) with the tile's a values and r
+//   band staged in LDS.
 #pragma once
 
 #include "saf_common.h"
@@ -31,6 +38,8 @@ constexpr int GQA_BM = 128;  // queries per workgroup
 constexpr int GQA_BN = 64;   // keys per tile
 constexpr int GQA_THREADS = 256;
 constexpr int GQA_BAND = GQA_BM + GQA_BN - 1;  // offsets met by one tile
+constexpr int GQA_BAND_STRIDE = (GQA_BAND + 7) / 8 * 8 + 8;  // every band copy 16-byte aligned
+static_assert(GQA_BAND <= GQA_THREADS, "one band entry per thread");
 
 struct GqaArgs {
     const void* q;
@@ -43,6 +52,9 @@ struct GqaArgs {
     uint64_t fixed_mask;
     int B, Hq, Hkv, N, ld_prior, n_qblocks;
     float scale_log2;  // log2(e) / sqrt(D)
+    // Key/value heads in order of decreasing work (an ordinary query head
+    // weighs 2, a fixed one 1), for slice_of's XCD assignment.
+    unsigned char kv_order[64];
 };
 
 struct GqaLane {
@@ -132,6 +144,106 @@ __device__ __forceinline__ void gqa_fix_tile(const T* vt, const float* as, const
     }
 }
 
+// Factorised fixed program: one lane's share of a tile in registers (a V row
+// unit per 16 bytes, that row's a, one band entry).
+template <typename T, int D>
+struct GqaFixStage {
+    u32x4 v[tile_units<T, D>()];
+    float a;
+    float rb;
+};
+
+// Band entry u of the tile at n0 holds er at offset (m0 - n0 + 127) - u.
+template <typename T, int D>
+__device__ __forceinline__ void gqa_fix_load(GqaFixStage<T, D>& st, const T* V, const float* arow,
+                                             const float* rrow, int n0, const GqaLane& L) {
+    const int key = n0 + unit_row<T>(L.w, L.lane);
+    const bool ok = key < L.N;
+#pragma unroll
+    for (int k = 0; k < tile_units<T, D>(); ++k) {
+        const u32x4 z = {0u, 0u, 0u, 0u};
+        st.v[k] = ok ? ld_unit(V + (size_t)key * D + unit_col<T>(L.w, L.lane, k)) : z;
+    }
+    st.a = ok ? arow[key] : -INFINITY;
+    const int delta = L.m0 - n0 + (GQA_BM - 1) - L.tid;
+    st.rb = (L.tid < GQA_BAND && delta >= 0 && delta < L.N) ? rrow[delta] : -INFINITY;
+}
+
+template <typename T, int D>
+__device__ __forceinline__ void gqa_fix_store(T* vs, T* band, const GqaFixStage<T, D>& st, const GqaLane& L,
+                                              float a_sh, float r_sh) {
+    const float e = fast_exp2(fmaf(st.a, LOG2E, -a_sh));
+    const int row = unit_row<T>(L.w, L.lane);
+#pragma unroll
+    for (int k = 0; k < tile_units<T, D>(); ++k)
+        st_unit_scaled(vs + toff<T>(row, unit_col<T>(L.w, L.lane, k)), st.v[k], e);
+    if (L.tid < GQA_BAND) {
+        const T b = (T)fast_exp2(fmaf(st.rb, LOG2E, -r_sh));
+#pragma unroll
+        for (int s = 0; s < BAND_COPIES; ++s)
+            if (L.tid >= s) band[s * GQA_BAND_STRIDE + L.tid - s] = b;
+    }
+}
+
+// O^T += (ea V)^T band^T over one tile: four 16-key chunks; the band operand
+// of lane (c, hf) in chunk G is entries u0 .. u0 + 7, u0 = 127 - ql + 16G +
+// 8hf, read from copy u0 % 8 at an aligned address.  Offsets below zero hold
+// 0, which masks the keys after the query.
+template <typename T, int D, bool MASK>
+__device__ __forceinline__ void gqa_band_tile(const T* vs, const T* band, int n0, const GqaLane& L,
+                                              f32x16 (&oacc)[D / 32]) {
+    typedef typename Vec<T>::x8 frag;
+    const int ql = L.q0 - L.m0 + L.c;
+#pragma unroll
+    for (int G = 0; G < 4; ++G) {
+        if (MASK && n0 + 16 * G > L.q0 + 31) continue;  // chunk wholly after this wavefront's queries
+        const int u0 = (GQA_BM - 1) - ql + 16 * G + 8 * L.hf;
+        const int s = u0 & 7;
+        const frag b = ld8<T>(band + s * GQA_BAND_STRIDE + u0 - s);
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db) mma(oacc[db], ld_tile_t<false>(vs, 16 * G, 32 * db), b);
+    }
+}
+
+// The tile schedule of run_slots with register-staged copies issued two
+// slots ahead: slot i computes on buffer i % 2 while the registers of stage
+// (i + 1) % 2 (issued one slot earlier) are written to the other buffer and
+// that stage is reloaded for slot i + 3.  issue(buf, t) loads tile t into
+// stage buf; finish(buf) writes stage buf into LDS buffer buf.
+template <typename TileOf, typename Issue, typename Finish, typename Compute>
+__device__ __forceinline__ void run_slots_ahead2(int P, int total, TileOf tile_of, Issue issue, Finish finish,
+                                                 Compute compute) {
+    auto pre = [&](auto buf, int i) {
+        if (i < total) {
+            const int t = tile_of(i);
+            if (t >= 0) issue(buf, t);
+        }
+    };
+    auto fin = [&](auto buf, int i) {
+        if (i < total && tile_of(i) >= 0) finish(buf);
+    };
+    auto body = [&](auto buf, auto other, int i, auto mask) {
+        if (tile_of(i) >= 0) compute(buf, tile_of(i), mask);
+        fin(other, i + 1);
+        pre(other, i + 3);
+        __syncthreads();
+    };
+    pre(Buf0{}, 0);
+    pre(Buf1{}, 1);
+    fin(Buf0{}, 0);
+    pre(Buf0{}, 2);
+    __syncthreads();
+    for (int i = 0; i < P; i += 2) {
+        body(Buf0{}, Buf1{}, i, std::true_type{});
+        body(Buf1{}, Buf0{}, i + 1, std::true_type{});
+    }
+    for (int i = P; i < total; i += 2) {
+        body(Buf0{}, Buf1{}, i, std::false_type{});
+        if (i + 1 >= total) break;
+        body(Buf1{}, Buf0{}, i + 1, std::false_type{});
+    }
+}
+
 template <typename T, int D>
 __global__ __launch_bounds__(GQA_THREADS) __attribute__((amdgpu_waves_per_eu(2))) void gqa_fwd_kernel(GqaArgs p) {
     __shared__ __attribute__((aligned(16))) T k0s[tile_elems<T, D>()];
@@ -140,12 +252,15 @@ __global__ __launch_bounds__(GQA_THREADS) __attribute__((amdgpu_waves_per_eu(2))
     __shared__ __attribute__((aligned(16))) T v1s[tile_elems<T, D>()];
     __shared__ float ab0[GQA_BN + GQA_BAND + 1];
     __shared__ float ab1[GQA_BN + GQA_BAND + 1];
-    const int n_bh = p.B * p.Hq;
-    const int qblk = p.n_qblocks - 1 - (int)(blockIdx.x / n_bh);  // longest first
-    const int bh = (int)(blockIdx.x % n_bh);
-    const int b = bh / p.Hq;
-    const int h = bh % p.Hq;
-    const int hkv = h / (p.Hq / p.Hkv);
+    __shared__ float red[8];
+    static_assert(BAND_COPIES * GQA_BAND_STRIDE <= tile_elems<T, D>(), "band copies fit in a K tile");
+    // Longest query blocks first; slices = (batch, key/value head).
+    const int group = p.Hq / p.Hkv;
+    const SliceOf sl = slice_of(blockIdx.x, p.B, p.Hkv, group, [&](int k) { return (int)p.kv_order[k]; });
+    const int qblk = p.n_qblocks - 1 - sl.level;
+    const int b = sl.b, h = sl.h;
+    const int bh = b * p.Hq + h;
+    const int hkv = h / group;
     const bool fixed = (p.fixed_mask >> h) & 1ull;
     GqaLane L;
     L.tid = threadIdx.x;
@@ -204,7 +319,39 @@ __global__ __launch_bounds__(GQA_THREADS) __attribute__((amdgpu_waves_per_eu(2))
         const float* arow = p.a + (size_t)h * p.ld_prior;
         const float* rrow = p.r + (size_t)h * p.ld_prior;
         const float lz = qq < N ? p.lse[row_base + qq] : 0.0f;
-        run_slots(
+        const int m1 = min(L.m0 + GQA_BM, N);
+        float am = -INFINITY, rm = -INFINITY;
+        for (int j = L.tid; j < m1; j += GQA_THREADS) {
+            am = fmaxf(am, arow[j]);
+            rm = fmaxf(rm, rrow[j]);
+        }
+        const float A = block_max(am, red);
+        const float R = block_max(rm, red + 4);
+        bool ok = true;
+        if (L.tid < GQA_BM && L.m0 + L.tid < N) {
+            const int i = L.m0 + L.tid;
+            ok = fmaxf(arow[i] + rrow[0], arow[0] + rrow[i]) - A - R >= -FAST_GUARD;
+        }
+        if (__syncthreads_and(ok)) {
+            // K is never read for a fixed head: its tiles hold the band.
+            const T* __restrict__ V = reinterpret_cast<const T*>(p.v) + kvbase;
+            const float a_sh = A * LOG2E, r_sh = R * LOG2E;
+            GqaFixStage<T, D> st0, st1;
+            run_slots_ahead2(
+                P, P + n_full, tile_of,
+                [&](auto buf, int t) {
+                    gqa_fix_load<T, D>(decltype(buf)::value ? st1 : st0, V, arow, rrow, t * GQA_BN, L);
+                },
+                [&](auto buf) {
+                    constexpr int B_ = decltype(buf)::value;
+                    gqa_fix_store<T, D>(B_ ? v1s : v0s, B_ ? k1s : k0s, B_ ? st1 : st0, L, a_sh, r_sh);
+                },
+                [&](auto buf, int t, auto mask) {
+                    constexpr int B_ = decltype(buf)::value;
+                    gqa_band_tile<T, D, decltype(mask)::value>(B_ ? v1s : v0s, B_ ? k1s : k0s, t * GQA_BN, L, oacc);
+                });
+            row_scale = fast_exp2((A + R - lz) * LOG2E);
+        } else run_slots(
             P, P + n_full, tile_of,
             [&](auto buf, int t) {
                 constexpr int B_ = decltype(buf)::value;

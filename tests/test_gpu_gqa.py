@@ -99,3 +99,23 @@ def test_gqa_prefill_shape_sampled():
                                   inp["a"][h] if fx else None, inp["r"][h] if fx else None, rows=rows)
         _check("bf16", O[0, h, rows], o)
         _check("bf16", LSE[0, h, rows], lse)
+
+
+@pytest.mark.parametrize("dtype,d", [("f32", 96), ("bf16", 128)])
+def test_gqa_fixed_exact_fallback(dtype, d):
+    """a is 60 nats lower on the first half of the keys: the blocks whose rows
+    lie in that half but whose maxima come from the second half must take the
+    exact per-entry program (the factorised one would underflow); the rest
+    take the factorised program."""
+    from oracle import saf_oracle as orc
+    announce(f"gqa fixed exact fallback {dtype} d={d}")
+    N = 600
+    inp = _inputs(dtype, 1, 4, 2, N, d, [0, 3], stream_id=54)
+    a = inp["a"].copy()
+    a[0, : N // 2] -= 60.0
+    a[3, : N // 2] -= 60.0
+    inp["a"] = a.astype(np.float32)
+    O, LSE = _run_gpu(inp, dtype)
+    Oo, LSEo = orc.layer_forward_gqa(inp["Q"], inp["K"], inp["V"], inp["is_fixed"], inp["a"], inp["r"])
+    _check(dtype, O, Oo)
+    _check(dtype, LSE, LSEo)
