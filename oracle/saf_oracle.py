@@ -307,6 +307,34 @@ def layer_forward_gqa(Q, K, V, is_fixed, a=None, r=None, row_block: int = 512,
     return O, LSE
 
 
+def layer_backward_gqa(Q, K, V, dO, is_fixed, a=None, r=None, row_block: int = 512):
+    """Gradients of ``sum(O * dO)`` for the grouped-query layer: ``dQ``
+    ``[B, Hq, N, d]``; ``dK``, ``dV`` ``[B, Hkv, N, d]``, each the sum over the
+    query heads of its group of the per-head gradients (a shared key/value
+    head receives the gradient of every query head that reads it).  A fixed
+    query head adds only to ``dV`` and gets exact zeros in ``dQ``."""
+    V = np.asarray(V)
+    B, Hkv, N, d = V.shape
+    is_fixed = np.asarray(is_fixed).astype(bool).reshape(-1)
+    Hq = is_fixed.shape[0]
+    if Hq % Hkv:
+        raise ValueError("query heads must be a multiple of key/value heads")
+    group = Hq // Hkv
+    dQ = np.zeros((B, Hq, N, d))
+    dK = np.zeros((B, Hkv, N, d))
+    dV = np.zeros((B, Hkv, N, d))
+    for b in range(B):
+        for h in range(Hq):
+            g = h // group
+            fx = bool(is_fixed[h])
+            dq, dk, dv = head_backward(None if fx else Q[b, h], None if fx else K[b, g], V[b, g], dO[b, h], fx,
+                                       a[h] if fx else None, r[h] if fx else None, row_block)
+            dQ[b, h] = dq
+            dK[b, g] += dk
+            dV[b, g] += dv
+    return dQ, dK, dV
+
+
 # ---------------------------------------------------------------------------
 # Gradients of trainable patterns
 # ---------------------------------------------------------------------------

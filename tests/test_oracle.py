@@ -347,6 +347,45 @@ def test_gqa_forward_equals_expanded_heads():
     np.testing.assert_allclose(O[:, 0:1], ref.numpy(), rtol=1e-12, atol=1e-13)
 
 
+def test_gqa_backward_matches_autograd_of_expanded_heads():
+    """Grouped-query gradients against torch autograd (float64) through the
+    forward with each key/value head repeated for its group: the repeat's
+    backward sums the group, which is what dK and dV must hold.  Fixed heads
+    read V only (pattern from Eq. compact-prior), so their Q rows get no
+    gradient; with one query head per group the result is the layer
+    backward."""
+    torch = pytest.importorskip("torch")
+    B, Hq, Hkv, N, d = 2, 6, 2, 9, 96
+    Q, dO = _rand(B, Hq, N, d), _rand(B, Hq, N, d)
+    K, V = _rand(B, Hkv, N, d), _rand(B, Hkv, N, d)
+    a, r = _rand(Hq, N), _rand(Hq, N)
+    is_fixed = np.array([1, 0, 0, 1, 1, 0], dtype=np.uint8)
+    dQ, dK, dV = orc.layer_backward_gqa(Q, K, V, dO, is_fixed, a, r)
+    tq, tk, tv = (torch.tensor(x, requires_grad=True) for x in (Q, K, V))
+    ke = tk.repeat_interleave(Hq // Hkv, dim=1)
+    ve = tv.repeat_interleave(Hq // Hkv, dim=1)
+    i = torch.arange(N)
+    off = i[:, None] - i[None, :]
+    outs = []
+    for h in range(Hq):
+        if is_fixed[h]:
+            L = (torch.tensor(a[h])[None, :] + torch.tensor(r[h])[off.clamp(min=0)]).masked_fill(off < 0, -np.inf)
+            outs.append(torch.softmax(L, dim=-1) @ ve[:, h])
+        else:
+            S = (tq[:, h] @ ke[:, h].transpose(-1, -2)) / np.sqrt(d)
+            outs.append(torch.softmax(S.masked_fill(off < 0, -np.inf), dim=-1) @ ve[:, h])
+    (torch.stack(outs, dim=1) * torch.tensor(dO)).sum().backward()
+    np.testing.assert_allclose(dQ, tq.grad.numpy(), rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(dK, tk.grad.numpy(), rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(dV, tv.grad.numpy(), rtol=1e-10, atol=1e-12)
+    assert not dQ[:, is_fixed.astype(bool)].any()
+    # One query head per group: the layer backward.
+    G1 = orc.layer_backward_gqa(Q[:, :2], K, V, dO[:, :2], is_fixed[:2], a[:2], r[:2])
+    G2 = orc.layer_backward(Q[:, :2], K, V, dO[:, :2], is_fixed[:2], a[:2], r[:2])
+    for x, y in zip(G1, G2):
+        np.testing.assert_array_equal(x, y)
+
+
 def test_fixed_heads_never_read_queries_or_keys():
     B, H, N, d = 2, 3, 16, 4
     Q, K, V, dO = (_rand(B, H, N, d) for _ in range(4))
