@@ -108,7 +108,7 @@ saf_status_t saf_hybrid_attn_fwd(saf_dtype_t dt,
  * N * d * sizeof(dt) < 2^31 bytes.  With Hkv == Hq and d == 64 it computes
  * what saf_hybrid_attn_fwd computes (a separate, simpler kernel: one 32-query
  * block per wavefront, a normaliser launch first when a head is fixed).
- * There is no backward for this layout in this build.
+ * Its backward is saf_hybrid_attn_bwd_gqa.
  */
 saf_status_t saf_hybrid_attn_fwd_gqa(saf_dtype_t dt,
                                      const void* Q, const void* K, const void* V,
@@ -116,6 +116,41 @@ saf_status_t saf_hybrid_attn_fwd_gqa(saf_dtype_t dt,
                                      const float* a, const float* r, int ld_prior,
                                      int B, int Hq, int Hkv, int N, int d,
                                      void* O, float* LSE,
+                                     hipStream_t stream);
+
+/* Bytes of device workspace saf_hybrid_attn_bwd_gqa needs (a multiple of
+ * 256).  Returns 0 for an empty or invalid problem. */
+size_t saf_hybrid_attn_bwd_gqa_workspace_bytes(saf_dtype_t dt, int B, int Hq, int Hkv, int N, int d);
+
+/*
+ * Backward of the grouped-query hybrid layer (head dimension 64, 96 or 128)
+ * for the loss sum(O * dO).  A shared key/value head receives the sum over
+ * the query heads of its group: ordinary query heads add to dK and dV as in
+ * saf_hybrid_attn_bwd, fixed query heads add P^T dO to dV only and get exact
+ * zeros in dQ (the grouped-query path keeps every shared key/value head and
+ * maps each ordinary query head to its group, Appendix "Mixed-head execution
+ * and numerical checks").  Three launches: row pre-pass, key-block pass (one
+ * workgroup per batch element, key/value head and 128 keys, looping over the
+ * group), query-block pass.
+ *   Q, O, dO : [B, Hq, N, d] `dt` (O and LSE as written by
+ *              saf_hybrid_attn_fwd_gqa);  LSE : [B, Hq, N] float32;
+ *   K, V     : [B, Hkv, N, d] `dt`;
+ *   dQ       : [B, Hq, N, d] `dt`, written (zeros for fixed heads);
+ *   dK, dV   : [B, Hkv, N, d] `dt`, written (dK is zero for a key/value head
+ *              whose query heads are all fixed);
+ *   workspace: DEVICE, >= saf_hybrid_attn_bwd_gqa_workspace_bytes(), owned
+ *              by the caller, 256-byte aligned; contents on entry ignored.
+ * Limits and errors as saf_hybrid_attn_fwd_gqa; SAF_ERR_SHAPE also when the
+ * workspace is too small.
+ */
+saf_status_t saf_hybrid_attn_bwd_gqa(saf_dtype_t dt,
+                                     const void* Q, const void* K, const void* V,
+                                     const void* O, const void* dO, const float* LSE,
+                                     const uint8_t* head_is_fixed,
+                                     const float* a, const float* r, int ld_prior,
+                                     int B, int Hq, int Hkv, int N, int d,
+                                     void* dQ, void* dK, void* dV,
+                                     void* workspace, size_t workspace_bytes,
                                      hipStream_t stream);
 
 /* Bytes of device workspace saf_hybrid_attn_bwd needs (a multiple of 256).

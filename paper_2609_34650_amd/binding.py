@@ -40,6 +40,8 @@ STATUS = {
 EXPORTS = (
     "saf_hybrid_attn_fwd",
     "saf_hybrid_attn_fwd_gqa",
+    "saf_hybrid_attn_bwd_gqa_workspace_bytes",
+    "saf_hybrid_attn_bwd_gqa",
     "saf_hybrid_attn_bwd_workspace_bytes",
     "saf_hybrid_attn_bwd",
     "saf_hybrid_attn_bwd_stage",
@@ -84,6 +86,11 @@ def load() -> ctypes.CDLL:
     lib.saf_hybrid_attn_fwd.argtypes = [i, vp, vp, vp, u8p, vp, vp, i, i, i, i, i, vp, vp, vp]
     lib.saf_hybrid_attn_fwd_gqa.restype = ctypes.c_int
     lib.saf_hybrid_attn_fwd_gqa.argtypes = [i, vp, vp, vp, u8p, vp, vp, i, i, i, i, i, i, vp, vp, vp]
+    lib.saf_hybrid_attn_bwd_gqa_workspace_bytes.restype = ctypes.c_size_t
+    lib.saf_hybrid_attn_bwd_gqa_workspace_bytes.argtypes = [i, i, i, i, i, i]
+    lib.saf_hybrid_attn_bwd_gqa.restype = ctypes.c_int
+    lib.saf_hybrid_attn_bwd_gqa.argtypes = [i, vp, vp, vp, vp, vp, vp, u8p, vp, vp, i, i, i, i, i, i, vp, vp, vp,
+                                            vp, ctypes.c_size_t, vp]
     lib.saf_hybrid_attn_bwd_workspace_bytes.restype = ctypes.c_size_t
     lib.saf_hybrid_attn_bwd_workspace_bytes.argtypes = [i, i, i, i, i]
     bwd_args = [i, vp, vp, vp, vp, vp, vp, u8p, vp, vp, i, i, i, i, i, vp, vp, vp, vp, ctypes.c_size_t, vp]
@@ -247,6 +254,46 @@ def saf_hybrid_attn_fwd_gqa(Q: Optional[torch.Tensor], K: Optional[torch.Tensor]
                                        B, Hq, Hkv, N, d, _ptr(O), _ptr(LSE), _stream(dev))
     _raise(code, "saf_hybrid_attn_fwd_gqa")
     return O, LSE
+
+
+def saf_hybrid_attn_bwd_gqa(Q, K, V, O, dO, LSE, head_is_fixed, a=None, r=None, dQ=None, dK=None, dV=None,
+                            workspace: Optional[torch.Tensor] = None):
+    """Grouped-query backward for ``sum(O * dO)``: ``Q``, ``O``, ``dO``
+    ``[B, Hq, N, d]``, ``K``, ``V`` ``[B, Hkv, N, d]``.  Returns ``(dQ, dK,
+    dV)`` with dK and dV summed over each group."""
+    lib = load()
+    B, Hkv, N, d = V.shape
+    dev = V.device
+    if isinstance(head_is_fixed, torch.Tensor):
+        head_is_fixed = head_is_fixed.detach().cpu().numpy()
+    flags = np.ascontiguousarray(np.asarray(head_is_fixed, dtype=np.uint8).reshape(-1))
+    Hq = flags.shape[0]
+    qshape = (B, Hq, N, d)
+    _check_act("V", V, V.shape, V.dtype, dev)
+    _check_act("K", K, V.shape, V.dtype, dev, allow_none=True)
+    _check_act("Q", Q, qshape, V.dtype, dev, allow_none=True)
+    for name, t in (("O", O), ("dO", dO)):
+        _check_act(name, t, qshape, V.dtype, dev)
+    _check_act("LSE", LSE, (B, Hq, N), torch.float32, dev)
+    dQ = torch.empty(qshape, dtype=V.dtype, device=dev) if dQ is None else dQ
+    dK = torch.empty_like(V) if dK is None else dK
+    dV = torch.empty_like(V) if dV is None else dV
+    _check_act("dQ", dQ, qshape, V.dtype, dev)
+    _check_act("dK", dK, V.shape, V.dtype, dev)
+    _check_act("dV", dV, V.shape, V.dtype, dev)
+    code = SAF_DTYPE_BF16 if V.dtype == torch.bfloat16 else SAF_DTYPE_F32
+    nbytes = int(lib.saf_hybrid_attn_bwd_gqa_workspace_bytes(code, B, Hq, Hkv, N, d))
+    if workspace is None:
+        workspace = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=dev)
+    pa, lda = _prior("a", a, Hq, N, dev)
+    pr, ldr = _prior("r", r, Hq, N, dev)
+    if pa is not None and pr is not None and lda != ldr:
+        raise ValueError("a and r must share one row stride")
+    _raise(lib.saf_hybrid_attn_bwd_gqa(_dtype_code(V), _ptr(Q), _ptr(K), _ptr(V), _ptr(O), _ptr(dO), _ptr(LSE),
+                                       flags.ctypes.data, pa, pr, lda, B, Hq, Hkv, N, d, _ptr(dQ), _ptr(dK),
+                                       _ptr(dV), workspace.data_ptr(), workspace.numel() * workspace.element_size(),
+                                       _stream(dev)), "saf_hybrid_attn_bwd_gqa")
+    return dQ, dK, dV
 
 
 def saf_hybrid_attn_bwd_workspace_bytes(dtype: torch.dtype, B: int, H: int, N: int, d: int) -> int:

@@ -14,6 +14,7 @@
 #include "saf_fit_kernels.h"
 #include "saf_fwd.h"
 #include "saf_gqa.h"
+#include "saf_gqa_bwd.h"
 #include "saf_pattern.h"
 
 #define SAF_EXPORT extern "C" __attribute__((visibility("default")))
@@ -273,10 +274,17 @@ void launch_gqa(const saf::GqaArgs& args, hipStream_t stream) {
 
 }  // namespace
 
-SAF_EXPORT saf_status_t saf_hybrid_attn_fwd_gqa(saf_dtype_t dt, const void* Q, const void* K, const void* V,
-                                                const uint8_t* head_is_fixed, const float* a, const float* r,
-                                                int ld_prior, int B, int Hq, int Hkv, int N, int d, void* O,
-                                                float* LSE, hipStream_t stream) {
+namespace {
+
+struct GqaProblem {
+    uint64_t mask = 0;
+    bool any_ordinary = false;
+    bool empty = false;
+};
+
+// Shape, flag and prior checks shared by the grouped-query entry points.
+saf_status_t check_gqa(saf_dtype_t dt, const uint8_t* head_is_fixed, const float* a, const float* r, int ld_prior,
+                       int B, int Hq, int Hkv, int N, int d, GqaProblem* pr) {
     if (dt != SAF_DTYPE_F32 && dt != SAF_DTYPE_BF16) return SAF_ERR_UNSUPPORTED;
     if (B < 0 || Hq < 0 || Hkv < 0 || N < 0 || d < 0) return SAF_ERR_SHAPE;
     if (d != 64 && d != 96 && d != 128) return SAF_ERR_UNSUPPORTED;
@@ -284,20 +292,67 @@ SAF_EXPORT saf_status_t saf_hybrid_attn_fwd_gqa(saf_dtype_t dt, const void* Q, c
     // One (batch, head) slice stays below 2^31 bytes for 32-bit buffer offsets.
     if ((int64_t)N * d * (dt == SAF_DTYPE_F32 ? 4 : 2) > INT32_MAX) return SAF_ERR_SHAPE;
     if ((int64_t)B * Hq * ((N + saf::GQA_BM - 1) / saf::GQA_BM) > INT32_MAX) return SAF_ERR_SHAPE;
-    if (B == 0 || Hq == 0 || N == 0) return SAF_OK;
+    if (B == 0 || Hq == 0 || N == 0) {
+        pr->empty = true;
+        return SAF_OK;
+    }
     if (Hkv == 0 || Hq % Hkv != 0) return SAF_ERR_SHAPE;
     if (head_is_fixed == nullptr) return SAF_ERR_NULL;
-    uint64_t mask = 0;
-    bool any_ordinary = false;
     for (int h = 0; h < Hq; ++h) {
         if (head_is_fixed[h] > 1) return SAF_ERR_FLAG;
-        if (head_is_fixed[h]) mask |= 1ull << h;
-        else any_ordinary = true;
+        if (head_is_fixed[h]) pr->mask |= 1ull << h;
+        else pr->any_ordinary = true;
     }
-    if (mask && (a == nullptr || r == nullptr)) return SAF_ERR_MISSING_PRIOR;
-    if (mask && ld_prior < N) return SAF_ERR_SHAPE;
+    if (pr->mask && (a == nullptr || r == nullptr)) return SAF_ERR_MISSING_PRIOR;
+    if (pr->mask && ld_prior < N) return SAF_ERR_SHAPE;
+    return SAF_OK;
+}
+
+// Key/value heads by decreasing work (an ordinary query head weighs 2, a
+// fixed one 1) for slice_of.
+void fill_kv_order(unsigned char* order, uint64_t mask, int Hq, int Hkv) {
+    const int group = Hq / Hkv;
+    int work[64];
+    for (int g = 0; g < Hkv; ++g) {
+        work[g] = 0;
+        for (int i = 0; i < group; ++i) work[g] += ((mask >> (g * group + i)) & 1ull) ? 1 : 2;
+        order[g] = (unsigned char)g;
+    }
+    std::stable_sort(order, order + Hkv, [&](unsigned char x, unsigned char y) { return work[x] > work[y]; });
+}
+
+size_t gqa_workspace_bytes(int B, int Hq, int N) {
+    return ((size_t)B * Hq * N * sizeof(float) + 255) & ~(size_t)255;
+}
+
+template <typename T, int D>
+void launch_gqa_bwd(const saf::GqaBwdArgs& base, bool any_ordinary, hipStream_t stream) {
+    saf::GqaBwdArgs args = base;
+    if (any_ordinary) {
+        const size_t rows = (size_t)args.B * args.Hq * args.N;
+        const unsigned grid = (unsigned)((rows + saf::GPRE_ROWS - 1) / saf::GPRE_ROWS);
+        hipLaunchKernelGGL((saf::gqa_bwd_pre_kernel<T, D>), dim3(grid), dim3(saf::GPRE_THREADS), 0, stream, args);
+    }
+    args.n_blocks = (args.N + saf::GKV_BN - 1) / saf::GKV_BN;
+    hipLaunchKernelGGL((saf::gqa_bwd_kv_kernel<T, D>), dim3((unsigned)((size_t)args.n_blocks * args.B * args.Hkv)),
+                       dim3(saf::GKV_THREADS), 0, stream, args);
+    args.n_blocks = (args.N + saf::GDQ_BM - 1) / saf::GDQ_BM;
+    hipLaunchKernelGGL((saf::gqa_bwd_dq_kernel<T, D>), dim3((unsigned)((size_t)args.n_blocks * args.B * args.Hq)),
+                       dim3(saf::GDQ_THREADS), 0, stream, args);
+}
+
+}  // namespace
+
+SAF_EXPORT saf_status_t saf_hybrid_attn_fwd_gqa(saf_dtype_t dt, const void* Q, const void* K, const void* V,
+                                                const uint8_t* head_is_fixed, const float* a, const float* r,
+                                                int ld_prior, int B, int Hq, int Hkv, int N, int d, void* O,
+                                                float* LSE, hipStream_t stream) {
+    GqaProblem pr;
+    saf_status_t st = check_gqa(dt, head_is_fixed, a, r, ld_prior, B, Hq, Hkv, N, d, &pr);
+    if (st != SAF_OK || pr.empty) return st;
+    const uint64_t mask = pr.mask;
     if (V == nullptr || O == nullptr || LSE == nullptr) return SAF_ERR_NULL;
-    if (any_ordinary && (Q == nullptr || K == nullptr)) return SAF_ERR_NULL;
+    if (pr.any_ordinary && (Q == nullptr || K == nullptr)) return SAF_ERR_NULL;
     if (!aligned16(V) || !aligned16(O) || !aligned16(LSE) || (Q && !aligned16(Q)) || (K && !aligned16(K)))
         return SAF_ERR_ALIGNMENT;
     if (mask) {
@@ -333,21 +388,69 @@ SAF_EXPORT saf_status_t saf_hybrid_attn_fwd_gqa(saf_dtype_t dt, const void* Q, c
     args.ld_prior = ld_prior;
     args.n_qblocks = (N + saf::GQA_BM - 1) / saf::GQA_BM;
     args.scale_log2 = saf::LOG2E / sqrtf((float)d);
-    {
-        const int group = Hq / Hkv;
-        int work[64];
-        for (int g = 0; g < Hkv; ++g) {
-            work[g] = 0;
-            for (int i = 0; i < group; ++i) work[g] += ((mask >> (g * group + i)) & 1ull) ? 1 : 2;
-            args.kv_order[g] = (unsigned char)g;
-        }
-        std::stable_sort(args.kv_order, args.kv_order + Hkv,
-                         [&](unsigned char x, unsigned char y) { return work[x] > work[y]; });
-    }
+    fill_kv_order(args.kv_order, mask, Hq, Hkv);
     const bool bf = dt == SAF_DTYPE_BF16;
     if (d == 64) bf ? launch_gqa<saf::bf16, 64>(args, stream) : launch_gqa<float, 64>(args, stream);
     else if (d == 96) bf ? launch_gqa<saf::bf16, 96>(args, stream) : launch_gqa<float, 96>(args, stream);
     else bf ? launch_gqa<saf::bf16, 128>(args, stream) : launch_gqa<float, 128>(args, stream);
+    return launched();
+}
+
+SAF_EXPORT size_t saf_hybrid_attn_bwd_gqa_workspace_bytes(saf_dtype_t dt, int B, int Hq, int Hkv, int N, int d) {
+    GqaProblem pr;
+    uint8_t none[64] = {0};
+    if (check_gqa(dt, none, nullptr, nullptr, N, B, Hq, Hkv, N, d, &pr) != SAF_OK || pr.empty) return 0;
+    return gqa_workspace_bytes(B, Hq, N);
+}
+
+SAF_EXPORT saf_status_t saf_hybrid_attn_bwd_gqa(saf_dtype_t dt, const void* Q, const void* K, const void* V,
+                                                const void* O, const void* dO, const float* LSE,
+                                                const uint8_t* head_is_fixed, const float* a, const float* r,
+                                                int ld_prior, int B, int Hq, int Hkv, int N, int d, void* dQ,
+                                                void* dK, void* dV, void* workspace, size_t workspace_bytes_given,
+                                                hipStream_t stream) {
+    GqaProblem pr;
+    saf_status_t st = check_gqa(dt, head_is_fixed, a, r, ld_prior, B, Hq, Hkv, N, d, &pr);
+    if (st != SAF_OK || pr.empty) return st;
+    if (V == nullptr || O == nullptr || dO == nullptr || LSE == nullptr || dQ == nullptr || dK == nullptr ||
+        dV == nullptr || workspace == nullptr)
+        return SAF_ERR_NULL;
+    if (pr.any_ordinary && (Q == nullptr || K == nullptr)) return SAF_ERR_NULL;
+    if (!aligned16(V) || !aligned16(O) || !aligned16(dO) || !aligned16(dQ) || !aligned16(dK) || !aligned16(dV) ||
+        !aligned16(LSE) || (Q && !aligned16(Q)) || (K && !aligned16(K)) ||
+        (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
+        return SAF_ERR_ALIGNMENT;
+    if (workspace_bytes_given < gqa_workspace_bytes(B, Hq, N)) return SAF_ERR_SHAPE;
+    saf::GqaBwdArgs args;
+    args.q = Q;
+    args.k = K;
+    args.v = V;
+    args.o = O;
+    args.dO = dO;
+    args.lse = LSE;
+    args.a = a;
+    args.r = r;
+    args.dq = dQ;
+    args.dk = dK;
+    args.dv = dV;
+    args.dsum = reinterpret_cast<float*>(workspace);
+    args.fixed_mask = pr.mask;
+    args.B = B;
+    args.Hq = Hq;
+    args.Hkv = Hkv;
+    args.N = N;
+    args.ld_prior = ld_prior;
+    args.n_blocks = 0;
+    args.scale = 1.0f / sqrtf((float)d);
+    args.scale_log2 = saf::LOG2E / sqrtf((float)d);
+    fill_kv_order(args.kv_order, pr.mask, Hq, Hkv);
+    const bool bf = dt == SAF_DTYPE_BF16;
+    if (d == 64) bf ? launch_gqa_bwd<saf::bf16, 64>(args, pr.any_ordinary, stream)
+                    : launch_gqa_bwd<float, 64>(args, pr.any_ordinary, stream);
+    else if (d == 96) bf ? launch_gqa_bwd<saf::bf16, 96>(args, pr.any_ordinary, stream)
+                         : launch_gqa_bwd<float, 96>(args, pr.any_ordinary, stream);
+    else bf ? launch_gqa_bwd<saf::bf16, 128>(args, pr.any_ordinary, stream)
+            : launch_gqa_bwd<float, 128>(args, pr.any_ordinary, stream);
     return launched();
 }
 

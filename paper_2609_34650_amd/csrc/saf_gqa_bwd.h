@@ -1,0 +1,432 @@
+// Backward of the grouped-query hybrid layer for head dimensions 64, 96 and
+// 128, for the loss sum(O * dO) (the training side of the layouts the
+// grouped-query forward serves: Section "Pretrained grouped-query models";
+// Appendix "Mixed-head execution and numerical checks", whose grouped-query
+// path keeps every shared key/value head and maps each ordinary query head to
+// its group).
+//
+// Q, O, dO, dQ: [B, Hq, N, D]; K, V, dK, dV: [B, Hkv, N, D]; query head h
+// reads key/value head h / (Hq / Hkv).  A shared head's dK and dV are sums
+// over the query heads of its group: ordinary heads add dS^T Q / sqrt(D) to
+// dK and P^T dO to dV (the FlashAttention-2 recurrences of the layer's own
+// backward); fixed heads add P^T dO to dV only, with P(i, j) = exp(a[j] +
+// r[i - j] - log Z(i)) evaluated per entry; they get exact zeros in dQ.
+//
+// Three launches: the row pre-pass D_i = sum_c dO * O for ordinary query
+// heads; the key-block pass (workgroup = (b, key/value head, 128 keys), one
+// 32-key block per wavefront, looping over the group's query heads with dK
+// and dV accumulated in registers); the query-block pass (workgroup = (b,
+// query head, 128 queries)).
+#pragma once
+
+#include "saf_common.h"
+
+namespace saf {
+
+struct GqaBwdArgs {
+    const void* q;
+    const void* k;
+    const void* v;
+    const void* o;
+    const void* dO;
+    const float* lse;
+    const float* a;
+    const float* r;
+    void* dq;
+    void* dk;
+    void* dv;
+    float* dsum;  // workspace: D, [B, Hq, N]
+    uint64_t fixed_mask;
+    int B, Hq, Hkv, N, ld_prior, n_blocks;
+    float scale;       // 1 / sqrt(D)
+    float scale_log2;  // log2(e) / sqrt(D)
+    unsigned char kv_order[64];  // key/value heads by decreasing work (slice_of)
+};
+
+// ---------------------------------------------------------------------------
+// Row pre-pass: eight lanes per row, D / 8 columns each.
+// ---------------------------------------------------------------------------
+constexpr int GPRE_THREADS = 256;
+constexpr int GPRE_ROWS = GPRE_THREADS / 8;
+
+template <typename T, int D>
+__global__ __launch_bounds__(GPRE_THREADS) void gqa_bwd_pre_kernel(GqaBwdArgs p) {
+    const size_t total = (size_t)p.B * p.Hq * p.N;
+    const size_t row = (size_t)blockIdx.x * GPRE_ROWS + (threadIdx.x >> 3);
+    const int part = threadIdx.x & 7;
+    float acc = 0.0f;
+    bool live = row < total;
+    if (live) {
+        const int h = (int)((row / p.N) % p.Hq);
+        live = !((p.fixed_mask >> h) & 1ull);
+    }
+    if (live) {
+        const T* o = reinterpret_cast<const T*>(p.o) + row * D + part * (D / 8);
+        const T* g = reinterpret_cast<const T*>(p.dO) + row * D + part * (D / 8);
+#pragma unroll
+        for (int c = 0; c < D / 8; c += 4) {
+            const typename Vec<T>::x4 ov = *reinterpret_cast<const typename Vec<T>::x4*>(o + c);
+            const typename Vec<T>::x4 gv = *reinterpret_cast<const typename Vec<T>::x4*>(g + c);
+#pragma unroll
+            for (int t = 0; t < 4; ++t) acc += (float)ov[t] * (float)gv[t];
+        }
+    }
+    acc += __shfl_xor(acc, 1);
+    acc += __shfl_xor(acc, 2);
+    acc += __shfl_xor(acc, 4);
+    if (row < total && part == 0) p.dsum[row] = acc;
+}
+
+// ---------------------------------------------------------------------------
+// Key-block pass.  A lane holds one key (l % 32) of its wavefront's 32 and,
+// for ordinary heads, forms S = Q K^T with queries in accumulator rows, so P
+// and dS feed the B operands of dV^T += dO^T P and dK^T += Q^T dS directly.
+// K and V of the wavefront's keys stay in registers; Q and dO tiles of 64
+// queries come by buffer loads straight to LDS, double-buffered.
+// ---------------------------------------------------------------------------
+constexpr int GKV_BN = 128;  // keys per workgroup
+constexpr int GKV_BM = TILE_ROWS;  // queries per tile
+constexpr int GKV_THREADS = 256;
+constexpr int GKV_MASK_TILES = GKV_BN / GKV_BM;
+constexpr int GKV_BAND = GKV_BM + GKV_BN - 1;  // offsets met by one tile
+
+struct GkvLane {
+    int tid, w, lane, c, hf, n0, kw, N;
+};
+
+template <typename T, int D, bool MASK>
+__device__ __forceinline__ void gkv_tile(const T* qt, const T* gt, const float* rows, int mq, const GkvLane& L,
+                                         const typename Vec<T>::x8 (&kf)[D / 16],
+                                         const typename Vec<T>::x8 (&vf)[D / 16], f32x16 (&dv)[D / 32],
+                                         f32x16 (&dk)[D / 32], float scale_log2) {
+    typedef typename Vec<T>::x8 frag;
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+        const int qs = mq + 32 * qb;
+        if (MASK && (qs + 31 < L.kw || qs >= L.N)) continue;  // no query of this half sees these keys
+        f32x16 s, dp;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) s[v] = 0.0f;
+#pragma unroll
+        for (int dc = 0; dc < D / 16; ++dc) mma(s, ld_row<T>(qt, 32 * qb + L.c, 16 * dc + 8 * L.hf), kf[dc]);
+        // dP - D in one go: the accumulator starts at -D of its rows.
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            const f32x4 nd4 = *reinterpret_cast<const f32x4*>(rows + GKV_BM + 32 * qb + 8 * g + 4 * L.hf);
+#pragma unroll
+            for (int u = 0; u < 4; ++u) dp[4 * g + u] = nd4[u];
+        }
+#pragma unroll
+        for (int dc = 0; dc < D / 16; ++dc) mma(dp, ld_row<T>(gt, 32 * qb + L.c, 16 * dc + 8 * L.hf), vf[dc]);
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            const f32x4 l4 = *reinterpret_cast<const f32x4*>(rows + 32 * qb + 8 * g + 4 * L.hf);
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int v = 4 * g + u;
+                float pv = fast_exp2(fmaf(s[v], scale_log2, -l4[u]));
+                if (MASK && qs + 8 * g + 4 * L.hf + u < L.kw + L.c) pv = 0.0f;
+                s[v] = pv;
+                dp[v] = pv * dp[v];
+            }
+        }
+#pragma unroll
+        for (int kc = 0; kc < 2; ++kc) {
+            const frag pb = to_operand<T>(s, 8 * kc);
+            const frag sb = to_operand<T>(dp, 8 * kc);
+#pragma unroll
+            for (int db = 0; db < D / 32; ++db) {
+                mma(dv[db], ld_tile_t<true>(gt, 32 * qb + 16 * kc, 32 * db), pb);
+                mma(dk[db], ld_tile_t<true>(qt, 32 * qb + 16 * kc, 32 * db), sb);
+            }
+        }
+    }
+}
+
+// Fixed query head: dV^T += dO^T P with P evaluated per entry.  The dO tile
+// is staged through registers into gt; lse2 holds log Z * log2(e) of the
+// tile's rows and rb the r values of the offsets it meets.
+template <typename T, int D>
+__device__ __forceinline__ void gkv_fixed_head(T* gt, float* lse2, float* rb, const T* dO, const float* LSE,
+                                               const float* rrow, float a_key, const GkvLane& L,
+                                               f32x16 (&dv)[D / 32]) {
+    typedef typename Vec<T>::x8 frag;
+    const int N = L.N;
+    const int row = unit_row<T>(L.w, L.lane);
+    const int kl = L.kw - L.n0 + L.c;  // key within the block
+    for (int mq = L.n0; mq < N; mq += GKV_BM) {
+        __syncthreads();
+#pragma unroll
+        for (int k = 0; k < tile_units<T, D>(); ++k) {
+            const int col = unit_col<T>(L.w, L.lane, k);
+            const u32x4 z = {0u, 0u, 0u, 0u};
+            const u32x4 x = mq + row < N ? ld_unit(dO + (size_t)(mq + row) * D + col) : z;
+            *reinterpret_cast<u32x4*>(gt + toff<T>(row, col)) = x;
+        }
+        if (L.tid < GKV_BM) lse2[L.tid] = mq + L.tid < N ? LSE[mq + L.tid] * LOG2E : INFINITY;
+        if (L.tid < GKV_BAND) {
+            const int delta = mq - L.n0 - (GKV_BN - 1) + L.tid;
+            rb[L.tid] = (delta >= 0 && delta < N) ? rrow[delta] : -INFINITY;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb) {
+            const int qs = mq + 32 * qb;
+            if (qs + 31 < L.kw || qs >= N) continue;
+            f32x16 pm;
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int ql = 32 * qb + 8 * (v >> 2) + 4 * L.hf + (v & 3);
+                pm[v] = fast_exp2(fmaf(a_key + rb[ql - kl + (GKV_BN - 1)], LOG2E, -lse2[ql]));
+            }
+#pragma unroll
+            for (int kc = 0; kc < 2; ++kc) {
+                const frag pb = to_operand<T>(pm, 8 * kc);
+#pragma unroll
+                for (int db = 0; db < D / 32; ++db) mma(dv[db], ld_tile_t<true>(gt, 32 * qb + 16 * kc, 32 * db), pb);
+            }
+        }
+    }
+    __syncthreads();
+}
+
+template <typename T, int D>
+__device__ __forceinline__ void gkv_store(T* base, const GkvLane& L, const f32x16 (&acc)[D / 32], float sc) {
+    const int key = L.kw + L.c;
+    if (key >= L.N) return;
+    T* row = base + (size_t)key * D;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+            st4<T>(row + 32 * db + 8 * g + 4 * L.hf, acc[db][4 * g] * sc, acc[db][4 * g + 1] * sc,
+                   acc[db][4 * g + 2] * sc, acc[db][4 * g + 3] * sc);
+}
+
+template <typename T, int D>
+__global__ __launch_bounds__(GKV_THREADS) __attribute__((amdgpu_waves_per_eu(1))) void gqa_bwd_kv_kernel(
+    GqaBwdArgs p) {
+    __shared__ __attribute__((aligned(16))) T q0s[tile_elems<T, D>()];
+    __shared__ __attribute__((aligned(16))) T q1s[tile_elems<T, D>()];
+    __shared__ __attribute__((aligned(16))) T g0s[tile_elems<T, D>()];
+    __shared__ __attribute__((aligned(16))) T g1s[tile_elems<T, D>()];
+    __shared__ __attribute__((aligned(16))) float x0[2 * GKV_BM];
+    __shared__ __attribute__((aligned(16))) float x1[2 * GKV_BM];
+    __shared__ float fx[GKV_BM + GKV_BAND + 1];
+    const SliceOf sl = slice_of(blockIdx.x, p.B, p.Hkv, 1, [&](int k) { return (int)p.kv_order[k]; });
+    const int kblk = sl.level;  // ascending: longest first
+    const int b = sl.b, hkv = sl.h;
+    const int group = p.Hq / p.Hkv;
+    const int N = p.N;
+    GkvLane L;
+    L.tid = threadIdx.x;
+    L.w = __builtin_amdgcn_readfirstlane(L.tid >> 6);
+    L.lane = L.tid & 63;
+    L.c = L.tid & 31;
+    L.hf = (L.tid >> 5) & 1;
+    L.n0 = kblk * GKV_BN;
+    L.kw = L.n0 + 32 * L.w;
+    L.N = N;
+    typedef typename Vec<T>::x8 frag;
+    const size_t kvbase = ((size_t)b * p.Hkv + hkv) * N * D;
+    const int key = L.kw + L.c;
+
+    f32x16 dv[D / 32], dk[D / 32];
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            dv[db][v] = 0.0f;
+            dk[db][v] = 0.0f;
+        }
+    const uint64_t gmask = ((p.fixed_mask >> (hkv * group)) & ((group == 64) ? ~0ull : ((1ull << group) - 1)));
+    const bool any_ordinary = gmask != ((group == 64) ? ~0ull : ((1ull << group) - 1));
+    frag kf[D / 16], vf[D / 16];
+    if (any_ordinary) {
+        const T* __restrict__ K = reinterpret_cast<const T*>(p.k) + kvbase;
+        const T* __restrict__ V = reinterpret_cast<const T*>(p.v) + kvbase;
+#pragma unroll
+        for (int dc = 0; dc < D / 16; ++dc) {
+            kf[dc] = key < N ? ld8<T>(K + (size_t)key * D + 16 * dc + 8 * L.hf) : zero8<T>();
+            vf[dc] = key < N ? ld8<T>(V + (size_t)key * D + 16 * dc + 8 * L.hf) : zero8<T>();
+        }
+    }
+    const int n_tiles = (N - L.n0 + GKV_BM - 1) / GKV_BM;
+    const int n_mask = min(GKV_MASK_TILES, n_tiles);
+    const int P = (n_mask + 1) & ~1;
+    for (int i = 0; i < group; ++i) {
+        const int h = hkv * group + i;
+        const size_t qbase = ((size_t)b * p.Hq + h) * N * D;
+        const size_t row_base = ((size_t)b * p.Hq + h) * N;
+        const float* __restrict__ LSE = p.lse + row_base;
+        if ((p.fixed_mask >> h) & 1ull) {
+            const float* arow = p.a + (size_t)h * p.ld_prior;
+            const float a_key = key < N ? arow[key] : -INFINITY;
+            gkv_fixed_head<T, D>(q0s, fx, fx + GKV_BM, reinterpret_cast<const T*>(p.dO) + qbase, LSE,
+                                 p.r + (size_t)h * p.ld_prior, a_key, L, dv);
+            continue;
+        }
+        const __amdgpu_buffer_rsrc_t rq = slice_rsrc<T, D>(reinterpret_cast<const T*>(p.q) + qbase, N);
+        const __amdgpu_buffer_rsrc_t rg = slice_rsrc<T, D>(reinterpret_cast<const T*>(p.dO) + qbase, N);
+        const float* __restrict__ Dsum = p.dsum + row_base;
+        run_slots(
+            P, P + n_tiles - n_mask, [&](int s) { return s < P ? (s < n_mask ? s : -1) : n_mask + (s - P); },
+            [&](auto buf, int t) {
+                constexpr int B_ = decltype(buf)::value;
+                const int mq = L.n0 + t * GKV_BM;
+                tile_load_lds<T, D>(B_ ? q1s : q0s, rq, mq, L.w, L.lane);
+                tile_load_lds<T, D>(B_ ? g1s : g0s, rg, mq, L.w, L.lane);
+                if (L.tid < GKV_BM) {
+                    float* xr = B_ ? x1 : x0;
+                    const bool ok = mq + L.tid < N;
+                    xr[L.tid] = ok ? LSE[mq + L.tid] * LOG2E : INFINITY;
+                    xr[GKV_BM + L.tid] = ok ? -Dsum[mq + L.tid] : 0.0f;
+                }
+            },
+            [&](auto) {},
+            [&](auto buf, int t, auto mask) {
+                constexpr int B_ = decltype(buf)::value;
+                gkv_tile<T, D, decltype(mask)::value>(B_ ? q1s : q0s, B_ ? g1s : g0s, B_ ? x1 : x0,
+                                                      L.n0 + t * GKV_BM, L, kf, vf, dv, dk, p.scale_log2);
+            });
+    }
+    gkv_store<T, D>(reinterpret_cast<T*>(p.dv) + kvbase, L, dv, 1.0f);
+    gkv_store<T, D>(reinterpret_cast<T*>(p.dk) + kvbase, L, dk, p.scale);
+}
+
+// ---------------------------------------------------------------------------
+// Query-block pass (ordinary query heads): S^T = K Q^T puts one query per
+// lane (LSE and D are per-lane scalars) and dS^T feeds the B operand of
+// dQ^T += K^T dS^T.  K and V tiles of the group's key/value head come by
+// buffer loads straight to LDS, double-buffered.  Fixed heads write zeros.
+// ---------------------------------------------------------------------------
+constexpr int GDQ_BM = 128;
+constexpr int GDQ_BN = TILE_ROWS;
+constexpr int GDQ_THREADS = 256;
+
+struct GdqLane {
+    int tid, w, lane, c, hf, m0, q0, qq, N;
+};
+
+template <typename T, int D, bool MASK>
+__device__ __forceinline__ void gdq_tile(const T* kt, const T* vt, int n0, const GdqLane& L,
+                                         const typename Vec<T>::x8 (&qf)[D / 16],
+                                         const typename Vec<T>::x8 (&gf)[D / 16], float lse2, float dsum,
+                                         f32x16 (&dq)[D / 32], float scale_log2) {
+    typedef typename Vec<T>::x8 frag;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+        const int k0 = n0 + 32 * kb;
+        if (MASK && !(k0 < L.q0 + 32 && k0 < L.N)) continue;  // keys wholly after this wavefront's queries
+        f32x16 s, dp;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            s[v] = 0.0f;
+            dp[v] = 0.0f;
+        }
+#pragma unroll
+        for (int dc = 0; dc < D / 16; ++dc) {
+            mma(s, ld_row<T>(kt, 32 * kb + L.c, 16 * dc + 8 * L.hf), qf[dc]);
+            mma(dp, ld_row<T>(vt, 32 * kb + L.c, 16 * dc + 8 * L.hf), gf[dc]);
+        }
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            float pv = fast_exp2(fmaf(s[v], scale_log2, -lse2));
+            if (MASK && k0 + 8 * (v >> 2) + 4 * L.hf + (v & 3) > L.qq) pv = 0.0f;
+            s[v] = pv * (dp[v] - dsum);  // dS^T
+        }
+#pragma unroll
+        for (int kc = 0; kc < 2; ++kc) {
+            const frag sb = to_operand<T>(s, 8 * kc);
+#pragma unroll
+            for (int db = 0; db < D / 32; ++db) mma(dq[db], ld_tile_t<true>(kt, 32 * kb + 16 * kc, 32 * db), sb);
+        }
+    }
+}
+
+template <typename T, int D>
+__global__ __launch_bounds__(GDQ_THREADS) __attribute__((amdgpu_waves_per_eu(2))) void gqa_bwd_dq_kernel(
+    GqaBwdArgs p) {
+    __shared__ __attribute__((aligned(16))) T k0s[tile_elems<T, D>()];
+    __shared__ __attribute__((aligned(16))) T k1s[tile_elems<T, D>()];
+    __shared__ __attribute__((aligned(16))) T v0s[tile_elems<T, D>()];
+    __shared__ __attribute__((aligned(16))) T v1s[tile_elems<T, D>()];
+    const int group = p.Hq / p.Hkv;
+    const SliceOf sl = slice_of(blockIdx.x, p.B, p.Hkv, group, [&](int k) { return (int)p.kv_order[k]; });
+    const int qblk = p.n_blocks - 1 - sl.level;  // longest first
+    const int b = sl.b, h = sl.h;
+    const int hkv = h / group;
+    const int N = p.N;
+    const size_t qbase = ((size_t)b * p.Hq + h) * N * D;
+    const size_t kvbase = ((size_t)b * p.Hkv + hkv) * N * D;
+    T* __restrict__ dQ = reinterpret_cast<T*>(p.dq) + qbase;
+    GdqLane L;
+    L.tid = threadIdx.x;
+    L.w = __builtin_amdgcn_readfirstlane(L.tid >> 6);
+    L.lane = L.tid & 63;
+    L.c = L.tid & 31;
+    L.hf = (L.tid >> 5) & 1;
+    L.m0 = qblk * GDQ_BM;
+    L.q0 = L.m0 + 32 * L.w;
+    L.qq = L.q0 + L.c;
+    L.N = N;
+
+    if ((p.fixed_mask >> h) & 1ull) {  // the whole workgroup takes this branch
+        for (int id = L.tid; id < GDQ_BM * (D / 8); id += GDQ_THREADS) {
+            const int row = L.m0 + id / (D / 8);
+            if (row < N) st8<T>(dQ + (size_t)row * D + (id % (D / 8)) * 8, zero8<T>());
+        }
+        return;
+    }
+
+    const T* __restrict__ Q = reinterpret_cast<const T*>(p.q) + qbase;
+    const T* __restrict__ dO = reinterpret_cast<const T*>(p.dO) + qbase;
+    const __amdgpu_buffer_rsrc_t rk = slice_rsrc<T, D>(reinterpret_cast<const T*>(p.k) + kvbase, N);
+    const __amdgpu_buffer_rsrc_t rv = slice_rsrc<T, D>(reinterpret_cast<const T*>(p.v) + kvbase, N);
+    typedef typename Vec<T>::x8 frag;
+    frag qf[D / 16], gf[D / 16];
+#pragma unroll
+    for (int dc = 0; dc < D / 16; ++dc) {
+        qf[dc] = L.qq < N ? ld8<T>(Q + (size_t)L.qq * D + 16 * dc + 8 * L.hf) : zero8<T>();
+        gf[dc] = L.qq < N ? ld8<T>(dO + (size_t)L.qq * D + 16 * dc + 8 * L.hf) : zero8<T>();
+    }
+    const size_t row_base = ((size_t)b * p.Hq + h) * N;
+    const float lse2 = L.qq < N ? p.lse[row_base + L.qq] * LOG2E : INFINITY;
+    const float dsum = L.qq < N ? p.dsum[row_base + L.qq] : 0.0f;
+
+    f32x16 dq[D / 32];
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) dq[db][v] = 0.0f;
+
+    const int n_tiles = (min(L.m0 + GDQ_BM, N) + GDQ_BN - 1) / GDQ_BN;
+    const int n_full = L.m0 / GDQ_BN;
+    const int n_mask = n_tiles - n_full;
+    const int P = (n_mask + 1) & ~1;
+    run_slots(
+        P, P + n_full, [&](int i) { return i < P ? (i < n_mask ? n_full + i : -1) : i - P; },
+        [&](auto buf, int t) {
+            constexpr int B_ = decltype(buf)::value;
+            tile_load_lds<T, D>(B_ ? k1s : k0s, rk, t * GDQ_BN, L.w, L.lane);
+            tile_load_lds<T, D>(B_ ? v1s : v0s, rv, t * GDQ_BN, L.w, L.lane);
+        },
+        [&](auto) {},
+        [&](auto buf, int t, auto mask) {
+            constexpr int B_ = decltype(buf)::value;
+            gdq_tile<T, D, decltype(mask)::value>(B_ ? k1s : k0s, B_ ? v1s : v0s, t * GDQ_BN, L, qf, gf, lse2, dsum,
+                                                  dq, p.scale_log2);
+        });
+
+    if (L.qq < N) {
+        T* row = dQ + (size_t)L.qq * D;
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+                st4<T>(row + 32 * db + 8 * g + 4 * L.hf, dq[db][4 * g] * p.scale, dq[db][4 * g + 1] * p.scale,
+                       dq[db][4 * g + 2] * p.scale, dq[db][4 * g + 3] * p.scale);
+    }
+}
+
+}  // namespace saf

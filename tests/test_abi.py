@@ -275,3 +275,27 @@ def test_gqa_forward_rejects_bad_arguments(lib):
     assert _gqa(lib, N=(1 << 23), d=128) == 2   # 2^23 rows x 256 B reaches 2^31
     assert _gqa(lib, flags=[0] * 65, Hkv=5) == 3
     assert _gqa(lib, N=0, Q=None, K=None, V=None, O=None, LSE=None) == 0
+
+
+# ---------------------------------------------------------------------------
+# Grouped-query backward (saf_hybrid_attn_bwd_gqa)
+# ---------------------------------------------------------------------------
+
+def test_gqa_backward_workspace_and_rejects(lib):
+    wsb = lib.saf_hybrid_attn_bwd_gqa_workspace_bytes
+    assert wsb(1, 2, 8, 2, 100, 128) == 6400          # B * Hq * N floats, rounded up to 256 bytes
+    assert wsb(0, 1, 4, 4, 33, 96) == 768
+    assert wsb(1, 2, 8, 2, 100, 80) == 0 and wsb(1, 2, 8, 3, 100, 64) == 0 and wsb(1, 0, 8, 2, 100, 64) == 0
+
+    def bwd(dt=1, Q=FAKE, K=FAKE, V=FAKE, O=FAKE, dO=FAKE, LSE=FAKE, flags=(0, 1, 0, 0), a=FAKE, r=FAKE, ld=8,
+            B=1, Hkv=2, N=8, d=96, dQ=FAKE, dK=FAKE, dV=FAKE, ws=FAKE, wsn=256):
+        f = np.asarray(flags, dtype=np.uint8)
+        return lib.saf_hybrid_attn_bwd_gqa(dt, Q, K, V, O, dO, LSE, f.ctypes.data, a, r, ld, B, f.shape[0], Hkv, N,
+                                           d, dQ, dK, dV, ws, wsn, None)
+    assert bwd(d=80) == 3 and bwd(dt=7) == 3
+    assert bwd(Hkv=3) == 2 and bwd(ld=4) == 2
+    assert bwd(flags=(0, 3, 0, 0)) == 7 and bwd(r=None) == 4
+    assert bwd(dQ=None) == 1 and bwd(ws=None) == 1 and bwd(K=None) == 1
+    assert bwd(wsn=64) == 2                           # 4 heads x 8 rows x 4 bytes rounds to 256
+    assert bwd(ws=FAKE + 16) == 6 and bwd(dV=FAKE + 4) == 6
+    assert bwd(N=0, Q=None, K=None, V=None, O=None, dO=None, LSE=None, dQ=None, dK=None, dV=None, ws=None) == 0

@@ -119,3 +119,73 @@ def test_gqa_fixed_exact_fallback(dtype, d):
     Oo, LSEo = orc.layer_forward_gqa(inp["Q"], inp["K"], inp["V"], inp["is_fixed"], inp["a"], inp["r"])
     _check(dtype, O, Oo)
     _check(dtype, LSE, LSEo)
+
+
+# ---------------------------------------------------------------------------
+# Backward (saf_hybrid_attn_bwd_gqa) against oracle.saf_oracle.layer_backward_gqa
+# ---------------------------------------------------------------------------
+
+def _bwd_inputs(dtype, B, Hq, Hkv, N, d, fixed, stream_id):
+    from paper_2609_34650_amd import inputs
+    inp = inputs.make_inputs(B, Hq, N, d, fixed, dtype, stream_id=stream_id, backward=True)
+    inp["K"] = np.ascontiguousarray(inp["K"][:, :Hkv])
+    inp["V"] = np.ascontiguousarray(inp["V"][:, :Hkv])
+    return inp
+
+
+def _run_gpu_bwd(inp, dtype):
+    torch = torch_cuda()
+    from paper_2609_34650_amd import binding
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    dev = torch.device("cuda", 0)
+    t = {k: torch.from_numpy(inp[k]).to(dev).to(tdt).contiguous() for k in ("Q", "K", "V", "dO")}
+    a = torch.from_numpy(inp["a"]).to(dev)
+    r = torch.from_numpy(inp["r"]).to(dev)
+    O, LSE = binding.saf_hybrid_attn_fwd_gqa(t["Q"], t["K"], t["V"], inp["is_fixed"], a, r)
+    dQ, dK, dV = binding.saf_hybrid_attn_bwd_gqa(t["Q"], t["K"], t["V"], O, t["dO"], LSE, inp["is_fixed"], a, r)
+    torch.cuda.synchronize()
+    return [x.double().cpu().numpy() for x in (dQ, dK, dV)]
+
+
+@pytest.mark.parametrize("dtype,B,Hq,Hkv,N,d,fixed", [
+    ("f32", 1, 4, 2, 200, 96, (1,)),
+    ("bf16", 2, 8, 2, 300, 128, (0, 5)),
+    ("bf16", 1, 6, 1, 77, 64, (2, 3)),
+    ("f32", 1, 4, 4, 130, 128, (0, 1, 2, 3)),   # every head fixed: dQ and dK are zeros
+    ("bf16", 1, 4, 2, 1, 96, (1,)),
+    ("f32", 1, 2, 1, 129, 64, ()),
+    ("bf16", 1, 8, 2, 1000, 128, (1, 2, 6)),    # several key blocks, mixed groups
+    ("f32", 1, 3, 3, 257, 96, (1,)),
+])
+def test_gqa_backward_matches_oracle(dtype, B, Hq, Hkv, N, d, fixed):
+    from oracle import saf_oracle as orc
+    announce(f"gqa bwd {dtype} B={B} Hq={Hq} Hkv={Hkv} N={N} d={d} fixed={fixed}")
+    inp = _bwd_inputs(dtype, B, Hq, Hkv, N, d, list(fixed), stream_id=55)
+    g = _run_gpu_bwd(inp, dtype)
+    o = orc.layer_backward_gqa(inp["Q"], inp["K"], inp["V"], inp["dO"], inp["is_fixed"], inp["a"], inp["r"])
+    for name, gv, ov in zip(("dQ", "dK", "dV"), g, o):
+        assert np.isfinite(gv).all(), name
+        _check(dtype, gv, ov)
+    fixed_q = np.asarray(inp["is_fixed"]).astype(bool)
+    assert not g[0][:, fixed_q].any(), "fixed heads must get zero dQ"
+    group = Hq // Hkv
+    for gk in range(Hkv):
+        if fixed_q[gk * group:(gk + 1) * group].all():
+            assert not g[1][:, gk].any(), "a group of fixed heads must give zero dK"
+
+
+def test_gqa_backward_equals_layer_backward_at_d64():
+    """One query head per key/value head at d = 64: the grouped-query
+    backward and the layer's own backward compute the same gradients."""
+    torch = torch_cuda()
+    from paper_2609_34650_amd import binding
+    announce("gqa bwd vs layer bwd d=64")
+    inp = _bwd_inputs("f32", 2, 4, 4, 333, 64, [1, 2], stream_id=56)
+    g = _run_gpu_bwd(inp, "f32")
+    dev = torch.device("cuda", 0)
+    t = {k: torch.from_numpy(inp[k]).to(dev) for k in ("Q", "K", "V", "dO", "a", "r")}
+    O, LSE = binding.saf_hybrid_attn_fwd(t["Q"], t["K"], t["V"], inp["is_fixed"], t["a"], t["r"])
+    ref = binding.saf_hybrid_attn_bwd(t["Q"], t["K"], t["V"], O, t["dO"], LSE, inp["is_fixed"], t["a"], t["r"])
+    torch.cuda.synchronize()
+    for gv, rv in zip(g, ref):
+        np.testing.assert_allclose(gv, rv.double().cpu().numpy(), rtol=0, atol=2e-5)
