@@ -40,6 +40,12 @@ head ordinary; torch's flash SDPA (forced, no fallback) is timed beside it
 for reference when available.  MFMA roofline: an ordinary head counts 2
 contractions (QK^T, PV), a fixed head 1 (PV).
 
+``--layer1b`` times one training layer of the paper's 1B model through the
+grouped-query entry points with one query head per key/value head:
+forward + backward at B = 2, H = 16, T = 8192, d = 96, bf16, at 25 % and
+50 % fixed heads against all-ordinary (MFMA roofline with the layer's
+algorithmic count: 7 contractions per ordinary head, 2 per fixed head).
+
 ``--fit`` times the compact fit of one 12-head layer at T = 4096: the
 targets from the calibration mean (floor, renormalise, marginals), then the
 fitter's 400 Adam steps and the acceptance KL, for all heads at once; its
@@ -176,6 +182,8 @@ def parse():
     ap.add_argument("--no-compare-ordinary", dest="compare", action="store_false")
     ap.add_argument("--pattern", action="store_true",
                     help="time the trainable-pattern gradients (da, dr) at the layer workload instead")
+    ap.add_argument("--layer1b", action="store_true",
+                    help="time the layer forward+backward at head dimension 96 (B=2, H=16, T=8192) instead")
     ap.add_argument("--gqa", action="store_true",
                     help="time the grouped-query prefill forward (B=4, T=4096, 32/8 heads, d=128) instead")
     ap.add_argument("--fit", action="store_true",
@@ -733,6 +741,133 @@ def main_gqa(args, torch):
     print(json.dumps(result), flush=True)
 
 
+# ---------------------------------------------------------------------------
+# Head dimension 96 training layer (1B model shape)
+# ---------------------------------------------------------------------------
+
+def _train_head_job(job):
+    from oracle import saf_oracle as orc
+    q, k, v, do, fx, a, r = job
+    orc.head_forward(q, k, v, fx, a, r, 512)
+    orc.head_backward(q, k, v, do, fx, a, r, 512)
+    return 1
+
+
+def layer1b_cpu_baseline(inp, flags, B, H):
+    """The oracle's dense fp64 forward+backward on three ordinary heads and
+    one fixed head of batch element 0 (one head per process), scaled to the
+    layer at 25 % fixed heads (B * H / 4 slices of that mix)."""
+    import multiprocessing as mp
+    try:
+        from threadpoolctl import threadpool_limits
+    except ImportError:  # pragma: no cover
+        threadpool_limits = None
+    ords = [h for h in range(H) if not flags[h]][:3]
+    fixs = [h for h in range(H) if flags[h]][:1]
+    jobs = []
+    for h in ords + fixs:
+        fx = bool(flags[h])
+        jobs.append((None if fx else inp["Q"][0, h], None if fx else inp["K"][0, h], inp["V"][0, h], inp["dO"][0, h],
+                     fx, inp["a"][h] if fx else None, inp["r"][h] if fx else None))
+    workers = max(1, min(MAX_HOST_WORKERS, len(os.sched_getaffinity(0)), len(jobs)))
+    ctx = threadpool_limits(limits=1) if threadpool_limits else None
+    t0 = time.perf_counter()
+    try:
+        with mp.get_context("fork").Pool(workers) as pool:
+            pool.map(_train_head_job, jobs, chunksize=1)
+    finally:
+        if ctx is not None and hasattr(ctx, "unregister"):
+            ctx.unregister()
+    wall = time.perf_counter() - t0
+    scale = B * H / len(jobs)
+    return {"value": round(wall * 1e3 * scale, 1), "unit": "ms/layer", "cores": workers, "kind": "oracle",
+            "sample": f"heads {ords + fixs} of batch element 0 (3 ordinary, 1 fixed), fp64 dense fwd+bwd, "
+                      f"{wall:.1f} s wall on {workers} processes, scaled by {scale:g} to the layer's {B * H} slices"}
+
+
+def main_layer1b(args, torch):
+    from paper_2609_34650_amd import binding
+    B, H, N, d = 2, 16, 8192, 96
+    inp = gen.make_inputs(B, H, N, d, [], "bf16", stream_id=62, backward=True)
+    dev = torch.device("cuda", 0)
+    t = {k: torch.from_numpy(inp[k]).to(dev).to(torch.bfloat16) for k in ("Q", "K", "V", "dO")}
+    a = torch.from_numpy(inp["a"]).to(dev)
+    r = torch.from_numpy(inp["r"]).to(dev)
+    O = torch.empty_like(t["Q"])
+    LSE = torch.empty((B, H, N), dtype=torch.float32, device=dev)
+    dQ, dK, dV = (torch.empty_like(t["Q"]) for _ in range(3))
+    code = binding.SAF_DTYPE_BF16
+    ws = torch.empty(max(256, int(binding.load().saf_hybrid_attn_bwd_gqa_workspace_bytes(code, B, H, H, N, d))),
+                     dtype=torch.uint8, device=dev)
+    C = contraction_flop(N, d) * B
+
+    def flags_for(n_fixed):
+        f = np.zeros(H, np.uint8)
+        f[gen.fixed_heads(H, n_fixed, stream_id=62)] = 1
+        return f
+
+    def step(fl):
+        binding.saf_hybrid_attn_fwd_gqa(t["Q"], t["K"], t["V"], fl, a, r, O=O, LSE=LSE)
+        binding.saf_hybrid_attn_bwd_gqa(t["Q"], t["K"], t["V"], O, t["dO"], LSE, fl, a, r, dQ=dQ, dK=dK, dV=dV,
+                                        workspace=ws)
+
+    def timed(fl, steps):
+        for _ in range(args.warmup):
+            step(fl)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            step(fl)
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps
+
+    steps = max(1, args.steps // 3)
+    n25, n50 = H // 4, H // 2
+    f25 = flags_for(n25)
+    for _ in range(args.warmup):
+        step(f25)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step(f25)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    ms25 = timed(f25, steps)
+    ms50 = timed(flags_for(n50), steps)
+    ms0 = timed(flags_for(0), steps)
+    flop25 = C * (7 * (H - n25) + 2 * n25)
+    tflops = flop25 / (ms25 * 1e-3) / 1e12
+    result = {
+        "metric": "1B-shape hybrid layer fwd+bwd ms/layer (B=2, H=16, T=8192, d=96, 25% fixed)",
+        "value": round(ms, 3),
+        "unit": "ms/layer",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 3),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "layer1b_8k: hybrid causal attention layer fwd+bwd at head dimension 96", "B": B,
+                   "H": H, "N": N, "d": d, "n_fixed": n25, "parallelism": "single GPU"},
+        "tflops": round(tflops, 1),
+        "ms_25pct": round(ms25, 3),
+        "ms_50pct": round(ms50, 3),
+        "ms_all_ordinary": round(ms0, 3),
+        "speedup_25pct": round(ms0 / ms25, 3),
+        "speedup_50pct": round(ms0 / ms50, 3),
+        "cpu_baseline": layer1b_cpu_baseline(inp, f25, B, H) if args.cpu_baseline else None,
+        "roofline": {"bound": "mfma", "kernel": "gqa fwd+bwd (layer)", "achieved": round(tflops, 1),
+                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(tflops / PEAK_BF16_TFLOPS, 4),
+                     "traffic": None},
+    }
+    print(json.dumps(result), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -764,6 +899,9 @@ def main():
         return
     if args.gqa:
         main_gqa(args, torch)
+        return
+    if args.layer1b:
+        main_layer1b(args, torch)
         return
 
     w = gen.WORKLOADS[args.workload]

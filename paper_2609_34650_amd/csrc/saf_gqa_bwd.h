@@ -143,51 +143,36 @@ __device__ __forceinline__ void gkv_tile(const T* qt, const T* gt, const float* 
     }
 }
 
-// Fixed query head: dV^T += dO^T P with P evaluated per entry.  The dO tile
-// is staged through registers into gt; lse2 holds log Z * log2(e) of the
-// tile's rows and rb the r values of the offsets it meets.
+// Fixed query head, one tile: dV^T += dO^T P with P evaluated per entry.
+// gt: the dO tile; lse2: log Z * log2(e) of the tile's rows; rb: r over the
+// offsets the tile meets (rb[x] = r(mq - n0 - 127 + x), -inf outside
+// 0 .. N - 1, which masks keys after the query).
 template <typename T, int D>
-__device__ __forceinline__ void gkv_fixed_head(T* gt, float* lse2, float* rb, const T* dO, const float* LSE,
-                                               const float* rrow, float a_key, const GkvLane& L,
-                                               f32x16 (&dv)[D / 32]) {
+__device__ __forceinline__ void gkv_fixed_tile(const T* gt, const float* lse2, const float* rb, int mq, float a_key,
+                                               const GkvLane& L, f32x16 (&dv)[D / 32]) {
     typedef typename Vec<T>::x8 frag;
-    const int N = L.N;
-    const int row = unit_row<T>(L.w, L.lane);
     const int kl = L.kw - L.n0 + L.c;  // key within the block
-    for (int mq = L.n0; mq < N; mq += GKV_BM) {
-        __syncthreads();
 #pragma unroll
-        for (int k = 0; k < tile_units<T, D>(); ++k) {
-            const int col = unit_col<T>(L.w, L.lane, k);
-            const u32x4 z = {0u, 0u, 0u, 0u};
-            const u32x4 x = mq + row < N ? ld_unit(dO + (size_t)(mq + row) * D + col) : z;
-            *reinterpret_cast<u32x4*>(gt + toff<T>(row, col)) = x;
-        }
-        if (L.tid < GKV_BM) lse2[L.tid] = mq + L.tid < N ? LSE[mq + L.tid] * LOG2E : INFINITY;
-        if (L.tid < GKV_BAND) {
-            const int delta = mq - L.n0 - (GKV_BN - 1) + L.tid;
-            rb[L.tid] = (delta >= 0 && delta < N) ? rrow[delta] : -INFINITY;
-        }
-        __syncthreads();
+    for (int qb = 0; qb < 2; ++qb) {
+        const int qs = mq + 32 * qb;
+        if (qs + 31 < L.kw || qs >= L.N) continue;  // no query of this half sees these keys
+        f32x16 pm;
 #pragma unroll
-        for (int qb = 0; qb < 2; ++qb) {
-            const int qs = mq + 32 * qb;
-            if (qs + 31 < L.kw || qs >= N) continue;
-            f32x16 pm;
+        for (int g = 0; g < 4; ++g) {
+            const f32x4 l4 = *reinterpret_cast<const f32x4*>(lse2 + 32 * qb + 8 * g + 4 * L.hf);
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int ql = 32 * qb + 8 * (v >> 2) + 4 * L.hf + (v & 3);
-                pm[v] = fast_exp2(fmaf(a_key + rb[ql - kl + (GKV_BN - 1)], LOG2E, -lse2[ql]));
+            for (int u = 0; u < 4; ++u) {
+                const int ql = 32 * qb + 8 * g + 4 * L.hf + u;
+                pm[4 * g + u] = fast_exp2(fmaf(a_key + rb[ql - kl + (GKV_BN - 1)], LOG2E, -l4[u]));
             }
+        }
 #pragma unroll
-            for (int kc = 0; kc < 2; ++kc) {
-                const frag pb = to_operand<T>(pm, 8 * kc);
+        for (int kc = 0; kc < 2; ++kc) {
+            const frag pb = to_operand<T>(pm, 8 * kc);
 #pragma unroll
-                for (int db = 0; db < D / 32; ++db) mma(dv[db], ld_tile_t<true>(gt, 32 * qb + 16 * kc, 32 * db), pb);
-            }
+            for (int db = 0; db < D / 32; ++db) mma(dv[db], ld_tile_t<true>(gt, 32 * qb + 16 * kc, 32 * db), pb);
         }
     }
-    __syncthreads();
 }
 
 template <typename T, int D>
@@ -204,7 +189,7 @@ __device__ __forceinline__ void gkv_store(T* base, const GkvLane& L, const f32x1
 }
 
 template <typename T, int D>
-__global__ __launch_bounds__(GKV_THREADS) __attribute__((amdgpu_waves_per_eu(1))) void gqa_bwd_kv_kernel(
+__global__ __launch_bounds__(GKV_THREADS) __attribute__((amdgpu_waves_per_eu(D * sizeof(T) <= 128 ? 2 : 1))) void gqa_bwd_kv_kernel(
     GqaBwdArgs p) {
     __shared__ __attribute__((aligned(16))) T q0s[tile_elems<T, D>()];
     __shared__ __attribute__((aligned(16))) T q1s[tile_elems<T, D>()];
@@ -212,7 +197,8 @@ __global__ __launch_bounds__(GKV_THREADS) __attribute__((amdgpu_waves_per_eu(1))
     __shared__ __attribute__((aligned(16))) T g1s[tile_elems<T, D>()];
     __shared__ __attribute__((aligned(16))) float x0[2 * GKV_BM];
     __shared__ __attribute__((aligned(16))) float x1[2 * GKV_BM];
-    __shared__ float fx[GKV_BM + GKV_BAND + 1];
+    __shared__ __attribute__((aligned(16))) float f0[GKV_BM + GKV_BAND + 1];
+    __shared__ __attribute__((aligned(16))) float f1[GKV_BM + GKV_BAND + 1];
     const SliceOf sl = slice_of(blockIdx.x, p.B, p.Hkv, 1, [&](int k) { return (int)p.kv_order[k]; });
     const int kblk = sl.level;  // ascending: longest first
     const int b = sl.b, hkv = sl.h;
@@ -259,15 +245,35 @@ __global__ __launch_bounds__(GKV_THREADS) __attribute__((amdgpu_waves_per_eu(1))
         const size_t qbase = ((size_t)b * p.Hq + h) * N * D;
         const size_t row_base = ((size_t)b * p.Hq + h) * N;
         const float* __restrict__ LSE = p.lse + row_base;
+        const __amdgpu_buffer_rsrc_t rg = slice_rsrc<T, D>(reinterpret_cast<const T*>(p.dO) + qbase, N);
         if ((p.fixed_mask >> h) & 1ull) {
+            // dO tiles by buffer loads to LDS; each buffer's LSE rows and r
+            // band are written while the other buffer is in use.
             const float* arow = p.a + (size_t)h * p.ld_prior;
+            const float* rrow = p.r + (size_t)h * p.ld_prior;
             const float a_key = key < N ? arow[key] : -INFINITY;
-            gkv_fixed_head<T, D>(q0s, fx, fx + GKV_BM, reinterpret_cast<const T*>(p.dO) + qbase, LSE,
-                                 p.r + (size_t)h * p.ld_prior, a_key, L, dv);
+            run_slots(
+                P, P + n_tiles - n_mask, [&](int s) { return s < P ? (s < n_mask ? s : -1) : n_mask + (s - P); },
+                [&](auto buf, int t) {
+                    constexpr int B_ = decltype(buf)::value;
+                    const int mq = L.n0 + t * GKV_BM;
+                    tile_load_lds<T, D>(B_ ? g1s : g0s, rg, mq, L.w, L.lane);
+                    float* fr = B_ ? f1 : f0;
+                    if (L.tid < GKV_BM) fr[L.tid] = mq + L.tid < N ? LSE[mq + L.tid] * LOG2E : INFINITY;
+                    if (L.tid < GKV_BAND) {
+                        const int delta = mq - L.n0 - (GKV_BN - 1) + L.tid;
+                        fr[GKV_BM + L.tid] = (delta >= 0 && delta < N) ? rrow[delta] : -INFINITY;
+                    }
+                },
+                [&](auto) {},
+                [&](auto buf, int t, auto) {
+                    constexpr int B_ = decltype(buf)::value;
+                    const float* fr = B_ ? f1 : f0;
+                    gkv_fixed_tile<T, D>(B_ ? g1s : g0s, fr, fr + GKV_BM, L.n0 + t * GKV_BM, a_key, L, dv);
+                });
             continue;
         }
         const __amdgpu_buffer_rsrc_t rq = slice_rsrc<T, D>(reinterpret_cast<const T*>(p.q) + qbase, N);
-        const __amdgpu_buffer_rsrc_t rg = slice_rsrc<T, D>(reinterpret_cast<const T*>(p.dO) + qbase, N);
         const float* __restrict__ Dsum = p.dsum + row_base;
         run_slots(
             P, P + n_tiles - n_mask, [&](int s) { return s < P ? (s < n_mask ? s : -1) : n_mask + (s - P); },
