@@ -9,8 +9,9 @@
 // reads key/value head h / (Hq / Hkv).  A shared head's dK and dV are sums
 // over the query heads of its group: ordinary heads add dS^T Q / sqrt(D) to
 // dK and P^T dO to dV (the FlashAttention-2 recurrences of the layer's own
-// backward); fixed heads add P^T dO to dV only, with P(i, j) = exp(a[j] +
-// r[i - j] - log Z(i)) evaluated per entry; they get exact zeros in dQ.
+// backward); fixed heads add P^T dO to dV only (factorised into a Toeplitz
+// band times a scaled dO, or, behind a guard, P(i, j) = exp(a[j] + r[i - j] -
+// log Z(i)) per entry); they get exact zeros in dQ.
 //
 // Three launches: the row pre-pass D_i = sum_c dO * O for ordinary query
 // heads; the key-block pass (workgroup = (b, key/value head, 128 keys), one
@@ -175,6 +176,86 @@ __device__ __forceinline__ void gkv_fixed_tile(const T* gt, const float* lse2, c
     }
 }
 
+// Fixed query head, factorised (the layer's key-block program): dV[j] +=
+// ea(j) sum_i er(i - j) g(i) dO[i] with ea = exp(a - A), er = exp(r - R),
+// g(i) = exp(A + R - log Z(i)) (A: maximum of a over the block's keys, R:
+// maximum of r over the offsets it meets).  The dO tile is staged through
+// registers scaled by g, the weight operand is the Toeplitz band er read
+// from LDS as a bf16 high part plus a bf16 low part (eight shifted copies of
+// each, so every 8-entry read is aligned; negative offsets hold 0), and the
+// head's sum is scaled by ea(j) once at the end: no exponential per entry.
+constexpr int GKV_BAND_STRIDE = (GKV_BAND + 8) / 8 * 8 + 8;  // every copy 16-byte aligned
+
+template <typename T, int D>
+struct GkvFixStage {
+    u32x4 g[tile_units<T, D>()];  // this lane's 16-byte units of the dO tile (one row)
+    float lse;                    // log Z of that row
+    float rb;                     // one band entry
+};
+
+template <typename T, int D>
+__device__ __forceinline__ void gkvf_load(GkvFixStage<T, D>& st, const T* dO, const float* LSE, const float* rrow,
+                                          int mq, const GkvLane& L) {
+    const int q = mq + unit_row<T>(L.w, L.lane);
+    const bool ok = q < L.N;
+#pragma unroll
+    for (int k = 0; k < tile_units<T, D>(); ++k) {
+        const u32x4 z = {0u, 0u, 0u, 0u};
+        st.g[k] = ok ? ld_unit(dO + (size_t)q * D + unit_col<T>(L.w, L.lane, k)) : z;
+    }
+    st.lse = ok ? LSE[q] : INFINITY;
+    const int delta = mq - L.n0 - (GKV_BN - 1) + L.tid;
+    st.rb = (L.tid < GKV_BAND && delta >= 0 && delta < L.N) ? rrow[delta] : -INFINITY;
+}
+
+// band: copy s of the high parts at s * GKV_BAND_STRIDE, of the low parts at
+// (BAND_COPIES + s) * GKV_BAND_STRIDE.
+template <typename T, int D>
+__device__ __forceinline__ void gkvf_store(T* dog, T* band, const GkvFixStage<T, D>& st, const GkvLane& L,
+                                           float g_sh, float r_sh) {
+    const float g = fast_exp2(fmaf(-st.lse, LOG2E, g_sh));
+    const int row = unit_row<T>(L.w, L.lane);
+#pragma unroll
+    for (int k = 0; k < tile_units<T, D>(); ++k)
+        st_unit_scaled(dog + toff<T>(row, unit_col<T>(L.w, L.lane, k)), st.g[k], g);
+    if (L.tid < GKV_BAND) {
+        const float e = fast_exp2(fmaf(st.rb, LOG2E, -r_sh));
+        const T hi = (T)e;
+        const T lo = (T)(e - (float)hi);
+#pragma unroll
+        for (int s = 0; s < BAND_COPIES; ++s)
+            if (L.tid >= s) {
+                band[s * GKV_BAND_STRIDE + L.tid - s] = hi;
+                band[(BAND_COPIES + s) * GKV_BAND_STRIDE + L.tid - s] = lo;
+            }
+    }
+}
+
+template <typename T, int D>
+__device__ __forceinline__ void gkvf_tile(const T* dog, const T* band, int mq, const GkvLane& L,
+                                          f32x16 (&acc)[D / 32]) {
+    typedef typename Vec<T>::x8 frag;
+    const int kl = L.kw - L.n0 + L.c;  // key within the block
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+        const int qs = mq + 32 * qb;
+        if (qs + 31 < L.kw || qs >= L.N) continue;  // no query of this half sees these keys
+#pragma unroll
+        for (int kc = 0; kc < 2; ++kc) {
+            const int u0 = 32 * qb + 16 * kc + 8 * L.hf - kl + (GKV_BN - 1);  // band index of this lane's first slot
+            const int s = u0 & 7;
+            const frag bh = ld8<T>(band + s * GKV_BAND_STRIDE + u0 - s);
+            const frag bl = ld8<T>(band + (BAND_COPIES + s) * GKV_BAND_STRIDE + u0 - s);
+#pragma unroll
+            for (int db = 0; db < D / 32; ++db) {
+                const frag ga = ld_tile_t<false>(dog, 32 * qb + 16 * kc, 32 * db);
+                mma(acc[db], ga, bh);
+                mma(acc[db], ga, bl);
+            }
+        }
+    }
+}
+
 template <typename T, int D>
 __device__ __forceinline__ void gkv_store(T* base, const GkvLane& L, const f32x16 (&acc)[D / 32], float sc) {
     const int key = L.kw + L.c;
@@ -189,7 +270,7 @@ __device__ __forceinline__ void gkv_store(T* base, const GkvLane& L, const f32x1
 }
 
 template <typename T, int D>
-__global__ __launch_bounds__(GKV_THREADS) __attribute__((amdgpu_waves_per_eu(D * sizeof(T) <= 128 ? 2 : 1))) void gqa_bwd_kv_kernel(
+__global__ __launch_bounds__(GKV_THREADS) __attribute__((amdgpu_waves_per_eu(D * sizeof(T) <= 192 ? 2 : 1))) void gqa_bwd_kv_kernel(
     GqaBwdArgs p) {
     __shared__ __attribute__((aligned(16))) T q0s[tile_elems<T, D>()];
     __shared__ __attribute__((aligned(16))) T q1s[tile_elems<T, D>()];
@@ -199,6 +280,8 @@ __global__ __launch_bounds__(GKV_THREADS) __attribute__((amdgpu_waves_per_eu(D *
     __shared__ __attribute__((aligned(16))) float x1[2 * GKV_BM];
     __shared__ __attribute__((aligned(16))) float f0[GKV_BM + GKV_BAND + 1];
     __shared__ __attribute__((aligned(16))) float f1[GKV_BM + GKV_BAND + 1];
+    __shared__ float red[4];
+    static_assert(2 * BAND_COPIES * GKV_BAND_STRIDE <= tile_elems<T, D>(), "hi/lo band copies fit in a tile");
     const SliceOf sl = slice_of(blockIdx.x, p.B, p.Hkv, 1, [&](int k) { return (int)p.kv_order[k]; });
     const int kblk = sl.level;  // ascending: longest first
     const int b = sl.b, hkv = sl.h;
@@ -221,80 +304,129 @@ __global__ __launch_bounds__(GKV_THREADS) __attribute__((amdgpu_waves_per_eu(D *
 #pragma unroll
     for (int db = 0; db < D / 32; ++db)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-            dv[db][v] = 0.0f;
-            dk[db][v] = 0.0f;
-        }
-    const uint64_t gmask = ((p.fixed_mask >> (hkv * group)) & ((group == 64) ? ~0ull : ((1ull << group) - 1)));
-    const bool any_ordinary = gmask != ((group == 64) ? ~0ull : ((1ull << group) - 1));
-    frag kf[D / 16], vf[D / 16];
-    if (any_ordinary) {
-        const T* __restrict__ K = reinterpret_cast<const T*>(p.k) + kvbase;
-        const T* __restrict__ V = reinterpret_cast<const T*>(p.v) + kvbase;
-#pragma unroll
-        for (int dc = 0; dc < D / 16; ++dc) {
-            kf[dc] = key < N ? ld8<T>(K + (size_t)key * D + 16 * dc + 8 * L.hf) : zero8<T>();
-            vf[dc] = key < N ? ld8<T>(V + (size_t)key * D + 16 * dc + 8 * L.hf) : zero8<T>();
-        }
-    }
+        for (int v = 0; v < 16; ++v) dv[db][v] = 0.0f;
+    const uint64_t all = (group == 64) ? ~0ull : ((1ull << group) - 1);
+    const uint64_t gmask = (p.fixed_mask >> (hkv * group)) & all;
     const int n_tiles = (N - L.n0 + GKV_BM - 1) / GKV_BM;
     const int n_mask = min(GKV_MASK_TILES, n_tiles);
     const int P = (n_mask + 1) & ~1;
+    // Fixed query heads first (only dV is live), then the ordinary ones with K
+    // and V of the block's keys in registers.
     for (int i = 0; i < group; ++i) {
+        if (!((gmask >> i) & 1ull)) continue;
         const int h = hkv * group + i;
         const size_t qbase = ((size_t)b * p.Hq + h) * N * D;
         const size_t row_base = ((size_t)b * p.Hq + h) * N;
         const float* __restrict__ LSE = p.lse + row_base;
         const __amdgpu_buffer_rsrc_t rg = slice_rsrc<T, D>(reinterpret_cast<const T*>(p.dO) + qbase, N);
-        if ((p.fixed_mask >> h) & 1ull) {
-            // dO tiles by buffer loads to LDS; each buffer's LSE rows and r
-            // band are written while the other buffer is in use.
-            const float* arow = p.a + (size_t)h * p.ld_prior;
-            const float* rrow = p.r + (size_t)h * p.ld_prior;
-            const float a_key = key < N ? arow[key] : -INFINITY;
+        const float* arow = p.a + (size_t)h * p.ld_prior;
+        const float* rrow = p.r + (size_t)h * p.ld_prior;
+        const float a_key = key < N ? arow[key] : -INFINITY;
+        // A: max of a over the block's keys; R: max of r over the offsets
+        // the block meets (0 .. N - 1 - n0); LO: min of log Z over its rows.
+        float am = -INFINITY, rm = -INFINITY, lo = INFINITY;
+        for (int j = L.tid; j < GKV_BN; j += GKV_THREADS)
+            if (L.n0 + j < N) am = fmaxf(am, arow[L.n0 + j]);
+        for (int j = L.tid; j < N - L.n0; j += GKV_THREADS) {
+            rm = fmaxf(rm, rrow[j]);
+            lo = fminf(lo, LSE[L.n0 + j]);
+        }
+        const float A = block_max(am, red);
+        const float R = block_max(rm, red);
+        const float LO = -block_max(-lo, red);
+        if (LO - A - R >= -FAST_GUARD) {  // no g(i) can overflow
+            const float g_sh = (A + R) * LOG2E, r_sh = R * LOG2E;
+            const T* __restrict__ dOh = reinterpret_cast<const T*>(p.dO) + qbase;
+            f32x16 acc[D / 32];
+#pragma unroll
+            for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) acc[db][v] = 0.0f;
+            GkvFixStage<T, D> st;
             run_slots(
-                P, P + n_tiles - n_mask, [&](int s) { return s < P ? (s < n_mask ? s : -1) : n_mask + (s - P); },
-                [&](auto buf, int t) {
+                P, P + n_tiles - n_mask,
+                [&](int s) { return s < P ? (s < n_mask ? s : -1) : n_mask + (s - P); },
+                [&](auto, int t) { gkvf_load<T, D>(st, dOh, LSE, rrow, L.n0 + t * GKV_BM, L); },
+                [&](auto buf) {
                     constexpr int B_ = decltype(buf)::value;
-                    const int mq = L.n0 + t * GKV_BM;
-                    tile_load_lds<T, D>(B_ ? g1s : g0s, rg, mq, L.w, L.lane);
-                    float* fr = B_ ? f1 : f0;
-                    if (L.tid < GKV_BM) fr[L.tid] = mq + L.tid < N ? LSE[mq + L.tid] * LOG2E : INFINITY;
-                    if (L.tid < GKV_BAND) {
-                        const int delta = mq - L.n0 - (GKV_BN - 1) + L.tid;
-                        fr[GKV_BM + L.tid] = (delta >= 0 && delta < N) ? rrow[delta] : -INFINITY;
-                    }
+                    gkvf_store<T, D>(B_ ? g1s : g0s, B_ ? q1s : q0s, st, L, g_sh, r_sh);
                 },
-                [&](auto) {},
                 [&](auto buf, int t, auto) {
                     constexpr int B_ = decltype(buf)::value;
-                    const float* fr = B_ ? f1 : f0;
-                    gkv_fixed_tile<T, D>(B_ ? g1s : g0s, fr, fr + GKV_BM, L.n0 + t * GKV_BM, a_key, L, dv);
+                    gkvf_tile<T, D>(B_ ? g1s : g0s, B_ ? q1s : q0s, L.n0 + t * GKV_BM, L, acc);
                 });
+            const float ea = key < N ? fast_exp2(fmaf(a_key, LOG2E, -A * LOG2E)) : 0.0f;
+#pragma unroll
+            for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) dv[db][v] = fmaf(ea, acc[db][v], dv[db][v]);
             continue;
         }
-        const __amdgpu_buffer_rsrc_t rq = slice_rsrc<T, D>(reinterpret_cast<const T*>(p.q) + qbase, N);
-        const float* __restrict__ Dsum = p.dsum + row_base;
+        // Exact program: dO tiles by buffer loads to LDS; each buffer's LSE
+        // rows and r band are written while the other buffer is in use.
         run_slots(
             P, P + n_tiles - n_mask, [&](int s) { return s < P ? (s < n_mask ? s : -1) : n_mask + (s - P); },
             [&](auto buf, int t) {
                 constexpr int B_ = decltype(buf)::value;
                 const int mq = L.n0 + t * GKV_BM;
-                tile_load_lds<T, D>(B_ ? q1s : q0s, rq, mq, L.w, L.lane);
                 tile_load_lds<T, D>(B_ ? g1s : g0s, rg, mq, L.w, L.lane);
-                if (L.tid < GKV_BM) {
-                    float* xr = B_ ? x1 : x0;
-                    const bool ok = mq + L.tid < N;
-                    xr[L.tid] = ok ? LSE[mq + L.tid] * LOG2E : INFINITY;
-                    xr[GKV_BM + L.tid] = ok ? -Dsum[mq + L.tid] : 0.0f;
+                float* fr = B_ ? f1 : f0;
+                if (L.tid < GKV_BM) fr[L.tid] = mq + L.tid < N ? LSE[mq + L.tid] * LOG2E : INFINITY;
+                if (L.tid < GKV_BAND) {
+                    const int delta = mq - L.n0 - (GKV_BN - 1) + L.tid;
+                    fr[GKV_BM + L.tid] = (delta >= 0 && delta < N) ? rrow[delta] : -INFINITY;
                 }
             },
             [&](auto) {},
-            [&](auto buf, int t, auto mask) {
+            [&](auto buf, int t, auto) {
                 constexpr int B_ = decltype(buf)::value;
-                gkv_tile<T, D, decltype(mask)::value>(B_ ? q1s : q0s, B_ ? g1s : g0s, B_ ? x1 : x0,
-                                                      L.n0 + t * GKV_BM, L, kf, vf, dv, dk, p.scale_log2);
+                const float* fr = B_ ? f1 : f0;
+                gkv_fixed_tile<T, D>(B_ ? g1s : g0s, fr, fr + GKV_BM, L.n0 + t * GKV_BM, a_key, L, dv);
             });
+    }
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) dk[db][v] = 0.0f;
+    if (gmask != all) {
+        const T* __restrict__ K = reinterpret_cast<const T*>(p.k) + kvbase;
+        const T* __restrict__ V = reinterpret_cast<const T*>(p.v) + kvbase;
+        frag kf[D / 16], vf[D / 16];
+#pragma unroll
+        for (int dc = 0; dc < D / 16; ++dc) {
+            kf[dc] = key < N ? ld8<T>(K + (size_t)key * D + 16 * dc + 8 * L.hf) : zero8<T>();
+            vf[dc] = key < N ? ld8<T>(V + (size_t)key * D + 16 * dc + 8 * L.hf) : zero8<T>();
+        }
+        for (int i = 0; i < group; ++i) {
+            if ((gmask >> i) & 1ull) continue;
+            const int h = hkv * group + i;
+            const size_t qbase = ((size_t)b * p.Hq + h) * N * D;
+            const size_t row_base = ((size_t)b * p.Hq + h) * N;
+            const float* __restrict__ LSE = p.lse + row_base;
+            const __amdgpu_buffer_rsrc_t rg = slice_rsrc<T, D>(reinterpret_cast<const T*>(p.dO) + qbase, N);
+            const __amdgpu_buffer_rsrc_t rq = slice_rsrc<T, D>(reinterpret_cast<const T*>(p.q) + qbase, N);
+            const float* __restrict__ Dsum = p.dsum + row_base;
+            run_slots(
+                P, P + n_tiles - n_mask, [&](int s) { return s < P ? (s < n_mask ? s : -1) : n_mask + (s - P); },
+                [&](auto buf, int t) {
+                    constexpr int B_ = decltype(buf)::value;
+                    const int mq = L.n0 + t * GKV_BM;
+                    tile_load_lds<T, D>(B_ ? q1s : q0s, rq, mq, L.w, L.lane);
+                    tile_load_lds<T, D>(B_ ? g1s : g0s, rg, mq, L.w, L.lane);
+                    if (L.tid < GKV_BM) {
+                        float* xr = B_ ? x1 : x0;
+                        const bool ok = mq + L.tid < N;
+                        xr[L.tid] = ok ? LSE[mq + L.tid] * LOG2E : INFINITY;
+                        xr[GKV_BM + L.tid] = ok ? -Dsum[mq + L.tid] : 0.0f;
+                    }
+                },
+                [&](auto) {},
+                [&](auto buf, int t, auto mask) {
+                    constexpr int B_ = decltype(buf)::value;
+                    gkv_tile<T, D, decltype(mask)::value>(B_ ? q1s : q0s, B_ ? g1s : g0s, B_ ? x1 : x0,
+                                                          L.n0 + t * GKV_BM, L, kf, vf, dv, dk, p.scale_log2);
+                });
+        }
     }
     gkv_store<T, D>(reinterpret_cast<T*>(p.dv) + kvbase, L, dv, 1.0f);
     gkv_store<T, D>(reinterpret_cast<T*>(p.dk) + kvbase, L, dk, p.scale);

@@ -105,12 +105,13 @@ def test_gqa_prefill_shape_sampled():
 def test_gqa_fixed_exact_fallback(dtype, d):
     """a is 60 nats lower on the first half of the keys: the blocks whose rows
     lie in that half but whose maxima come from the second half must take the
-    exact per-entry program (the factorised one would underflow); the rest
-    take the factorised program."""
+    exact per-entry programs (the factorised ones would underflow or
+    overflow): the forward's query block and the backward's key block that
+    straddle the middle; the rest take the factorised programs."""
     from oracle import saf_oracle as orc
     announce(f"gqa fixed exact fallback {dtype} d={d}")
     N = 600
-    inp = _inputs(dtype, 1, 4, 2, N, d, [0, 3], stream_id=54)
+    inp = _bwd_inputs(dtype, 1, 4, 2, N, d, [0, 3], stream_id=54)
     a = inp["a"].copy()
     a[0, : N // 2] -= 60.0
     a[3, : N // 2] -= 60.0
@@ -119,6 +120,10 @@ def test_gqa_fixed_exact_fallback(dtype, d):
     Oo, LSEo = orc.layer_forward_gqa(inp["Q"], inp["K"], inp["V"], inp["is_fixed"], inp["a"], inp["r"])
     _check(dtype, O, Oo)
     _check(dtype, LSE, LSEo)
+    g = _run_gpu_bwd(inp, dtype)
+    o = orc.layer_backward_gqa(inp["Q"], inp["K"], inp["V"], inp["dO"], inp["is_fixed"], inp["a"], inp["r"])
+    for gv, ov in zip(g, o):
+        _check(dtype, gv, ov)
 
 
 # ---------------------------------------------------------------------------
