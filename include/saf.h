@@ -161,8 +161,9 @@ size_t saf_hybrid_attn_bwd_workspace_bytes(saf_dtype_t dt, int B, int H, int N, 
  * Backward of the hybrid layer for the loss sum(O * dO) (Appendix "Mixed-head
  * execution and numerical checks": key-block programs produce dV for every
  * head and dK for ordinary heads; a separate query-block pass produces dQ for
- * ordinary heads only).  Three launches: a row pre-pass D_i = sum_c dO*O for
- * ordinary heads, the key-block pass, the query-block pass.
+ * ordinary heads only).  Two launches: the query-block pass, which also forms
+ * D_i = sum_c dO*O for ordinary heads and leaves it in the workspace, then the
+ * key-block pass, which reads it.
  *   Q, K, V, O, dO : [B,H,N,d] `dt` (O and LSE as written by the forward).
  *   LSE            : [B,H,N] float32 from the forward.
  *   dQ, dK, dV     : [B,H,N,d] `dt`, written; fixed heads get exact zeros in
@@ -181,10 +182,13 @@ saf_status_t saf_hybrid_attn_bwd(saf_dtype_t dt,
                                  void* workspace, size_t workspace_bytes,
                                  hipStream_t stream);
 
-/* The three launches of saf_hybrid_attn_bwd, enqueued one at a time (same
- * arguments and contract).  Running SAF_BWD_PREPROCESS, then SAF_BWD_DKDV and
- * SAF_BWD_DQ (in either order) on one stream with one workspace equals
- * saf_hybrid_attn_bwd.  DKDV writes dK and dV; DQ writes dQ. */
+/* The backward as three separate launches, enqueued one at a time (same
+ * arguments and contract): a row pre-pass that writes D into the workspace,
+ * the key-block pass and the query-block pass (both read D).  Running
+ * SAF_BWD_PREPROCESS, then SAF_BWD_DKDV and SAF_BWD_DQ (in either order) on
+ * one stream with one workspace gives what saf_hybrid_attn_bwd gives, up to
+ * the float32 rounding of D (saf_hybrid_attn_bwd forms D inside its
+ * query-block pass).  DKDV writes dK and dV; DQ writes dQ. */
 typedef enum {
     SAF_BWD_PREPROCESS = 0,
     SAF_BWD_DKDV = 1,

@@ -186,6 +186,7 @@ saf::BwdArgs make_bwd_args(const void* Q, const void* K, const void* V, const vo
     args.dv = dV;
     args.dsum = reinterpret_cast<float*>(workspace);
     args.fixed_mask = pr.fixed_mask;
+    args.dq_writes_dsum = 0;
     fill_head_order(args.head_order, pr.fixed_mask, H);
     args.B = B;
     args.H = H;
@@ -487,12 +488,13 @@ SAF_EXPORT saf_status_t saf_hybrid_attn_bwd(saf_dtype_t dt, const void* Q, const
     if (st != SAF_OK || pr.empty) return st;
     const saf::BwdArgs args =
         make_bwd_args(Q, K, V, O, dO, LSE, a, r, ld_prior, B, H, N, dQ, dK, dV, workspace, pr);
-    const saf_bwd_stage_t order[3] = {SAF_BWD_PREPROCESS, SAF_BWD_DKDV, SAF_BWD_DQ};
-    for (saf_bwd_stage_t s : order) {
-        st = run_bwd_stage(s, dt, args, stream);
-        if (st != SAF_OK) return st;
-    }
-    return SAF_OK;
+    // The query-block pass forms D itself and writes it for the key-block
+    // pass, so no row pre-pass runs here.
+    saf::BwdArgs fused = args;
+    fused.dq_writes_dsum = 1;
+    st = run_bwd_stage(SAF_BWD_DQ, dt, fused, stream);
+    if (st != SAF_OK) return st;
+    return run_bwd_stage(SAF_BWD_DKDV, dt, args, stream);
 }
 
 SAF_EXPORT size_t saf_hybrid_attn_bwd_pattern_workspace_bytes(saf_dtype_t dt, int B, int H, int N, int d) {

@@ -33,6 +33,7 @@ struct BwdArgs {
     int B, H, N, ld_prior, n_blocks;
     float scale;       // 1 / sqrt(d)
     float scale_log2;  // log2(e) / sqrt(d)
+    int dq_writes_dsum;  // query-block pass: form D from O and dO and write it (no row pre-pass)
     unsigned char head_order[64];  // ordinary heads, then fixed heads (slice_of)
 };
 
@@ -649,7 +650,21 @@ __global__ __launch_bounds__(DQ_THREADS) __attribute__((amdgpu_waves_per_eu(3)))
         gf[dc] = L.qq < N ? ld8<T>(dO + (size_t)L.qq * HEAD_DIM + 16 * dc + 8 * L.hf) : zero8<T>();
     }
     const float lse2 = L.qq < N ? p.lse[(size_t)bh * N + L.qq] * LOG2E : INFINITY;
-    const float dsum = L.qq < N ? p.dsum[(size_t)bh * N + L.qq] : 0.0f;
+    float dsum;
+    if (p.dq_writes_dsum) {
+        // D_i = sum_c dO * O of this lane's query, from the dO fragments
+        // already in registers and O's matching columns.
+        const T* __restrict__ Orow = reinterpret_cast<const T*>(p.o) + base + (size_t)L.qq * HEAD_DIM;
+        float part = 0.0f;
+        if (L.qq < N) {
+#pragma unroll
+            for (int dc = 0; dc < 4; ++dc) part = dot8(ld8<T>(Orow + 16 * dc + 8 * L.hf), gf[dc], part);
+        }
+        dsum = pair_sum(part);
+        if (L.qq < N && L.hf == 0) p.dsum[(size_t)bh * N + L.qq] = dsum;
+    } else {
+        dsum = L.qq < N ? p.dsum[(size_t)bh * N + L.qq] : 0.0f;
+    }
 
     f32x16 dq[2];
 #pragma unroll
