@@ -17,12 +17,11 @@
 // exp(a[j] + r[i - j] - log Z(i)) with log Z from the forward's LSE and the
 // offsets' r values from an LDS band copied per tile.  dr needs sums along
 // the diagonals of each 32 x 32 block of dL: a wavefront writes the block
-// into its own LDS scratch (column-major, rows padded to 36 floats), then lane
-// d (0..62) walks diagonal d - 31 (address stride 37, so the 64 lanes hit 64
-// different banks) and adds the sum into the wavefront's ring of 256 floats
-// indexed by offset mod 256 (distinct lanes, distinct slots: no atomics; LDS
-// atomic adds per entry were six times slower than the whole rest of the
-// kernel).  Tile t touches offsets 64t - 127 .. 64t + 63, so once tile t is
+// into its own LDS scratch skewed so that each scratch row holds (parts of)
+// two diagonals (rows padded to 36 floats), sums the rows with 16-byte reads
+// and adds the diagonal sums into the wavefront's ring of 256 floats indexed
+// by offset mod 256 (distinct lanes, distinct slots: no atomics; LDS atomic
+// adds per entry were six times slower than the whole rest of the kernel).  Tile t touches offsets 64t - 127 .. 64t + 63, so once tile t is
 // done the offsets below 64(t+1) - 127 are final; the next tile stores their
 // sum over the four rings into the workgroup's own row of partial sums and
 // clears the slots, which the tile after it is the first to reuse.  Plain stores, no global atomics:
@@ -43,7 +42,7 @@ constexpr int PAT_BM = TILE_ROWS;  // queries per tile
 constexpr int PAT_THREADS = 256;
 constexpr int PAT_BAND = 192;    // r entries per tile (offsets 64t - 127 .. 64t + 64)
 constexpr int PAT_RING = 256;    // dr ring slots
-constexpr int PAT_SCR = 36;      // scratch column stride (floats): 16-byte aligned columns
+constexpr int PAT_SCR = 36;      // scratch row stride (floats): 16-byte aligned rows, conflict-free skewed writes
 static_assert(PAT_BM + PAT_BN - 1 <= PAT_BAND, "a tile's offsets fit in the band");
 static_assert(PAT_BAND + PAT_BM <= PAT_RING, "live offsets never share a ring slot");
 
@@ -74,6 +73,12 @@ __host__ __device__ inline int pat_chunks(int J, int N, int chunk_tiles) {
 // One query tile t (queries q0 .. q0+63, q0 = k0 + 64 t) against the
 // wavefront's 32 keys.  MASK: the tile meets the diagonal or runs past N.
 // scr: the wavefront's 32 x PAT_SCR scratch; ring: its 256 offset slots.
+//
+// Each 32 x 32 block of dL is written into the scratch skewed: entry (row r,
+// column c) goes to scratch row (r - c) mod 32, column c, so scratch row k
+// holds diagonal k in its columns c < 32 - k and diagonal k - 32 in the
+// rest.  Lane k (and lane k + 32, for the other half of the columns) then
+// reads its row with four 16-byte loads and splits the sum at column 32 - k.
 template <typename T, bool MASK>
 __device__ __forceinline__ void pat_tile(const T* gt, const float* rows, const float* band, float* scr, float* ring,
                                          int t, int q0, int k0, int w, int c, int hf, int lane, int N,
@@ -82,41 +87,52 @@ __device__ __forceinline__ void pat_tile(const T* gt, const float* rows, const f
     for (int rb = 0; rb < 2; ++rb) {
         // Rows of this block all precede the wavefront's first key.
         if (MASK && 2 * t + rb < w) continue;
+        // dP - D in one go: the accumulator starts at -D of its rows.
         f32x16 dp;
 #pragma unroll
-        for (int v = 0; v < 16; ++v) dp[v] = 0.0f;
+        for (int g = 0; g < 4; ++g) {
+            const f32x4 d4 = *reinterpret_cast<const f32x4*>(rows + PAT_BM + 32 * rb + 8 * g + 4 * hf);
+#pragma unroll
+            for (int u = 0; u < 4; ++u) dp[4 * g + u] = -d4[u];
+        }
 #pragma unroll
         for (int dc = 0; dc < 4; ++dc) mma(dp, ld_row<T>(gt, 32 * rb + c, 16 * dc + 8 * hf), vf[dc]);
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
             const f32x4 l4 = *reinterpret_cast<const f32x4*>(rows + 32 * rb + 8 * g + 4 * hf);
-            const f32x4 d4 = *reinterpret_cast<const f32x4*>(rows + PAT_BM + 32 * rb + 8 * g + 4 * hf);
-            f32x4 dl4;
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
                 const int v = 4 * g + u;
-                const int ql = 32 * rb + 8 * g + 4 * hf + u;        // query - q0
-                const int bi = ql - 32 * w - c + (PAT_BN - 1);       // band index of i - j
-                float pv = fast_exp2((a_key + band[bi] - l4[u]) * LOG2E);
-                if (MASK && (ql < 32 * w + c - 64 * t || q0 + ql >= N)) pv = 0.0f;
-                const float dl = pv * (dp[v] - d4[u]);
+                const int r = 8 * g + 4 * hf + u;                  // row within the block
+                const int bi = 32 * rb + r - 32 * w - c + (PAT_BN - 1);  // band index of i - j
+                float pv = fast_exp2((a_key - l4[u] + band[bi]) * LOG2E);
+                if (MASK && (32 * rb + r < 32 * w + c - 64 * t || q0 + 32 * rb + r >= N)) pv = 0.0f;
+                const float dl = pv * dp[v];
                 da_acc += dl;
-                dl4[u] = dl;
+                scr[((r - c) & 31) * PAT_SCR + c] = dl;
             }
-            // Block row 8g + 4hf + u of column c.
-            *reinterpret_cast<f32x4*>(scr + c * PAT_SCR + 8 * g + 4 * hf) = dl4;
         }
-        // Lane d sums block diagonal d - 31 (row - column); the wavefront's
-        // own LDS writes above are visible to its later reads.
-        const int d = lane - 31;
-        float sum = 0.0f;
+        // The wavefront's own LDS writes above are visible to its later reads.
+        const int k = lane & 31;
+        const int half = lane >> 5;  // columns 16 half .. 16 half + 15
+        const float* src = scr + k * PAT_SCR + 16 * half;
+        float s_lo = 0.0f, s_hi = 0.0f;  // diagonal k, diagonal k - 32
 #pragma unroll
-        for (int k = 0; k < 32; ++k) {
-            const int row = k + d;  // entry (row, column k)
-            if (row >= 0 && row < 32) sum += scr[k * PAT_SCR + row];
+        for (int q = 0; q < 4; ++q) {
+            const f32x4 x = *reinterpret_cast<const f32x4*>(src + 4 * q);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const bool lo = 16 * half + 4 * q + e < 32 - k;
+                s_lo += lo ? x[e] : 0.0f;
+                s_hi += lo ? 0.0f : x[e];
+            }
         }
+        s_lo += __shfl_xor(s_lo, 32);
+        s_hi += __shfl_xor(s_hi, 32);
+        // Lane k adds diagonal k, lane k + 32 diagonal k - 32 (k >= 1).
+        const int d = half ? k - 32 : k;
         const int delta = 64 * t + 32 * rb - 32 * w + d;
-        if (lane < 63 && delta >= 0) ring[delta & (PAT_RING - 1)] += sum;
+        if ((half == 0 || k > 0) && delta >= 0) ring[delta & (PAT_RING - 1)] += half ? s_hi : s_lo;
     }
 }
 
