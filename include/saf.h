@@ -224,9 +224,10 @@ saf_status_t saf_hybrid_attn_bwd_stage(saf_bwd_stage_t stage, saf_dtype_t dt,
  *   workspace : DEVICE, >= saf_hybrid_attn_bwd_pattern_workspace_bytes(),
  *               256-byte aligned, contents on entry ignored (about
  *               B * H * N^2 / 64 bytes: 25 MB at B = 8, H = 12, N = 4096).
- * Five launches: two zero fills, the row pre-pass D for the fixed heads, one
- * workgroup per (batch element, fixed head, block of 128 keys), and the
- * reduction of the partial sums.
+ * Three launches: the row pre-pass D for the fixed heads, one workgroup per
+ * (batch element, fixed head, block of 128 keys, chunk of query tiles), and
+ * the reduction of the partial sums, which also writes the ordinary heads'
+ * zeros (with no fixed head: two zero fills only).
  */
 size_t saf_hybrid_attn_bwd_pattern_workspace_bytes(saf_dtype_t dt, int B, int H, int N, int d);
 

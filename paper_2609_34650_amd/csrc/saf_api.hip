@@ -519,11 +519,12 @@ SAF_EXPORT saf_status_t saf_hybrid_attn_bwd_pattern(saf_dtype_t dt, const void* 
         return SAF_ERR_ALIGNMENT;
     if ((size_t)H * N > INT32_MAX || B > 65535 || workspace_bytes_given < pattern_workspace_bytes(B, H, N))
         return SAF_ERR_SHAPE;
-    const size_t n_out = (size_t)H * N;
-    hipLaunchKernelGGL(saf::pat_fill_kernel, dim3(fill_grid(n_out)), dim3(256), 0, stream, da, n_out);
-    hipLaunchKernelGGL(saf::pat_fill_kernel, dim3(fill_grid(n_out)), dim3(256), 0, stream, dr, n_out);
-    if (launched() != SAF_OK) return SAF_ERR_LAUNCH;
-    if (!pr.any_fixed) return SAF_OK;
+    if (!pr.any_fixed) {  // every row is an ordinary head's: zeros
+        const size_t n_out = (size_t)H * N;
+        hipLaunchKernelGGL(saf::pat_fill_kernel, dim3(fill_grid(n_out)), dim3(256), 0, stream, da, n_out);
+        hipLaunchKernelGGL(saf::pat_fill_kernel, dim3(fill_grid(n_out)), dim3(256), 0, stream, dr, n_out);
+        return launched();
+    }
     // D for the fixed heads: the row pre-pass with the ordinary heads masked out.
     const uint64_t all = H == 64 ? ~0ull : ((1ull << H) - 1);
     Problem inv = pr;
@@ -555,8 +556,12 @@ SAF_EXPORT saf_status_t saf_hybrid_attn_bwd_pattern(saf_dtype_t dt, const void* 
     pa.N = N;
     pa.ld_prior = ld_prior;
     pa.n_fixed = 0;
+    for (int h = 0; h < 64; ++h) pa.fixed_index[h] = 255;
     for (int h = 0; h < H; ++h)
-        if ((pr.fixed_mask >> h) & 1ull) pa.heads[pa.n_fixed++] = (unsigned char)h;
+        if ((pr.fixed_mask >> h) & 1ull) {
+            pa.fixed_index[h] = (unsigned char)pa.n_fixed;
+            pa.heads[pa.n_fixed++] = (unsigned char)h;
+        }
     pa.n_kblocks = geo.n_kblocks;
     const dim3 grid((unsigned)((size_t)pa.n_kblocks * B * pa.n_fixed), (unsigned)geo.n_chunks);
     if (dt == SAF_DTYPE_BF16)
@@ -564,8 +569,8 @@ SAF_EXPORT saf_status_t saf_hybrid_attn_bwd_pattern(saf_dtype_t dt, const void* 
     else
         hipLaunchKernelGGL(saf::bwd_pattern_kernel<float>, grid, dim3(saf::PAT_THREADS), 0, stream, pa);
     if (launched() != SAF_OK) return SAF_ERR_LAUNCH;
-    const dim3 rgrid((unsigned)((size_t)pa.n_fixed * ((N + 255) / 256)), (unsigned)B);
-    hipLaunchKernelGGL(saf::pat_reduce_kernel, rgrid, dim3(256), 0, stream, pa);
+    const unsigned rgrid = (unsigned)((size_t)H * ((N + saf::PRED_X - 1) / saf::PRED_X));
+    hipLaunchKernelGGL(saf::pat_reduce_kernel, dim3(rgrid), dim3(256), 0, stream, pa);
     return launched();
 }
 

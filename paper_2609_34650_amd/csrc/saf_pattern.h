@@ -30,7 +30,8 @@
 // rows over batch elements and key blocks (and the da partials over batch
 // elements).  The dO tile, the tile's LSE and D rows and the r band are
 // copied by buffer loads straight to LDS (rows or offsets outside 0 .. N-1
-// arrive as 0 and are masked), double-buffered over tiles.
+// arrive as 0 and are masked), double-buffered over tiles.  A second kernel
+// sums the partial rows (and writes the ordinary heads' zeros).
 #pragma once
 
 #include "saf_common.h"
@@ -62,6 +63,7 @@ struct PatArgs {
     int n_chunks;        // chunks of the longest key block (the grid's y extent)
     int part_len;        // 64 * chunk_tiles + 127: offsets one chunk touches
     unsigned char heads[64];  // the fixed heads
+    unsigned char fixed_index[64];  // head -> its index in heads, or 255 for an ordinary head
 };
 
 // Query tiles of key block J, and its chunks.
@@ -254,36 +256,61 @@ __global__ __launch_bounds__(PAT_THREADS) void bwd_pattern_kernel(PatArgs p) {
     if (hf == 0 && key < N) p.da_part[(part * p.n_chunks + chunk) * N + key] = da_key;
 }
 
-// da[h][j] += sum over the chunks of j's key block of da_part, and
-// dr[h][delta] += sum over the key blocks J with 128 J <= N - 1 - delta, and
-// over the (one or two) chunks of J whose offsets include delta, of dr_part;
-// for one batch element (blockIdx.y) per thread, added atomically into the
-// zeroed outputs.  Consecutive threads read consecutive addresses.
+// da[h][j] = sum over batch elements and over the chunks of j's key block of
+// da_part; dr[h][delta] = sum over batch elements, over the key blocks J with
+// 128 J <= N - 1 - delta and over the (one or two) chunks of J whose offsets
+// include delta, of dr_part.  Workgroup = (head, 32 positions): eight groups
+// of 32 threads take every eighth (batch element, key block) pair (and
+// (batch element, chunk) pair), then group 0 adds the eight partial sums in
+// a fixed order and stores the result, so the output does not depend on
+// scheduling.  Rows of ordinary heads get zeros.  Consecutive threads read
+// consecutive addresses.
+constexpr int PRED_X = 32;                // positions per workgroup
+constexpr int PRED_G = 256 / PRED_X;      // thread groups per position
+
 __global__ __launch_bounds__(256) void pat_reduce_kernel(PatArgs p) {
-    const int per_head = (p.N + 255) / 256;
-    const int hidx = (int)(blockIdx.x / per_head);
-    const int x = (int)(blockIdx.x % per_head) * 256 + (int)threadIdx.x;
-    if (x >= p.N) return;
-    const int b = (int)blockIdx.y;
-    const int h = p.heads[hidx];
+    __shared__ float red[2][PRED_G][PRED_X];
+    const int per_head = (p.N + PRED_X - 1) / PRED_X;
+    const int h = (int)(blockIdx.x / per_head);
+    const int xl = (int)threadIdx.x % PRED_X;
+    const int jg = (int)threadIdx.x / PRED_X;
+    const int x = (int)(blockIdx.x % per_head) * PRED_X + xl;
     const int N = p.N;
-    const int cq = PAT_BM * p.chunk_tiles;  // queries per chunk
-    const size_t part = (size_t)(b * p.n_fixed + hidx);
-    float sa = 0.0f;
-    const int nc_key = pat_chunks(x / PAT_BN, N, p.chunk_tiles);
-    for (int ch = 0; ch < nc_key; ++ch) sa += p.da_part[(part * p.n_chunks + ch) * N + x];
-    float sr = 0.0f;
-    const int j_max = (N - 1 - x) / PAT_BN;  // key blocks that reach offset x
-    const int ca = x / cq;                  // the chunk whose own queries give offset x
-    for (int J = 0; J <= j_max; ++J) {
-        const int nc = pat_chunks(J, N, p.chunk_tiles);
-        const float* rows = p.dr_part + (part * p.n_kblocks + J) * p.n_chunks * (size_t)p.part_len;
-        if (ca < nc) sr += rows[(size_t)ca * p.part_len + (x - (cq * ca - (PAT_BN - 1)))];
-        if (ca + 1 < nc && x >= cq * (ca + 1) - (PAT_BN - 1))
-            sr += rows[(size_t)(ca + 1) * p.part_len + (x - (cq * (ca + 1) - (PAT_BN - 1)))];
+    const int hidx = p.fixed_index[h];
+    float sa = 0.0f, sr = 0.0f;
+    if (hidx < p.n_fixed && x < N) {
+        const int cq = PAT_BM * p.chunk_tiles;  // queries per chunk
+        const int nc_key = pat_chunks(x / PAT_BN, N, p.chunk_tiles);
+        const int n_j = (N - 1 - x) / PAT_BN + 1;  // key blocks that reach offset x
+        const int ca = x / cq;                    // the chunk whose own queries give offset x
+        for (int q = jg; q < p.B * nc_key; q += PRED_G) {
+            const size_t part = (size_t)((q / nc_key) * p.n_fixed + hidx);
+            sa += p.da_part[(part * p.n_chunks + q % nc_key) * N + x];
+        }
+#pragma unroll 4
+        for (int q = jg; q < p.B * n_j; q += PRED_G) {
+            const int J = q % n_j;
+            const size_t part = (size_t)((q / n_j) * p.n_fixed + hidx);
+            const int nc = pat_chunks(J, N, p.chunk_tiles);
+            const float* rows = p.dr_part + (part * p.n_kblocks + J) * p.n_chunks * (size_t)p.part_len;
+            if (ca < nc) sr += rows[(size_t)ca * p.part_len + (x - (cq * ca - (PAT_BN - 1)))];
+            if (ca + 1 < nc && x >= cq * (ca + 1) - (PAT_BN - 1))
+                sr += rows[(size_t)(ca + 1) * p.part_len + (x - (cq * (ca + 1) - (PAT_BN - 1)))];
+        }
     }
-    atomicAdd(p.da + (size_t)h * N + x, sa);
-    atomicAdd(p.dr + (size_t)h * N + x, sr);
+    red[0][jg][xl] = sa;
+    red[1][jg][xl] = sr;
+    __syncthreads();
+    if (jg == 0 && x < N) {
+        float ta = 0.0f, tr = 0.0f;
+#pragma unroll
+        for (int g = 0; g < PRED_G; ++g) {
+            ta += red[0][g][xl];
+            tr += red[1][g][xl];
+        }
+        p.da[(size_t)h * N + x] = ta;
+        p.dr[(size_t)h * N + x] = tr;
+    }
 }
 
 __global__ void pat_fill_kernel(float* p, size_t n) {

@@ -75,3 +75,21 @@ def test_pattern_gradient_124m_shape():
     announce(f"pattern grad 124m shape B=2 fixed={fixed}")
     g, o, is_fixed = _run("bf16", 2, w.H, w.N, fixed, stream_id=32)
     _check("bf16", g, o, is_fixed)
+
+
+def test_pattern_gradient_is_deterministic():
+    """The partial sums are added in a fixed order: two calls give the same
+    bits, and ordinary heads' rows are zeros even over stale outputs."""
+    torch = torch_cuda()
+    from paper_2609_34650_amd import binding, inputs
+    announce("pattern grad determinism")
+    inp = inputs.make_inputs(3, 4, 700, 64, [0, 2], "bf16", stream_id=33)
+    t = to_device(inp, "bf16")
+    O, LSE = binding.saf_hybrid_attn_fwd(t["Q"], t["K"], t["V"], t["is_fixed"], t["a"], t["r"])
+    da1, dr1 = binding.saf_hybrid_attn_bwd_pattern(t["V"], O, t["dO"], LSE, t["is_fixed"], t["a"], t["r"])
+    da2 = torch.full_like(da1, 7.0)
+    dr2 = torch.full_like(dr1, 7.0)
+    binding.saf_hybrid_attn_bwd_pattern(t["V"], O, t["dO"], LSE, t["is_fixed"], t["a"], t["r"], da=da2, dr=dr2)
+    torch.cuda.synchronize()
+    assert torch.equal(da1, da2) and torch.equal(dr1, dr2)
+    assert not da2[[1, 3]].any() and not dr2[[1, 3]].any()
