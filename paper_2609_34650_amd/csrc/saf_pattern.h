@@ -81,10 +81,13 @@ __host__ __device__ inline int pat_chunks(int J, int N, int chunk_tiles) {
 // holds diagonal k in its columns c < 32 - k and diagonal k - 32 in the
 // rest.  Lane k (and lane k + 32, for the other half of the columns) then
 // reads its row with four 16-byte loads and splits the sum at column 32 - k.
+// w_lo[e]: 1 if column 16 (lane / 32) + e of scratch row lane % 32 holds
+// the row's first diagonal, else 0 (fixed per lane).
 template <typename T, bool MASK>
 __device__ __forceinline__ void pat_tile(const T* gt, const float* rows, const float* band, float* scr, float* ring,
                                          int t, int q0, int k0, int w, int c, int hf, int lane, int N,
-                                         const typename Vec<T>::x8 (&vf)[4], float a_key, float& da_acc) {
+                                         const typename Vec<T>::x8 (&vf)[4], const float (&w_lo)[16], float a_key,
+                                         float& da_acc) {
 #pragma unroll
     for (int rb = 0; rb < 2; ++rb) {
         // Rows of this block all precede the wavefront's first key.
@@ -118,17 +121,17 @@ __device__ __forceinline__ void pat_tile(const T* gt, const float* rows, const f
         const int k = lane & 31;
         const int half = lane >> 5;  // columns 16 half .. 16 half + 15
         const float* src = scr + k * PAT_SCR + 16 * half;
-        float s_lo = 0.0f, s_hi = 0.0f;  // diagonal k, diagonal k - 32
+        float s_lo = 0.0f, s_all = 0.0f;  // diagonal k; both diagonals
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             const f32x4 x = *reinterpret_cast<const f32x4*>(src + 4 * q);
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                const bool lo = 16 * half + 4 * q + e < 32 - k;
-                s_lo += lo ? x[e] : 0.0f;
-                s_hi += lo ? 0.0f : x[e];
+                s_lo = fmaf(x[e], w_lo[4 * q + e], s_lo);
+                s_all += x[e];
             }
         }
+        float s_hi = s_all - s_lo;  // diagonal k - 32
         s_lo += __shfl_xor(s_lo, 32);
         s_hi += __shfl_xor(s_hi, 32);
         // Lane k adds diagonal k, lane k + 32 diagonal k - 32 (k >= 1).
@@ -179,6 +182,9 @@ __global__ __launch_bounds__(PAT_THREADS) void bwd_pattern_kernel(PatArgs p) {
 #pragma unroll
     for (int dc = 0; dc < 4; ++dc) vf[dc] = key < N ? ld8<T>(V + (size_t)key * HEAD_DIM + 16 * dc + 8 * hf) : zero8<T>();
     const float a_key = key < N ? arow[key] : -INFINITY;
+    float w_lo[16];
+#pragma unroll
+    for (int e = 0; e < 16; ++e) w_lo[e] = 16 * (lane >> 5) + e < 32 - (lane & 31) ? 1.0f : 0.0f;
 
     const __amdgpu_buffer_rsrc_t rg = slice_rsrc<T>(reinterpret_cast<const T*>(p.dO) + slice * HEAD_DIM, N);
     const __amdgpu_buffer_rsrc_t rl =
@@ -232,7 +238,7 @@ __global__ __launch_bounds__(PAT_THREADS) void bwd_pattern_kernel(PatArgs p) {
         constexpr int B_ = decltype(buf)::value;
         if (t > t0) flush(PAT_BM * t - (PAT_BM + PAT_BN - 1), PAT_BM);  // final after tile t-1
         pat_tile<T, decltype(mask)::value>(B_ ? g1 : g0, B_ ? rows1 : rows0, B_ ? band1 : band0, scratch[w],
-                                           ring[w], t, k0 + PAT_BM * t, k0, w, c, hf, lane, N, vf, a_key, da_acc);
+                                           ring[w], t, k0 + PAT_BM * t, k0, w, c, hf, lane, N, vf, w_lo, a_key, da_acc);
     };
     // Tiles in order.  run_slots wants the masked slots first, so a ragged
     // last tile gets a masked pass of its own after the others.
