@@ -265,13 +265,12 @@ __global__ __launch_bounds__(PAT_THREADS) void bwd_pattern_kernel(PatArgs p) {
 // da[h][j] = sum over batch elements and over the chunks of j's key block of
 // da_part; dr[h][delta] = sum over batch elements, over the key blocks J with
 // 128 J <= N - 1 - delta and over the (one or two) chunks of J whose offsets
-// include delta, of dr_part.  Workgroup = (head, 32 positions): eight groups
-// of 32 threads take every eighth (batch element, key block) pair (and
-// (batch element, chunk) pair), then group 0 adds the eight partial sums in
-// a fixed order and stores the result, so the output does not depend on
-// scheduling.  Rows of ordinary heads get zeros.  Consecutive threads read
+// include delta, of dr_part.  Workgroup = (head, 8 positions): 32 groups
+// of 8 threads take every 32nd key block (and chunk) of every batch
+// element, then group 0 adds the 32 partial sums in a fixed order and
+// stores the result, so the output does not depend on scheduling.  Rows of ordinary heads get zeros.  Consecutive threads read
 // consecutive addresses.
-constexpr int PRED_X = 32;                // positions per workgroup
+constexpr int PRED_X = 8;                 // positions per workgroup
 constexpr int PRED_G = 256 / PRED_X;      // thread groups per position
 
 __global__ __launch_bounds__(256) void pat_reduce_kernel(PatArgs p) {
@@ -289,19 +288,20 @@ __global__ __launch_bounds__(256) void pat_reduce_kernel(PatArgs p) {
         const int nc_key = pat_chunks(x / PAT_BN, N, p.chunk_tiles);
         const int n_j = (N - 1 - x) / PAT_BN + 1;  // key blocks that reach offset x
         const int ca = x / cq;                    // the chunk whose own queries give offset x
-        for (int q = jg; q < p.B * nc_key; q += PRED_G) {
-            const size_t part = (size_t)((q / nc_key) * p.n_fixed + hidx);
-            sa += p.da_part[(part * p.n_chunks + q % nc_key) * N + x];
-        }
-#pragma unroll 4
-        for (int q = jg; q < p.B * n_j; q += PRED_G) {
-            const int J = q % n_j;
-            const size_t part = (size_t)((q / n_j) * p.n_fixed + hidx);
-            const int nc = pat_chunks(J, N, p.chunk_tiles);
-            const float* rows = p.dr_part + (part * p.n_kblocks + J) * p.n_chunks * (size_t)p.part_len;
-            if (ca < nc) sr += rows[(size_t)ca * p.part_len + (x - (cq * ca - (PAT_BN - 1)))];
-            if (ca + 1 < nc && x >= cq * (ca + 1) - (PAT_BN - 1))
-                sr += rows[(size_t)(ca + 1) * p.part_len + (x - (cq * (ca + 1) - (PAT_BN - 1)))];
+        const int c0 = ca * p.chunk_tiles;  // first tile of chunk ca
+        const int c1 = c0 + p.chunk_tiles;  // first tile of chunk ca + 1
+        for (int b = 0; b < p.B; ++b) {
+            const size_t part = (size_t)(b * p.n_fixed + hidx);
+            for (int ch = jg; ch < nc_key; ch += PRED_G) sa += p.da_part[(part * p.n_chunks + ch) * N + x];
+            const float* rows_b = p.dr_part + part * p.n_kblocks * p.n_chunks * (size_t)p.part_len;
+#pragma unroll 2
+            for (int J = jg; J < n_j; J += PRED_G) {
+                const int tiles = (N - J * PAT_BN + PAT_BM - 1) / PAT_BM;  // chunk ch exists iff ch * chunk_tiles < tiles
+                const float* rows = rows_b + (size_t)J * p.n_chunks * p.part_len;
+                if (c0 < tiles) sr += rows[(size_t)ca * p.part_len + (x - (cq * ca - (PAT_BN - 1)))];
+                if (c1 < tiles && x >= cq * (ca + 1) - (PAT_BN - 1))
+                    sr += rows[(size_t)(ca + 1) * p.part_len + (x - (cq * (ca + 1) - (PAT_BN - 1)))];
+            }
         }
     }
     red[0][jg][xl] = sa;
