@@ -268,8 +268,8 @@ __global__ __launch_bounds__(PAT_THREADS) void bwd_pattern_kernel(PatArgs p) {
 // include delta, of dr_part.  Workgroup = (head, 8 positions): 32 groups
 // of 8 threads take every 32nd key block (and chunk) of every batch
 // element, then group 0 adds the 32 partial sums in a fixed order and
-// stores the result, so the output does not depend on scheduling.  Rows of ordinary heads get zeros.  Consecutive threads read
-// consecutive addresses.
+// stores the result, so the output does not depend on scheduling.  Rows of
+// ordinary heads get zeros.  Consecutive threads read consecutive addresses.
 constexpr int PRED_X = 8;                 // positions per workgroup
 constexpr int PRED_G = 256 / PRED_X;      // thread groups per position
 
