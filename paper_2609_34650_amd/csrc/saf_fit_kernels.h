@@ -156,10 +156,28 @@ __global__ void fit_init_kernel(FitArgs p) {
 // The block's rho and alpha values (offsets and keys i - j for its rows and
 // columns: 511 of each) and its rows' log Z are staged in LDS first, so the
 // walk reads consecutive LDS words across a wavefront.
+//
+// Factorised form (no exponential per entry): with A and R the maxima of
+// alpha and rho over the values the block touches, P(i, j) = ea(j) er(i - j)
+// w(i), ea = exp(alpha - A), er = exp(rho - R), w(i) = exp(A + R - log Z(i)),
+// so column j's sum is ea(j) sum_i er(i - j) w(i) and diagonal d's sum is
+// er(d) sum_i ea(i - d) w(i): two multiply-adds per row, with ea, er and w
+// staged in LDS instead of the raw values (entries at negative positions are
+// 0, which masks i < j).  Every term is at most 1, so ea and er cannot
+// overflow; w can, when a row's log Z lies far below A + R, and a block with
+// such a row (more than FAST_GUARD below) evaluates every entry exactly.
+// In the factorised form each staged array is kept as four copies, copy m
+// shifted by m entries, so that a lane's four consecutive entries (whose
+// alignment is fixed per lane) are one aligned 16-byte read; the copies sit
+// FIT_STAGE floats apart (a stride that keeps those reads free of bank
+// conflicts).  The exact form uses copy 0 only.
+constexpr int FIT_STAGE = 2 * FIT_COLS + 16;
+
 __global__ __launch_bounds__(FIT_COLS) void fit_marginals_kernel(FitArgs p) {
-    __shared__ float rs[2 * FIT_COLS];
-    __shared__ float as[2 * FIT_COLS];
-    __shared__ float zs[FIT_ROWS];
+    __shared__ __attribute__((aligned(16))) float rs[4 * FIT_STAGE];
+    __shared__ __attribute__((aligned(16))) float as[4 * FIT_STAGE];
+    __shared__ __attribute__((aligned(16))) float zs[FIT_ROWS];
+    __shared__ float red[4];
     const int per_head = p.n_rchunks * p.n_cgroups;
     const int h = (int)(blockIdx.x / per_head);
     const int rem = (int)(blockIdx.x % per_head);
@@ -169,44 +187,105 @@ __global__ __launch_bounds__(FIT_COLS) void fit_marginals_kernel(FitArgs p) {
     const int T = p.T;
     const int tid = (int)threadIdx.x;
     const int j = j_first + tid;
+    const bool col_ok = j < T;
     const float* __restrict__ al = p.alpha + (size_t)h * T;
     const float* __restrict__ rh = p.rho + (size_t)h * T;
     const float* __restrict__ lz = p.logz + (size_t)h * T;
     // Staged index x holds position base + x, base = i0 - j_first - (FIT_COLS - 1).
     const int base = i0 - j_first - (FIT_COLS - 1);
+    float rv[2], av[2];
+    bool in[2];
+    float am = col_ok ? al[j] : -INFINITY, rm = col_ok ? rh[j] : -INFINITY;
 #pragma unroll
     for (int k = 0; k < 2; ++k) {
-        const int x = tid + FIT_COLS * k;
-        const int q = base + x;
-        const bool in = q >= 0 && q < T;
-        rs[x] = in ? rh[q] : 0.0f;
-        as[x] = in ? al[q] : 0.0f;
+        const int q = base + tid + FIT_COLS * k;
+        in[k] = q >= 0 && q < T;
+        rv[k] = in[k] ? rh[q] : 0.0f;
+        av[k] = in[k] ? al[q] : 0.0f;
+        if (in[k]) {
+            am = fmaxf(am, av[k]);
+            rm = fmaxf(rm, rv[k]);
+        }
     }
-    zs[tid] = i0 + tid < T ? lz[i0 + tid] : 0.0f;
-    __syncthreads();
-    if (j >= T) return;
-    const int n_rows = min(FIT_ROWS, T - i0);
-    const float aj = al[j] * LOG2E;  // column j's alpha
-    const float rj = rh[j] * LOG2E;  // diagonal j's rho
+    const bool row_ok = i0 + tid < T;
+    const float zv = row_ok ? lz[i0 + tid] : 0.0f;
+    const float A = block_max(am, red);
+    const float R = block_max(rm, red);
+    const bool fast = __syncthreads_and(!row_ok || A + R - zv <= FAST_GUARD);
+    const float aj = col_ok ? al[j] : 0.0f;  // column j's alpha
+    const float rj = col_ok ? rh[j] : 0.0f;  // diagonal j's rho
     const int off = j_first - j + (FIT_COLS - 1);  // staged index of position i - j is (i - i0) + off
     const int r_beg = max(0, j - i0);               // rows i >= j
-    float c0 = 0.0f, c1 = 0.0f, d0 = 0.0f, d1 = 0.0f;
-    int r = r_beg;
-    for (; r + 2 <= n_rows; r += 2) {
-        const float z0 = zs[r] * LOG2E, z1 = zs[r + 1] * LOG2E;
-        c0 += fast_exp2(fmaf(rs[r + off], LOG2E, aj - z0));
-        c1 += fast_exp2(fmaf(rs[r + 1 + off], LOG2E, aj - z1));
-        d0 += fast_exp2(fmaf(as[r + off], LOG2E, rj - z0));
-        d1 += fast_exp2(fmaf(as[r + 1 + off], LOG2E, rj - z1));
+    float c = 0.0f, d = 0.0f;
+    if (fast) {
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+            const int x = tid + FIT_COLS * k;
+            const float er = in[k] ? fast_exp2((rv[k] - R) * LOG2E) : 0.0f;
+            const float ea = in[k] ? fast_exp2((av[k] - A) * LOG2E) : 0.0f;
+#pragma unroll
+            for (int m = 0; m < 4; ++m)
+                if (x >= m) {
+                    rs[m * FIT_STAGE + x - m] = er;
+                    as[m * FIT_STAGE + x - m] = ea;
+                }
+        }
+        zs[tid] = row_ok ? fast_exp2((A + R - zv) * LOG2E) : 0.0f;
+        __syncthreads();
+        if (!col_ok) return;
+        // Rows from r_beg rounded down to a multiple of 4 (the rows below
+        // r_beg meet staged zeros); rows past T have w = 0.  Entry r + off
+        // of the staged arrays is entry r + off - m of copy m, m = off mod 4.
+        const int m = off & 3;
+        const float* rsm = rs + m * FIT_STAGE + off - m;
+        const float* asm_ = as + m * FIT_STAGE + off - m;
+        float c1 = 0.0f, d1 = 0.0f;
+        for (int r = r_beg & ~3; r < FIT_ROWS; r += 4) {
+            const f32x4 w4 = *reinterpret_cast<const f32x4*>(zs + r);
+            const f32x4 e4 = *reinterpret_cast<const f32x4*>(rsm + r);
+            const f32x4 a4 = *reinterpret_cast<const f32x4*>(asm_ + r);
+            c = fmaf(e4[0], w4[0], c);
+            d = fmaf(a4[0], w4[0], d);
+            c1 = fmaf(e4[1], w4[1], c1);
+            d1 = fmaf(a4[1], w4[1], d1);
+            c = fmaf(e4[2], w4[2], c);
+            d = fmaf(a4[2], w4[2], d);
+            c1 = fmaf(e4[3], w4[3], c1);
+            d1 = fmaf(a4[3], w4[3], d1);
+        }
+        c = (c + c1) * fast_exp2((aj - A) * LOG2E);
+        d = (d + d1) * fast_exp2((rj - R) * LOG2E);
+    } else {
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+            rs[tid + FIT_COLS * k] = rv[k];
+            as[tid + FIT_COLS * k] = av[k];
+        }
+        zs[tid] = zv;
+        __syncthreads();
+        if (!col_ok) return;
+        const int n_rows = min(FIT_ROWS, T - i0);
+        const float aj2 = aj * LOG2E, rj2 = rj * LOG2E;
+        float c1 = 0.0f, d1 = 0.0f;
+        int r = r_beg;
+        for (; r + 2 <= n_rows; r += 2) {
+            const float z0 = zs[r] * LOG2E, z1 = zs[r + 1] * LOG2E;
+            c += fast_exp2(fmaf(rs[r + off], LOG2E, aj2 - z0));
+            c1 += fast_exp2(fmaf(rs[r + 1 + off], LOG2E, aj2 - z1));
+            d += fast_exp2(fmaf(as[r + off], LOG2E, rj2 - z0));
+            d1 += fast_exp2(fmaf(as[r + 1 + off], LOG2E, rj2 - z1));
+        }
+        if (r < n_rows) {
+            const float z0 = zs[r] * LOG2E;
+            c += fast_exp2(fmaf(rs[r + off], LOG2E, aj2 - z0));
+            d += fast_exp2(fmaf(as[r + off], LOG2E, rj2 - z0));
+        }
+        c += c1;
+        d += d1;
     }
-    if (r < n_rows) {
-        const float z0 = zs[r] * LOG2E;
-        c0 += fast_exp2(fmaf(rs[r + off], LOG2E, aj - z0));
-        d0 += fast_exp2(fmaf(as[r + off], LOG2E, rj - z0));
-    }
-    if (r_beg < n_rows) {
-        atomicAdd(p.col + (size_t)h * T + j, c0 + c1);
-        atomicAdd(p.diag + (size_t)h * T + j, d0 + d1);
+    if (r_beg < min(FIT_ROWS, T - i0)) {
+        atomicAdd(p.col + (size_t)h * T + j, c);
+        atomicAdd(p.diag + (size_t)h * T + j, d);
     }
 }
 
