@@ -105,23 +105,6 @@ __device__ __forceinline__ void st4(T* p, float x0, float x1, float x2, float x3
     *reinterpret_cast<typename Vec<T>::x4*>(p) = v;
 }
 
-template <typename T>
-__device__ __forceinline__ void st2(T* p, T x0, T x1) {
-    typename Vec<T>::x2 v;
-    v[0] = x0;
-    v[1] = x1;
-    *reinterpret_cast<typename Vec<T>::x2*>(p) = v;
-}
-
-// Position of row/key k of a 64-wide tile inside a transposed LDS tile.
-// Bits 2 and 3 are swapped, so that in each 16-wide group the eight keys
-// {4*hf + u, 8 + 4*hf + u : u = 0..3} -- the keys that lane half hf holds in
-// an accumulator (rows 8*g + 4*hf + u) -- sit at eight consecutive positions
-// 8*hf .. 8*hf + 7 and one 16-byte LDS read fetches them.
-__device__ __forceinline__ int tpos(int k) {
-    return (k & ~12) | ((k & 4) << 1) | ((k & 8) >> 1);
-}
-
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // IEEE maximum (NaN-propagating): lowers to v_maximum3_f32 chains with no
@@ -338,121 +321,6 @@ __device__ __forceinline__ void st_unit_scaled(float* dst, const u32x4& a, float
 #pragma unroll
     for (int m = 0; m < 4; ++m) o[m] = __float_as_uint(__uint_as_float(a[m]) * e);
     *reinterpret_cast<u32x4*>(dst) = o;
-}
-
-// Transposed operand from a row-major LDS tile (element stride ld): the A
-// operand whose row m is tile column col0 + m and whose k-slot t of lane half
-// hf is tile row
-//   row0 + 8*(t/4) + 4*hf + (t%4)   (ACC_ORDER: the order in which an MFMA
-//                                     accumulator holds its rows), or
-//   row0 + 8*hf + t                 (natural order).
-// bf16: two ds_read_b64_tr_b16.  Within each 16-lane group that instruction
-// hands lane 4a+b element b of the 8-byte chunks addressed by lanes a, a+4,
-// a+8 and a+12, so lane i of a group addresses tile row (slot base + i/4) at
-// column col0 + 16*(group parity) + 4*(i%4) and receives four k-slots of its
-// own column.  float32: eight scalar LDS reads.
-typedef __attribute__((ext_vector_type(4))) short s16x4;
-typedef __attribute__((ext_vector_type(8))) short s16x8;
-typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
-
-template <bool ACC_ORDER>
-__device__ __forceinline__ bf16x8 ld_t(const bf16* tile, int ld, int row0, int col0) {
-    const int l = threadIdx.x & 63;
-    const int i = l & 15;
-    const int hf = l >> 5;
-    const int gp = (l >> 4) & 1;
-    const int r = row0 + (ACC_ORDER ? 4 * hf : 8 * hf) + (i >> 2);
-    const bf16* p = tile + r * ld + col0 + 16 * gp + 4 * (i & 3);
-    const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p));
-    const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p + (ACC_ORDER ? 8 : 4) * ld));
-    const s16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-    return __builtin_bit_cast(bf16x8, v);
-}
-template <bool ACC_ORDER>
-__device__ __forceinline__ f32x8 ld_t(const float* tile, int ld, int row0, int col0) {
-    const int l = threadIdx.x & 63;
-    const int c = l & 31;
-    const int hf = l >> 5;
-    f32x8 v;
-#pragma unroll
-    for (int t = 0; t < 8; ++t) {
-        const int r = row0 + (ACC_ORDER ? 8 * (t >> 2) + 4 * hf + (t & 3) : 8 * hf + t);
-        v[t] = tile[r * ld + col0 + c];
-    }
-    return v;
-}
-
-// Row-major store of eight consecutive values scaled by e (rounded once).
-__device__ __forceinline__ void st8_scaled(bf16* dst, const bf16x8& x, float e) {
-    const u32x4 a = __builtin_bit_cast(u32x4, x);
-    u32x4 o;
-#pragma unroll
-    for (int m = 0; m < 4; ++m)
-        o[m] = pack_bf16(__uint_as_float(a[m] << 16) * e, __uint_as_float(a[m] & 0xffff0000u) * e);
-    *reinterpret_cast<u32x4*>(dst) = o;
-}
-__device__ __forceinline__ void st8_scaled(float* dst, const f32x8& x, float e) {
-    *reinterpret_cast<f32x8*>(dst) = x * e;
-}
-
-// Transposed store of two consecutive rows x0, x1 (eight consecutive columns
-// each): dst[t * ld] = (x0[t], x1[t]) as an adjacent pair, t = 0..7.  The bf16
-// version packs the halves of 32-bit words with v_perm_b32 (no per-element
-// vector shuffles, which the compiler would route through scratch memory).
-__device__ __forceinline__ void st_pair_t(bf16* dst, int ld, const bf16x8& x0, const bf16x8& x1) {
-    const u32x4 a = __builtin_bit_cast(u32x4, x0);
-    const u32x4 b = __builtin_bit_cast(u32x4, x1);
-#pragma unroll
-    for (int m = 0; m < 4; ++m) {
-        *reinterpret_cast<unsigned int*>(dst + (2 * m) * ld) = __builtin_amdgcn_perm(b[m], a[m], 0x05040100u);
-        *reinterpret_cast<unsigned int*>(dst + (2 * m + 1) * ld) = __builtin_amdgcn_perm(b[m], a[m], 0x07060302u);
-    }
-}
-__device__ __forceinline__ void st_pair_t(float* dst, int ld, const f32x8& x0, const f32x8& x1) {
-#pragma unroll
-    for (int t = 0; t < 8; ++t) {
-        const f32x2 v = {x0[t], x1[t]};
-        *reinterpret_cast<f32x2*>(dst + t * ld) = v;
-    }
-}
-
-// As st_pair_t, with row x0 scaled by e0 and row x1 by e1 (rounded once).
-__device__ __forceinline__ void st_pair_t_scaled(bf16* dst, int ld, const bf16x8& x0, const bf16x8& x1, float e0,
-                                                 float e1) {
-    const u32x4 a = __builtin_bit_cast(u32x4, x0);
-    const u32x4 b = __builtin_bit_cast(u32x4, x1);
-#pragma unroll
-    for (int m = 0; m < 4; ++m) {
-        const float a_lo = __uint_as_float(a[m] << 16), a_hi = __uint_as_float(a[m] & 0xffff0000u);
-        const float b_lo = __uint_as_float(b[m] << 16), b_hi = __uint_as_float(b[m] & 0xffff0000u);
-        *reinterpret_cast<unsigned int*>(dst + (2 * m) * ld) = pack_bf16(a_lo * e0, b_lo * e1);
-        *reinterpret_cast<unsigned int*>(dst + (2 * m + 1) * ld) = pack_bf16(a_hi * e0, b_hi * e1);
-    }
-}
-__device__ __forceinline__ void st_pair_t_scaled(float* dst, int ld, const f32x8& x0, const f32x8& x1, float e0,
-                                                 float e1) {
-#pragma unroll
-    for (int t = 0; t < 8; ++t) {
-        const f32x2 v = {x0[t] * e0, x1[t] * e1};
-        *reinterpret_cast<f32x2*>(dst + t * ld) = v;
-    }
-}
-
-// Sum of the eight operand values: for bf16 the rounded values that enter
-// the product (four packed dot products against ones), for float32 plain adds.
-__device__ __forceinline__ float sum8(const bf16x8& x, float acc) {
-    const bf16x2 one = {(bf16)1.0f, (bf16)1.0f};
-#pragma unroll
-    for (int t = 0; t < 8; t += 2) {
-        const bf16x2 pr = {x[t], x[t + 1]};
-        acc = __builtin_amdgcn_fdot2_f32_bf16(pr, one, acc, false);
-    }
-    return acc;
-}
-__device__ __forceinline__ float sum8(const f32x8& x, float acc) {
-#pragma unroll
-    for (int t = 0; t < 8; ++t) acc += x[t];
-    return acc;
 }
 
 // acc + sum_t x[t] * y[t] over eight operand values.
