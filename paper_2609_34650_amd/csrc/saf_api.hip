@@ -110,7 +110,7 @@ saf_status_t launch_fwd(const saf::FwdArgs& args, hipStream_t stream) {
         for (int h = 0; h < args.H; ++h)
             if ((args.fixed_mask >> h) & 1ull) na.heads[na.n_fixed++] = (unsigned char)h;
         const unsigned ngrid = (unsigned)((size_t)na.n_rblocks * na.n_fixed);
-        hipLaunchKernelGGL(saf::fixed_lse_kernel, dim3(ngrid), dim3(saf::NORM_THREADS), 0, stream, na);
+        hipLaunchKernelGGL(saf::fixed_lse_kernel<1>, dim3(ngrid), dim3(saf::NORM_THREADS), 0, stream, na);
         if (launched() != SAF_OK) return SAF_ERR_LAUNCH;
     }
     const unsigned grid = (unsigned)((size_t)args.n_qblocks * args.B * args.H);
@@ -370,7 +370,7 @@ SAF_EXPORT saf_status_t saf_hybrid_attn_fwd_gqa(saf_dtype_t dt, const void* Q, c
         for (int h = 0; h < Hq; ++h)
             if ((mask >> h) & 1ull) na.heads[na.n_fixed++] = (unsigned char)h;
         const unsigned ngrid = (unsigned)((size_t)na.n_rblocks * na.n_fixed);
-        hipLaunchKernelGGL(saf::fixed_lse_kernel, dim3(ngrid), dim3(saf::NORM_THREADS), 0, stream, na);
+        hipLaunchKernelGGL(saf::fixed_lse_kernel<1>, dim3(ngrid), dim3(saf::NORM_THREADS), 0, stream, na);
         if (launched() != SAF_OK) return SAF_ERR_LAUNCH;
     }
     saf::GqaArgs args;
@@ -782,12 +782,12 @@ SAF_EXPORT saf_status_t saf_compact_fit(int H, int T, const float* eta_abs, cons
         p2 *= (double)saf::FIT_ADAM_BETA2;
         f.bc1 = (float)(1.0 - p1);
         f.bc2 = (float)(1.0 - p2);
-        hipLaunchKernelGGL(saf::fixed_lse_kernel, dim3(lse_grid), dim3(saf::NORM_THREADS), 0, stream, na);
+        hipLaunchKernelGGL(saf::fixed_lse_kernel<6>, dim3(lse_grid), dim3(saf::NORM_THREADS), 0, stream, na);
         hipLaunchKernelGGL(saf::fit_marginals_kernel, dim3(marg_grid), dim3(saf::FIT_COLS), 0, stream, f);
         hipLaunchKernelGGL(saf::fit_adam_kernel, dim3(elem_grid), dim3(256), 0, stream, f);
         if (launched() != SAF_OK) return SAF_ERR_LAUNCH;
     }
-    hipLaunchKernelGGL(saf::fixed_lse_kernel, dim3(lse_grid), dim3(saf::NORM_THREADS), 0, stream, na);
+    hipLaunchKernelGGL(saf::fixed_lse_kernel<6>, dim3(lse_grid), dim3(saf::NORM_THREADS), 0, stream, na);
     hipLaunchKernelGGL(saf::fit_kl_kernel, dim3(H), dim3(256), 0, stream, f);
     return launched();
 }

@@ -502,9 +502,12 @@ __device__ __forceinline__ void fwd_fixed(const Tiles<T>& sm, const FwdArgs& p, 
 // er = exp(r - R_t) shifted by the tile's maxima A_t, R_t; the tiles combine
 // online under the largest shift M seen so far, so log Z = M + log Z'.  A
 // row whose Z' ends below 2^-80 (its terms underflowed) is summed exactly,
-// with a running maximum.  At most about 80 VGPRs (six wavefronts per SIMD):
-// left free, the scheduler hoists every LDS read of the key loop into
-// registers (164 VGPRs, three wavefronts per SIMD, 7 % slower).
+// with a running maximum.  WAVES: the wavefronts per SIMD the register
+// budget must allow.  The fitter, which launches 1536 workgroups per step,
+// asks for six (about 80 VGPRs; left free, the scheduler hoists every LDS
+// read of the key loop into registers: 164 VGPRs, three wavefronts per SIMD,
+// 7 % slower); the layer's few workgroups (one per fixed head and 32 rows)
+// run fastest with the registers free (WAVES = 1).
 // ---------------------------------------------------------------------------
 constexpr int NORM_THREADS = 256;
 constexpr int NORM_ROWS = 32;
@@ -521,7 +524,9 @@ struct NormArgs {
     unsigned char heads[64];  // the fixed heads, ascending
 };
 
-__global__ __launch_bounds__(NORM_THREADS) __attribute__((amdgpu_waves_per_eu(6))) void fixed_lse_kernel(NormArgs p) {
+template <int WAVES>
+__global__ __launch_bounds__(NORM_THREADS) __attribute__((amdgpu_waves_per_eu(WAVES))) void fixed_lse_kernel(
+    NormArgs p) {
     __shared__ __attribute__((aligned(16))) float ea_s[NORM_KT];
     __shared__ float er_s[NORM_BAND + 1];
     __shared__ float red[2][4];
