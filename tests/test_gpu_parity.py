@@ -343,3 +343,39 @@ def test_autograd_wrapper_matches_abi():
     assert np.array_equal(o.detach().cpu().numpy(), ref["O"].astype(np.float32))
     assert np.array_equal(v.grad.cpu().numpy(), ref["dV"].astype(np.float32))
     assert np.array_equal(q.grad.cpu().numpy(), ref["dQ"].astype(np.float32))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_golden_compact_prior_on_gpu(dtype):
+    """The hand-derived pattern of tests/golden/compact_prior_n4.txt through
+    the C ABI: one fixed head beside one ordinary head, V = identity rows and
+    dO = identity rows, so O holds P, LSE holds ln Z and dV holds P^T."""
+    import os
+    import sys
+    sys.path.insert(0, os.path.dirname(__file__))
+    from test_oracle import _golden_compact_prior
+    torch = torch_cuda()
+    from paper_2609_34650_amd import binding
+    announce(f"golden compact prior {dtype}")
+    a, r, P, lz = _golden_compact_prior()
+    n = len(a)
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    dev = torch.device("cuda", 0)
+    eye = np.zeros((n, 64))
+    eye[np.arange(n), np.arange(n)] = 1.0
+    V = np.stack([eye, eye])[None]                       # [1, 2, n, 64]
+    rng = np.random.default_rng(3)
+    Q = rng.standard_normal((1, 2, n, 64))
+    t = {k: torch.tensor(x, dtype=tdt, device=dev) for k, x in (("Q", Q), ("K", Q), ("V", V), ("dO", V))}
+    aa = torch.tensor(np.stack([a, a]), dtype=torch.float32, device=dev)
+    rr = torch.tensor(np.stack([r, r]), dtype=torch.float32, device=dev)
+    flags = [0, 1]
+    O, LSE = binding.saf_hybrid_attn_fwd(t["Q"], t["K"], t["V"], flags, aa, rr)
+    dQ, dK, dV = binding.saf_hybrid_attn_bwd(t["Q"], t["K"], t["V"], O, t["dO"], LSE, flags, aa, rr)
+    torch.cuda.synchronize()
+    tol = 1e-6 if dtype == "f32" else 4e-3   # bf16 rounds each output once
+    np.testing.assert_allclose(O[0, 1, :, :n].float().cpu().numpy(), P, rtol=0, atol=tol)
+    assert not O[0, 1, :, n:].any()
+    np.testing.assert_allclose(LSE[0, 1].cpu().numpy(), lz, rtol=0, atol=1e-6)
+    np.testing.assert_allclose(dV[0, 1, :, :n].float().cpu().numpy(), P.T, rtol=0, atol=tol)
+    assert not dQ[0, 1].any() and not dK[0, 1].any()

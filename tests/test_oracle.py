@@ -449,3 +449,42 @@ def test_parallel_driver_runs():
     used = orc.layer_forward_backward_parallel(Q, K, V, dO, np.array([0, 1]), a, r,
                                                heads=[(0, 0), (0, 1)], workers=2)
     assert used == 2
+
+
+def _golden_compact_prior():
+    """Parse tests/golden/compact_prior_n4.txt (hand-derived P and Z)."""
+    import os
+    from fractions import Fraction
+    path = os.path.join(os.path.dirname(__file__), "golden", "compact_prior_n4.txt")
+    a = r = z = None
+    rows = {}
+    for line in open(path):
+        if not line.strip() or line.startswith("#"):
+            continue
+        parts = line.split()
+        if parts[0] == "a_exp":
+            a = np.log(np.array([float(x) for x in parts[1:]]))
+        elif parts[0] == "r_exp":
+            r = np.log(np.array([float(x) for x in parts[1:]]))
+        elif parts[0] == "P":
+            rows[int(parts[1])] = [float(Fraction(x)) for x in parts[2:]]
+        elif parts[0] == "Z":
+            z = np.array([float(x) for x in parts[1:]])
+    n = len(a)
+    P = np.zeros((n, n))
+    for i, vals in rows.items():
+        P[i, : len(vals)] = vals
+    return a, r, P, np.log(z)
+
+
+def test_golden_compact_prior_by_hand():
+    """The oracle's fixed pattern and normaliser equal the hand-derived
+    values of the golden fixture (Eq. compact-prior)."""
+    a, r, P, lz = _golden_compact_prior()
+    np.testing.assert_allclose(orc.fixed_pattern(a, r), P, rtol=1e-14, atol=1e-15)
+    np.testing.assert_allclose(orc.fixed_log_normaliser(a, r), lz, rtol=1e-14, atol=1e-15)
+    # A fixed head with V = identity returns P itself.
+    n = len(a)
+    o, lse = orc.head_forward(None, None, np.eye(n), True, a, r)
+    np.testing.assert_allclose(o, P, rtol=1e-14, atol=1e-15)
+    np.testing.assert_allclose(lse, lz, rtol=1e-14, atol=1e-15)
