@@ -88,16 +88,15 @@ __global__ __launch_bounds__(PRE_THREADS) void bwd_pre_kernel(BwdArgs p) {
 // Fixed heads: dV[j] = sum_i P(i,j) dO[i] with P(i,j) = ea(j) er(i-j) g(i),
 // ea = exp(a - A), er = exp(r - R), g(i) = exp(A + R - log Z(i)) (A: maximum
 // of a over the block's keys, R: maximum of r over the offsets it meets, log Z
-// from the forward's LSE).  The dO tile is staged scaled by g(i), the weight
-// operand is the Toeplitz band er(i-j) read from LDS (8 shifted copies, so any
-// lane's eight consecutive offsets are one aligned 16-byte read; negative
-// offsets hold 0, the causal mask), and the accumulator is scaled by ea(j) at
-// the end: no exponential per element.  The band is kept as a bf16 high part
-// plus a bf16 low part (er - hi), two products per chunk, so each term is
-// rounded once (in g * dO), as in the exact program.  If some row's log Z
-// lies more than FAST_GUARD below A + R (g could overflow), the block runs
-// the exact per-element program instead.  dK of a fixed head is written as
-// zeros.
+// from the forward's LSE).  The dO tile comes by buffer loads straight to LDS,
+// unscaled; the Toeplitz band er(i-j) is kept in float32 in LDS (8 shifted
+// copies, so any lane's eight consecutive offsets are aligned reads; negative
+// offsets hold 0, the causal mask) beside g of the tile's rows, and the weight
+// operand er(i-j) g(i) is formed in float32 per chunk and rounded once, as P
+// is in the exact program; the accumulator is scaled by ea(j) at the end: no
+// exponential per element.  If some row's log Z lies more than FAST_GUARD
+// below A + R (g could overflow), the block runs the exact per-element
+// program instead.  dK of a fixed head is written as zeros.
 // ---------------------------------------------------------------------------
 constexpr int KV_KB = 1;               // 32-key sub-blocks per wavefront
 constexpr int KV_BN = 4 * 32 * KV_KB;  // keys per workgroup
@@ -106,7 +105,7 @@ constexpr int KV_THREADS = 256;
 constexpr int KV_MASK_TILES = KV_BN / KV_BM;               // tiles that meet the diagonal
 constexpr int KV_BAND = KV_BM + KV_BN - 1;                 // offsets per tile
 constexpr int KV_BAND_STRIDE = (KV_BAND + 8) / 8 * 8 + 8;  // every copy 16-byte aligned
-static_assert(2 * BAND_COPIES * KV_BAND_STRIDE <= tile_elems<bf16>(), "hi/lo band copies fit in a tile");
+static_assert(BAND_COPIES * KV_BAND_STRIDE * 4 <= tile_elems<bf16>() * 2, "float32 band copies fit in a tile");
 static_assert((KV_BM + KV_BAND + 1) * 4 <= tile_elems<bf16>() * 2, "exact-program rows fit in a tile");
 
 struct KvLane {
@@ -374,24 +373,16 @@ __device__ __forceinline__ void kv_fixed_exact(const Tiles<T>& sm, const BwdArgs
 
 // --- fixed heads: factorised program ----------------------------------------
 
-template <typename T>
+// Small per-tile values in registers between their loads (issued a tile
+// ahead) and their LDS stores: log Z of one row, two band entries.
 struct KvFixStage {
-    u32x4 g[tile_units<T>()];  // this lane's 16-byte units of the dO tile (one row)
-    float lse;                 // log Z of that row
-    float rb[2];               // band entries
+    float lse;    // log Z of row L.tid of the tile (L.tid < KV_BM)
+    float rb[2];  // band entries
 };
 
-template <typename T>
-__device__ __forceinline__ void kvf_load(KvFixStage<T>& st, const T* dO, const float* LSE, const float* rrow, int mq,
+__device__ __forceinline__ void kvf_load(KvFixStage& st, const float* LSE, const float* rrow, int mq,
                                          const KvLane& L) {
-    const int q = mq + unit_row<T>(L.w, L.lane);
-    const bool ok = q < L.N;
-#pragma unroll
-    for (int k = 0; k < tile_units<T>(); ++k) {
-        const u32x4 z = {0u, 0u, 0u, 0u};
-        st.g[k] = ok ? ld_unit(dO + (size_t)q * HEAD_DIM + unit_col<T>(L.w, L.lane, k)) : z;
-    }
-    st.lse = ok ? LSE[q] : INFINITY;
+    st.lse = (L.tid < KV_BM && mq + L.tid < L.N) ? LSE[mq + L.tid] : INFINITY;
 #pragma unroll
     for (int k = 0; k < 2; ++k) {
         const int x = L.tid + KV_THREADS * k;
@@ -400,35 +391,27 @@ __device__ __forceinline__ void kvf_load(KvFixStage<T>& st, const T* dO, const f
     }
 }
 
-// band: copy s of the high parts at s * KV_BAND_STRIDE, of the low parts at
-// (BAND_COPIES + s) * KV_BAND_STRIDE.
-template <typename T>
-__device__ __forceinline__ void kvf_store(T* dog, T* band, const KvFixStage<T>& st, const KvLane& L, float g_sh,
+// gs: g of the tile's rows; band: copy s of er at s * KV_BAND_STRIDE, float32.
+__device__ __forceinline__ void kvf_store(float* gs, float* band, const KvFixStage& st, const KvLane& L, float g_sh,
                                           float r_sh) {
-    const float g = fast_exp2(fmaf(-st.lse, LOG2E, g_sh));
-    const int row = unit_row<T>(L.w, L.lane);
-#pragma unroll
-    for (int k = 0; k < tile_units<T>(); ++k)
-        st_unit_scaled(dog + toff<T>(row, unit_col<T>(L.w, L.lane, k)), st.g[k], g);
+    if (L.tid < KV_BM) gs[L.tid] = fast_exp2(fmaf(-st.lse, LOG2E, g_sh));  // 0 past N
 #pragma unroll
     for (int k = 0; k < 2; ++k) {
         const int x = L.tid + KV_THREADS * k;
         if (x < KV_BAND) {
             const float e = fast_exp2(fmaf(st.rb[k], LOG2E, -r_sh));
-            const T hi = (T)e;
-            const T lo = (T)(e - (float)hi);
 #pragma unroll
             for (int s = 0; s < BAND_COPIES; ++s)
-                if (x >= s) {
-                    band[s * KV_BAND_STRIDE + x - s] = hi;
-                    band[(BAND_COPIES + s) * KV_BAND_STRIDE + x - s] = lo;
-                }
+                if (x >= s) band[s * KV_BAND_STRIDE + x - s] = e;
         }
     }
 }
 
+// dV^T += dO^T (er g): the weight operand of lane (key c, half hf) in chunk
+// (qb, kc) is er(q - key) g(q) for its eight queries q, formed in float32
+// from the band and g and rounded once.
 template <typename T, bool MASK>
-__device__ __forceinline__ void kvf_tile(const T* dog, const T* band, int mq, const KvLane& L,
+__device__ __forceinline__ void kvf_tile(const T* dot, const float* band, const float* gs, int mq, const KvLane& L,
                                          f32x16 (&dv)[KV_KB][2]) {
     typedef typename Vec<T>::x8 frag;
 #pragma unroll
@@ -440,19 +423,25 @@ __device__ __forceinline__ void kvf_tile(const T* dog, const T* band, int mq, co
             const int col = 32 * qb + 16 * kc + 8 * L.hf;  // first query (within the tile) of this lane's slots
             frag gta[2];
 #pragma unroll
-            for (int db = 0; db < 2; ++db) gta[db] = ld_tile_t<false>(dog, 32 * qb + 16 * kc, 32 * db);
+            for (int db = 0; db < 2; ++db) gta[db] = ld_tile_t<false>(dot, 32 * qb + 16 * kc, 32 * db);
+            const f32x4 g0 = *reinterpret_cast<const f32x4*>(gs + col);
+            const f32x4 g1 = *reinterpret_cast<const f32x4*>(gs + col + 4);
 #pragma unroll
             for (int kb = 0; kb < KV_KB; ++kb) {
                 const int kl = L.kw - L.n0 + 32 * kb + L.c;
                 const int u0 = col - kl + (KV_BN - 1);  // band index of offset (mq + col) - (n0 + kl)
                 const int s = u0 & 7;
-                const frag bh = ld8<T>(band + s * KV_BAND_STRIDE + u0 - s);
-                const frag bl = ld8<T>(band + (BAND_COPIES + s) * KV_BAND_STRIDE + u0 - s);
+                const float* bp = band + s * KV_BAND_STRIDE + u0 - s;
+                const f32x4 b0 = *reinterpret_cast<const f32x4*>(bp);
+                const f32x4 b1 = *reinterpret_cast<const f32x4*>(bp + 4);
+                frag w;
 #pragma unroll
-                for (int db = 0; db < 2; ++db) {
-                    mma(dv[kb][db], gta[db], bh);
-                    mma(dv[kb][db], gta[db], bl);
+                for (int t = 0; t < 4; ++t) {
+                    w[t] = (T)(b0[t] * g0[t]);
+                    w[4 + t] = (T)(b1[t] * g1[t]);
                 }
+#pragma unroll
+                for (int db = 0; db < 2; ++db) mma(dv[kb][db], gta[db], w);
             }
         }
     }
@@ -461,7 +450,8 @@ __device__ __forceinline__ void kvf_tile(const T* dog, const T* band, int mq, co
 template <typename T>
 __device__ __forceinline__ void kv_fixed(const Tiles<T>& sm, const BwdArgs& p, const KvLane& L, size_t base,
                                          size_t row_base, int h) {
-    // Tiles: g * dO in t[0] / t[1], the hi/lo band in t[2] / t[3].
+    // Tiles: dO in t[0] / t[1] (buffer loads to LDS), the float32 band in
+    // t[2] / t[3]; g of the tile's rows in aux[0] / aux[1].
     const T* __restrict__ dO = reinterpret_cast<const T*>(p.dO) + base;
     const float* __restrict__ LSE = p.lse + row_base;
     const float* __restrict__ arow = p.a + (size_t)h * p.ld_prior;
@@ -498,13 +488,21 @@ __device__ __forceinline__ void kv_fixed(const Tiles<T>& sm, const BwdArgs& p, c
     const int n_tiles = (N - L.n0 + KV_BM - 1) / KV_BM;
     const int n_mask = min(KV_MASK_TILES, n_tiles);
     const int P = (n_mask + 1) & ~1;
-    KvFixStage<T> st;
+    const __amdgpu_buffer_rsrc_t rg = slice_rsrc<T>(dO, N);
+    KvFixStage st;
     run_slots(
         P, P + n_tiles - n_mask, [&](int i) { return i < P ? (i < n_mask ? i : -1) : n_mask + (i - P); },
-        [&](auto, int t) { kvf_load<T>(st, dO, LSE, rrow, L.n0 + t * KV_BM, L); },
-        [&](auto buf) { kvf_store<T>(sm.t[decltype(buf)::value], sm.t[2 + decltype(buf)::value], st, L, g_sh, r_sh); },
+        [&](auto buf, int t) {
+            tile_load_lds<T>(sm.t[decltype(buf)::value], rg, L.n0 + t * KV_BM, L.w, L.lane);
+            kvf_load(st, LSE, rrow, L.n0 + t * KV_BM, L);
+        },
+        [&](auto buf) {
+            constexpr int b = decltype(buf)::value;
+            kvf_store(sm.aux[b], reinterpret_cast<float*>(sm.t[2 + b]), st, L, g_sh, r_sh);
+        },
         [&](auto buf, int t, auto mask) {
-            kvf_tile<T, decltype(mask)::value>(sm.t[decltype(buf)::value], sm.t[2 + decltype(buf)::value],
+            constexpr int b = decltype(buf)::value;
+            kvf_tile<T, decltype(mask)::value>(sm.t[b], reinterpret_cast<const float*>(sm.t[2 + b]), sm.aux[b],
                                                L.n0 + t * KV_BM, L, dv);
         });
     float ea[KV_KB];
