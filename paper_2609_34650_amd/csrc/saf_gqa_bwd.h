@@ -179,61 +179,41 @@ __device__ __forceinline__ void gkv_fixed_tile(const T* gt, const float* lse2, c
 // Fixed query head, factorised (the layer's key-block program): dV[j] +=
 // ea(j) sum_i er(i - j) g(i) dO[i] with ea = exp(a - A), er = exp(r - R),
 // g(i) = exp(A + R - log Z(i)) (A: maximum of a over the block's keys, R:
-// maximum of r over the offsets it meets).  The dO tile is staged through
-// registers scaled by g, the weight operand is the Toeplitz band er read
-// from LDS as a bf16 high part plus a bf16 low part (eight shifted copies of
-// each, so every 8-entry read is aligned; negative offsets hold 0), and the
-// head's sum is scaled by ea(j) once at the end: no exponential per entry.
-constexpr int GKV_BAND_STRIDE = (GKV_BAND + 8) / 8 * 8 + 8;  // every copy 16-byte aligned
+// maximum of r over the offsets it meets).  The dO tile comes by buffer
+// loads to LDS unscaled; the Toeplitz band er is kept in float32 in LDS
+// (eight shifted copies, so every 8-entry read is aligned; negative offsets
+// hold 0) beside g of the tile's rows, and the weight operand er(i - j) g(i)
+// is formed in float32 per chunk and rounded once; the head's sum is scaled
+// by ea(j) once at the end: no exponential per entry.
+constexpr int GKV_BAND_STRIDE = (GKV_BAND + 8) / 8 * 8 + 8;  // every copy 32-byte aligned
 
-template <typename T, int D>
 struct GkvFixStage {
-    u32x4 g[tile_units<T, D>()];  // this lane's 16-byte units of the dO tile (one row)
-    float lse;                    // log Z of that row
-    float rb;                     // one band entry
+    float lse;  // log Z of row L.tid of the tile (L.tid < GKV_BM)
+    float rb;   // one band entry
 };
 
-template <typename T, int D>
-__device__ __forceinline__ void gkvf_load(GkvFixStage<T, D>& st, const T* dO, const float* LSE, const float* rrow,
-                                          int mq, const GkvLane& L) {
-    const int q = mq + unit_row<T>(L.w, L.lane);
-    const bool ok = q < L.N;
-#pragma unroll
-    for (int k = 0; k < tile_units<T, D>(); ++k) {
-        const u32x4 z = {0u, 0u, 0u, 0u};
-        st.g[k] = ok ? ld_unit(dO + (size_t)q * D + unit_col<T>(L.w, L.lane, k)) : z;
-    }
-    st.lse = ok ? LSE[q] : INFINITY;
+__device__ __forceinline__ void gkvf_load(GkvFixStage& st, const float* LSE, const float* rrow, int mq,
+                                          const GkvLane& L) {
+    st.lse = (L.tid < GKV_BM && mq + L.tid < L.N) ? LSE[mq + L.tid] : INFINITY;
     const int delta = mq - L.n0 - (GKV_BN - 1) + L.tid;
     st.rb = (L.tid < GKV_BAND && delta >= 0 && delta < L.N) ? rrow[delta] : -INFINITY;
 }
 
-// band: copy s of the high parts at s * GKV_BAND_STRIDE, of the low parts at
-// (BAND_COPIES + s) * GKV_BAND_STRIDE.
-template <typename T, int D>
-__device__ __forceinline__ void gkvf_store(T* dog, T* band, const GkvFixStage<T, D>& st, const GkvLane& L,
+// gs: g of the tile's rows; band: copy s of er at s * GKV_BAND_STRIDE.
+__device__ __forceinline__ void gkvf_store(float* gs, float* band, const GkvFixStage& st, const GkvLane& L,
                                            float g_sh, float r_sh) {
-    const float g = fast_exp2(fmaf(-st.lse, LOG2E, g_sh));
-    const int row = unit_row<T>(L.w, L.lane);
-#pragma unroll
-    for (int k = 0; k < tile_units<T, D>(); ++k)
-        st_unit_scaled(dog + toff<T>(row, unit_col<T>(L.w, L.lane, k)), st.g[k], g);
+    if (L.tid < GKV_BM) gs[L.tid] = fast_exp2(fmaf(-st.lse, LOG2E, g_sh));  // 0 past N
     if (L.tid < GKV_BAND) {
         const float e = fast_exp2(fmaf(st.rb, LOG2E, -r_sh));
-        const T hi = (T)e;
-        const T lo = (T)(e - (float)hi);
 #pragma unroll
         for (int s = 0; s < BAND_COPIES; ++s)
-            if (L.tid >= s) {
-                band[s * GKV_BAND_STRIDE + L.tid - s] = hi;
-                band[(BAND_COPIES + s) * GKV_BAND_STRIDE + L.tid - s] = lo;
-            }
+            if (L.tid >= s) band[s * GKV_BAND_STRIDE + L.tid - s] = e;
     }
 }
 
 template <typename T, int D>
-__device__ __forceinline__ void gkvf_tile(const T* dog, const T* band, int mq, const GkvLane& L,
-                                          f32x16 (&acc)[D / 32]) {
+__device__ __forceinline__ void gkvf_tile(const T* dot, const float* band, const float* gs, int mq,
+                                          const GkvLane& L, f32x16 (&acc)[D / 32]) {
     typedef typename Vec<T>::x8 frag;
     const int kl = L.kw - L.n0 + L.c;  // key within the block
 #pragma unroll
@@ -242,16 +222,22 @@ __device__ __forceinline__ void gkvf_tile(const T* dog, const T* band, int mq, c
         if (qs + 31 < L.kw || qs >= L.N) continue;  // no query of this half sees these keys
 #pragma unroll
         for (int kc = 0; kc < 2; ++kc) {
-            const int u0 = 32 * qb + 16 * kc + 8 * L.hf - kl + (GKV_BN - 1);  // band index of this lane's first slot
+            const int col = 32 * qb + 16 * kc + 8 * L.hf;  // this lane's first query within the tile
+            const int u0 = col - kl + (GKV_BN - 1);       // band index of its first slot
             const int s = u0 & 7;
-            const frag bh = ld8<T>(band + s * GKV_BAND_STRIDE + u0 - s);
-            const frag bl = ld8<T>(band + (BAND_COPIES + s) * GKV_BAND_STRIDE + u0 - s);
+            const float* bp = band + s * GKV_BAND_STRIDE + u0 - s;
+            const f32x4 b0 = *reinterpret_cast<const f32x4*>(bp);
+            const f32x4 b1 = *reinterpret_cast<const f32x4*>(bp + 4);
+            const f32x4 g0 = *reinterpret_cast<const f32x4*>(gs + col);
+            const f32x4 g1 = *reinterpret_cast<const f32x4*>(gs + col + 4);
+            frag wt;
 #pragma unroll
-            for (int db = 0; db < D / 32; ++db) {
-                const frag ga = ld_tile_t<false>(dog, 32 * qb + 16 * kc, 32 * db);
-                mma(acc[db], ga, bh);
-                mma(acc[db], ga, bl);
+            for (int t = 0; t < 4; ++t) {
+                wt[t] = (T)(b0[t] * g0[t]);
+                wt[4 + t] = (T)(b1[t] * g1[t]);
             }
+#pragma unroll
+            for (int db = 0; db < D / 32; ++db) mma(acc[db], ld_tile_t<false>(dot, 32 * qb + 16 * kc, 32 * db), wt);
         }
     }
 }
@@ -281,7 +267,8 @@ __global__ __launch_bounds__(GKV_THREADS) __attribute__((amdgpu_waves_per_eu(D *
     __shared__ __attribute__((aligned(16))) float f0[GKV_BM + GKV_BAND + 1];
     __shared__ __attribute__((aligned(16))) float f1[GKV_BM + GKV_BAND + 1];
     __shared__ float red[4];
-    static_assert(2 * BAND_COPIES * GKV_BAND_STRIDE <= tile_elems<T, D>(), "hi/lo band copies fit in a tile");
+    static_assert(BAND_COPIES * GKV_BAND_STRIDE * 4 <= tile_elems<T, D>() * (int)sizeof(T),
+                  "float32 band copies fit in a tile");
     const SliceOf sl = slice_of(blockIdx.x, p.B, p.Hkv, 1, [&](int k) { return (int)p.kv_order[k]; });
     const int kblk = sl.level;  // ascending: longest first
     const int b = sl.b, hkv = sl.h;
@@ -336,24 +323,27 @@ __global__ __launch_bounds__(GKV_THREADS) __attribute__((amdgpu_waves_per_eu(D *
         const float LO = -block_max(-lo, red);
         if (LO - A - R >= -FAST_GUARD) {  // no g(i) can overflow
             const float g_sh = (A + R) * LOG2E, r_sh = R * LOG2E;
-            const T* __restrict__ dOh = reinterpret_cast<const T*>(p.dO) + qbase;
             f32x16 acc[D / 32];
 #pragma unroll
             for (int db = 0; db < D / 32; ++db)
 #pragma unroll
                 for (int v = 0; v < 16; ++v) acc[db][v] = 0.0f;
-            GkvFixStage<T, D> st;
+            GkvFixStage st;
             run_slots(
                 P, P + n_tiles - n_mask,
                 [&](int s) { return s < P ? (s < n_mask ? s : -1) : n_mask + (s - P); },
-                [&](auto, int t) { gkvf_load<T, D>(st, dOh, LSE, rrow, L.n0 + t * GKV_BM, L); },
+                [&](auto buf, int t) {
+                    tile_load_lds<T, D>(decltype(buf)::value ? g1s : g0s, rg, L.n0 + t * GKV_BM, L.w, L.lane);
+                    gkvf_load(st, LSE, rrow, L.n0 + t * GKV_BM, L);
+                },
                 [&](auto buf) {
                     constexpr int B_ = decltype(buf)::value;
-                    gkvf_store<T, D>(B_ ? g1s : g0s, B_ ? q1s : q0s, st, L, g_sh, r_sh);
+                    gkvf_store(B_ ? x1 : x0, reinterpret_cast<float*>(B_ ? q1s : q0s), st, L, g_sh, r_sh);
                 },
                 [&](auto buf, int t, auto) {
                     constexpr int B_ = decltype(buf)::value;
-                    gkvf_tile<T, D>(B_ ? g1s : g0s, B_ ? q1s : q0s, L.n0 + t * GKV_BM, L, acc);
+                    gkvf_tile<T, D>(B_ ? g1s : g0s, reinterpret_cast<const float*>(B_ ? q1s : q0s), B_ ? x1 : x0,
+                                    L.n0 + t * GKV_BM, L, acc);
                 });
             const float ea = key < N ? fast_exp2(fmaf(a_key, LOG2E, -A * LOG2E)) : 0.0f;
 #pragma unroll
