@@ -20,10 +20,10 @@
 //   Fixed head, factorised (as in the layer forward): P(i, j) =
 //   ea(j) er(i - j) exp(A + R - log Z(i)) with ea = exp(a - A), er =
 //   exp(r - R) and A, R the maxima of a and r over the block's positions.  V
-//   rows are scaled by ea while they are staged through registers into LDS,
-//   and the weight operand is the Toeplitz band er read from LDS (eight
-//   shifted copies keep every 8-entry read aligned): no exponential per
-//   entry.  log Z comes from the normaliser pre-pass (the layer forward's
+//   tiles come by buffer loads to LDS unscaled, and the weight operand is
+//   the Toeplitz band er (float32 in LDS, eight shifted copies keep every
+//   8-entry read aligned) times ea of the chunk's keys, formed in float32
+//   and rounded once: no exponential per entry.  log Z comes from the normaliser pre-pass (the layer forward's
 //   fixed_lse_kernel).  A block where some row's diagonal and sink terms both
 //   lie more than FAST_GUARD below A + R takes the exact per-entry program:
 //   P(i, j) = exp(a[j] + r[i - j] - log Z(i)) with the tile's a values and r
@@ -144,54 +144,43 @@ __device__ __forceinline__ void gqa_fix_tile(const T* vt, const float* as, const
     }
 }
 
-// Factorised fixed program: one lane's share of a tile in registers (a V row
-// unit per 16 bytes, that row's a, one band entry).
-template <typename T, int D>
+// Factorised fixed program: V tiles come by buffer loads to LDS unscaled;
+// per tile, ea of its 64 keys and the band er of the offsets it meets go
+// through registers (loaded a tile ahead) into LDS, ea in float32 beside the
+// a values of the exact program, the band as eight shifted float32 copies in
+// the unused K tile.
 struct GqaFixStage {
-    u32x4 v[tile_units<T, D>()];
-    float a;
-    float rb;
+    float a;   // a of key n0 + L.tid (L.tid < GQA_BN)
+    float rb;  // one band entry
 };
 
 // Band entry u of the tile at n0 holds er at offset (m0 - n0 + 127) - u.
-template <typename T, int D>
-__device__ __forceinline__ void gqa_fix_load(GqaFixStage<T, D>& st, const T* V, const float* arow,
-                                             const float* rrow, int n0, const GqaLane& L) {
-    const int key = n0 + unit_row<T>(L.w, L.lane);
-    const bool ok = key < L.N;
-#pragma unroll
-    for (int k = 0; k < tile_units<T, D>(); ++k) {
-        const u32x4 z = {0u, 0u, 0u, 0u};
-        st.v[k] = ok ? ld_unit(V + (size_t)key * D + unit_col<T>(L.w, L.lane, k)) : z;
-    }
-    st.a = ok ? arow[key] : -INFINITY;
+__device__ __forceinline__ void gqa_fix_load(GqaFixStage& st, const float* arow, const float* rrow, int n0,
+                                             const GqaLane& L) {
+    st.a = (L.tid < GQA_BN && n0 + L.tid < L.N) ? arow[n0 + L.tid] : -INFINITY;
     const int delta = L.m0 - n0 + (GQA_BM - 1) - L.tid;
     st.rb = (L.tid < GQA_BAND && delta >= 0 && delta < L.N) ? rrow[delta] : -INFINITY;
 }
 
-template <typename T, int D>
-__device__ __forceinline__ void gqa_fix_store(T* vs, T* band, const GqaFixStage<T, D>& st, const GqaLane& L,
+__device__ __forceinline__ void gqa_fix_store(float* eas, float* band, const GqaFixStage& st, const GqaLane& L,
                                               float a_sh, float r_sh) {
-    const float e = fast_exp2(fmaf(st.a, LOG2E, -a_sh));
-    const int row = unit_row<T>(L.w, L.lane);
-#pragma unroll
-    for (int k = 0; k < tile_units<T, D>(); ++k)
-        st_unit_scaled(vs + toff<T>(row, unit_col<T>(L.w, L.lane, k)), st.v[k], e);
+    if (L.tid < GQA_BN) eas[L.tid] = fast_exp2(fmaf(st.a, LOG2E, -a_sh));  // 0 past N
     if (L.tid < GQA_BAND) {
-        const T b = (T)fast_exp2(fmaf(st.rb, LOG2E, -r_sh));
+        const float e = fast_exp2(fmaf(st.rb, LOG2E, -r_sh));
 #pragma unroll
         for (int s = 0; s < BAND_COPIES; ++s)
-            if (L.tid >= s) band[s * GQA_BAND_STRIDE + L.tid - s] = b;
+            if (L.tid >= s) band[s * GQA_BAND_STRIDE + L.tid - s] = e;
     }
 }
 
-// O^T += (ea V)^T band^T over one tile: four 16-key chunks; the band operand
-// of lane (c, hf) in chunk G is entries u0 .. u0 + 7, u0 = 127 - ql + 16G +
-// 8hf, read from copy u0 % 8 at an aligned address.  Offsets below zero hold
-// 0, which masks the keys after the query.
+// O^T += V^T (band ea)^T over one tile: four 16-key chunks; the weight
+// operand of lane (c, hf) in chunk G is band entries u0 .. u0 + 7 (u0 =
+// 127 - ql + 16G + 8hf, read from copy u0 % 8 at an aligned address) times
+// ea of keys 16G + 8hf .. 16G + 8hf + 7, formed in float32 and rounded once.
+// Offsets below zero hold 0, which masks the keys after the query.
 template <typename T, int D, bool MASK>
-__device__ __forceinline__ void gqa_band_tile(const T* vs, const T* band, int n0, const GqaLane& L,
-                                              f32x16 (&oacc)[D / 32]) {
+__device__ __forceinline__ void gqa_band_tile(const T* vs, const float* band, const float* eas, int n0,
+                                              const GqaLane& L, f32x16 (&oacc)[D / 32]) {
     typedef typename Vec<T>::x8 frag;
     const int ql = L.q0 - L.m0 + L.c;
 #pragma unroll
@@ -199,48 +188,19 @@ __device__ __forceinline__ void gqa_band_tile(const T* vs, const T* band, int n0
         if (MASK && n0 + 16 * G > L.q0 + 31) continue;  // chunk wholly after this wavefront's queries
         const int u0 = (GQA_BM - 1) - ql + 16 * G + 8 * L.hf;
         const int s = u0 & 7;
-        const frag b = ld8<T>(band + s * GQA_BAND_STRIDE + u0 - s);
+        const float* bp = band + s * GQA_BAND_STRIDE + u0 - s;
+        const f32x4 b0 = *reinterpret_cast<const f32x4*>(bp);
+        const f32x4 b1 = *reinterpret_cast<const f32x4*>(bp + 4);
+        const f32x4 e0 = *reinterpret_cast<const f32x4*>(eas + 16 * G + 8 * L.hf);
+        const f32x4 e1 = *reinterpret_cast<const f32x4*>(eas + 16 * G + 8 * L.hf + 4);
+        frag b;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            b[t] = (T)(b0[t] * e0[t]);
+            b[4 + t] = (T)(b1[t] * e1[t]);
+        }
 #pragma unroll
         for (int db = 0; db < D / 32; ++db) mma(oacc[db], ld_tile_t<false>(vs, 16 * G, 32 * db), b);
-    }
-}
-
-// The tile schedule of run_slots with register-staged copies issued two
-// slots ahead: slot i computes on buffer i % 2 while the registers of stage
-// (i + 1) % 2 (issued one slot earlier) are written to the other buffer and
-// that stage is reloaded for slot i + 3.  issue(buf, t) loads tile t into
-// stage buf; finish(buf) writes stage buf into LDS buffer buf.
-template <typename TileOf, typename Issue, typename Finish, typename Compute>
-__device__ __forceinline__ void run_slots_ahead2(int P, int total, TileOf tile_of, Issue issue, Finish finish,
-                                                 Compute compute) {
-    auto pre = [&](auto buf, int i) {
-        if (i < total) {
-            const int t = tile_of(i);
-            if (t >= 0) issue(buf, t);
-        }
-    };
-    auto fin = [&](auto buf, int i) {
-        if (i < total && tile_of(i) >= 0) finish(buf);
-    };
-    auto body = [&](auto buf, auto other, int i, auto mask) {
-        if (tile_of(i) >= 0) compute(buf, tile_of(i), mask);
-        fin(other, i + 1);
-        pre(other, i + 3);
-        __syncthreads();
-    };
-    pre(Buf0{}, 0);
-    pre(Buf1{}, 1);
-    fin(Buf0{}, 0);
-    pre(Buf0{}, 2);
-    __syncthreads();
-    for (int i = 0; i < P; i += 2) {
-        body(Buf0{}, Buf1{}, i, std::true_type{});
-        body(Buf1{}, Buf0{}, i + 1, std::true_type{});
-    }
-    for (int i = P; i < total; i += 2) {
-        body(Buf0{}, Buf1{}, i, std::false_type{});
-        if (i + 1 >= total) break;
-        body(Buf1{}, Buf0{}, i + 1, std::false_type{});
     }
 }
 
@@ -250,10 +210,11 @@ __global__ __launch_bounds__(GQA_THREADS) __attribute__((amdgpu_waves_per_eu(2))
     __shared__ __attribute__((aligned(16))) T k1s[tile_elems<T, D>()];
     __shared__ __attribute__((aligned(16))) T v0s[tile_elems<T, D>()];
     __shared__ __attribute__((aligned(16))) T v1s[tile_elems<T, D>()];
-    __shared__ float ab0[GQA_BN + GQA_BAND + 1];
-    __shared__ float ab1[GQA_BN + GQA_BAND + 1];
+    __shared__ __attribute__((aligned(16))) float ab0[GQA_BN + GQA_BAND + 1];
+    __shared__ __attribute__((aligned(16))) float ab1[GQA_BN + GQA_BAND + 1];
     __shared__ float red[8];
-    static_assert(BAND_COPIES * GQA_BAND_STRIDE <= tile_elems<T, D>(), "band copies fit in a K tile");
+    static_assert(BAND_COPIES * GQA_BAND_STRIDE * 4 <= tile_elems<T, D>() * (int)sizeof(T),
+                  "float32 band copies fit in a K tile");
     // Longest query blocks first; slices = (batch, key/value head).
     const int group = p.Hq / p.Hkv;
     const SliceOf sl = slice_of(blockIdx.x, p.B, p.Hkv, group, [&](int k) { return (int)p.kv_order[k]; });
@@ -334,21 +295,23 @@ __global__ __launch_bounds__(GQA_THREADS) __attribute__((amdgpu_waves_per_eu(2))
         }
         if (__syncthreads_and(ok)) {
             // K is never read for a fixed head: its tiles hold the band.
-            const T* __restrict__ V = reinterpret_cast<const T*>(p.v) + kvbase;
             const float a_sh = A * LOG2E, r_sh = R * LOG2E;
-            GqaFixStage<T, D> st0, st1;
-            run_slots_ahead2(
+            GqaFixStage st;
+            run_slots(
                 P, P + n_full, tile_of,
                 [&](auto buf, int t) {
-                    gqa_fix_load<T, D>(decltype(buf)::value ? st1 : st0, V, arow, rrow, t * GQA_BN, L);
+                    tile_load_lds<T, D>(decltype(buf)::value ? v1s : v0s, rv, t * GQA_BN, L.w, L.lane);
+                    gqa_fix_load(st, arow, rrow, t * GQA_BN, L);
                 },
                 [&](auto buf) {
                     constexpr int B_ = decltype(buf)::value;
-                    gqa_fix_store<T, D>(B_ ? v1s : v0s, B_ ? k1s : k0s, B_ ? st1 : st0, L, a_sh, r_sh);
+                    gqa_fix_store(B_ ? ab1 : ab0, reinterpret_cast<float*>(B_ ? k1s : k0s), st, L, a_sh, r_sh);
                 },
                 [&](auto buf, int t, auto mask) {
                     constexpr int B_ = decltype(buf)::value;
-                    gqa_band_tile<T, D, decltype(mask)::value>(B_ ? v1s : v0s, B_ ? k1s : k0s, t * GQA_BN, L, oacc);
+                    gqa_band_tile<T, D, decltype(mask)::value>(B_ ? v1s : v0s,
+                                                               reinterpret_cast<const float*>(B_ ? k1s : k0s),
+                                                               B_ ? ab1 : ab0, t * GQA_BN, L, oacc);
                 });
             row_scale = fast_exp2((A + R - lz) * LOG2E);
         } else run_slots(
