@@ -75,10 +75,10 @@ typedef enum {
  * execution"; Appendix "Mixed-head execution and numerical checks"): one
  * launch of the attention kernel for all heads, in which every workgroup
  * takes one (batch, head, block of queries) and the head's flag selects its
- * path; outputs land in the original head order.  When some head is fixed, a
- * small normaliser launch runs first and writes log Z(i) of the fixed heads
- * into LSE (the paper precomputes these normalisers; here they are recomputed
- * from a and r on every call, in float32).
+ * path; outputs land in the original head order.  A fixed head's workgroup
+ * sums its row normalisers Z(i) from a and r as it forms the weights (the
+ * paper precomputes these normalisers; here they are recomputed on every
+ * call, in float32) and writes log Z(i) into LSE.
  *   Q, K : [B,H,N,d] `dt`; read for ordinary heads only (fixed-head slices may
  *          hold anything, NaN included).  May be NULL if every head is fixed.
  *   V    : [B,H,N,d] `dt`.

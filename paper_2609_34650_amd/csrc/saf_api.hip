@@ -93,26 +93,19 @@ size_t pattern_workspace_bytes(int B, int H, int N) {
            align256(bh * g.n_kblocks * g.n_chunks * (size_t)g.part_len * 4);
 }
 
+// The normaliser pre-pass: with many workgroups (long sequences, many fixed
+// heads) the copy with a budget of six wavefronts per SIMD keeps more of them
+// in flight; with few, the copy with free registers finishes each sooner.
+void launch_fixed_lse(const saf::NormArgs& na, unsigned grid, hipStream_t stream) {
+    if (grid >= 1024)
+        hipLaunchKernelGGL(saf::fixed_lse_kernel<6>, dim3(grid), dim3(saf::NORM_THREADS), 0, stream, na);
+    else
+        hipLaunchKernelGGL(saf::fixed_lse_kernel<1>, dim3(grid), dim3(saf::NORM_THREADS), 0, stream, na);
+}
+
 template <typename T>
 saf_status_t launch_fwd(const saf::FwdArgs& args, hipStream_t stream) {
-    if (args.fixed_mask) {
-        // Fixed-head row normalisers first: the main kernel reads them.
-        saf::NormArgs na;
-        na.a = args.a;
-        na.r = args.r;
-        na.lse = args.lse;
-        na.B = args.B;
-        na.H = args.H;
-        na.N = args.N;
-        na.ld_prior = args.ld_prior;
-        na.n_rblocks = (args.N + saf::NORM_ROWS - 1) / saf::NORM_ROWS;
-        na.n_fixed = 0;
-        for (int h = 0; h < args.H; ++h)
-            if ((args.fixed_mask >> h) & 1ull) na.heads[na.n_fixed++] = (unsigned char)h;
-        const unsigned ngrid = (unsigned)((size_t)na.n_rblocks * na.n_fixed);
-        hipLaunchKernelGGL(saf::fixed_lse_kernel<1>, dim3(ngrid), dim3(saf::NORM_THREADS), 0, stream, na);
-        if (launched() != SAF_OK) return SAF_ERR_LAUNCH;
-    }
+    // One launch: fixed heads form their own row normalisers.
     const unsigned grid = (unsigned)((size_t)args.n_qblocks * args.B * args.H);
     hipLaunchKernelGGL(saf::fwd_kernel<T>, dim3(grid), dim3(saf::FWD_THREADS), 0, stream, args);
     return launched();
@@ -370,7 +363,7 @@ SAF_EXPORT saf_status_t saf_hybrid_attn_fwd_gqa(saf_dtype_t dt, const void* Q, c
         for (int h = 0; h < Hq; ++h)
             if ((mask >> h) & 1ull) na.heads[na.n_fixed++] = (unsigned char)h;
         const unsigned ngrid = (unsigned)((size_t)na.n_rblocks * na.n_fixed);
-        hipLaunchKernelGGL(saf::fixed_lse_kernel<1>, dim3(ngrid), dim3(saf::NORM_THREADS), 0, stream, na);
+        launch_fixed_lse(na, ngrid, stream);
         if (launched() != SAF_OK) return SAF_ERR_LAUNCH;
     }
     saf::GqaArgs args;

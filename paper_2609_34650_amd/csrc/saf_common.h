@@ -354,8 +354,9 @@ __device__ __forceinline__ float dot8(const f32x8& x, const f32x8& y, float acc)
 //     order(m / B)), so every XCD gets an equal share of ordinary and fixed
 //     heads;
 //   * an XCD works through its slices level by level.
-// Otherwise workgroups go level by level with the slices in plain order.
-// Level 0 is dispatched first; kernels map it to their longest blocks.
+// Otherwise workgroups go level by level, each level dealing the slices in
+// order of decreasing work, rotated by one position per level.  Level 0 is
+// dispatched first; kernels map it to their longest blocks.
 // ---------------------------------------------------------------------------
 struct SliceOf {
     int level, b, h;
@@ -376,11 +377,16 @@ __device__ __forceinline__ SliceOf slice_of(unsigned blk, int B, int Hs, int gro
         s.b = m % B;
         s.h = order(m / B) * group + within % group;
     } else {
+        // Slices in order of decreasing work, rotated by one position per
+        // level, so that every XCD sees every slice over the levels (with a
+        // fixed order, a slice count such as 12 sends the same slices to the
+        // same XCD at every other level).
         const int n_bh = n_slices * group;
         s.level = (int)(blk / n_bh);
-        const int bh = (int)(blk % n_bh);
-        s.b = bh / (Hs * group);
-        s.h = bh % (Hs * group);
+        const int k = (int)((blk % n_bh + (unsigned)s.level) % n_bh);
+        const int m = k / group;  // rank of the slice by work
+        s.b = m % B;
+        s.h = order(m / B) * group + k % group;
     }
     return s;
 }

@@ -30,17 +30,18 @@
 //
 // Fixed heads (Eq. compact-prior): P(i,j) = exp(a[j] + r[i-j]) / Z(i) factors
 // as ea(j) * er(i-j) / Z'(i) with ea = exp(a - A*), er = exp(r - R*) and
-// A*, R* the maxima of a and r over the positions the block touches.  Each V
-// row is scaled by ea(j) while it is staged in LDS, so the weight tile is the
-// Toeplitz band er(i-j) -- read from LDS with no exponential, no score and no
-// softmax per element; a band entry of a negative offset is 0, which is the
-// causal mask.  The row normalisers are precomputed, as in the paper: a
-// pre-pass (fixed_lse_kernel) writes log Z(i) in float32 into LSE for every
-// batch element, and the block scales its accumulator by
-// exp(A* + R* - log Z(i)).  This is exact up to rounding as long as no row's
-// terms all underflow; a block where the largest of a row's diagonal and sink
-// terms lies more than FAST_GUARD below A* + R* runs the exact per-element
-// program instead.
+// A*, R* the maxima of a and r over the positions the block touches.  V
+// tiles come by buffer loads straight to LDS; the Toeplitz band er(i-j) is
+// kept in float32 in LDS beside ea of the tile's keys, and each chunk's
+// weight operand er(i-j) ea(j) is formed in float32 and rounded once -- no
+// exponential, no score and no softmax per element; a band entry of a
+// negative offset is 0, which is the causal mask.  The same float32 weights
+// are summed into Z'(i) as they are formed, so the block writes O = acc / Z'
+// and log Z = A* + R* + ln Z' itself (the paper precomputes the normalisers;
+// here no pre-pass is needed).  This is exact up to rounding as long as no
+// row's terms all underflow; a block where the largest of a row's diagonal
+// and sink terms lies more than FAST_GUARD below A* + R* runs the exact
+// per-element program instead, an online softmax that also writes log Z.
 #pragma once
 
 #include "saf_common.h"
@@ -349,12 +350,11 @@ __device__ __forceinline__ void fwd_fixed_exact(const Tiles<T>& sm, const FwdArg
             }
         }
     }
-    // LSE of fixed heads comes from the normaliser pre-pass.
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
         const float l_tot = pair_sum(l_run[qb]);
         store_rows<T>(reinterpret_cast<T*>(p.o) + base, p.lse + row_base, L, L.q0 + 32 * qb + L.c, oacc[qb],
-                      1.0f / l_tot, 0.0f, false);
+                      1.0f / l_tot, (m_run[qb] + __log2f(l_tot)) * LN2, true);
     }
 }
 
@@ -362,25 +362,18 @@ __device__ __forceinline__ void fwd_fixed_exact(const Tiles<T>& sm, const FwdArg
 // Fixed heads, factorised program
 // ---------------------------------------------------------------------------
 
-template <typename T>
+// Small per-tile values in registers between their loads (issued a tile
+// ahead) and their LDS stores: a of one key, two band entries.  V tiles come
+// by buffer loads straight to LDS, unscaled.
 struct FixStage {
-    u32x4 v[tile_units<T>()];  // this lane's 16-byte units of the V tile (one row)
-    float a;                   // a of that row's key
-    float rb[2];               // two band entries
+    float a;      // a of key n0 + L.tid (L.tid < FWD_BN)
+    float rb[2];  // band entries
 };
 
 // Band entry u of the tile at n0 holds offset (m0 - n0 + FWD_BM - 1) - u.
-template <typename T>
-__device__ __forceinline__ void fix_load(FixStage<T>& st, const T* V, const float* arow, const float* rrow, int n0,
+__device__ __forceinline__ void fix_load(FixStage& st, const float* arow, const float* rrow, int n0,
                                          const FwdLane& L) {
-    const int key = n0 + unit_row<T>(L.w, L.lane);
-    const bool ok = key < L.N;
-#pragma unroll
-    for (int k = 0; k < tile_units<T>(); ++k) {
-        const u32x4 z = {0u, 0u, 0u, 0u};
-        st.v[k] = ok ? ld_unit(V + (size_t)key * HEAD_DIM + unit_col<T>(L.w, L.lane, k)) : z;
-    }
-    st.a = ok ? arow[key] : -INFINITY;
+    st.a = (L.tid < FWD_BN && n0 + L.tid < L.N) ? arow[n0 + L.tid] : -INFINITY;
 #pragma unroll
     for (int k = 0; k < 2; ++k) {
         const int u = L.tid + FWD_THREADS * k;
@@ -389,29 +382,35 @@ __device__ __forceinline__ void fix_load(FixStage<T>& st, const T* V, const floa
     }
 }
 
-template <typename T>
-__device__ __forceinline__ void fix_store(T* vs, T* band, const FixStage<T>& st, const FwdLane& L, float a_sh,
+// eas: ea of the tile's keys; band: copy s of er (float32) at
+// s * FWD_BAND_STRIDE, FIX_BAND_COPIES copies (16-byte reads of float32 need
+// four).
+constexpr int FIX_BAND_COPIES = 4;
+static_assert(FIX_BAND_COPIES * FWD_BAND_STRIDE * 4 <= tile_elems<bf16>() * 2, "float32 band copies fit in a tile");
+
+__device__ __forceinline__ void fix_store(float* eas, float* band, const FixStage& st, const FwdLane& L, float a_sh,
                                           float r_sh) {
-    const float e = fast_exp2(fmaf(st.a, LOG2E, -a_sh));
-    const int row = unit_row<T>(L.w, L.lane);
-#pragma unroll
-    for (int k = 0; k < tile_units<T>(); ++k)
-        st_unit_scaled(vs + toff<T>(row, unit_col<T>(L.w, L.lane, k)), st.v[k], e);
+    if (L.tid < FWD_BN) eas[L.tid] = fast_exp2(fmaf(st.a, LOG2E, -a_sh));  // 0 past N
 #pragma unroll
     for (int k = 0; k < 2; ++k) {
         const int u = L.tid + FWD_THREADS * k;
         if (u < FWD_BAND) {
-            const T b = (T)fast_exp2(fmaf(st.rb[k], LOG2E, -r_sh));
+            const float e = fast_exp2(fmaf(st.rb[k], LOG2E, -r_sh));
 #pragma unroll
-            for (int s = 0; s < BAND_COPIES; ++s)
-                if (u >= s) band[s * FWD_BAND_STRIDE + u - s] = b;
+            for (int s = 0; s < FIX_BAND_COPIES; ++s)
+                if (u >= s) band[s * FWD_BAND_STRIDE + u - s] = e;
         }
     }
 }
 
+// O^T += V^T (band ea)^T: four 16-key chunks; the weight operand of lane
+// (query column c, half hf) in chunk G is band entries u0 .. u0 + 7 times ea
+// of keys 16G + 8hf .. 16G + 8hf + 7, formed in float32 and rounded once.
+// z[qb] collects this lane's share of the row sum Z'(i) of the float32
+// weights (the other lane half holds the other eight keys of each chunk).
 template <typename T, bool MASK>
-__device__ __forceinline__ void fix_tile(const T* vs, const T* band, int n0, const FwdLane& L,
-                                         f32x16 (&oacc)[2][2]) {
+__device__ __forceinline__ void fix_tile(const T* vs, const float* band, const float* eas, int n0, const FwdLane& L,
+                                         f32x16 (&oacc)[2][2], float (&z)[2]) {
     typedef typename Vec<T>::x8 frag;
 #pragma unroll
     for (int G = 0; G < 4; ++G) {
@@ -419,15 +418,27 @@ __device__ __forceinline__ void fix_tile(const T* vs, const T* band, int n0, con
         frag vf[2];
 #pragma unroll
         for (int db = 0; db < 2; ++db) vf[db] = ld_tile_t<false>(vs, 16 * G, 32 * db);
+        const f32x4 e0 = *reinterpret_cast<const f32x4*>(eas + 16 * G + 8 * L.hf);
+        const f32x4 e1 = *reinterpret_cast<const f32x4*>(eas + 16 * G + 8 * L.hf + 4);
 #pragma unroll
         for (int qb = 0; qb < 2; ++qb) {
             if (MASK && n0 + 16 * G > L.q0 + 32 * qb + 31) continue;
             const int ql = L.q0 - L.m0 + 32 * qb + L.c;  // query within the block
             const int u0 = (FWD_BM - 1) - ql + 16 * G + 8 * L.hf;
-            const int s = u0 & 7;
-            const frag b = ld8<T>(band + s * FWD_BAND_STRIDE + u0 - s);
+            const int s = u0 & (FIX_BAND_COPIES - 1);
+            const float* bp = band + s * FWD_BAND_STRIDE + u0 - s;
+            const f32x4 b0 = *reinterpret_cast<const f32x4*>(bp);
+            const f32x4 b1 = *reinterpret_cast<const f32x4*>(bp + 4);
+            frag w;
 #pragma unroll
-            for (int db = 0; db < 2; ++db) mma(oacc[qb][db], vf[db], b);
+            for (int t = 0; t < 4; ++t) {
+                const float x0 = b0[t] * e0[t], x1 = b1[t] * e1[t];
+                w[t] = (T)x0;
+                w[4 + t] = (T)x1;
+                z[qb] += x0 + x1;
+            }
+#pragma unroll
+            for (int db = 0; db < 2; ++db) mma(oacc[qb][db], vf[db], w);
         }
     }
 }
@@ -475,27 +486,37 @@ __device__ __forceinline__ void fwd_fixed(const Tiles<T>& sm, const FwdArgs& p, 
     const int n_full = L.m0 / FWD_BN;
     const int n_mask = n_tiles - n_full;
     const int P = (n_mask + 1) & ~1;
-    FixStage<T> st;
+    const __amdgpu_buffer_rsrc_t rv = slice_rsrc<T>(V, N);
+    float z[2] = {0.0f, 0.0f};
+    FixStage st;
     run_slots(
         P, P + n_full, [&](int i) { return i < P ? (i < n_mask ? n_full + i : -1) : i - P; },
-        [&](auto, int t) { fix_load<T>(st, V, arow, rrow, t * FWD_BN, L); },
-        [&](auto buf) { fix_store<T>(sm.t[decltype(buf)::value], sm.t[2 + decltype(buf)::value], st, L, a_sh, r_sh); },
+        [&](auto buf, int t) {
+            tile_load_lds<T>(sm.t[decltype(buf)::value], rv, t * FWD_BN, L.w, L.lane);
+            fix_load(st, arow, rrow, t * FWD_BN, L);
+        },
+        [&](auto buf) {
+            constexpr int b = decltype(buf)::value;
+            fix_store(sm.aux[b], reinterpret_cast<float*>(sm.t[2 + b]), st, L, a_sh, r_sh);
+        },
         [&](auto buf, int t, auto mask) {
-            fix_tile<T, decltype(mask)::value>(sm.t[decltype(buf)::value], sm.t[2 + decltype(buf)::value],
-                                               t * FWD_BN, L, oacc);
+            constexpr int b = decltype(buf)::value;
+            fix_tile<T, decltype(mask)::value>(sm.t[b], reinterpret_cast<const float*>(sm.t[2 + b]), sm.aux[b],
+                                               t * FWD_BN, L, oacc, z);
         });
-    // 1 / Z'(i) = exp(A + R - log Z(i)), with log Z from the normaliser pre-pass.
+    // O(i) = acc(i) / Z'(i) and log Z(i) = A + R + ln Z'(i), with Z'(i) the
+    // sum of the same float32 weights (the guard keeps it above e^-40).
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
-        const int qq = L.q0 + 32 * qb + L.c;
-        const float lse = qq < N ? p.lse[row_base + qq] : 0.0f;
-        const float inv = fast_exp2((A + R - lse) * LOG2E);
-        store_rows<T>(reinterpret_cast<T*>(p.o) + base, p.lse + row_base, L, qq, oacc[qb], inv, 0.0f, false);
+        const float zt = pair_sum(z[qb]);
+        store_rows<T>(reinterpret_cast<T*>(p.o) + base, p.lse + row_base, L, L.q0 + 32 * qb + L.c, oacc[qb],
+                      1.0f / zt, A + R + __log2f(zt) * LN2, true);
     }
 }
 
 // ---------------------------------------------------------------------------
-// Fixed-head normaliser pre-pass: LSE[b, h, i] = log Z(i) for every batch
+// Fixed-head normaliser pass (the compact fitter's log Z, and the grouped-query
+// forward's fixed heads): LSE[b, h, i] = log Z(i) for every batch
 // element b (Z depends on a and r only).  Workgroup = (fixed head, 32 rows);
 // eight threads share a row and each sums a 64-key slice of every 512-key
 // tile: Z'(i) = sum_j ea(j) er(i - j) in float32, with ea = exp(a - A_t) and
@@ -631,8 +652,10 @@ __global__ __launch_bounds__(FWD_THREADS) __attribute__((amdgpu_waves_per_eu(2))
     __shared__ __attribute__((aligned(16))) T t1[tile_elems<T>()];
     __shared__ __attribute__((aligned(16))) T t2[tile_elems<T>()];
     __shared__ __attribute__((aligned(16))) T t3[tile_elems<T>()];
+    __shared__ __attribute__((aligned(16))) float ea0[FWD_BN];
+    __shared__ __attribute__((aligned(16))) float ea1[FWD_BN];
     __shared__ float red[4];
-    const Tiles<T> sm = {{t0, t1, t2, t3}, {nullptr, nullptr}, red};
+    const Tiles<T> sm = {{t0, t1, t2, t3}, {ea0, ea1}, red};
     // Longest blocks first: level -> query block in descending order.
     const SliceOf sl = slice_of(blockIdx.x, p.B, p.H, 1, [&](int k) { return (int)p.head_order[k]; });
     const int qblk = p.n_qblocks - 1 - sl.level;
