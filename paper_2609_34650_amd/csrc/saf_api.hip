@@ -93,16 +93,6 @@ size_t pattern_workspace_bytes(int B, int H, int N) {
            align256(bh * g.n_kblocks * g.n_chunks * (size_t)g.part_len * 4);
 }
 
-// The normaliser pre-pass: with many workgroups (long sequences, many fixed
-// heads) the copy with a budget of six wavefronts per SIMD keeps more of them
-// in flight; with few, the copy with free registers finishes each sooner.
-void launch_fixed_lse(const saf::NormArgs& na, unsigned grid, hipStream_t stream) {
-    if (grid >= 1024)
-        hipLaunchKernelGGL(saf::fixed_lse_kernel<6>, dim3(grid), dim3(saf::NORM_THREADS), 0, stream, na);
-    else
-        hipLaunchKernelGGL(saf::fixed_lse_kernel<1>, dim3(grid), dim3(saf::NORM_THREADS), 0, stream, na);
-}
-
 template <typename T>
 saf_status_t launch_fwd(const saf::FwdArgs& args, hipStream_t stream) {
     // One launch: fixed heads form their own row normalisers.
@@ -349,23 +339,6 @@ SAF_EXPORT saf_status_t saf_hybrid_attn_fwd_gqa(saf_dtype_t dt, const void* Q, c
     if (pr.any_ordinary && (Q == nullptr || K == nullptr)) return SAF_ERR_NULL;
     if (!aligned16(V) || !aligned16(O) || !aligned16(LSE) || (Q && !aligned16(Q)) || (K && !aligned16(K)))
         return SAF_ERR_ALIGNMENT;
-    if (mask) {
-        saf::NormArgs na = {};
-        na.a = a;
-        na.r = r;
-        na.lse = LSE;
-        na.B = B;
-        na.H = Hq;
-        na.N = N;
-        na.ld_prior = ld_prior;
-        na.n_rblocks = (N + saf::NORM_ROWS - 1) / saf::NORM_ROWS;
-        na.n_fixed = 0;
-        for (int h = 0; h < Hq; ++h)
-            if ((mask >> h) & 1ull) na.heads[na.n_fixed++] = (unsigned char)h;
-        const unsigned ngrid = (unsigned)((size_t)na.n_rblocks * na.n_fixed);
-        launch_fixed_lse(na, ngrid, stream);
-        if (launched() != SAF_OK) return SAF_ERR_LAUNCH;
-    }
     saf::GqaArgs args;
     args.q = Q;
     args.k = K;
@@ -775,12 +748,12 @@ SAF_EXPORT saf_status_t saf_compact_fit(int H, int T, const float* eta_abs, cons
         p2 *= (double)saf::FIT_ADAM_BETA2;
         f.bc1 = (float)(1.0 - p1);
         f.bc2 = (float)(1.0 - p2);
-        hipLaunchKernelGGL(saf::fixed_lse_kernel<6>, dim3(lse_grid), dim3(saf::NORM_THREADS), 0, stream, na);
+        hipLaunchKernelGGL(saf::fixed_lse_kernel, dim3(lse_grid), dim3(saf::NORM_THREADS), 0, stream, na);
         hipLaunchKernelGGL(saf::fit_marginals_kernel, dim3(marg_grid), dim3(saf::FIT_COLS), 0, stream, f);
         hipLaunchKernelGGL(saf::fit_adam_kernel, dim3(elem_grid), dim3(256), 0, stream, f);
         if (launched() != SAF_OK) return SAF_ERR_LAUNCH;
     }
-    hipLaunchKernelGGL(saf::fixed_lse_kernel<6>, dim3(lse_grid), dim3(saf::NORM_THREADS), 0, stream, na);
+    hipLaunchKernelGGL(saf::fixed_lse_kernel, dim3(lse_grid), dim3(saf::NORM_THREADS), 0, stream, na);
     hipLaunchKernelGGL(saf::fit_kl_kernel, dim3(H), dim3(256), 0, stream, f);
     return launched();
 }

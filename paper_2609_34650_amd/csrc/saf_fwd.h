@@ -515,20 +515,18 @@ __device__ __forceinline__ void fwd_fixed(const Tiles<T>& sm, const FwdArgs& p, 
 }
 
 // ---------------------------------------------------------------------------
-// Fixed-head normaliser pass (the compact fitter's log Z, and the grouped-query
-// forward's fixed heads): LSE[b, h, i] = log Z(i) for every batch
+// Fixed-head normaliser pass (the compact fitter's log Z of each step):
+// LSE[b, h, i] = log Z(i) for every batch
 // element b (Z depends on a and r only).  Workgroup = (fixed head, 32 rows);
 // eight threads share a row and each sums a 64-key slice of every 512-key
 // tile: Z'(i) = sum_j ea(j) er(i - j) in float32, with ea = exp(a - A_t) and
 // er = exp(r - R_t) shifted by the tile's maxima A_t, R_t; the tiles combine
 // online under the largest shift M seen so far, so log Z = M + log Z'.  A
 // row whose Z' ends below 2^-80 (its terms underflowed) is summed exactly,
-// with a running maximum.  WAVES: the wavefronts per SIMD the register
-// budget must allow.  The fitter, which launches 1536 workgroups per step,
-// asks for six (about 80 VGPRs; left free, the scheduler hoists every LDS
-// read of the key loop into registers: 164 VGPRs, three wavefronts per SIMD,
-// 7 % slower); the layer's few workgroups (one per fixed head and 32 rows)
-// run fastest with the registers free (WAVES = 1).
+// with a running maximum.  A budget of six wavefronts per SIMD (about 80
+// VGPRs): the fitter launches 1536 workgroups per step, and left free the
+// scheduler hoists every LDS read of the key loop into registers (164
+// VGPRs, three wavefronts per SIMD, 7 % slower).
 // ---------------------------------------------------------------------------
 constexpr int NORM_THREADS = 256;
 constexpr int NORM_ROWS = 32;
@@ -545,8 +543,7 @@ struct NormArgs {
     unsigned char heads[64];  // the fixed heads, ascending
 };
 
-template <int WAVES>
-__global__ __launch_bounds__(NORM_THREADS) __attribute__((amdgpu_waves_per_eu(WAVES))) void fixed_lse_kernel(
+__global__ __launch_bounds__(NORM_THREADS) __attribute__((amdgpu_waves_per_eu(6))) void fixed_lse_kernel(
     NormArgs p) {
     __shared__ __attribute__((aligned(16))) float ea_s[NORM_KT];
     __shared__ float er_s[NORM_BAND + 1];

@@ -18,16 +18,17 @@
 //   exceeds it, accumulator and sum rescaled), O^T += V^T P^T on MFMA, LSE =
 //   m + ln l.
 //   Fixed head, factorised (as in the layer forward): P(i, j) =
-//   ea(j) er(i - j) exp(A + R - log Z(i)) with ea = exp(a - A), er =
-//   exp(r - R) and A, R the maxima of a and r over the block's positions.  V
-//   tiles come by buffer loads to LDS unscaled, and the weight operand is
-//   the Toeplitz band er (float32 in LDS, eight shifted copies keep every
-//   8-entry read aligned) times ea of the chunk's keys, formed in float32
-//   and rounded once: no exponential per entry.  log Z comes from the normaliser pre-pass (the layer forward's
-//   fixed_lse_kernel).  A block where some row's diagonal and sink terms both
-//   lie more than FAST_GUARD below A + R takes the exact per-entry program:
-//   P(i, j) = exp(a[j] + r[i - j] - log Z(i)) with the tile's a values and r
-//   band staged in LDS.
+//   ea(j) er(i - j) / Z'(i) with ea = exp(a - A), er = exp(r - R) and A, R
+//   the maxima of a and r over the block's positions.  V tiles come by
+//   buffer loads to LDS unscaled, and the weight operand is the Toeplitz
+//   band er (float32 in LDS, eight shifted copies keep every 8-entry read
+//   aligned) times ea of the chunk's keys, formed in float32 and rounded
+//   once: no exponential per entry.  The same weights are summed into Z'(i),
+//   so O = acc / Z' and LSE = log Z = A + R + ln Z' come out of this kernel.
+//   A block where some row's diagonal and sink terms both lie more than
+//   FAST_GUARD below A + R takes the exact per-entry program: the logits
+//   a[j] + r[i - j] (the tile's a values and r band staged in LDS) through
+//   an online softmax, as for an ordinary head's scores.
 #pragma once
 
 #include "saf_common.h"
@@ -114,11 +115,13 @@ __device__ __forceinline__ void gqa_ord_tile(const T* kt, const T* vt, int n0, c
     }
 }
 
-// One 64-key tile of a fixed head.  as[k]: a of the tile's key k; rb[x]:
-// r(m0 - n0 - 63 + x); lz: log Z of this lane's query.
+// One 64-key tile of a fixed head, exact program: the logits a[j] + r[i - j]
+// of each 32-key sub-block (as[k]: a of the tile's key k; rb[x]:
+// r(m0 - n0 - 63 + x)) go through the same online softmax as an ordinary
+// head's scores (running maximum raised when a sub-block exceeds it).
 template <typename T, int D, bool MASK>
 __device__ __forceinline__ void gqa_fix_tile(const T* vt, const float* as, const float* rb, int n0, const GqaLane& L,
-                                             float lz, f32x16 (&oacc)[D / 32]) {
+                                             f32x16 (&oacc)[D / 32], float& m_run, float& l_run) {
     typedef typename Vec<T>::x8 frag;
     const int qq = L.q0 + L.c;
     const int ql = qq - L.m0;
@@ -126,14 +129,34 @@ __device__ __forceinline__ void gqa_fix_tile(const T* vt, const float* as, const
     for (int kb = 0; kb < 2; ++kb) {
         const int k0 = n0 + 32 * kb;
         if (MASK && k0 > L.q0 + 31) break;
-        f32x16 pr;
+        f32x16 sc;
+        float mx = -INFINITY;
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
             const int kl = 32 * kb + 8 * (v >> 2) + 4 * L.hf + (v & 3);  // key within the tile
-            float x = fast_exp2((as[kl] + rb[ql - kl + (GQA_BN - 1)] - lz) * LOG2E);
-            if (MASK && n0 + kl > qq) x = 0.0f;
-            pr[v] = x;
+            float x = (as[kl] + rb[ql - kl + (GQA_BN - 1)]) * LOG2E;
+            if (MASK && n0 + kl > qq) x = -INFINITY;
+            sc[v] = x;
+            mx = vmax(mx, x);
         }
+        mx = pair_max(mx);
+        if (mx > m_run) {
+            const float alpha = fast_exp2(m_run - mx);
+            m_run = mx;
+            l_run *= alpha;
+#pragma unroll
+            for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) oacc[db][v] *= alpha;
+        }
+        f32x16 pr;
+        float t = 0.0f;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            pr[v] = fast_exp2(sc[v] - m_run);
+            t += pr[v];
+        }
+        l_run += t;
         frag pb[2];
 #pragma unroll
         for (int kc = 0; kc < 2; ++kc) pb[kc] = to_operand<T>(pr, 8 * kc);
@@ -178,9 +201,10 @@ __device__ __forceinline__ void gqa_fix_store(float* eas, float* band, const Gqa
 // 127 - ql + 16G + 8hf, read from copy u0 % 8 at an aligned address) times
 // ea of keys 16G + 8hf .. 16G + 8hf + 7, formed in float32 and rounded once.
 // Offsets below zero hold 0, which masks the keys after the query.
+// z collects this lane's share of the row sum Z'(i) of the float32 weights.
 template <typename T, int D, bool MASK>
 __device__ __forceinline__ void gqa_band_tile(const T* vs, const float* band, const float* eas, int n0,
-                                              const GqaLane& L, f32x16 (&oacc)[D / 32]) {
+                                              const GqaLane& L, f32x16 (&oacc)[D / 32], float& z) {
     typedef typename Vec<T>::x8 frag;
     const int ql = L.q0 - L.m0 + L.c;
 #pragma unroll
@@ -196,8 +220,10 @@ __device__ __forceinline__ void gqa_band_tile(const T* vs, const float* band, co
         frag b;
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
-            b[t] = (T)(b0[t] * e0[t]);
-            b[4 + t] = (T)(b1[t] * e1[t]);
+            const float x0 = b0[t] * e0[t], x1 = b1[t] * e1[t];
+            b[t] = (T)x0;
+            b[4 + t] = (T)x1;
+            z += x0 + x1;
         }
 #pragma unroll
         for (int db = 0; db < D / 32; ++db) mma(oacc[db], ld_tile_t<false>(vs, 16 * G, 32 * db), b);
@@ -279,7 +305,6 @@ __global__ __launch_bounds__(GQA_THREADS) __attribute__((amdgpu_waves_per_eu(2))
     } else {
         const float* arow = p.a + (size_t)h * p.ld_prior;
         const float* rrow = p.r + (size_t)h * p.ld_prior;
-        const float lz = qq < N ? p.lse[row_base + qq] : 0.0f;
         const int m1 = min(L.m0 + GQA_BM, N);
         float am = -INFINITY, rm = -INFINITY;
         for (int j = L.tid; j < m1; j += GQA_THREADS) {
@@ -296,6 +321,7 @@ __global__ __launch_bounds__(GQA_THREADS) __attribute__((amdgpu_waves_per_eu(2))
         if (__syncthreads_and(ok)) {
             // K is never read for a fixed head: its tiles hold the band.
             const float a_sh = A * LOG2E, r_sh = R * LOG2E;
+            float z = 0.0f;
             GqaFixStage st;
             run_slots(
                 P, P + n_full, tile_of,
@@ -311,10 +337,15 @@ __global__ __launch_bounds__(GQA_THREADS) __attribute__((amdgpu_waves_per_eu(2))
                     constexpr int B_ = decltype(buf)::value;
                     gqa_band_tile<T, D, decltype(mask)::value>(B_ ? v1s : v0s,
                                                                reinterpret_cast<const float*>(B_ ? k1s : k0s),
-                                                               B_ ? ab1 : ab0, t * GQA_BN, L, oacc);
+                                                               B_ ? ab1 : ab0, t * GQA_BN, L, oacc, z);
                 });
-            row_scale = fast_exp2((A + R - lz) * LOG2E);
-        } else run_slots(
+            // O = acc / Z' and log Z = A + R + ln Z' (the guard keeps Z' above e^-40).
+            const float zt = pair_sum(z);
+            row_scale = 1.0f / zt;
+            lse_out = A + R + __log2f(zt) * LN2;
+        } else {
+            float m_run = NEG_BIG, l_run = 0.0f;
+            run_slots(
             P, P + n_full, tile_of,
             [&](auto buf, int t) {
                 constexpr int B_ = decltype(buf)::value;
@@ -337,8 +368,13 @@ __global__ __launch_bounds__(GQA_THREADS) __attribute__((amdgpu_waves_per_eu(2))
             [&](auto buf, int t, auto mask) {
                 constexpr int B_ = decltype(buf)::value;
                 const float* ab = B_ ? ab1 : ab0;
-                gqa_fix_tile<T, D, decltype(mask)::value>(B_ ? v1s : v0s, ab, ab + GQA_BN, t * GQA_BN, L, lz, oacc);
+                gqa_fix_tile<T, D, decltype(mask)::value>(B_ ? v1s : v0s, ab, ab + GQA_BN, t * GQA_BN, L, oacc,
+                                                          m_run, l_run);
             });
+            const float l_tot = pair_sum(l_run);
+            row_scale = 1.0f / l_tot;
+            lse_out = (m_run + __log2f(l_tot)) * LN2;
+        }
     }
     if (qq < N) {
         T* orow = reinterpret_cast<T*>(p.o) + qbase + (size_t)qq * D;
@@ -349,7 +385,7 @@ __global__ __launch_bounds__(GQA_THREADS) __attribute__((amdgpu_waves_per_eu(2))
                 st4<T>(orow + 32 * db + 8 * g + 4 * L.hf, oacc[db][4 * g] * row_scale,
                        oacc[db][4 * g + 1] * row_scale, oacc[db][4 * g + 2] * row_scale,
                        oacc[db][4 * g + 3] * row_scale);
-        if (!fixed && L.hf == 0) p.lse[row_base + qq] = lse_out;
+        if (L.hf == 0) p.lse[row_base + qq] = lse_out;
     }
 }
 
