@@ -2,8 +2,10 @@
 """Benchmark of the fused hybrid causal-attention layer (forward + backward)
 on one MI355X.
 
-One step = one full layer: the forward launch followed by the three backward
-launches, over one batch of synthetic inputs already resident in HBM.  The
+One step = one full layer: the forward launch followed by the backward's two
+launches (the query-block pass, which also forms D = rowsum(dO * O), then the
+key-block pass: what saf_hybrid_attn_bwd enqueues), over one batch of
+synthetic inputs already resident in HBM.  The
 default workload is the 124M-style layer: B=8, H=12 with 3 fixed heads (25 %),
 N=4096, d=64, bf16 with float32 accumulation.
 
@@ -101,9 +103,8 @@ def layer_flop(B: int, H: int, N: int, d: int, n_fixed: int, backward: bool = Tr
     n_ord = H - n_fixed
     out = {"fwd": c * (2 * n_ord + 1 * n_fixed)}
     if backward:
-        out["bwd_pre"] = 0.0
-        out["bwd_dkdv"] = c * (4 * n_ord + 1 * n_fixed)
         out["bwd_dq"] = c * (1 * n_ord)
+        out["bwd_dkdv"] = c * (4 * n_ord + 1 * n_fixed)
     return out
 
 
@@ -114,9 +115,9 @@ def stage_bytes(B: int, H: int, N: int, d: int, n_fixed: int, elem: int):
     n_ord = H - n_fixed
     return {
         "fwd": n_ord * (3 * t + t + row) + n_fixed * (t + t + row),
-        "bwd_pre": n_ord * (2 * t + row),
+        # query-block pass: Q, K, V, dO, O and LSE read; dQ and D written
+        "bwd_dq": n_ord * (5 * t + row + t + row) + n_fixed * t,
         "bwd_dkdv": n_ord * (4 * t + 2 * row + 2 * t) + n_fixed * (t + row + 2 * t),
-        "bwd_dq": n_ord * (4 * t + 2 * row + t) + n_fixed * t,
     }
 
 
@@ -221,7 +222,8 @@ class Layer:
             self.dQ, self.dK, self.dV = (torch.empty_like(self.V) for _ in range(3))
             nbytes = binding.saf_hybrid_attn_bwd_workspace_bytes(tdt, B, H, N, d)
             self.ws = torch.empty(nbytes, dtype=torch.uint8, device=dev)
-        self.stages = ["fwd"] + (["bwd_pre", "bwd_dkdv", "bwd_dq"] if backward else [])
+        # The backward's two launches, as saf_hybrid_attn_bwd enqueues them.
+        self.stages = ["fwd"] + (["bwd_dq", "bwd_dkdv"] if backward else [])
 
     def step(self, flags, events=None):
         b = self.b
@@ -232,7 +234,7 @@ class Layer:
         if ev is not None:
             ev[1].record()
         if self.backward:
-            for i, st in enumerate((b.SAF_BWD_PREPROCESS, b.SAF_BWD_DKDV, b.SAF_BWD_DQ)):
+            for i, st in enumerate((b.SAF_BWD_DQ_WITH_D, b.SAF_BWD_DKDV)):
                 b.saf_hybrid_attn_bwd_stage(st, self.Q, self.K, self.V, self.O, self.dO, self.LSE, flags,
                                             self.a, self.r, self.dQ, self.dK, self.dV, self.ws)
                 if ev is not None:

@@ -129,9 +129,10 @@ size_t saf_hybrid_attn_bwd_gqa_workspace_bytes(saf_dtype_t dt, int B, int Hq, in
  * saf_hybrid_attn_bwd, fixed query heads add P^T dO to dV only and get exact
  * zeros in dQ (the grouped-query path keeps every shared key/value head and
  * maps each ordinary query head to its group, Appendix "Mixed-head execution
- * and numerical checks").  Three launches: row pre-pass, key-block pass (one
- * workgroup per batch element, key/value head and 128 keys, looping over the
- * group), query-block pass.
+ * and numerical checks").  Two launches: the query-block pass, which also
+ * forms D = rowsum(dO * O) of the ordinary heads and writes it to the
+ * workspace, then the key-block pass (one workgroup per batch element,
+ * key/value head and 128 keys, looping over the group).
  *   Q, O, dO : [B, Hq, N, d] `dt` (O and LSE as written by
  *              saf_hybrid_attn_fwd_gqa);  LSE : [B, Hq, N] float32;
  *   K, V     : [B, Hkv, N, d] `dt`;
@@ -182,17 +183,22 @@ saf_status_t saf_hybrid_attn_bwd(saf_dtype_t dt,
                                  void* workspace, size_t workspace_bytes,
                                  hipStream_t stream);
 
-/* The backward as three separate launches, enqueued one at a time (same
- * arguments and contract): a row pre-pass that writes D into the workspace,
- * the key-block pass and the query-block pass (both read D).  Running
- * SAF_BWD_PREPROCESS, then SAF_BWD_DKDV and SAF_BWD_DQ (in either order) on
- * one stream with one workspace gives what saf_hybrid_attn_bwd gives, up to
- * the float32 rounding of D (saf_hybrid_attn_bwd forms D inside its
- * query-block pass).  DKDV writes dK and dV; DQ writes dQ. */
+/* The backward's launches, enqueued one at a time (same arguments and
+ * contract).  Two sequences give the gradients, on one stream with one
+ * workspace:
+ *   SAF_BWD_DQ_WITH_D, then SAF_BWD_DKDV: exactly the launches of
+ *     saf_hybrid_attn_bwd (the query-block pass forms D = rowsum(dO * O)
+ *     from the dO fragments it holds and writes it into the workspace);
+ *   SAF_BWD_PREPROCESS (a row pre-pass that writes D), then SAF_BWD_DKDV
+ *     and SAF_BWD_DQ in either order (both read D): the same gradients up
+ *     to the float32 rounding order of D.
+ * DKDV writes dK and dV; DQ and DQ_WITH_D write dQ.  Any other value is
+ * SAF_ERR_UNSUPPORTED. */
 typedef enum {
     SAF_BWD_PREPROCESS = 0,
     SAF_BWD_DKDV = 1,
-    SAF_BWD_DQ = 2
+    SAF_BWD_DQ = 2,
+    SAF_BWD_DQ_WITH_D = 3
 } saf_bwd_stage_t;
 
 saf_status_t saf_hybrid_attn_bwd_stage(saf_bwd_stage_t stage, saf_dtype_t dt,

@@ -25,6 +25,7 @@ SAF_DTYPE_BF16 = 1
 SAF_BWD_PREPROCESS = 0
 SAF_BWD_DKDV = 1
 SAF_BWD_DQ = 2
+SAF_BWD_DQ_WITH_D = 3
 
 STATUS = {
     0: "SAF_OK",
@@ -341,9 +342,11 @@ def saf_hybrid_attn_bwd(Q, K, V, O, dO, LSE, head_is_fixed, a=None, r=None, dQ=N
 
 def saf_hybrid_attn_bwd_stage(stage: int, Q, K, V, O, dO, LSE, head_is_fixed, a=None, r=None, dQ=None,
                               dK=None, dV=None, workspace: Optional[torch.Tensor] = None):
-    """One of the three launches of the backward (``SAF_BWD_PREPROCESS``,
-    ``SAF_BWD_DKDV``, ``SAF_BWD_DQ``); returns ``(dQ, dK, dV)`` as passed or
-    allocated.  Pass the same ``workspace`` to every stage."""
+    """One launch of the backward (``SAF_BWD_PREPROCESS``, ``SAF_BWD_DKDV``,
+    ``SAF_BWD_DQ``, ``SAF_BWD_DQ_WITH_D``); returns ``(dQ, dK, dV)`` as passed
+    or allocated.  Pass the same ``workspace`` to every stage:
+    ``SAF_BWD_DQ_WITH_D`` then ``SAF_BWD_DKDV`` are the launches of
+    ``saf_hybrid_attn_bwd``."""
     lib = load()
     args, outs, _flags_keep, _ws_keep = _bwd_common(Q, K, V, O, dO, LSE, head_is_fixed, a, r, dQ, dK, dV,
                                                     workspace)

@@ -126,6 +126,9 @@ saf_status_t launch_bwd_stage(saf_bwd_stage_t stage, const saf::BwdArgs& base, h
         const unsigned grid = (unsigned)((size_t)args.n_blocks * args.B * args.H);
         hipLaunchKernelGGL(saf::bwd_kv_kernel<T>, dim3(grid), dim3(saf::KV_THREADS), 0, stream, args);
     } else {
+        // SAF_BWD_DQ reads D from the workspace; SAF_BWD_DQ_WITH_D forms it
+        // and writes it there for a key-block pass enqueued after it.
+        args.dq_writes_dsum = stage == SAF_BWD_DQ_WITH_D ? 1 : 0;
         args.n_blocks = (args.N + saf::DQ_BM - 1) / saf::DQ_BM;
         const unsigned grid = (unsigned)((size_t)args.n_blocks * args.B * args.H);
         hipLaunchKernelGGL(saf::bwd_dq_kernel<T>, dim3(grid), dim3(saf::DQ_THREADS), 0, stream, args);
@@ -137,7 +140,8 @@ saf_status_t check_bwd(saf_bwd_stage_t stage, saf_dtype_t dt, const void* Q, con
                        const void* O, const void* dO, const float* LSE, const uint8_t* head_is_fixed,
                        const float* a, const float* r, int ld_prior, int B, int H, int N, int d, void* dQ,
                        void* dK, void* dV, void* workspace, size_t workspace_bytes_given, Problem* pr) {
-    if (stage != SAF_BWD_PREPROCESS && stage != SAF_BWD_DKDV && stage != SAF_BWD_DQ) return SAF_ERR_UNSUPPORTED;
+    if (stage != SAF_BWD_PREPROCESS && stage != SAF_BWD_DKDV && stage != SAF_BWD_DQ && stage != SAF_BWD_DQ_WITH_D)
+        return SAF_ERR_UNSUPPORTED;
     saf_status_t st = check_common(dt, head_is_fixed, a, r, ld_prior, B, H, N, d, pr);
     if (st != SAF_OK || pr->empty) return st;
     if (V == nullptr || O == nullptr || dO == nullptr || LSE == nullptr || dQ == nullptr || dK == nullptr ||
@@ -310,19 +314,16 @@ size_t gqa_workspace_bytes(int B, int Hq, int N) {
 }
 
 template <typename T, int D>
-void launch_gqa_bwd(const saf::GqaBwdArgs& base, bool any_ordinary, hipStream_t stream) {
+void launch_gqa_bwd(const saf::GqaBwdArgs& base, hipStream_t stream) {
     saf::GqaBwdArgs args = base;
-    if (any_ordinary) {
-        const size_t rows = (size_t)args.B * args.Hq * args.N;
-        const unsigned grid = (unsigned)((rows + saf::GPRE_ROWS - 1) / saf::GPRE_ROWS);
-        hipLaunchKernelGGL((saf::gqa_bwd_pre_kernel<T, D>), dim3(grid), dim3(saf::GPRE_THREADS), 0, stream, args);
-    }
-    args.n_blocks = (args.N + saf::GKV_BN - 1) / saf::GKV_BN;
-    hipLaunchKernelGGL((saf::gqa_bwd_kv_kernel<T, D>), dim3((unsigned)((size_t)args.n_blocks * args.B * args.Hkv)),
-                       dim3(saf::GKV_THREADS), 0, stream, args);
+    // The query-block pass runs first: it forms D of the ordinary heads'
+    // rows and writes it to the workspace for the key-block pass.
     args.n_blocks = (args.N + saf::GDQ_BM - 1) / saf::GDQ_BM;
     hipLaunchKernelGGL((saf::gqa_bwd_dq_kernel<T, D>), dim3((unsigned)((size_t)args.n_blocks * args.B * args.Hq)),
                        dim3(saf::GDQ_THREADS), 0, stream, args);
+    args.n_blocks = (args.N + saf::GKV_BN - 1) / saf::GKV_BN;
+    hipLaunchKernelGGL((saf::gqa_bwd_kv_kernel<T, D>), dim3((unsigned)((size_t)args.n_blocks * args.B * args.Hkv)),
+                       dim3(saf::GKV_THREADS), 0, stream, args);
 }
 
 }  // namespace
@@ -412,12 +413,12 @@ SAF_EXPORT saf_status_t saf_hybrid_attn_bwd_gqa(saf_dtype_t dt, const void* Q, c
     args.scale_log2 = saf::LOG2E / sqrtf((float)d);
     fill_kv_order(args.kv_order, pr.mask, Hq, Hkv);
     const bool bf = dt == SAF_DTYPE_BF16;
-    if (d == 64) bf ? launch_gqa_bwd<saf::bf16, 64>(args, pr.any_ordinary, stream)
-                    : launch_gqa_bwd<float, 64>(args, pr.any_ordinary, stream);
-    else if (d == 96) bf ? launch_gqa_bwd<saf::bf16, 96>(args, pr.any_ordinary, stream)
-                         : launch_gqa_bwd<float, 96>(args, pr.any_ordinary, stream);
-    else bf ? launch_gqa_bwd<saf::bf16, 128>(args, pr.any_ordinary, stream)
-            : launch_gqa_bwd<float, 128>(args, pr.any_ordinary, stream);
+    if (d == 64) bf ? launch_gqa_bwd<saf::bf16, 64>(args, stream)
+                    : launch_gqa_bwd<float, 64>(args, stream);
+    else if (d == 96) bf ? launch_gqa_bwd<saf::bf16, 96>(args, stream)
+                         : launch_gqa_bwd<float, 96>(args, stream);
+    else bf ? launch_gqa_bwd<saf::bf16, 128>(args, stream)
+            : launch_gqa_bwd<float, 128>(args, stream);
     return launched();
 }
 
@@ -456,9 +457,7 @@ SAF_EXPORT saf_status_t saf_hybrid_attn_bwd(saf_dtype_t dt, const void* Q, const
         make_bwd_args(Q, K, V, O, dO, LSE, a, r, ld_prior, B, H, N, dQ, dK, dV, workspace, pr);
     // The query-block pass forms D itself and writes it for the key-block
     // pass, so no row pre-pass runs here.
-    saf::BwdArgs fused = args;
-    fused.dq_writes_dsum = 1;
-    st = run_bwd_stage(SAF_BWD_DQ, dt, fused, stream);
+    st = run_bwd_stage(SAF_BWD_DQ_WITH_D, dt, args, stream);
     if (st != SAF_OK) return st;
     return run_bwd_stage(SAF_BWD_DKDV, dt, args, stream);
 }

@@ -446,7 +446,7 @@ __device__ __forceinline__ void fix_tile(const T* vs, const float* band, const f
 template <typename T>
 __device__ __forceinline__ void fwd_fixed(const Tiles<T>& sm, const FwdArgs& p, const FwdLane& L, size_t base,
                                           size_t row_base, int h) {
-    // Tiles: ea * V in t[0] / t[1], the band in t[2] / t[3].
+    // Tiles: V in t[0] / t[1], the float32 band in t[2] / t[3], ea in aux.
     const T* __restrict__ V = reinterpret_cast<const T*>(p.v) + base;
     const float* __restrict__ arow = p.a + (size_t)h * p.ld_prior;
     const float* __restrict__ rrow = p.r + (size_t)h * p.ld_prior;

@@ -36,47 +36,13 @@ struct GqaBwdArgs {
     void* dq;
     void* dk;
     void* dv;
-    float* dsum;  // workspace: D, [B, Hq, N]
+    float* dsum;  // workspace: D, [B, Hq, N], written by the query-block pass, read by the key-block pass
     uint64_t fixed_mask;
     int B, Hq, Hkv, N, ld_prior, n_blocks;
     float scale;       // 1 / sqrt(D)
     float scale_log2;  // log2(e) / sqrt(D)
     unsigned char kv_order[64];  // key/value heads by decreasing work (slice_of)
 };
-
-// ---------------------------------------------------------------------------
-// Row pre-pass: eight lanes per row, D / 8 columns each.
-// ---------------------------------------------------------------------------
-constexpr int GPRE_THREADS = 256;
-constexpr int GPRE_ROWS = GPRE_THREADS / 8;
-
-template <typename T, int D>
-__global__ __launch_bounds__(GPRE_THREADS) void gqa_bwd_pre_kernel(GqaBwdArgs p) {
-    const size_t total = (size_t)p.B * p.Hq * p.N;
-    const size_t row = (size_t)blockIdx.x * GPRE_ROWS + (threadIdx.x >> 3);
-    const int part = threadIdx.x & 7;
-    float acc = 0.0f;
-    bool live = row < total;
-    if (live) {
-        const int h = (int)((row / p.N) % p.Hq);
-        live = !((p.fixed_mask >> h) & 1ull);
-    }
-    if (live) {
-        const T* o = reinterpret_cast<const T*>(p.o) + row * D + part * (D / 8);
-        const T* g = reinterpret_cast<const T*>(p.dO) + row * D + part * (D / 8);
-#pragma unroll
-        for (int c = 0; c < D / 8; c += 4) {
-            const typename Vec<T>::x4 ov = *reinterpret_cast<const typename Vec<T>::x4*>(o + c);
-            const typename Vec<T>::x4 gv = *reinterpret_cast<const typename Vec<T>::x4*>(g + c);
-#pragma unroll
-            for (int t = 0; t < 4; ++t) acc += (float)ov[t] * (float)gv[t];
-        }
-    }
-    acc += __shfl_xor(acc, 1);
-    acc += __shfl_xor(acc, 2);
-    acc += __shfl_xor(acc, 4);
-    if (row < total && part == 0) p.dsum[row] = acc;
-}
 
 // ---------------------------------------------------------------------------
 // Key-block pass.  A lane holds one key (l % 32) of its wavefront's 32 and,
@@ -520,7 +486,20 @@ __global__ __launch_bounds__(GDQ_THREADS) __attribute__((amdgpu_waves_per_eu(2))
     }
     const size_t row_base = ((size_t)b * p.Hq + h) * N;
     const float lse2 = L.qq < N ? p.lse[row_base + L.qq] * LOG2E : INFINITY;
-    const float dsum = L.qq < N ? p.dsum[row_base + L.qq] : 0.0f;
+    // D_i = sum_c dO * O of this lane's query, from the dO fragments already
+    // in registers and O's matching columns; written for the key-block pass,
+    // which runs after this one.
+    float dsum;
+    {
+        const T* __restrict__ Orow = reinterpret_cast<const T*>(p.o) + qbase + (size_t)L.qq * D;
+        float part = 0.0f;
+        if (L.qq < N) {
+#pragma unroll
+            for (int dc = 0; dc < D / 16; ++dc) part = dot8(ld8<T>(Orow + 16 * dc + 8 * L.hf), gf[dc], part);
+        }
+        dsum = pair_sum(part);
+        if (L.qq < N && L.hf == 0) p.dsum[row_base + L.qq] = dsum;
+    }
 
     f32x16 dq[D / 32];
 #pragma unroll

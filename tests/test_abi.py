@@ -97,7 +97,7 @@ def test_empty_problems_are_no_ops(lib):
 
 
 def test_backward_argument_errors(lib):
-    for stage in (None, 0, 1, 2):
+    for stage in (None, 0, 1, 2, 3):
         assert _bwd(lib, stage, dt=9) == 3
         assert _bwd(lib, stage, d=96) == 3
         assert _bwd(lib, stage, a=None) == 4
@@ -108,7 +108,8 @@ def test_backward_argument_errors(lib):
         assert _bwd(lib, stage, dK=FAKE + 2) == 6
         assert _bwd(lib, stage, flags=(3, 0)) == 7
         assert _bwd(lib, stage, B=0) == 0
-    assert _bwd(lib, 5) == 3                           # unknown stage
+    assert _bwd(lib, 4) == 3                           # unknown stage
+    assert _bwd(lib, -1) == 3
 
 
 def test_workspace_size(lib):

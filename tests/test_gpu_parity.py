@@ -268,13 +268,27 @@ def test_stages_equal_full_backward():
     full = binding.saf_hybrid_attn_bwd(t["Q"], t["K"], t["V"], O, t["dO"], L, t["is_fixed"], t["a"], t["r"])
     nbytes = binding.saf_hybrid_attn_bwd_workspace_bytes(torch.bfloat16, 1, 3, 260, 64)
     ws = torch.empty(nbytes, dtype=torch.uint8, device=O.device)
+    # The fused entry's own launches: bit-identical.
     dQ, dK, dV = (torch.empty_like(O) for _ in range(3))
-    for st in (binding.SAF_BWD_PREPROCESS, binding.SAF_BWD_DQ, binding.SAF_BWD_DKDV):
+    for st in (binding.SAF_BWD_DQ_WITH_D, binding.SAF_BWD_DKDV):
         binding.saf_hybrid_attn_bwd_stage(st, t["Q"], t["K"], t["V"], O, t["dO"], L, t["is_fixed"], t["a"],
                                           t["r"], dQ, dK, dV, ws)
     torch.cuda.synchronize()
     for x, y in zip(full, (dQ, dK, dV)):
         assert torch.equal(x, y)
+    # With the row pre-pass, D is summed in another order: equal to the
+    # rounding of one bf16 ulp of the gradients.
+    for order in ((binding.SAF_BWD_PREPROCESS, binding.SAF_BWD_DQ, binding.SAF_BWD_DKDV),
+                  (binding.SAF_BWD_PREPROCESS, binding.SAF_BWD_DKDV, binding.SAF_BWD_DQ)):
+        ws.zero_()
+        dQ, dK, dV = (torch.empty_like(O) for _ in range(3))
+        for st in order:
+            binding.saf_hybrid_attn_bwd_stage(st, t["Q"], t["K"], t["V"], O, t["dO"], L, t["is_fixed"], t["a"],
+                                              t["r"], dQ, dK, dV, ws)
+        torch.cuda.synchronize()
+        for x, y in zip(full, (dQ, dK, dV)):
+            x, y = x.float(), y.float()
+            assert torch.all((x - y).abs() <= 1e-2 * y.abs() + 1e-4)
 
 
 def _guarded(torch, shape, dtype, dev, guard=4096):
