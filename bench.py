@@ -16,6 +16,11 @@ Prints one JSON line with:
   fraction of the MI355X dense bf16 MFMA peak;
 * ``kernels``: average duration of each launch, measured with HIP events on
   the stream the library launches on;
+* ``ms_median_events``: the median over the timed steps of each step's event
+  duration (forward start to backward end);
+* ``sclk_mhz``: the shader clock read from sysfs every 2 ms while the timed
+  steps run (median, minimum, sample count; null where the driver does not
+  show it);
 * ``roofline``: the dominant launch's algorithmic FLOP / its duration;
 * ``speedup_vs_all_ordinary``: the same kernels with every head ordinary, at
   the same shape, timed in alternating (ABBA) blocks;
@@ -69,10 +74,13 @@ over its duration.
 from __future__ import annotations
 
 import argparse
+import glob
 import hashlib
 import json
 import os
+import re
 import sys
+import threading
 import time
 
 import numpy as np
@@ -172,8 +180,11 @@ def measured_traffic(workload: str, stage: str):
 def parse():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=30)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=100)
+    # The shader clock climbs from idle to its sustained level over about
+    # 0.12 s of continuous work; the default warm-up covers that (0.28 s at
+    # the 124M layer), so the timed steps run at the sustained clock.
+    ap.add_argument("--warmup", type=int, default=300)
     ap.add_argument("--workload", default="gpt124m_4k", choices=sorted(gen.WORKLOADS))
     ap.add_argument("--cpu-baseline", dest="cpu_baseline", action="store_true", default=True)
     ap.add_argument("--no-cpu-baseline", dest="cpu_baseline", action="store_false")
@@ -241,22 +252,83 @@ class Layer:
                     ev[2 + i].record()
 
 
-def timed_block(torch, layer, flags, steps, with_events):
+def read_sclk_mhz(torch):
+    """Shader clock of the GPU in use, in MHz: the DPM level marked '*' in the
+    pp_dpm_sclk file of the DRM card on the same PCI address; None where
+    sysfs does not show it."""
+    try:
+        p = torch.cuda.get_device_properties(0)
+        want = f"{p.pci_domain_id:04x}:{p.pci_bus_id:02x}:{p.pci_device_id:02x}."
+    except (AttributeError, RuntimeError):
+        return None
+    for card in sorted(glob.glob("/sys/class/drm/card*/device")):
+        try:
+            if not os.path.basename(os.path.realpath(card)).startswith(want):
+                continue
+            with open(os.path.join(card, "pp_dpm_sclk")) as f:
+                for line in f:
+                    if line.rstrip().endswith("*"):
+                        m = re.search(r"(\d+)\s*mhz", line, re.IGNORECASE)
+                        return int(m.group(1)) if m else None
+        except OSError:
+            return None
+    return None
+
+
+class ClockSampler:
+    """Reads the shader clock every `period_s` on a host thread between
+    start() and stop(); stop() returns the median and the minimum in MHz
+    (None where sysfs does not show the clock)."""
+
+    def __init__(self, torch, period_s=0.002):
+        self.torch, self.period, self.samples = torch, period_s, []
+        self._stop = threading.Event()
+        self._thread = None
+
+    def _run(self):
+        while not self._stop.is_set():
+            v = read_sclk_mhz(self.torch)
+            if v is None:
+                return
+            self.samples.append(v)
+            self._stop.wait(self.period)
+
+    def start(self):
+        self._thread = threading.Thread(target=self._run, daemon=True)
+        self._thread.start()
+
+    def stop(self):
+        self._stop.set()
+        self._thread.join()
+        if not self.samples:
+            return None
+        return {"median": int(np.median(self.samples)), "min": int(min(self.samples)), "samples": len(self.samples)}
+
+
+def timed_block(torch, layer, flags, steps, with_events, clock=None):
     """Run `steps` steps between two device synchronisations; returns wall ms
-    per step and, if requested, per-stage event milliseconds per step."""
+    per step and, if requested, per-stage event milliseconds per step (plus
+    "layer_median": the median of the per-step event totals).  A list passed
+    as `clock` receives the shader clock sampled while the steps run."""
     n_ev = len(layer.stages) + 1
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(n_ev)] for _ in range(steps)] if with_events else None
     torch.cuda.synchronize()
+    sampler = ClockSampler(torch) if clock is not None else None
+    if sampler:
+        sampler.start()
     t0 = time.perf_counter()
     for s in range(steps):
         layer.step(flags, evs[s] if with_events else None)
     torch.cuda.synchronize()
+    if sampler:
+        clock.append(sampler.stop())
     wall = (time.perf_counter() - t0) * 1e3 / steps
     per_stage = None
     if with_events:
         per_stage = {}
         for i, name in enumerate(layer.stages):
             per_stage[name] = float(np.mean([e[i].elapsed_time(e[i + 1]) for e in evs]))
+        per_stage["layer_median"] = float(np.median([e[0].elapsed_time(e[-1]) for e in evs]))
     return wall, per_stage
 
 
@@ -959,7 +1031,9 @@ def main():
     torch.cuda.synchronize()
 
     # Timed region: exactly `steps` hybrid layers.
-    ms, per_stage = timed_block(torch, layer, hybrid_flags, args.steps, with_events=True)
+    sclk = []
+    ms, per_stage = timed_block(torch, layer, hybrid_flags, args.steps, with_events=True, clock=sclk)
+    ms_median = per_stage.pop("layer_median")
 
     flop = layer_flop(B, H, N, d, n_fixed, w.backward)
     total_flop = sum(flop.values())
@@ -989,6 +1063,8 @@ def main():
                    "N": N, "d": d, "passes": "fwd+bwd" if w.backward else "fwd", "parallelism": "single GPU"},
         "tflops": round(tflops, 1),
         "mfma_util": round(tflops / peak, 4),
+        "ms_median_events": round(ms_median, 4),
+        "sclk_mhz": sclk[0],   # {"median", "min", "samples"} over the timed steps, or null
         "kernels": {k: {"ms": round(v, 4), "tflops": round(flop[k] / (v * 1e-3) / 1e12, 1),
                         "min_hbm_gbs": round(sbytes[k] / (v * 1e-3) / 1e9, 1)} for k, v in per_stage.items()},
         "roofline": {"bound": "mfma", "kernel": dominant, "achieved": round(dom_tflops, 1), "peak": peak,
