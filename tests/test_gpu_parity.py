@@ -61,6 +61,16 @@ def test_uniform_head_sets(dtype, fixed):
     compare_layer(run_gpu(inp, dtype), inp, dtype)
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_max_heads(dtype):
+    """H = 64, the largest head count the packed 64-bit head mask holds,
+    with fixed heads at both ends of it (bits 0 and 63) and in the middle."""
+    fixed = [0, 5, 31, 32, 62, 63]
+    announce(f"max heads H=64 {dtype} fixed={fixed}")
+    inp = _inp(1, 64, 97, fixed, dtype)
+    compare_layer(run_gpu(inp, dtype), inp, dtype)
+
+
 def test_bf16_several_tiles_ragged():
     announce("bf16 B=2 H=4 N=1000")
     inp = _inp(2, 4, 1000, [1, 2], "bf16")
