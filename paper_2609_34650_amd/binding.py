@@ -386,8 +386,12 @@ def saf_hybrid_attn_bwd_pattern(V, O, dO, LSE, head_is_fixed, a, r, da=None, dr=
 
 
 class HybridAttention(torch.autograd.Function):
-    """Autograd wrapper over the forward/backward pair.  ``a`` and ``r`` take no
-    gradient; fixed heads return zero gradients for Q and K."""
+    """Autograd wrapper over the forward/backward pair.  Fixed heads return
+    zero gradients for Q and K.  ``a`` and ``r`` take a gradient only when
+    they require one (trainable fixed patterns): then the backward also runs
+    ``saf_hybrid_attn_bwd_pattern``; its ``[H, N]`` result goes into the
+    first N columns of a gradient shaped like ``a`` (later columns and
+    ordinary heads' rows are zero)."""
 
     @staticmethod
     def forward(ctx, Q, K, V, head_is_fixed, a, r):
@@ -399,8 +403,19 @@ class HybridAttention(torch.autograd.Function):
     @staticmethod
     def backward(ctx, dO):
         Q, K, V, O, LSE, a, r = ctx.saved_tensors
-        dQ, dK, dV = saf_hybrid_attn_bwd(Q, K, V, O, dO.contiguous(), LSE, ctx.flags, a, r)
-        return dQ, dK, dV, None, None, None
+        dO = dO.contiguous()
+        dQ, dK, dV = saf_hybrid_attn_bwd(Q, K, V, O, dO, LSE, ctx.flags, a, r)
+        ga = gr = None
+        if ctx.needs_input_grad[4] or ctx.needs_input_grad[5]:
+            N = V.shape[2]
+            da, dr = saf_hybrid_attn_bwd_pattern(V, O, dO, LSE, ctx.flags, a.detach(), r.detach())
+            if ctx.needs_input_grad[4]:
+                ga = torch.zeros_like(a)
+                ga[:, :N] = da
+            if ctx.needs_input_grad[5]:
+                gr = torch.zeros_like(r)
+                gr[:, :N] = dr
+        return dQ, dK, dV, None, ga, gr
 
 
 # ---------------------------------------------------------------------------

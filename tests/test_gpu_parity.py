@@ -369,6 +369,33 @@ def test_autograd_wrapper_matches_abi():
     assert np.array_equal(q.grad.cpu().numpy(), ref["dQ"].astype(np.float32))
 
 
+def test_autograd_wrapper_pattern_gradients():
+    """With a and r requiring gradients the wrapper returns the trainable-
+    pattern gradients of the C ABI, padded with zeros past N (prior rows
+    longer than the sequence), and leaves Q, K, V gradients unchanged."""
+    torch = torch_cuda()
+    from paper_2609_34650_amd import binding
+    announce("autograd wrapper, trainable patterns")
+    inp = _inp(2, 3, 130, [0, 2], "f32", prior_len=160)
+    t = to_device(inp, "f32")
+    q, k, v = (t[x].clone().requires_grad_(True) for x in ("Q", "K", "V"))
+    a = t["a"].clone().requires_grad_(True)
+    r = t["r"].clone().requires_grad_(True)
+    o = binding.HybridAttention.apply(q, k, v, t["is_fixed"], a, r)
+    o.backward(t["dO"])
+    O, LSE = binding.saf_hybrid_attn_fwd(t["Q"], t["K"], t["V"], t["is_fixed"], t["a"], t["r"])
+    da, dr = binding.saf_hybrid_attn_bwd_pattern(t["V"], O, t["dO"], LSE, t["is_fixed"], t["a"], t["r"])
+    ref = run_gpu(inp, "f32")
+    torch.cuda.synchronize()
+    assert a.grad.shape == a.shape and r.grad.shape == r.shape
+    assert torch.equal(a.grad[:, :130], da) and torch.equal(r.grad[:, :130], dr)
+    assert not a.grad[:, 130:].any() and not r.grad[:, 130:].any()
+    assert not a.grad[1].any() and not r.grad[1].any()          # head 1 is ordinary
+    assert a.grad[0].abs().sum() > 0 and r.grad[2].abs().sum() > 0
+    assert np.array_equal(v.grad.cpu().numpy(), ref["dV"].astype(np.float32))
+    assert np.array_equal(q.grad.cpu().numpy(), ref["dQ"].astype(np.float32))
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_golden_compact_prior_on_gpu(dtype):
     """The hand-derived pattern of tests/golden/compact_prior_n4.txt through
