@@ -418,6 +418,26 @@ class HybridAttention(torch.autograd.Function):
         return dQ, dK, dV, None, ga, gr
 
 
+class HybridAttentionGQA(torch.autograd.Function):
+    """Autograd wrapper over the grouped-query pair (Q ``[B, Hq, N, d]``, K
+    and V ``[B, Hkv, N, d]``, d in {64, 96, 128}).  Patterns are frozen:
+    ``a`` and ``r`` take no gradient; fixed query heads get zero dQ and add
+    only to their group's dV."""
+
+    @staticmethod
+    def forward(ctx, Q, K, V, head_is_fixed, a, r):
+        O, LSE = saf_hybrid_attn_fwd_gqa(Q, K, V, head_is_fixed, a, r)
+        ctx.save_for_backward(Q, K, V, O, LSE, a, r)
+        ctx.flags = _flags(head_is_fixed, Q.shape[1])
+        return O
+
+    @staticmethod
+    def backward(ctx, dO):
+        Q, K, V, O, LSE, a, r = ctx.saved_tensors
+        dQ, dK, dV = saf_hybrid_attn_bwd_gqa(Q, K, V, O, dO.contiguous(), LSE, ctx.flags, a, r)
+        return dQ, dK, dV, None, None, None
+
+
 # ---------------------------------------------------------------------------
 # Calibration statistics
 # ---------------------------------------------------------------------------

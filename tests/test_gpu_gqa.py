@@ -200,3 +200,24 @@ def test_gqa_backward_equals_layer_backward_at_d64():
     torch.cuda.synchronize()
     for gv, rv in zip(g, ref):
         np.testing.assert_allclose(gv, rv.double().cpu().numpy(), rtol=0, atol=2e-5)
+
+
+def test_gqa_autograd_wrapper_matches_abi():
+    """The grouped-query autograd wrapper returns exactly what the two C ABI
+    calls return."""
+    torch = torch_cuda()
+    from paper_2609_34650_amd import binding
+    announce("gqa autograd wrapper")
+    inp = _bwd_inputs("bf16", 1, 8, 2, 200, 96, [1, 6], stream_id=57)
+    dev = torch.device("cuda", 0)
+    t = {k: torch.from_numpy(inp[k]).to(dev).to(torch.bfloat16).contiguous() for k in ("Q", "K", "V", "dO")}
+    a = torch.from_numpy(inp["a"]).to(dev)
+    r = torch.from_numpy(inp["r"]).to(dev)
+    q, k, v = (t[x].clone().requires_grad_(True) for x in ("Q", "K", "V"))
+    o = binding.HybridAttentionGQA.apply(q, k, v, inp["is_fixed"], a, r)
+    o.backward(t["dO"])
+    O, LSE = binding.saf_hybrid_attn_fwd_gqa(t["Q"], t["K"], t["V"], inp["is_fixed"], a, r)
+    dQ, dK, dV = binding.saf_hybrid_attn_bwd_gqa(t["Q"], t["K"], t["V"], O, t["dO"], LSE, inp["is_fixed"], a, r)
+    torch.cuda.synchronize()
+    assert torch.equal(o.detach(), O)
+    assert torch.equal(q.grad, dQ) and torch.equal(k.grad, dK) and torch.equal(v.grad, dV)
