@@ -787,7 +787,7 @@ def main_gqa(args, torch):
             e1.record()
             torch.cuda.synchronize()
             sdpa = round(e0.elapsed_time(e1) / args.steps, 4)
-    except Exception as exc:  # no flash kernel for this build or shape: report none
+    except Exception as exc:  # no flash kernel for this torch or shape: report none
         sdpa = f"unavailable: {type(exc).__name__}"
     table = None
     if args.table:
@@ -983,7 +983,7 @@ def main_layer1b(args, torch):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; multi-GPU runs are not part of it",
+        print(json.dumps({"error": "bench.py measures one GPU; runs on more than one GPU are not supported",
                           "n_gpus": args.gpus}))
         sys.exit(2)
     import torch

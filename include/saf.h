@@ -35,7 +35,7 @@
  * - Arguments are checked before anything is enqueued; on any error nothing
  *   is launched and nothing is written.  A kernel fault surfaces at the
  *   caller's next synchronisation, not here.
- * - Limits of this build: d == 64, 1 <= H <= 64, N <= 2^24 for bf16 and
+ * - Limits of this entry point: d == 64, 1 <= H <= 64, N <= 2^24 for bf16 and
  *   N <= 2^23 for float32 (one (batch, head) slice stays below 2^31 bytes),
  *   and B * H * ceil(N / 32) <= 2^31 - 1.  B, H or N equal to 0 is an empty
  *   problem: SAF_OK, nothing launched.
