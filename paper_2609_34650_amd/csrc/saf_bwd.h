@@ -230,7 +230,9 @@ __device__ __forceinline__ void kv_tile(const T* qt, const T* gt, const float* r
 template <typename T>
 __device__ __forceinline__ void kv_ordinary(const Tiles<T>& sm, const BwdArgs& p, const KvLane& L, size_t base,
                                             size_t row_base) {
-    // Tiles: Q in t[0] / t[1], dO in t[2] / t[3]; LSE and D rows in aux[0] / aux[1].
+    // Tiles of a step's first 64 queries: Q in t[0] / t[1], dO in t[2] / t[3];
+    // of its second 64: Q in t[4] / t[5], dO in t[6] / t[7]; LSE and -D rows of
+    // both in aux[0] / aux[1] (64 LSE, 64 -D, then the same for the second).
     const T* __restrict__ K = reinterpret_cast<const T*>(p.k) + base;
     const T* __restrict__ V = reinterpret_cast<const T*>(p.v) + base;
     const __amdgpu_buffer_rsrc_t rq = slice_rsrc<T>(reinterpret_cast<const T*>(p.q) + base, L.N);
@@ -259,28 +261,37 @@ __device__ __forceinline__ void kv_ordinary(const Tiles<T>& sm, const BwdArgs& p
                 dk[kb][db][v] = 0.0f;
             }
 
-    // Slots: the tiles that meet the diagonal first (masked), then the rest.
-    const int n_tiles = (L.N - L.n0 + KV_BM - 1) / KV_BM;
-    const int n_mask = min(KV_MASK_TILES, n_tiles);
-    const int P = (n_mask + 1) & ~1;
+    // Steps of two 64-query tiles (one barrier per 128 queries): the step
+    // that meets the diagonal first (masked), then the rest.  Rows past N
+    // arrive as zeros with LSE = +inf, so they add nothing.
+    constexpr int SB = 2 * KV_BM;
+    const int n_steps = (L.N - L.n0 + SB - 1) / SB;
     run_slots(
-        P, P + n_tiles - n_mask, [&](int i) { return i < P ? (i < n_mask ? i : -1) : n_mask + (i - P); },
+        2, 2 + n_steps - 1, [&](int i) { return i < 2 ? (i == 0 ? 0 : -1) : i - 1; },
         [&](auto buf, int t) {
             constexpr int b = decltype(buf)::value;
-            const int mq = L.n0 + t * KV_BM;
+            const int mq = L.n0 + t * SB;
             tile_load_lds<T>(sm.t[b], rq, mq, L.w, L.lane);
             tile_load_lds<T>(sm.t[2 + b], rg, mq, L.w, L.lane);
-            if (L.tid < KV_BM) {
-                const bool ok = mq + L.tid < L.N;
-                sm.aux[b][L.tid] = ok ? LSE[mq + L.tid] * LOG2E : INFINITY;
-                sm.aux[b][KV_BM + L.tid] = ok ? -Dsum[mq + L.tid] : 0.0f;
+            tile_load_lds<T>(sm.t[4 + b], rq, mq + KV_BM, L.w, L.lane);
+            tile_load_lds<T>(sm.t[6 + b], rg, mq + KV_BM, L.w, L.lane);
+            if (L.tid < SB) {
+                const int row = mq + L.tid;
+                const bool ok = row < L.N;
+                float* x = sm.aux[b] + (L.tid / KV_BM) * 2 * KV_BM + (L.tid % KV_BM);
+                x[0] = ok ? LSE[row] * LOG2E : INFINITY;
+                x[KV_BM] = ok ? -Dsum[row] : 0.0f;
             }
         },
         [&](auto) {},
         [&](auto buf, int t, auto mask) {
             constexpr int b = decltype(buf)::value;
-            kv_tile<T, decltype(mask)::value>(sm.t[b], sm.t[2 + b], sm.aux[b], L.n0 + t * KV_BM, L, kf, vf, dv, dk,
+            const int mq = L.n0 + t * SB;
+            kv_tile<T, decltype(mask)::value>(sm.t[b], sm.t[2 + b], sm.aux[b], mq, L, kf, vf, dv, dk,
                                               p.scale_log2);
+            if (mq + KV_BM < L.N)
+                kv_tile<T, decltype(mask)::value>(sm.t[4 + b], sm.t[6 + b], sm.aux[b] + 2 * KV_BM, mq + KV_BM, L, kf,
+                                                  vf, dv, dk, p.scale_log2);
         });
     float one[KV_KB], ks[KV_KB];
 #pragma unroll
@@ -521,10 +532,14 @@ __global__ __launch_bounds__(KV_THREADS) __attribute__((amdgpu_waves_per_eu(size
     __shared__ __attribute__((aligned(16))) T t1[tile_elems<T>()];
     __shared__ __attribute__((aligned(16))) T t2[tile_elems<T>()];
     __shared__ __attribute__((aligned(16))) T t3[tile_elems<T>()];
-    __shared__ __attribute__((aligned(16))) float x0[2 * KV_BM];
-    __shared__ __attribute__((aligned(16))) float x1[2 * KV_BM];
+    __shared__ __attribute__((aligned(16))) T t4[tile_elems<T>()];
+    __shared__ __attribute__((aligned(16))) T t5[tile_elems<T>()];
+    __shared__ __attribute__((aligned(16))) T t6[tile_elems<T>()];
+    __shared__ __attribute__((aligned(16))) T t7[tile_elems<T>()];
+    __shared__ __attribute__((aligned(16))) float x0[4 * KV_BM];
+    __shared__ __attribute__((aligned(16))) float x1[4 * KV_BM];
     __shared__ float red[4];
-    const Tiles<T> sm = {{t0, t1, t2, t3}, {x0, x1}, red};
+    const Tiles<T> sm = {{t0, t1, t2, t3, t4, t5, t6, t7}, {x0, x1}, red};
     const SliceOf sl = slice_of(blockIdx.x, p.B, p.H, 1, [&](int k) { return (int)p.head_order[k]; });
     const int kblk = sl.level;  // ascending: longest first
     const int h = sl.h;

@@ -190,14 +190,15 @@ __device__ __forceinline__ void tile_load_lds(T* tile, __amdgpu_buffer_rsrc_t rs
     }
 }
 
-// The LDS of a workgroup: four tiles, each its own __shared__ array, so that
+// The LDS of a workgroup: four tiles (eight in the key-block pass, which
+// takes 128 queries per step), each its own __shared__ array, so that
 // the compiler can tell a tile being filled by in-flight buffer loads from the
 // one being read (and skips waiting for those loads before the reads); two
 // small per-buffer float arrays; a few floats for reductions.  Each program
 // gives the tiles its own roles.
 template <typename T>
 struct Tiles {
-    T* t[4];
+    T* t[8];
     float* aux[2];
     float* red;
 };
