@@ -215,7 +215,10 @@ size_t calib_workspace_bytes(int H, int T) {
 template <typename T>
 saf_status_t launch_calib_accum(const saf::CalibArgs& args, hipStream_t stream) {
     const unsigned grid = (unsigned)((size_t)args.H * args.n_tiles * args.n_tiles);
-    hipLaunchKernelGGL(saf::calib_accum_kernel<T>, dim3(grid), dim3(saf::CAL_THREADS), 0, stream, args);
+    if (args.m2 != nullptr)
+        hipLaunchKernelGGL((saf::calib_accum_kernel<T, true>), dim3(grid), dim3(saf::CAL_THREADS), 0, stream, args);
+    else
+        hipLaunchKernelGGL((saf::calib_accum_kernel<T, false>), dim3(grid), dim3(saf::CAL_THREADS), 0, stream, args);
     return launched();
 }
 

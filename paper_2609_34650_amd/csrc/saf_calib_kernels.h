@@ -98,10 +98,11 @@ struct CalLane {
 // 0 past T).  MASK: the tile needs per-entry checks -- keys after the query on
 // a diagonal tile, rows at or past T (rows_valid < 128) on the last row of
 // tiles.
-template <typename T, bool MASK, typename Q0, typename Q1, typename K0, typename K1, typename LS>
+template <typename T, bool MASK, bool M2, typename Q0, typename Q1, typename K0, typename K1, typename LS,
+          typename INC>
 __device__ __forceinline__ void calib_input(Q0 qa, Q1 qb, K0 ka, K1 kb, LS ls, int b, const CalibArgs& p,
                                             const CalLane& L, bool diag, int rows_valid, f32x16 (&mean)[4],
-                                            f32x16 (&inc)[4], float& ent) {
+                                            INC& inc, float& inc_s, float& ent) {
     typedef typename Vec<T>::x8 frag;
     const T* kt = (L.w >> 1) ? kb : ka;
     frag kf[4];
@@ -134,14 +135,17 @@ __device__ __forceinline__ void calib_input(Q0 qa, Q1 qb, K0 ka, K1 kb, LS ls, i
                 ent = fmaf(pv, x, ent);
                 const float d1 = pv - mean[rb][v];
                 mean[rb][v] = fmaf(d1, rn, mean[rb][v]);
-                inc[rb][v] = fmaf(d1, pv - mean[rb][v], inc[rb][v]);
+                if constexpr (M2)
+                    inc[rb][v] = fmaf(d1, pv - mean[rb][v], inc[rb][v]);
+                else
+                    inc_s = fmaf(d1, pv - mean[rb][v], inc_s);
             }
         }
     }
 }
 
-template <typename T>
-__global__ __launch_bounds__(CAL_THREADS) __attribute__((amdgpu_waves_per_eu(2))) void calib_accum_kernel(
+template <typename T, bool M2>
+__global__ __launch_bounds__(CAL_THREADS) __attribute__((amdgpu_waves_per_eu(M2 ? 2 : 3))) void calib_accum_kernel(
     CalibArgs p) {
     __shared__ __attribute__((aligned(16))) T q0a[tile_elems<T>()];
     __shared__ __attribute__((aligned(16))) T q0b[tile_elems<T>()];
@@ -174,7 +178,7 @@ __global__ __launch_bounds__(CAL_THREADS) __attribute__((amdgpu_waves_per_eu(2))
     // uniform multiple of T.
     const size_t tile_base = (size_t)h * p.T * p.T + (size_t)L.row0 * p.T;
     float* __restrict__ Mg = p.mean + tile_base;
-    float* __restrict__ M2g = p.m2 != nullptr ? p.m2 + tile_base : nullptr;
+    float* __restrict__ M2g = M2 ? p.m2 + tile_base : nullptr;
     const int col = L.col0 + 32 * L.w + L.c;
     auto row_of = [&](int rb, int v) { return L.row0 + 32 * rb + 8 * (v >> 2) + 4 * L.hf + (v & 3); };
     auto row_step = [&](int rb, int v) { return (32 * rb + 8 * (v >> 2) + (v & 3)) * L.T; };
@@ -186,13 +190,16 @@ __global__ __launch_bounds__(CAL_THREADS) __attribute__((amdgpu_waves_per_eu(2))
         return o;
     };
 
-    f32x16 mean[4], inc[4];
+    // Per-entry increments of the squared deviations only when they are
+    // kept; otherwise one running sum per lane.
+    f32x16 mean[4], inc[M2 ? 4 : 1];
+    float inc_s = 0.0f;
 #pragma unroll
     for (int rb = 0; rb < 4; ++rb)
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
             mean[rb][v] = 0.0f;
-            inc[rb][v] = 0.0f;
+            if constexpr (M2) inc[rb][v] = 0.0f;
         }
     double* slot = p.stats + 2 * (size_t)blockIdx.x;
     const bool diag = (I == J);
@@ -243,18 +250,36 @@ __global__ __launch_bounds__(CAL_THREADS) __attribute__((amdgpu_waves_per_eu(2))
                                                      (L.row0 + 64 * L.w + L.lane) * 4, 0, 0, 0);
         }
     };
-    auto compute = [&](auto buf, int b, auto mask) {
-        constexpr int B_ = decltype(buf)::value;
-        constexpr bool M_ = decltype(mask)::value;
-        if (B_)
-            calib_input<T, M_>(q1a, q1b, k1a, k1b, ls1, b, p, L, diag, rows_valid, mean, inc, ent);
-        else
-            calib_input<T, M_>(q0a, q0b, k0a, k0b, ls0, b, p, L, diag, rows_valid, mean, inc, ent);
-    };
-    const int P = (diag || rows_valid < CAL_TILE) ? (p.B + 1) & ~1 : 0;
-    run_slots(P, P ? P : p.B, [&](int i) { return i < p.B ? i : -1; }, issue, [&](auto) {}, compute);
+    const bool masked = diag || rows_valid < CAL_TILE;
+    if constexpr (M2) {
+        // Per-entry increments take 64 more registers: two workgroups per CU,
+        // so the inputs are double-buffered (one loads while one is folded in).
+        auto compute = [&](auto buf, int b, auto mask) {
+            constexpr int B_ = decltype(buf)::value;
+            constexpr bool M_ = decltype(mask)::value;
+            if (B_)
+                calib_input<T, M_, M2>(q1a, q1b, k1a, k1b, ls1, b, p, L, diag, rows_valid, mean, inc, inc_s, ent);
+            else
+                calib_input<T, M_, M2>(q0a, q0b, k0a, k0b, ls0, b, p, L, diag, rows_valid, mean, inc, inc_s, ent);
+        };
+        const int P = masked ? (p.B + 1) & ~1 : 0;
+        run_slots(P, P ? P : p.B, [&](int i) { return i < p.B ? i : -1; }, issue, [&](auto) {}, compute);
+    } else {
+        // One buffer of input tiles (35 KB of LDS for bf16), so that three
+        // workgroups fit on a CU: each input is loaded, then folded in.
+        for (int b = 0; b < p.B; ++b) {
+            issue(Buf0{}, b);
+            __syncthreads();
+            if (masked)
+                calib_input<T, true, M2>(q0a, q0b, k0a, k0b, ls0, b, p, L, diag, rows_valid, mean, inc, inc_s, ent);
+            else
+                calib_input<T, false, M2>(q0a, q0b, k0a, k0b, ls0, b, p, L, diag, rows_valid, mean, inc, inc_s,
+                                          ent);
+            __syncthreads();
+        }
+    }
 
-    float inc_sum = 0.0f;
+    float inc_sum = M2 ? 0.0f : inc_s;
     if (col < L.T) {
         const int lo = lane_off();
 #pragma unroll
@@ -264,8 +289,10 @@ __global__ __launch_bounds__(CAL_THREADS) __attribute__((amdgpu_waves_per_eu(2))
                 if (row_of(rb, v) < L.T) {
                     const int at = lo + row_step(rb, v);
                     Mg[at] = mean[rb][v];
-                    if (M2g) M2g[at] = p.n_seen > 0 ? M2g[at] + inc[rb][v] : inc[rb][v];
-                    inc_sum += inc[rb][v];
+                    if constexpr (M2) {
+                        M2g[at] = p.n_seen > 0 ? M2g[at] + inc[rb][v] : inc[rb][v];
+                        inc_sum += inc[rb][v];
+                    }
                 }
             }
     }
