@@ -18,12 +18,20 @@ Prints one JSON line with:
   the stream the library launches on;
 * ``ms_median_events``: the median over the timed steps of each step's event
   duration (forward start to backward end);
-* ``sclk_mhz``: the shader clock read from sysfs every 2 ms while the timed
-  steps run (median, minimum, sample count; null where the driver does not
-  show it);
+* ``warmup_floor``: untimed steps run beyond ``--warmup`` until
+  ``--warmup-floor-s`` seconds of warm-up have passed, so the timed steps do
+  not run while the shader clock is still ramping up;
+* ``shader_clock_mhz``: the mean shader clock while hybrid layers run, from
+  the GPU's own counters (the library's clock probe: s_memtime against the
+  100 MHz s_memrealtime, one wavefront on a second stream spanning ~30 ms of
+  layer steps after the timed region), and the bf16 peak at that clock;
 * ``roofline``: the dominant launch's algorithmic FLOP / its duration;
 * ``speedup_vs_all_ordinary``: the same kernels with every head ordinary, at
-  the same shape, timed in alternating (ABBA) blocks;
+  the same shape: the median of the within-pair time ratios over
+  ``--abba-pairs`` pairs of blocks whose order alternates (hybrid first, then
+  ordinary first, ...); ``speedup_protocol`` lists every pair's ratio and the
+  zero-replacement control, the same protocol with two identical all-ordinary
+  arms, whose median is expected at 1.00 +- 0.01;
 * ``cpu_baseline``: the fp64 oracle timed on this host's cores on a bounded
   sample of (batch, head) slices, scaled to one layer.
 
@@ -43,8 +51,7 @@ product, and the two sums) against the chip's float32 vector rate
 in the layout of the paper's grouped-query prefill measurement: B = 4,
 T = 4096, 32 query heads sharing 8 key/value heads, d = 128, bf16, at 30 %
 fixed heads (and a sweep over 0-75 %), against the same kernel with every
-head ordinary; torch's flash SDPA (forced, no fallback) is timed beside it
-for reference when available.  MFMA roofline: an ordinary head counts 2
+head ordinary.  MFMA roofline: an ordinary head counts 2
 contractions (QK^T, PV), a fixed head 1 (PV).
 
 ``--layer1b`` times one training layer of the paper's 1B model through the
@@ -74,13 +81,10 @@ over its duration.
 from __future__ import annotations
 
 import argparse
-import glob
 import hashlib
 import json
 import os
-import re
 import sys
-import threading
 import time
 
 import numpy as np
@@ -185,6 +189,12 @@ def parse():
     # 0.12 s of continuous work; the default warm-up covers that (0.28 s at
     # the 124M layer), so the timed steps run at the sustained clock.
     ap.add_argument("--warmup", type=int, default=300)
+    ap.add_argument("--warmup-floor-s", type=float, default=1.0,
+                    help="after the --warmup steps, keep running untimed steps until this many seconds of "
+                         "warm-up have passed (the shader clock ramps up over ~0.1 s of continuous work)")
+    ap.add_argument("--abba-pairs", type=int, default=8,
+                    help="pairs of (hybrid, all-ordinary) blocks for the speedup, alternating the order")
+    ap.add_argument("--abba-block", type=int, default=10, help="steps per ABBA block")
     ap.add_argument("--workload", default="gpt124m_4k", choices=sorted(gen.WORKLOADS))
     ap.add_argument("--cpu-baseline", dest="cpu_baseline", action="store_true", default=True)
     ap.add_argument("--no-cpu-baseline", dest="cpu_baseline", action="store_false")
@@ -205,8 +215,9 @@ def parse():
     ap.add_argument("--calib", action="store_true",
                     help="time the calibration statistics (workload calib124m_4k) instead of the layer")
     ap.add_argument("--copy-calibration", action="store_true",
-                    help="run one plain 64 MiB read + 64 MiB write elementwise kernel (torch.neg) before the "
-                         "timed steps: a known-size reference for HBM byte counters in a profiler run")
+                    help="run one plain 64 MiB read + 64 MiB write elementwise kernel (torch.neg), then one "
+                         "64 MiB read through buffer loads straight to LDS (saf_lds_read_probe), before the "
+                         "timed steps: known-size references for HBM byte counters in a profiler run")
     return ap.parse_args()
 
 
@@ -252,76 +263,37 @@ class Layer:
                     ev[2 + i].record()
 
 
-def read_sclk_mhz(torch):
-    """Shader clock of the GPU in use, in MHz: the DPM level marked '*' in the
-    pp_dpm_sclk file of the DRM card on the same PCI address; None where
-    sysfs does not show it."""
+def shader_clock_during(torch, run, duration_us):
+    """Mean shader clock in MHz while `run()` enqueues work on the current
+    stream: the library's clock probe (s_memtime against the 100 MHz
+    s_memrealtime counter, one wavefront) is enqueued first on a second
+    stream and spans `duration_us` of that work.  Returns None if the probe
+    is unavailable."""
+    from paper_2609_34650_amd import binding
+    out = torch.zeros(2, dtype=torch.int64, device="cuda")
+    side = torch.cuda.Stream()
+    torch.cuda.synchronize()
     try:
-        p = torch.cuda.get_device_properties(0)
-        want = f"{p.pci_domain_id:04x}:{p.pci_bus_id:02x}:{p.pci_device_id:02x}."
-    except (AttributeError, RuntimeError):
+        binding.saf_clock_probe(out, duration_us, stream=side)
+    except Exception:  # noqa: BLE001 - the field is optional
         return None
-    for card in sorted(glob.glob("/sys/class/drm/card*/device")):
-        try:
-            if not os.path.basename(os.path.realpath(card)).startswith(want):
-                continue
-            with open(os.path.join(card, "pp_dpm_sclk")) as f:
-                for line in f:
-                    if line.rstrip().endswith("*"):
-                        m = re.search(r"(\d+)\s*mhz", line, re.IGNORECASE)
-                        return int(m.group(1)) if m else None
-        except OSError:
-            return None
-    return None
+    run()
+    torch.cuda.synchronize()
+    cyc, ticks = (int(x) for x in out.cpu().tolist())
+    return round(cyc / ticks * 100.0, 1) if ticks > 0 else None
 
 
-class ClockSampler:
-    """Reads the shader clock every `period_s` on a host thread between
-    start() and stop(); stop() returns the median and the minimum in MHz
-    (None where sysfs does not show the clock)."""
-
-    def __init__(self, torch, period_s=0.002):
-        self.torch, self.period, self.samples = torch, period_s, []
-        self._stop = threading.Event()
-        self._thread = None
-
-    def _run(self):
-        while not self._stop.is_set():
-            v = read_sclk_mhz(self.torch)
-            if v is None:
-                return
-            self.samples.append(v)
-            self._stop.wait(self.period)
-
-    def start(self):
-        self._thread = threading.Thread(target=self._run, daemon=True)
-        self._thread.start()
-
-    def stop(self):
-        self._stop.set()
-        self._thread.join()
-        if not self.samples:
-            return None
-        return {"median": int(np.median(self.samples)), "min": int(min(self.samples)), "samples": len(self.samples)}
-
-
-def timed_block(torch, layer, flags, steps, with_events, clock=None):
+def timed_block(torch, layer, flags, steps, with_events):
     """Run `steps` steps between two device synchronisations; returns wall ms
     per step and, if requested, per-stage event milliseconds per step (plus
-    "layer_median": the median of the per-step event totals).  A list passed
-    as `clock` receives the shader clock sampled while the steps run."""
+    "layer_median": the median of the per-step event totals)."""
     n_ev = len(layer.stages) + 1
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(n_ev)] for _ in range(steps)] if with_events else None
     torch.cuda.synchronize()
-    sampler = ClockSampler(torch) if clock is not None else None
-    if sampler:
-        sampler.start()
     t0 = time.perf_counter()
     for s in range(steps):
         layer.step(flags, evs[s] if with_events else None)
     torch.cuda.synchronize()
-    if sampler:
-        clock.append(sampler.stop())
     wall = (time.perf_counter() - t0) * 1e3 / steps
     per_stage = None
     if with_events:
@@ -773,22 +745,6 @@ def main_gqa(args, torch):
         nf = round(rate * Hq)
         t = timed(flags_for(nf), args.steps)
         sweep[f"{int(rate * 100)}%"] = {"n_fixed": nf, "ms": round(t, 4), "speedup_vs_all_ordinary": round(ms_ord / t, 3)}
-    sdpa = None
-    try:
-        from torch.nn.attention import SDPBackend, sdpa_kernel
-        with sdpa_kernel([SDPBackend.FLASH_ATTENTION]):
-            for _ in range(args.warmup):
-                torch.nn.functional.scaled_dot_product_attention(Q, K, V, is_causal=True, enable_gqa=True)
-            torch.cuda.synchronize()
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record()
-            for _ in range(args.steps):
-                torch.nn.functional.scaled_dot_product_attention(Q, K, V, is_causal=True, enable_gqa=True)
-            e1.record()
-            torch.cuda.synchronize()
-            sdpa = round(e0.elapsed_time(e1) / args.steps, 4)
-    except Exception as exc:  # no flash kernel for this torch or shape: report none
-        sdpa = f"unavailable: {type(exc).__name__}"
     table = None
     if args.table:
         # The paper's prefill grid: attention-op time at each fixed rate over
@@ -843,7 +799,6 @@ def main_gqa(args, torch):
         "all_ordinary_ms": round(ms_ord, 4),
         "speedup_vs_all_ordinary": round(ms_ord / ms_ev, 3),
         "sweep": sweep,
-        "torch_flash_sdpa_all_ordinary_ms": sdpa,
         "speedup_table": table,
         "cpu_baseline": gqa_cpu_baseline(inp, Hkv, fl) if args.cpu_baseline else None,
         "roofline": {"bound": "mfma", "kernel": "gqa_fwd", "achieved": round(tflops, 1), "peak": PEAK_BF16_TFLOPS,
@@ -999,6 +954,10 @@ def main():
         torch.cuda.synchronize()
         torch.neg(src, out=dst)
         torch.cuda.synchronize()
+        # The same 64 MiB read once more through the layer kernels' own load
+        # path (buffer loads straight to LDS), nothing written but 256 bytes.
+        binding.saf_lds_read_probe(src)
+        torch.cuda.synchronize()
         del src, dst
     if args.calib:
         main_calib(args, torch)
@@ -1024,15 +983,26 @@ def main():
     ordinary_flags = np.zeros_like(hybrid_flags)
     layer = Layer(torch, inp, w.dtype, w.backward)
 
-    for _ in range(args.warmup):
+    def warm():
         layer.step(hybrid_flags)
         if args.compare:
             layer.step(ordinary_flags)
+
+    # Warm-up: the requested steps, then more until the time floor has passed.
+    t_w = time.perf_counter()
+    for _ in range(args.warmup):
+        warm()
     torch.cuda.synchronize()
+    extra = 0
+    while time.perf_counter() - t_w < args.warmup_floor_s:
+        for _ in range(10):
+            warm()
+        extra += 10
+        torch.cuda.synchronize()
+    warm_s = time.perf_counter() - t_w
 
     # Timed region: exactly `steps` hybrid layers.
-    sclk = []
-    ms, per_stage = timed_block(torch, layer, hybrid_flags, args.steps, with_events=True, clock=sclk)
+    ms, per_stage = timed_block(torch, layer, hybrid_flags, args.steps, with_events=True)
     ms_median = per_stage.pop("layer_median")
 
     flop = layer_flop(B, H, N, d, n_fixed, w.backward)
@@ -1064,7 +1034,8 @@ def main():
         "tflops": round(tflops, 1),
         "mfma_util": round(tflops / peak, 4),
         "ms_median_events": round(ms_median, 4),
-        "sclk_mhz": sclk[0],   # {"median", "min", "samples"} over the timed steps, or null
+        "warmup_floor": {"seconds": round(warm_s, 3), "extra_steps": extra,
+                         "note": "untimed steps beyond --warmup until the floor passed"},
         "kernels": {k: {"ms": round(v, 4), "tflops": round(flop[k] / (v * 1e-3) / 1e12, 1),
                         "min_hbm_gbs": round(sbytes[k] / (v * 1e-3) / 1e9, 1)} for k, v in per_stage.items()},
         "roofline": {"bound": "mfma", "kernel": dominant, "achieved": round(dom_tflops, 1), "peak": peak,
@@ -1072,17 +1043,52 @@ def main():
                      "traffic": measured_traffic(w.name, dominant)},
     }
 
+    # Shader clock while hybrid layers run (outside the timed region): the
+    # library's counter probe spans about 30 ms of layer steps.
+    n_clk = max(10, int(30.0 / max(ms, 0.05)))
+    mhz = shader_clock_during(torch, lambda: [layer.step(hybrid_flags) for _ in range(n_clk)],
+                              int(n_clk * ms * 1e3 * 0.8))
+    result["shader_clock_mhz"] = {
+        "during_layer_steps": mhz,
+        "method": "s_memtime / s_memrealtime (100 MHz) on a one-wavefront probe on a second stream, "
+                  f"spanning {n_clk} layer steps after the timed region",
+        "bf16_peak_at_this_clock_tflops": round(PEAK_BF16_TFLOPS * mhz / 2400.0, 1) if mhz else None,
+    }
+
     if args.compare:
-        # ABBA blocks: hybrid, all-ordinary, all-ordinary, hybrid.
-        blk = max(1, args.steps // 2)
-        t = {"h": [], "o": []}
-        for tag, fl in (("h", hybrid_flags), ("o", ordinary_flags), ("o", ordinary_flags), ("h", hybrid_flags)):
-            t[tag].append(timed_block(torch, layer, fl, blk, with_events=False)[0])
-        ms_h, ms_o = float(np.mean(t["h"])), float(np.mean(t["o"]))
+        # Alternating pairs of blocks, the order flipped in every other pair
+        # (hybrid/ordinary, ordinary/hybrid, ...); the speedup is the median of
+        # the within-pair ratios.  The zero-replacement control runs the same
+        # protocol with two identical arms (every flag 0 in both): the
+        # protocol's own noise, expected at 1.00 +- 0.01.
+        blk, pairs = max(1, args.abba_block), max(1, args.abba_pairs)
+
+        def pair_ratios(fa, fb):
+            ra, ta, tb = [], [], []
+            for k in range(pairs):
+                order = ((fa, "a"), (fb, "b")) if k % 2 == 0 else ((fb, "b"), (fa, "a"))
+                t = {}
+                for fl, tag in order:
+                    t[tag] = timed_block(torch, layer, fl, blk, with_events=False)[0]
+                ra.append(t["b"] / t["a"])
+                ta.append(t["a"])
+                tb.append(t["b"])
+            return ra, ta, tb
+
+        ratios, th, to = pair_ratios(hybrid_flags, ordinary_flags)
+        ctrl, _, _ = pair_ratios(ordinary_flags, ordinary_flags.copy())
+        ms_h, ms_o = float(np.median(th)), float(np.median(to))
         flop_o = sum(layer_flop(B, H, N, d, 0, w.backward).values())
+        c_med = float(np.median(ctrl))
         result["all_ordinary"] = {"ms": round(ms_o, 4), "tflops": round(flop_o / (ms_o * 1e-3) / 1e12, 1),
                                   "hybrid_ms_same_blocks": round(ms_h, 4)}
-        result["speedup_vs_all_ordinary"] = round(ms_o / ms_h, 4)
+        result["speedup_vs_all_ordinary"] = round(float(np.median(ratios)), 4)
+        result["speedup_protocol"] = {
+            "pairs": pairs, "steps_per_block": blk, "statistic": "median of within-pair ratios",
+            "pair_ratios": [round(x, 4) for x in ratios],
+            "zero_replacement_control": {"median": round(c_med, 4), "pair_ratios": [round(x, 4) for x in ctrl],
+                                         "within_1pct": bool(abs(c_med - 1.0) <= 0.01)},
+        }
 
     if args.cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(inp, w, args.cpu_slices)

@@ -97,8 +97,9 @@ saf_status_t saf_hybrid_attn_fwd(saf_dtype_t dt,
 /*
  * Forward of the hybrid layer with grouped-query attention and head
  * dimension 64, 96 or 128 (the paper's grouped-query prefill layout --
- * Section "Pretrained grouped-query models" -- and its 1B model's head
- * width).  Query head h uses key/value head h / (Hq / Hkv); a fixed query
+ * Appendix "Replacement in pretrained models", subsection "GQA prefill
+ * measurements": 32 query heads sharing 8 key/value heads at d = 128 -- and
+ * its 1B model's head width, Appendix "1B training and evaluation").  Query head h uses key/value head h / (Hq / Hkv); a fixed query
  * head reads only V of its group (the grouped-query implementation keeps the
  * shared key and value heads, Appendix "Mixed-head execution and numerical
  * checks").  Same conventions and outputs as saf_hybrid_attn_fwd, with
@@ -107,7 +108,8 @@ saf_status_t saf_hybrid_attn_fwd(saf_dtype_t dt,
  * Limits: d in {64, 96, 128}, Hq <= 64, Hq a multiple of Hkv, one slice
  * N * d * sizeof(dt) < 2^31 bytes.  With Hkv == Hq and d == 64 it computes
  * what saf_hybrid_attn_fwd computes (a separate, simpler kernel: one 32-query
- * block per wavefront, a normaliser launch first when a head is fixed).
+ * block per wavefront; one launch, in which a fixed head's workgroup sums its
+ * row normalisers from the weights it forms, as in saf_hybrid_attn_fwd).
  * Its backward is saf_hybrid_attn_bwd_gqa.
  */
 saf_status_t saf_hybrid_attn_fwd_gqa(saf_dtype_t dt,

@@ -56,6 +56,8 @@ EXPORTS = (
     "saf_fit_workspace_bytes",
     "saf_fit_targets",
     "saf_compact_fit",
+    "saf_clock_probe",
+    "saf_lds_read_probe",
 )
 
 
@@ -119,6 +121,10 @@ def load() -> ctypes.CDLL:
     lib.saf_compact_fit.restype = ctypes.c_int
     lib.saf_compact_fit.argtypes = [i, i, vp, vp, vp, i, ctypes.c_float, ctypes.c_float, vp, vp, vp, vp, vp,
                                     ctypes.c_size_t, vp]
+    lib.saf_clock_probe.restype = ctypes.c_int
+    lib.saf_clock_probe.argtypes = [vp, i, vp]
+    lib.saf_lds_read_probe.restype = ctypes.c_int
+    lib.saf_lds_read_probe.argtypes = [vp, ctypes.c_size_t, vp, vp]
     lib.saf_status_str.restype = ctypes.c_char_p
     lib.saf_status_str.argtypes = [i]
     del f32p
@@ -559,3 +565,33 @@ def saf_compact_fit(eta_abs: torch.Tensor, eta_rel: torch.Tensor, neg_entropy: t
                                workspace.numel() * workspace.element_size(), _stream(dev))
     _raise(code, "saf_compact_fit")
     return a, r, log_z, kl
+
+
+# ---------------------------------------------------------------------------
+# Measurement aids (include/saf_measure.h)
+# ---------------------------------------------------------------------------
+
+def saf_clock_probe(out: torch.Tensor, duration_us: int, stream: Optional["torch.cuda.Stream"] = None):
+    """Enqueue the shader-clock probe on `stream` (default: the current
+    stream).  `out` is a device int64 tensor of 2 elements; after the stream
+    completes, out[0] / out[1] * 100 is the mean shader clock in MHz."""
+    if out.dtype != torch.int64 or out.numel() < 2 or not out.is_cuda:
+        raise ValueError("out must be a device int64 tensor with 2 elements")
+    st = (stream or torch.cuda.current_stream(out.device)).cuda_stream
+    _raise(load().saf_clock_probe(out.data_ptr(), int(duration_us), st), "saf_clock_probe")
+
+
+def saf_lds_read_probe(src: torch.Tensor, sink: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Read every byte of the contiguous device tensor `src` once through
+    buffer loads straight to LDS (a known-size reference for HBM byte
+    counters); returns the per-workgroup sink."""
+    nbytes = src.numel() * src.element_size()
+    if not src.is_cuda or not src.is_contiguous():
+        raise ValueError("src must be a contiguous device tensor")
+    n_wg = (nbytes + (1 << 20) - 1) >> 20
+    if sink is None:
+        sink = torch.empty(n_wg, dtype=torch.float32, device=src.device)
+    _raise(load().saf_lds_read_probe(src.data_ptr(), nbytes, sink.data_ptr(), _stream(src.device)),
+           "saf_lds_read_probe")
+    return sink
+

@@ -4,6 +4,7 @@
 #include "saf.h"
 #include "saf_calib.h"
 #include "saf_fit.h"
+#include "saf_measure.h"
 
 #include <math.h>
 #include <algorithm>
@@ -15,6 +16,7 @@
 #include "saf_fwd.h"
 #include "saf_gqa.h"
 #include "saf_gqa_bwd.h"
+#include "saf_measure_kernels.h"
 #include "saf_pattern.h"
 
 #define SAF_EXPORT extern "C" __attribute__((visibility("default")))
@@ -757,6 +759,28 @@ SAF_EXPORT saf_status_t saf_compact_fit(int H, int T, const float* eta_abs, cons
     }
     hipLaunchKernelGGL(saf::fixed_lse_kernel, dim3(lse_grid), dim3(saf::NORM_THREADS), 0, stream, na);
     hipLaunchKernelGGL(saf::fit_kl_kernel, dim3(H), dim3(256), 0, stream, f);
+    return launched();
+}
+
+// Measurement aids.
+SAF_EXPORT saf_status_t saf_clock_probe(uint64_t* out, int duration_us, hipStream_t stream) {
+    if (out == nullptr) return SAF_ERR_NULL;
+    if (duration_us < 1 || duration_us > 1000000) return SAF_ERR_SHAPE;
+    if ((reinterpret_cast<uintptr_t>(out) & 7u) != 0) return SAF_ERR_ALIGNMENT;
+    const uint64_t ticks = (uint64_t)duration_us * 100u;  // reference clock: 100 MHz
+    hipLaunchKernelGGL(saf::clock_probe_kernel, dim3(1), dim3(64), 0, stream, out, ticks);
+    return launched();
+}
+
+SAF_EXPORT saf_status_t saf_lds_read_probe(const void* src, size_t bytes, float* sink, hipStream_t stream) {
+    if (src == nullptr || sink == nullptr) return SAF_ERR_NULL;
+    if (bytes < (size_t)saf::PROBE_UNIT || bytes % saf::PROBE_UNIT != 0 || bytes > ((size_t)1 << 40))
+        return SAF_ERR_SHAPE;
+    if (!aligned16(src) || (reinterpret_cast<uintptr_t>(sink) & 3u) != 0) return SAF_ERR_ALIGNMENT;
+    const unsigned long long units = bytes / saf::PROBE_UNIT;
+    const unsigned grid = (unsigned)((units + saf::PROBE_UNITS_PER_WG - 1) / saf::PROBE_UNITS_PER_WG);
+    hipLaunchKernelGGL(saf::lds_read_probe_kernel, dim3(grid), dim3(saf::PROBE_THREADS), 0, stream,
+                       reinterpret_cast<const char*>(src), units, sink);
     return launched();
 }
 

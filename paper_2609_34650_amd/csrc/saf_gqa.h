@@ -1,7 +1,8 @@
 // Forward of the hybrid layer with grouped-query attention and head
 // dimensions 64, 96 or 128 (the layouts of the paper's grouped-query prefill
-// measurement and of its 1B model's head width: Section "Pretrained
-// grouped-query models" and Appendix "Mixed-head execution and numerical
+// measurement and of its 1B model's head width: Appendix "Replacement in
+// pretrained models", subsection "GQA prefill measurements"; Appendix "1B
+// training and evaluation"; and Appendix "Mixed-head execution and numerical
 // checks", where the grouped-query implementation drops the replaced heads'
 // query projections but keeps every shared key and value head).
 //

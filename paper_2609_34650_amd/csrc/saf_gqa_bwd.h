@@ -1,9 +1,9 @@
 // Backward of the grouped-query hybrid layer for head dimensions 64, 96 and
 // 128, for the loss sum(O * dO) (the training side of the layouts the
-// grouped-query forward serves: Section "Pretrained grouped-query models";
-// Appendix "Mixed-head execution and numerical checks", whose grouped-query
-// path keeps every shared key/value head and maps each ordinary query head to
-// its group).
+// grouped-query forward serves: Appendix "Replacement in pretrained models",
+// subsection "GQA prefill measurements"; Appendix "Mixed-head execution
+// and numerical checks", whose grouped-query path keeps every shared
+// key/value head and maps each ordinary query head to its group).
 //
 // Q, O, dO, dQ: [B, Hq, N, D]; K, V, dK, dV: [B, Hkv, N, D]; query head h
 // reads key/value head h / (Hq / Hkv).  A shared head's dK and dV are sums

@@ -300,3 +300,20 @@ def test_gqa_backward_workspace_and_rejects(lib):
     assert bwd(wsn=64) == 2                           # 4 heads x 8 rows x 4 bytes rounds to 256
     assert bwd(ws=FAKE + 16) == 6 and bwd(dV=FAKE + 4) == 6
     assert bwd(N=0, Q=None, K=None, V=None, O=None, dO=None, LSE=None, dQ=None, dK=None, dV=None, ws=None) == 0
+
+
+def test_measurement_probe_argument_errors(lib):
+    # shader-clock probe
+    assert lib.saf_clock_probe(None, 100, None) == 1
+    assert lib.saf_clock_probe(FAKE, 0, None) == 2
+    assert lib.saf_clock_probe(FAKE, 1000001, None) == 2
+    assert lib.saf_clock_probe(FAKE + 4, 100, None) == 6
+    # known-size read
+    assert lib.saf_lds_read_probe(None, 4096, FAKE, None) == 1
+    assert lib.saf_lds_read_probe(FAKE, 4096, None, None) == 1
+    assert lib.saf_lds_read_probe(FAKE, 0, FAKE, None) == 2
+    assert lib.saf_lds_read_probe(FAKE, 4095, FAKE, None) == 2
+    assert lib.saf_lds_read_probe(FAKE, 6000, FAKE, None) == 2
+    assert lib.saf_lds_read_probe(FAKE, (1 << 40) + 4096, FAKE, None) == 2
+    assert lib.saf_lds_read_probe(FAKE + 8, 4096, FAKE, None) == 6
+    assert lib.saf_lds_read_probe(FAKE, 4096, FAKE + 2, None) == 6
