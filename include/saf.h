@@ -185,6 +185,33 @@ saf_status_t saf_hybrid_attn_bwd(saf_dtype_t dt,
                                  void* workspace, size_t workspace_bytes,
                                  hipStream_t stream);
 
+/*
+ * Backward of the hybrid layer that allocates nothing and takes no workspace,
+ * for callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc).  Same
+ * arguments (minus the workspace), launches, results and errors as
+ * saf_hybrid_attn_bwd; its one scratch buffer, the row vector D, is a
+ * file-scope device array of the library holding 2^22 float32 (16 MiB), one
+ * copy per GPU, kept until the process ends.
+ *   Limit: B * H * N <= 4,194,304; larger problems return SAF_ERR_SHAPE
+ *          before anything is launched.
+ *   The current HIP device must be the device `stream` belongs to (the
+ *   array's address is looked up for the current device on its first call
+ *   there).  SAF_ERR_LAUNCH if that lookup fails.
+ *   Every call on one GPU shares that GPU's array: calls that overlap in
+ *   time on one GPU (two streams, or two threads) race and must not be
+ *   issued.  Calls in order on one stream are safe: each call writes every
+ *   entry of D it reads before reading it.
+ */
+saf_status_t saf_hybrid_attn_bwd_noalloc(saf_dtype_t dt,
+                                         const void* Q, const void* K, const void* V,
+                                         const void* O, const void* dO, const float* LSE,
+                                         const uint8_t* head_is_fixed,
+                                         const float* a, const float* r, int ld_prior,
+                                         int B, int H, int N, int d,
+                                         void* dQ, void* dK, void* dV,
+                                         hipStream_t stream);
+
 /* The backward's launches, enqueued one at a time (same arguments and
  * contract).  Two sequences give the gradients, on one stream with one
  * workspace:

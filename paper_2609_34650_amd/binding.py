@@ -56,6 +56,7 @@ EXPORTS = (
     "saf_fit_workspace_bytes",
     "saf_fit_targets",
     "saf_compact_fit",
+    "saf_hybrid_attn_bwd_noalloc",
     "saf_clock_probe",
     "saf_lds_read_probe",
 )
@@ -99,6 +100,8 @@ def load() -> ctypes.CDLL:
     bwd_args = [i, vp, vp, vp, vp, vp, vp, u8p, vp, vp, i, i, i, i, i, vp, vp, vp, vp, ctypes.c_size_t, vp]
     lib.saf_hybrid_attn_bwd.restype = ctypes.c_int
     lib.saf_hybrid_attn_bwd.argtypes = bwd_args
+    lib.saf_hybrid_attn_bwd_noalloc.restype = ctypes.c_int
+    lib.saf_hybrid_attn_bwd_noalloc.argtypes = bwd_args[:18] + [vp]
     lib.saf_hybrid_attn_bwd_stage.restype = ctypes.c_int
     lib.saf_hybrid_attn_bwd_stage.argtypes = [i] + bwd_args
     lib.saf_hybrid_attn_bwd_pattern_workspace_bytes.restype = ctypes.c_size_t
@@ -343,6 +346,18 @@ def saf_hybrid_attn_bwd(Q, K, V, O, dO, LSE, head_is_fixed, a=None, r=None, dQ=N
     args, outs, _flags_keep, _ws_keep = _bwd_common(Q, K, V, O, dO, LSE, head_is_fixed, a, r, dQ, dK, dV,
                                                     workspace)
     _raise(lib.saf_hybrid_attn_bwd(*args), "saf_hybrid_attn_bwd")
+    return outs
+
+
+def saf_hybrid_attn_bwd_noalloc(Q, K, V, O, dO, LSE, head_is_fixed, a=None, r=None, dQ=None, dK=None,
+                                dV=None):
+    """Backward through ``saf_hybrid_attn_bwd_noalloc``: no workspace (the
+    library's per-GPU scratch array holds D).  Returns ``(dQ, dK, dV)``, the
+    outputs as passed (or allocated here when None)."""
+    lib = load()
+    args, outs, _flags_keep, _ws_keep = _bwd_common(Q, K, V, O, dO, LSE, head_is_fixed, a, r, dQ, dK, dV,
+                                                    torch.empty(0, dtype=torch.uint8, device=V.device))
+    _raise(lib.saf_hybrid_attn_bwd_noalloc(*(args[:18] + [args[-1]])), "saf_hybrid_attn_bwd_noalloc")
     return outs
 
 

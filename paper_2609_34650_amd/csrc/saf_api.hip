@@ -1,6 +1,8 @@
 // Host side of libsaf.so: argument checks and kernel launches for the C ABI
-// declared in include/saf.h, include/saf_calib.h and include/saf_fit.h.  No
-// allocation, no synchronisation, no global mutable state.
+// declared in include/saf.h, include/saf_calib.h, include/saf_fit.h and
+// include/saf_measure.h.  No allocation, no synchronisation; the only global
+// state is the per-device address of the no-allocation backward's scratch
+// array, looked up once per device.
 #include "saf.h"
 #include "saf_calib.h"
 #include "saf_fit.h"
@@ -8,6 +10,7 @@
 
 #include <math.h>
 #include <algorithm>
+#include <mutex>
 #include <stdint.h>
 
 #include "saf_bwd.h"
@@ -462,6 +465,62 @@ SAF_EXPORT saf_status_t saf_hybrid_attn_bwd(saf_dtype_t dt, const void* Q, const
         make_bwd_args(Q, K, V, O, dO, LSE, a, r, ld_prior, B, H, N, dQ, dK, dV, workspace, pr);
     // The query-block pass forms D itself and writes it for the key-block
     // pass, so no row pre-pass runs here.
+    st = run_bwd_stage(SAF_BWD_DQ_WITH_D, dt, args, stream);
+    if (st != SAF_OK) return st;
+    return run_bwd_stage(SAF_BWD_DKDV, dt, args, stream);
+}
+
+// ---------------------------------------------------------------------------
+// Backward without a caller workspace (saf_hybrid_attn_bwd_noalloc).  Its only
+// scratch, the row vector D, lives in this file-scope device array: one copy
+// per GPU, held until the process ends.  Host code never passes the array's
+// name to a kernel (on the host it is a stand-in, not a device address); it
+// uses the address hipGetSymbolAddress returns for the current device, looked
+// up once per device and kept in `g_scratch_ptr`.
+// ---------------------------------------------------------------------------
+namespace {
+
+constexpr size_t kNoAllocMaxRows = (size_t)1 << 22;  // B * H * N <= 4,194,304 rows: 16 MiB of float32
+static __device__ __align__(256) float scratch[kNoAllocMaxRows];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+float* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of `scratch` on the current device (nullptr on failure).
+float* scratch_on_current_device() {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (g_scratch_ptr[dev] == nullptr) {
+        void* ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || ptr == nullptr) return nullptr;
+        g_scratch_ptr[dev] = reinterpret_cast<float*>(ptr);
+    }
+    return g_scratch_ptr[dev];
+}
+
+}  // namespace
+
+SAF_EXPORT saf_status_t saf_hybrid_attn_bwd_noalloc(saf_dtype_t dt, const void* Q, const void* K, const void* V,
+                                                    const void* O, const void* dO, const float* LSE,
+                                                    const uint8_t* head_is_fixed, const float* a, const float* r,
+                                                    int ld_prior, int B, int H, int N, int d, void* dQ, void* dK,
+                                                    void* dV, hipStream_t stream) {
+    // Validate as saf_hybrid_attn_bwd does, with a stand-in workspace of the
+    // right size (the check reads only its alignment and size).
+    Problem pr;
+    const size_t need = (B > 0 && H > 0 && N > 0) ? workspace_bytes(B, H, N) : 0;
+    void* const probe = reinterpret_cast<void*>((uintptr_t)256);
+    saf_status_t st = check_bwd(SAF_BWD_PREPROCESS, dt, Q, K, V, O, dO, LSE, head_is_fixed, a, r, ld_prior, B, H,
+                                N, d, dQ, dK, dV, probe, need, &pr);
+    if (st != SAF_OK || pr.empty) return st;
+    if ((size_t)B * H * N > kNoAllocMaxRows) return SAF_ERR_SHAPE;
+    float* ws = scratch_on_current_device();
+    if (ws == nullptr) return SAF_ERR_LAUNCH;
+    // D is written by the query-block pass for every row the key-block pass
+    // reads, so nothing needs clearing between calls.
+    const saf::BwdArgs args = make_bwd_args(Q, K, V, O, dO, LSE, a, r, ld_prior, B, H, N, dQ, dK, dV, ws, pr);
     st = run_bwd_stage(SAF_BWD_DQ_WITH_D, dt, args, stream);
     if (st != SAF_OK) return st;
     return run_bwd_stage(SAF_BWD_DKDV, dt, args, stream);
