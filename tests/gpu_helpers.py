@@ -60,7 +60,7 @@ def run_gpu(inp: dict, dtype: str, backward: bool = True):
     return {k: v.float().cpu().numpy().astype(np.float64) for k, v in res.items()}
 
 
-def check_close(name: str, got: np.ndarray, ref: np.ndarray, dtype: str):
+def check_close(name: str, got: np.ndarray, ref: np.ndarray, dtype: str, extra=0.0):
     assert got.shape == ref.shape, (name, got.shape, ref.shape)
     assert np.isfinite(got).all(), f"{name}: non-finite GPU values"
     err = np.abs(got - ref)
@@ -68,7 +68,7 @@ def check_close(name: str, got: np.ndarray, ref: np.ndarray, dtype: str):
         worst = float(err.max()) if err.size else 0.0
         assert worst <= F32_ATOL, f"{name}: max abs err {worst:.3e} > {F32_ATOL}"
     else:
-        bound = BF16_ATOL + BF16_RTOL * np.abs(ref)
+        bound = BF16_ATOL + BF16_RTOL * np.abs(ref) + extra
         ratio = err / bound
         if ratio.size:
             i = np.unravel_index(int(np.argmax(ratio)), ratio.shape)
@@ -77,8 +77,10 @@ def check_close(name: str, got: np.ndarray, ref: np.ndarray, dtype: str):
     return float(err.max()) if err.size else 0.0
 
 
-def compare_layer(gpu: dict, inp: dict, dtype: str, backward: bool = True, heads=None):
-    """Compare every listed (b, h) slice (all if ``heads`` is None)."""
+def compare_layer(gpu: dict, inp: dict, dtype: str, backward: bool = True, heads=None, extra=None):
+    """Compare every listed (b, h) slice (all if ``heads`` is None).
+    ``extra``: optional per-element additions to the bf16 bar for dQ, dK, dV
+    (``bf16_rounding_bound``)."""
     from oracle import saf_oracle as orc
     O, LSE = orc.layer_forward(inp["Q"], inp["K"], inp["V"], inp["is_fixed"], inp["a"], inp["r"],
                                heads=heads)
@@ -89,13 +91,58 @@ def compare_layer(gpu: dict, inp: dict, dtype: str, backward: bool = True, heads
         refs.update(dQ=dQ, dK=dK, dV=dV)
     errs = {}
     sel = heads if heads is not None else [(b, h) for b in range(O.shape[0]) for h in range(O.shape[1])]
+    ex = dict(zip(("dQ", "dK", "dV"), extra)) if extra is not None else {}
     for name, ref in refs.items():
         got = np.stack([gpu[name][b, h] for b, h in sel])
         want = np.stack([ref[b, h] for b, h in sel])
-        errs[name] = check_close(name, got, want, dtype)
+        add = np.stack([ex[name][b, h] for b, h in sel]) if name in ex else 0.0
+        errs[name] = check_close(name, got, want, dtype, add)
     if backward:
         fixed = np.asarray(inp["is_fixed"]).astype(bool)
         for b, h in sel:
             if fixed[h]:
                 assert not gpu["dQ"][b, h].any() and not gpu["dK"][b, h].any(), "fixed head dQ/dK not zero"
     return errs
+
+
+def bf16_rounding_bound(inp, Hkv=None):
+    """Per element of (dQ, dK, dV): the largest change that rounding the
+    backward's operands to bf16 can make, evaluated in float64 from the
+    oracle's quantities.  The kernels round P (or, for fixed heads, P scaled
+    per key) to bf16 before P^T dO, round dS to bf16 before dS^T Q and dS K,
+    and take D from the forward output as stored in bf16; each rounding has
+    relative error at most u = 2^-9.  With E_i = sum_c |dO_ic O_ic| (so
+    |D_kernel - D_i| <= u E_i, moving dS(i, j) by at most u P(i, j) E_i):
+      dV(j, c) <- u sum_h sum_i P(i, j) |dO(i, c)|
+      dK(j, c) <- u scale sum_h sum_i (|dS(i, j)| + P(i, j) E_i) |Q(i, c)|
+      dQ(i, c) <- u scale sum_j (|dS(i, j)| + P(i, j) E_i) |K(j, c)|
+    summed over the query heads h of the key/value group for dK and dV
+    (``Hkv`` key/value heads; None: one per query head, the layer)."""
+    from oracle import saf_oracle as orc
+    u = 2.0 ** -9
+    Q, K, V, dO = (inp[k].astype(np.float64) for k in ("Q", "K", "V", "dO"))
+    B, Hq, N, d = Q.shape
+    group = Hq // (Hkv or Hq)
+    scale = 1.0 / np.sqrt(d)
+    wq, wk, wv = np.zeros(Q.shape), np.zeros(K.shape), np.zeros(V.shape)
+    rows = np.arange(N)
+    for b in range(B):
+        for h in range(Hq):
+            g = h // group
+            if inp["is_fixed"][h]:
+                P = orc.fixed_pattern(inp["a"][h], inp["r"][h], N)
+            else:
+                s_ = orc.ordinary_logits(Q[b, h], K[b, g], rows)
+                P = np.exp(s_ - s_.max(axis=1, keepdims=True))
+                P /= P.sum(axis=1, keepdims=True)
+            wv[b, g] += u * P.T @ np.abs(dO[b, h])
+            if inp["is_fixed"][h]:
+                continue
+            dp = dO[b, h] @ V[b, g].T
+            Dr = np.sum(P * dp, axis=1)
+            dS = P * (dp - Dr[:, None])
+            E = np.sum(np.abs(dO[b, h] * (P @ V[b, g])), axis=1)
+            M = np.abs(dS) + P * E[:, None]
+            wk[b, g] += u * scale * M.T @ np.abs(Q[b, h])
+            wq[b, h] += u * scale * M @ np.abs(K[b, g])
+    return wq, wk, wv

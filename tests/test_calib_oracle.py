@@ -135,3 +135,22 @@ def test_single_input_variance_is_undefined():
     st = co.calibration_stats(Q, K)
     assert np.isnan(st["s_var"][0])
     assert st["s_kl"][0] == 0.0
+
+
+def test_calib_golden_file_invariants():
+    """tests/golden/calib124m_4k_head0.npz (written by
+    make_calib124m_head0.py from the oracle) is self-consistent: both
+    marginals of the mean attention total T, the stored mean rows are
+    row-stochastic and causal, and both scores are positive."""
+    import os
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "calib124m_4k_head0.npz")
+    ref = np.load(path)
+    T = ref["eta_abs"].shape[0]
+    assert T == 4096
+    np.testing.assert_allclose(ref["eta_abs"].sum(), T, rtol=1e-12)
+    np.testing.assert_allclose(ref["eta_rel"].sum(), T, rtol=1e-12)
+    rows = ref["rows"]
+    np.testing.assert_allclose(ref["A_mean_rows"].sum(axis=1), 1.0, atol=1e-12)
+    for li, i in enumerate(rows):
+        assert not ref["A_mean_rows"][li, i + 1:].any()
+    assert float(ref["s_var"]) > 0 and float(ref["s_kl"]) > 0

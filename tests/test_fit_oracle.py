@@ -134,3 +134,29 @@ def test_initialisation_closed_form():
     a, r = fo.fit(t["eta_abs"], t["eta_rel"], steps=0)
     assert not a.any()
     np.testing.assert_allclose(r, [math.log((harm[T] - harm[d]) / (T - d)) for d in range(T)], rtol=1e-14)
+
+
+def test_fit_golden_file_invariants():
+    """tests/golden/fit_golden.npz (written by make_fit_golden.py from the
+    oracle) is self-consistent: each stored pattern row sums to one, the
+    column and diagonal sums each total T, the stored log Z is the oracle's
+    normaliser of the stored alpha and rho, and the KL is non-negative."""
+    import os
+    from oracle import fit_oracle as fo
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "fit_golden.npz")
+    ref = np.load(path)
+    keys = sorted({k.rsplit("_", 1)[0] for k in ref.files if k.endswith("_kl")})
+    assert keys == ["t1024_h0", "t1024_h1", "t4096_h0"]
+    for key in keys:
+        T = ref[key + "_a"].shape[0]
+        np.testing.assert_allclose(ref[key + "_P_rows"].sum(axis=1), 1.0, atol=1e-12)
+        np.testing.assert_allclose(ref[key + "_col"].sum(), T, rtol=1e-12)
+        np.testing.assert_allclose(ref[key + "_diag"].sum(), T, rtol=1e-12)
+        assert float(ref[key + "_kl"]) >= 0.0
+        if T <= 1024:
+            rows = ref[key + "_rows"]
+            L = fo.compact_logits(ref[key + "_a"], ref[key + "_r"])[rows]
+            m = L.max(axis=1)
+            lz = m + np.log(np.exp(L - m[:, None]).sum(axis=1))
+            np.testing.assert_allclose(ref[key + "_logz"][rows], lz, rtol=0, atol=1e-12)
+            np.testing.assert_allclose(ref[key + "_P_rows"], np.exp(L - lz[:, None]), rtol=0, atol=1e-15)

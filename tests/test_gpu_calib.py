@@ -13,6 +13,9 @@ a few 1e-6 (LSE rounding and exp2), so
   of size ~ln T).
 """
 
+import functools
+import os
+
 import numpy as np
 import pytest
 
@@ -79,6 +82,10 @@ def _compare(g, o, T):
     ("bf16", 4, 2, 260, (3, 1), False),
     ("bf16", 3, 1, 128, (3,), False),          # exactly one tile
     ("bf16", 2, 2, 37, (2,), True),            # one partial tile
+    # The accumulation path the benchmark times (no per-entry squared
+    # deviations, micro-batches of two) over eight 128-query tiles.
+    ("bf16", 8, 2, 1024, (2, 2, 2, 2), False),
+    ("f32", 8, 1, 1024, (2, 2, 2, 2), False),
 ])
 def test_calib_matches_oracle(dtype, N, H, T, micro, keep_m2):
     from oracle import calib_oracle as co
@@ -129,18 +136,51 @@ def test_calib_single_input_and_single_position():
     np.testing.assert_allclose(g["s_kl"], 0.0, atol=SKL_ATOL)
 
 
-@pytest.mark.slow
-def test_calib_full_size_sampled_rows():
-    """The 124M-style calibration workload (32 inputs of T = 4096 in
-    micro-batches of two, 12 heads, bf16): sampled rows of the mean attention
-    and their share of the variance score against the oracle; the marginals
-    and the scores against sums over the GPU's own state (float64), which
-    hold at any size; the marginals sum to T."""
-    from oracle import calib_oracle as co
+@functools.lru_cache(maxsize=1)
+def _full_inputs():
     from paper_2609_34650_amd import inputs
     w = inputs.CALIB_WORKLOADS["calib124m_4k"]
-    announce(f"calib full size {w.name}")
-    inp = inputs.calib_inputs(w.n_cal, w.H, w.T, w.d, w.dtype, stream_id=w.stream_id)
+    return w, inputs.calib_inputs(w.n_cal, w.H, w.T, w.d, w.dtype, stream_id=w.stream_id)
+
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "calib124m_4k_head0.npz")
+
+
+@pytest.mark.slow
+def test_calib_full_size_no_m2():
+    """The accumulation path the benchmark times (no per-entry squared
+    deviations) on the 124M-style workload (32 inputs of T = 4096 in
+    micro-batches of two, 12 heads, bf16): head 0 against the oracle's
+    statistics over every row (tests/golden/calib124m_4k_head0.npz, written by
+    make_calib124m_head0.py from the oracle alone) -- mean rows, both
+    marginals elementwise, both scores -- and sampled mean rows of every head
+    against the oracle computed here."""
+    from oracle import calib_oracle as co
+    w, inp = _full_inputs()
+    announce(f"calib full size {w.name} without m2")
+    g, _ = _gpu_stats(inp["Q"], inp["K"], w.dtype, (w.micro,) * (w.n_cal // w.micro), keep_m2=False)
+    ref = np.load(GOLDEN)
+    rows = ref["rows"]
+    np.testing.assert_allclose(g["A_mean"][0, rows], ref["A_mean_rows"], rtol=A_RTOL, atol=A_ATOL)
+    np.testing.assert_allclose(g["eta_abs"][0], ref["eta_abs"], rtol=A_RTOL, atol=A_ATOL * w.T)
+    np.testing.assert_allclose(g["eta_rel"][0], ref["eta_rel"], rtol=A_RTOL, atol=A_ATOL * w.T)
+    np.testing.assert_allclose(g["s_var"][0], float(ref["s_var"]), rtol=SVAR_RTOL)
+    np.testing.assert_allclose(g["s_kl"][0], float(ref["s_kl"]), rtol=0, atol=SKL_ATOL)
+    o = co.calibration_stats(inp["Q"], inp["K"], rows=rows)
+    np.testing.assert_allclose(g["A_mean"][:, rows], o["A_mean"], rtol=A_RTOL, atol=A_ATOL)
+    np.testing.assert_allclose(g["eta_abs"].sum(axis=1), w.T, rtol=1e-4)
+    np.testing.assert_allclose(g["eta_rel"].sum(axis=1), w.T, rtol=1e-4)
+
+
+@pytest.mark.slow
+def test_calib_full_size_sampled_rows():
+    """The same workload with the per-entry squared deviations kept: sampled
+    rows of the mean attention and their share of the variance score against
+    the oracle; the marginals and the scores against sums over the GPU's own
+    state (float64), which hold at any size; the marginals sum to T."""
+    from oracle import calib_oracle as co
+    w, inp = _full_inputs()
+    announce(f"calib full size {w.name} with m2")
     g, _ = _gpu_stats(inp["Q"], inp["K"], w.dtype, (w.micro,) * (w.n_cal // w.micro), keep_m2=True)
     rows = np.array([0, 1, 127, 128, 2049, 4000, w.T - 1])
     o = co.calibration_stats(inp["Q"], inp["K"], rows=rows)
@@ -154,4 +194,7 @@ def test_calib_full_size_sampled_rows():
     np.testing.assert_allclose(g["eta_abs"].sum(axis=1), w.T, rtol=1e-4)
     np.testing.assert_allclose(g["eta_rel"].sum(axis=1), w.T, rtol=1e-4)
     np.testing.assert_allclose(g["s_var"], g["m2"].sum(axis=(1, 2)) / ((w.n_cal - 1) * w.T * w.T), rtol=1e-4)
+    ref = np.load(GOLDEN)
+    np.testing.assert_allclose(g["s_var"][0], float(ref["s_var"]), rtol=SVAR_RTOL)
+    np.testing.assert_allclose(g["s_kl"][0], float(ref["s_kl"]), rtol=0, atol=SKL_ATOL)
     assert np.all(g["s_kl"] > 0) and np.all(np.isfinite(g["s_kl"]))

@@ -15,6 +15,8 @@ given parameters, and the gauge of the parameters cancels in it only with
 both vectors) is compared through the fitted pattern's row normalisers.
 """
 
+import os
+
 import numpy as np
 import pytest
 
@@ -92,3 +94,48 @@ def test_compact_fit_long_context():
         oa, orr = fo.fit(t["eta_abs"], t["eta_rel"])
         okl = fo.fit_kl(oa, orr, t["eta_abs"], t["eta_rel"], t["neg_entropy"])
         np.testing.assert_allclose(float(kl[h]), okl, rtol=1e-3, atol=1e-4)
+
+
+FIT_GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "fit_golden.npz")
+FIT_CASES = {"t1024": (2, 1024, 43), "t4096": (1, 4096, 44)}
+# The float32 fitter follows the float64 oracle's Adam trajectory closely all
+# the way (measured on MI355X: pattern entries and both marginals within 2e-5
+# relative after 400 steps, KL within 1e-6), so the bars are 1e-3 relative.
+P_ATOL, P_RTOL = 1e-6, 1e-3      # fitted pattern entries
+M_ATOL, M_RTOL = 1e-5, 1e-3      # its column and diagonal sums
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("case", sorted(FIT_CASES))
+def test_compact_fit_400_steps_pattern_matches_oracle(case):
+    """After the full 400 Adam steps the fitted pattern itself -- unique at
+    the optimum, unlike (alpha, rho), which share a gauge -- against the fp64
+    oracle's (tests/golden/fit_golden.npz, written by make_fit_golden.py from
+    the oracle alone): whole sampled rows of P_hat, its column sums and
+    diagonal sums (the marginals the fit matches to the target's), and the
+    acceptance KL.  The GPU's pattern is evaluated in float64 from its
+    returned alpha, rho and log Z, so a wrong normaliser shows as rows that
+    miss the oracle's.  Cases: two heads at T = 1024 and head 0 of the
+    benchmarked 12-head layer at T = 4096."""
+    torch = torch_cuda()
+    from oracle import fit_oracle as fo
+    from paper_2609_34650_amd import binding, inputs
+    H, T, sid = FIT_CASES[case]
+    announce(f"compact fit 400 steps {case} H={H} T={T}")
+    mean = inputs.fit_target_means(H, T, stream_id=sid)
+    ea, er, ne = _targets_gpu(mean)
+    a, r, log_z, kl = binding.saf_compact_fit(ea, er, ne)
+    torch.cuda.synchronize()
+    ref = np.load(FIT_GOLDEN)
+    for h in range(H):
+        key = f"{case}_h{h}"
+        ga, gr, glz = (x[h].double().cpu().numpy() for x in (a, r, log_z))
+        P = np.exp(fo.compact_logits(ga, gr) - glz[:, None])
+        rows = ref[key + "_rows"]
+        np.testing.assert_allclose(P[rows], ref[key + "_P_rows"], rtol=P_RTOL, atol=P_ATOL)
+        np.testing.assert_allclose(P.sum(axis=1), 1.0, rtol=0, atol=1e-4)
+        np.testing.assert_allclose(P.sum(axis=0), ref[key + "_col"], rtol=M_RTOL, atol=M_ATOL)
+        diag = np.array([np.trace(P, offset=-d) for d in range(T)])
+        np.testing.assert_allclose(diag, ref[key + "_diag"], rtol=M_RTOL, atol=M_ATOL)
+        np.testing.assert_allclose(float(kl[h]), float(ref[key + "_kl"]), rtol=1e-4, atol=1e-6)
+

@@ -11,7 +11,7 @@ float32 ``max |gpu - oracle| <= 1e-4``; bf16 ``|gpu - oracle| <= 1e-2 +
 import numpy as np
 import pytest
 
-from gpu_helpers import BF16_ATOL, BF16_RTOL, F32_ATOL, announce, torch_cuda
+from gpu_helpers import BF16_ATOL, BF16_RTOL, F32_ATOL, announce, bf16_rounding_bound, torch_cuda
 
 pytestmark = pytest.mark.gpu
 
@@ -37,11 +37,11 @@ def _run_gpu(inp, dtype):
     return O.double().cpu().numpy(), LSE.double().cpu().numpy()
 
 
-def _check(dtype, g, o):
+def _check(dtype, g, o, extra=0.0):
     if dtype == "f32":
         assert np.max(np.abs(g - o)) <= F32_ATOL
     else:
-        excess = np.abs(g - o) - (BF16_ATOL + BF16_RTOL * np.abs(o))
+        excess = np.abs(g - o) - (BF16_ATOL + BF16_RTOL * np.abs(o) + extra)
         assert np.max(excess) <= 0, float(np.max(excess))
 
 
@@ -162,11 +162,14 @@ def _run_gpu_bwd(inp, dtype):
     ("f32", 1, 2, 1, 129, 64, ()),
     ("bf16", 1, 8, 2, 1000, 128, (1, 2, 6)),    # several key blocks, mixed groups
     ("f32", 1, 3, 3, 257, 96, (1,)),
-    # The largest head count (mask bit 63), checked in float32: at d = 128 in
-    # bf16 a few of 64 heads' elements pass the elementwise bar only narrowly
-    # or not at all (gradients up to ~9 in size, errors ~0.4 % of that), for
-    # ordinary heads as much as for fixed ones.
+    # The largest head count (mask bit 63), float32 and bf16.  In bf16 at
+    # d = 128 the gradients reach ~9 in size and a few small elements of 64
+    # heads miss the plain elementwise bar; that case is held to the plain bar
+    # plus the worst-case effect of the bf16 operand rounding on each element
+    # (``gpu_helpers.bf16_rounding_bound``, computed in float64 from the oracle's P, dS
+    # and the inputs).
     ("f32", 1, 64, 16, 90, 128, (1, 2, 3, 62, 63)),
+    ("bf16", 1, 64, 16, 90, 128, (1, 2, 3, 62, 63)),
 ])
 def test_gqa_backward_matches_oracle(dtype, B, Hq, Hkv, N, d, fixed):
     from oracle import saf_oracle as orc
@@ -174,9 +177,10 @@ def test_gqa_backward_matches_oracle(dtype, B, Hq, Hkv, N, d, fixed):
     inp = _bwd_inputs(dtype, B, Hq, Hkv, N, d, list(fixed), stream_id=55)
     g = _run_gpu_bwd(inp, dtype)
     o = orc.layer_backward_gqa(inp["Q"], inp["K"], inp["V"], inp["dO"], inp["is_fixed"], inp["a"], inp["r"])
-    for name, gv, ov in zip(("dQ", "dK", "dV"), g, o):
+    extra = bf16_rounding_bound(inp, Hkv) if (dtype == "bf16" and Hq == 64) else (0.0, 0.0, 0.0)
+    for name, gv, ov, w in zip(("dQ", "dK", "dV"), g, o, extra):
         assert np.isfinite(gv).all(), name
-        _check(dtype, gv, ov)
+        _check(dtype, gv, ov, w)
     fixed_q = np.asarray(inp["is_fixed"]).astype(bool)
     assert not g[0][:, fixed_q].any(), "fixed heads must get zero dQ"
     group = Hq // Hkv

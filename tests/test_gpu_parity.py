@@ -11,7 +11,7 @@ query rows for the 32K forward.
 import numpy as np
 import pytest
 
-from gpu_helpers import announce, check_close, compare_layer, run_gpu, to_device, torch_cuda
+from gpu_helpers import announce, bf16_rounding_bound, check_close, compare_layer, run_gpu, to_device, torch_cuda
 from paper_2609_34650_amd import inputs as gen
 
 pytestmark = pytest.mark.gpu
@@ -99,14 +99,24 @@ def test_scores_growing_along_keys_f32():
 
 
 def test_scores_growing_along_keys_bf16_forward():
-    """The same inputs in bf16, forward only (O and LSE, where the rescaling
-    lives).  The bf16 backward of such peaked rows is not held to the bar:
-    with O rounded to bf16, D = rowsum(dO * O) alone moves dQ by more than
-    1e-2 + 2e-2 |dQ| here, for any kernel that rounds O and dS to bf16 (a
-    float64 simulation of that rounding reaches 1.2 times the bound)."""
+    """The same inputs in bf16, forward (O and LSE, where the rescaling
+    lives) at the plain bf16 bar."""
     announce("growing scores bf16 forward")
     inp = _growing_scores_inputs("bf16", False)
     print(compare_layer(run_gpu(inp, "bf16", backward=False), inp, "bf16", backward=False))
+
+
+def test_scores_growing_along_keys_bf16_backward():
+    """The same inputs in bf16, forward and backward.  On these peaked rows
+    the bf16 rounding of O (through D = rowsum(dO * O)) and of dS moves dQ by
+    more than the plain bar 1e-2 + 2e-2 |dQ| for any kernel that rounds those
+    operands to bf16, so the gradients are held to the plain bar plus the
+    worst-case effect of that rounding on each element
+    (``gpu_helpers.bf16_rounding_bound``, float64 from the oracle's P, dS and
+    the inputs)."""
+    announce("growing scores bf16 backward")
+    inp = _growing_scores_inputs("bf16", True)
+    print(compare_layer(run_gpu(inp, "bf16"), inp, "bf16", extra=bf16_rounding_bound(inp)))
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
