@@ -418,12 +418,14 @@ __device__ __forceinline__ void kvf_store(float* gs, float* band, const KvFixSta
     }
 }
 
-// dV^T += dO^T (er g): the weight operand of lane (key c, half hf) in chunk
-// (qb, kc) is er(q - key) g(q) for its eight queries q, formed in float32
-// from the band and g and rounded once.
-template <typename T, bool MASK>
-__device__ __forceinline__ void kvf_tile(const T* dot, const float* band, const float* gs, int mq, const KvLane& L,
-                                         f32x16 (&dv)[KV_KB][2]) {
+// dV^T += dO^T (er g) for NB batch elements at once: the weight operand of
+// lane (key c, half hf) in chunk (qb, kc) is er(q - key) g(q) for its eight
+// queries q, formed in float32 from the band and g and rounded once, then fed
+// to the MFMAs of every batch element's dO tile (the pattern and its
+// normalisers do not depend on the input).
+template <typename T, int NB, bool MASK>
+__device__ __forceinline__ void kvf_tile(const T* const (&dot)[NB], const float* band, const float* gs, int mq,
+                                         const KvLane& L, f32x16 (&dv)[NB][KV_KB][2]) {
     typedef typename Vec<T>::x8 frag;
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
@@ -432,11 +434,9 @@ __device__ __forceinline__ void kvf_tile(const T* dot, const float* band, const 
 #pragma unroll
         for (int kc = 0; kc < 2; ++kc) {
             const int col = 32 * qb + 16 * kc + 8 * L.hf;  // first query (within the tile) of this lane's slots
-            frag gta[2];
-#pragma unroll
-            for (int db = 0; db < 2; ++db) gta[db] = ld_tile_t<false>(dot, 32 * qb + 16 * kc, 32 * db);
             const f32x4 g0 = *reinterpret_cast<const f32x4*>(gs + col);
             const f32x4 g1 = *reinterpret_cast<const f32x4*>(gs + col + 4);
+            frag w[KV_KB];
 #pragma unroll
             for (int kb = 0; kb < KV_KB; ++kb) {
                 const int kl = L.kw - L.n0 + 32 * kb + L.c;
@@ -445,25 +445,37 @@ __device__ __forceinline__ void kvf_tile(const T* dot, const float* band, const 
                 const float* bp = band + s * KV_BAND_STRIDE + u0 - s;
                 const f32x4 b0 = *reinterpret_cast<const f32x4*>(bp);
                 const f32x4 b1 = *reinterpret_cast<const f32x4*>(bp + 4);
-                frag w;
 #pragma unroll
                 for (int t = 0; t < 4; ++t) {
-                    w[t] = (T)(b0[t] * g0[t]);
-                    w[4 + t] = (T)(b1[t] * g1[t]);
+                    w[kb][t] = (T)(b0[t] * g0[t]);
+                    w[kb][4 + t] = (T)(b1[t] * g1[t]);
                 }
+            }
 #pragma unroll
-                for (int db = 0; db < 2; ++db) mma(dv[kb][db], gta[db], w);
+            for (int nb = 0; nb < NB; ++nb) {
+                frag gta[2];
+#pragma unroll
+                for (int db = 0; db < 2; ++db) gta[db] = ld_tile_t<false>(dot[nb], 32 * qb + 16 * kc, 32 * db);
+#pragma unroll
+                for (int kb = 0; kb < KV_KB; ++kb)
+#pragma unroll
+                    for (int db = 0; db < 2; ++db) mma(dv[nb][kb][db], gta[db], w[kb]);
             }
         }
     }
 }
 
-template <typename T>
+// NB batch elements b, b + 1, .. of one fixed head and key block (slice
+// offsets base + nb * slice; log Z is read from batch element b, the same
+// for all).
+template <typename T, int NB>
 __device__ __forceinline__ void kv_fixed(const Tiles<T>& sm, const BwdArgs& p, const KvLane& L, size_t base,
                                          size_t row_base, int h) {
-    // Tiles: dO in t[0] / t[1] (buffer loads to LDS), the float32 band in
-    // t[2] / t[3]; g of the tile's rows in aux[0] / aux[1].
-    const T* __restrict__ dO = reinterpret_cast<const T*>(p.dO) + base;
+    // Tiles: dO of batch element nb in t[4 nb] / t[4 nb + 1] (buffer loads to
+    // LDS), the float32 band in t[2] / t[3]; g of the tile's rows in aux[0] /
+    // aux[1].
+    const size_t slice = (size_t)p.H * p.N * HEAD_DIM;
+    const size_t rows = (size_t)p.H * p.N;
     const float* __restrict__ LSE = p.lse + row_base;
     const float* __restrict__ arow = p.a + (size_t)h * p.ld_prior;
     const float* __restrict__ rrow = p.r + (size_t)h * p.ld_prior;
@@ -483,28 +495,37 @@ __device__ __forceinline__ void kv_fixed(const Tiles<T>& sm, const BwdArgs& p, c
     const float R = block_max(rm, sm.red);
     const float LO = -block_max(-lo, sm.red);
     if (!(LO - A - R >= -FAST_GUARD)) {  // some g(i) could overflow
-        kv_fixed_exact<T>(sm, p, L, base, row_base, arow, rrow);
+        for (int nb = 0; nb < NB; ++nb) {
+            if (nb > 0) __syncthreads();
+            kv_fixed_exact<T>(sm, p, L, base + nb * slice, row_base + nb * rows, arow, rrow);
+        }
         return;
     }
     const float g_sh = (A + R) * LOG2E, r_sh = R * LOG2E, a_sh = A * LOG2E;
 
-    f32x16 dv[KV_KB][2];
+    f32x16 dv[NB][KV_KB][2];
 #pragma unroll
-    for (int kb = 0; kb < KV_KB; ++kb)
+    for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-        for (int db = 0; db < 2; ++db)
+        for (int kb = 0; kb < KV_KB; ++kb)
 #pragma unroll
-            for (int v = 0; v < 16; ++v) dv[kb][db][v] = 0.0f;
+            for (int db = 0; db < 2; ++db)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) dv[nb][kb][db][v] = 0.0f;
 
     const int n_tiles = (N - L.n0 + KV_BM - 1) / KV_BM;
     const int n_mask = min(KV_MASK_TILES, n_tiles);
     const int P = (n_mask + 1) & ~1;
-    const __amdgpu_buffer_rsrc_t rg = slice_rsrc<T>(dO, N);
+    __amdgpu_buffer_rsrc_t rg[NB];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) rg[nb] = slice_rsrc<T>(reinterpret_cast<const T*>(p.dO) + base + nb * slice, N);
     KvFixStage st;
     run_slots(
         P, P + n_tiles - n_mask, [&](int i) { return i < P ? (i < n_mask ? i : -1) : n_mask + (i - P); },
         [&](auto buf, int t) {
-            tile_load_lds<T>(sm.t[decltype(buf)::value], rg, L.n0 + t * KV_BM, L.w, L.lane);
+            constexpr int b = decltype(buf)::value;
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb) tile_load_lds<T>(sm.t[4 * nb + b], rg[nb], L.n0 + t * KV_BM, L.w, L.lane);
             kvf_load(st, LSE, rrow, L.n0 + t * KV_BM, L);
         },
         [&](auto buf) {
@@ -513,8 +534,11 @@ __device__ __forceinline__ void kv_fixed(const Tiles<T>& sm, const BwdArgs& p, c
         },
         [&](auto buf, int t, auto mask) {
             constexpr int b = decltype(buf)::value;
-            kvf_tile<T, decltype(mask)::value>(sm.t[b], reinterpret_cast<const float*>(sm.t[2 + b]), sm.aux[b],
-                                               L.n0 + t * KV_BM, L, dv);
+            const T* dot[NB];
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb) dot[nb] = sm.t[4 * nb + b];
+            kvf_tile<T, NB, decltype(mask)::value>(dot, reinterpret_cast<const float*>(sm.t[2 + b]), sm.aux[b],
+                                                   L.n0 + t * KV_BM, L, dv);
         });
     float ea[KV_KB];
 #pragma unroll
@@ -522,8 +546,11 @@ __device__ __forceinline__ void kv_fixed(const Tiles<T>& sm, const BwdArgs& p, c
         const int key = L.kw + 32 * kb + L.c;
         ea[kb] = key < N ? fast_exp2(fmaf(arow[key], LOG2E, -a_sh)) : 0.0f;
     }
-    kv_store_rows<T>(reinterpret_cast<T*>(p.dv) + base, L, dv, ea);
-    kv_store_zero<T>(reinterpret_cast<T*>(p.dk) + base, L);
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+        kv_store_rows<T>(reinterpret_cast<T*>(p.dv) + base + nb * slice, L, dv[nb], ea);
+        kv_store_zero<T>(reinterpret_cast<T*>(p.dk) + base + nb * slice, L);
+    }
 }
 
 template <typename T>
@@ -553,12 +580,23 @@ __global__ __launch_bounds__(KV_THREADS) __attribute__((amdgpu_waves_per_eu(size
     L.n0 = kblk * KV_BN;
     L.kw = L.n0 + 32 * KV_KB * L.w;
     L.N = p.N;
-    const size_t base = (size_t)bh * p.N * HEAD_DIM;
-    const size_t row_base = (size_t)bh * p.N;
-    if ((p.fixed_mask >> h) & 1ull)
-        kv_fixed<T>(sm, p, L, base, row_base, h);
-    else
-        kv_ordinary<T>(sm, p, L, base, row_base);
+    if ((p.fixed_mask >> h) & 1ull) {
+        // Batch elements pair up as in the forward: one workgroup of the pair
+        // (the one whose batch parity matches the key block's) forms the
+        // weights once and serves both; an unpaired last element (odd B) is
+        // served alone.
+        const int b0 = sl.b & ~1;
+        const bool paired = b0 + 1 < p.B;
+        if (paired && (sl.b & 1) != (kblk & 1)) return;
+        const size_t base = ((size_t)b0 * p.H + h) * p.N * HEAD_DIM;
+        const size_t row_base = ((size_t)b0 * p.H + h) * p.N;
+        if (paired)
+            kv_fixed<T, 2>(sm, p, L, base, row_base, h);
+        else
+            kv_fixed<T, 1>(sm, p, L, base, row_base, h);
+    } else {
+        kv_ordinary<T>(sm, p, L, (size_t)bh * p.N * HEAD_DIM, (size_t)bh * p.N);
+    }
 }
 
 // ---------------------------------------------------------------------------

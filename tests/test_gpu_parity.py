@@ -62,6 +62,18 @@ def test_uniform_head_sets(dtype, fixed):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("B,N", [(3, 300), (5, 517), (1, 700)])
+def test_fixed_heads_batch_pairs(dtype, B, N):
+    """Fixed-head workgroups serve two batch elements at once (the weights do
+    not depend on the input); odd B leaves the last element unpaired.  Every
+    element of every slice, forward and backward, with several query and key
+    blocks (both parities of the pair-serving rule)."""
+    announce(f"batch pairs {dtype} B={B} N={N}")
+    inp = _inp(B, 3, N, [0, 2], dtype, seed=17)
+    compare_layer(run_gpu(inp, dtype), inp, dtype)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_max_heads(dtype):
     """H = 64, the largest head count the packed 64-bit head mask holds,
     with fixed heads at both ends of it (bits 0 and 63) and in the middle."""
