@@ -147,7 +147,10 @@ __device__ __forceinline__ void kv_store_zero(T* base, const KvLane& L) {
 // --- ordinary heads ---------------------------------------------------------
 
 // One query tile: qt / gt are the Q / dO tiles, rows holds LSE * log2(e)
-// (first KV_BM floats) and -D (next KV_BM).
+// (first KV_BM floats) and -D (next KV_BM).  Per 32-query half the row
+// operands and row values are read first; the transposed operands of dV and
+// dK are issued right after the S and dP products, so they arrive while the
+// softmax runs instead of stalling the dV / dK products.
 template <typename T, bool MASK>
 __device__ __forceinline__ void kv_tile(const T* qt, const T* gt, const float* rows, int mq, const KvLane& L,
                                         const typename Vec<T>::x8 (&kf)[KV_KB][4],
@@ -158,45 +161,49 @@ __device__ __forceinline__ void kv_tile(const T* qt, const T* gt, const float* r
     for (int qb = 0; qb < 2; ++qb) {
         const int qs = mq + 32 * qb;
         if (MASK && (qs + 31 < L.kw || qs >= L.N)) continue;  // no query of this half sees these keys
-        f32x16 s[KV_KB], dp[KV_KB];
-        {
-            frag qa[4];
+        frag qa[4], ga[4], gta[2][2], qta[2][2];
+        f32x4 l4[4], nd4[4];
 #pragma unroll
-            for (int dc = 0; dc < 4; ++dc) qa[dc] = ld_row<T>(qt, 32 * qb + L.c, 16 * dc + 8 * L.hf);
+        for (int dc = 0; dc < 4; ++dc) qa[dc] = ld_row<T>(qt, 32 * qb + L.c, 16 * dc + 8 * L.hf);
 #pragma unroll
-            for (int kb = 0; kb < KV_KB; ++kb) {
-#pragma unroll
-                for (int v = 0; v < 16; ++v) s[kb][v] = 0.0f;
-#pragma unroll
-                for (int dc = 0; dc < 4; ++dc) mma(s[kb], qa[dc], kf[kb][dc]);
-            }
-        }
-        {
-            // dP - D in one go: the accumulator starts at -D of its rows.
-            frag ga[4];
-#pragma unroll
-            for (int dc = 0; dc < 4; ++dc) ga[dc] = ld_row<T>(gt, 32 * qb + L.c, 16 * dc + 8 * L.hf);
-#pragma unroll
-            for (int kb = 0; kb < KV_KB; ++kb) {
-#pragma unroll
-                for (int g = 0; g < 4; ++g) {
-                    const f32x4 nd4 = *reinterpret_cast<const f32x4*>(rows + KV_BM + 32 * qb + 8 * g + 4 * L.hf);
-#pragma unroll
-                    for (int u = 0; u < 4; ++u) dp[kb][4 * g + u] = nd4[u];
-                }
-#pragma unroll
-                for (int dc = 0; dc < 4; ++dc) mma(dp[kb], ga[dc], vf[kb][dc]);
-            }
-        }
+        for (int dc = 0; dc < 4; ++dc) ga[dc] = ld_row<T>(gt, 32 * qb + L.c, 16 * dc + 8 * L.hf);
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
-            const f32x4 l4 = *reinterpret_cast<const f32x4*>(rows + 32 * qb + 8 * g + 4 * L.hf);
+            nd4[g] = *reinterpret_cast<const f32x4*>(rows + KV_BM + 32 * qb + 8 * g + 4 * L.hf);
+            l4[g] = *reinterpret_cast<const f32x4*>(rows + 32 * qb + 8 * g + 4 * L.hf);
+        }
+        f32x16 s[KV_KB], dp[KV_KB];
+#pragma unroll
+        for (int kb = 0; kb < KV_KB; ++kb) {
+#pragma unroll
+            for (int v = 0; v < 16; ++v) s[kb][v] = 0.0f;
+#pragma unroll
+            for (int dc = 0; dc < 4; ++dc) mma(s[kb], qa[dc], kf[kb][dc]);
+            // dP - D in one go: the accumulator starts at -D of its rows.
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+#pragma unroll
+                for (int u = 0; u < 4; ++u) dp[kb][4 * g + u] = nd4[g][u];
+#pragma unroll
+            for (int dc = 0; dc < 4; ++dc) mma(dp[kb], ga[dc], vf[kb][dc]);
+        }
+        // The transposed operands of dV and dK, in flight during the softmax.
+#pragma unroll
+        for (int kc = 0; kc < 2; ++kc)
+#pragma unroll
+            for (int db = 0; db < 2; ++db) {
+                gta[kc][db] = ld_tile_t<true>(gt, 32 * qb + 16 * kc, 32 * db);
+                qta[kc][db] = ld_tile_t<true>(qt, 32 * qb + 16 * kc, 32 * db);
+            }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
 #pragma unroll
             for (int kb = 0; kb < KV_KB; ++kb)
 #pragma unroll
                 for (int u = 0; u < 4; ++u) {
                     const int v = 4 * g + u;
-                    float pv = fast_exp2(fmaf(s[kb][v], scale_log2, -l4[u]));
+                    float pv = fast_exp2(fmaf(s[kb][v], scale_log2, -l4[g][u]));
                     if (MASK) {
                         const int row = qs + 8 * g + 4 * L.hf + u;
                         if (row < L.kw + 32 * kb + L.c) pv = 0.0f;
@@ -207,20 +214,14 @@ __device__ __forceinline__ void kv_tile(const T* qt, const T* gt, const float* r
         }
 #pragma unroll
         for (int kc = 0; kc < 2; ++kc) {
-            frag gta[2], qta[2];
-#pragma unroll
-            for (int db = 0; db < 2; ++db) {
-                gta[db] = ld_tile_t<true>(gt, 32 * qb + 16 * kc, 32 * db);
-                qta[db] = ld_tile_t<true>(qt, 32 * qb + 16 * kc, 32 * db);
-            }
 #pragma unroll
             for (int kb = 0; kb < KV_KB; ++kb) {
                 const frag pb = to_operand<T>(s[kb], 8 * kc);
                 const frag sb = to_operand<T>(dp[kb], 8 * kc);
 #pragma unroll
                 for (int db = 0; db < 2; ++db) {
-                    mma(dv[kb][db], gta[db], pb);
-                    mma(dk[kb][db], qta[db], sb);
+                    mma(dv[kb][db], gta[kc][db], pb);
+                    mma(dk[kb][db], qta[kc][db], sb);
                 }
             }
         }
@@ -636,6 +637,13 @@ __device__ __forceinline__ void dq_tile(const T* kt, const T* vt, int n0, const 
             mma(s, ld_row<T>(kt, 32 * kb + L.c, 16 * dc + 8 * L.hf), qf[dc]);
             mma(dp, ld_row<T>(vt, 32 * kb + L.c, 16 * dc + 8 * L.hf), gf[dc]);
         }
+        // K^T operands of dQ, in flight during the softmax.
+        frag kta[2][2];
+#pragma unroll
+        for (int kc = 0; kc < 2; ++kc)
+#pragma unroll
+            for (int db = 0; db < 2; ++db) kta[kc][db] = ld_tile_t<true>(kt, 32 * kb + 16 * kc, 32 * db);
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
             float pv = fast_exp2(fmaf(s[v], scale_log2, -lse2));
@@ -649,7 +657,7 @@ __device__ __forceinline__ void dq_tile(const T* kt, const T* vt, int n0, const 
         for (int kc = 0; kc < 2; ++kc) {
             const frag sb = to_operand<T>(s, 8 * kc);
 #pragma unroll
-            for (int db = 0; db < 2; ++db) mma(dq[db], ld_tile_t<true>(kt, 32 * kb + 16 * kc, 32 * db), sb);
+            for (int db = 0; db < 2; ++db) mma(dq[db], kta[kc][db], sb);
         }
     }
 }
