@@ -59,6 +59,9 @@ grouped-query entry points with one query head per key/value head:
 forward + backward at B = 2, H = 16, T = 8192, d = 96, bf16, at 25 % and
 50 % fixed heads against all-ordinary (MFMA roofline with the layer's
 algorithmic count: 7 contractions per ordinary head, 2 per fixed head).
+``--layer128`` does the same for a grouped-query layer at head dimension 128
+(the paper's grouped-query model shape: 32 query heads sharing 8 key/value
+heads) at B = 4, T = 4096.
 
 ``--fit`` times the compact fit of one 12-head layer at T = 4096: the
 targets from the calibration mean (floor, renormalise, marginals), then the
@@ -206,6 +209,9 @@ def parse():
                     help="time the trainable-pattern gradients (da, dr) at the layer workload instead")
     ap.add_argument("--layer1b", action="store_true",
                     help="time the layer forward+backward at head dimension 96 (B=2, H=16, T=8192) instead")
+    ap.add_argument("--layer128", action="store_true",
+                    help="time one grouped-query training layer at head dimension 128 (B=4, 32 query / 8 kv "
+                         "heads, T=4096) instead")
     ap.add_argument("--table", action="store_true",
                     help="with --gqa: also sweep B in {4, 8} and T in {2048, 4096, 8192}")
     ap.add_argument("--gqa", action="store_true",
@@ -820,10 +826,11 @@ def _train_head_job(job):
     return 1
 
 
-def layer1b_cpu_baseline(inp, flags, B, H):
+def layer1b_cpu_baseline(inp, flags, B, H, Hkv=None):
     """The oracle's dense fp64 forward+backward on three ordinary heads and
-    one fixed head of batch element 0 (one head per process), scaled to the
-    layer at 25 % fixed heads (B * H / 4 slices of that mix)."""
+    one fixed head of batch element 0 (one head per process, each with its
+    group's key/value head), scaled to the layer at 25 % fixed heads
+    (B * H / 4 slices of that mix)."""
     import multiprocessing as mp
     try:
         from threadpoolctl import threadpool_limits
@@ -832,9 +839,11 @@ def layer1b_cpu_baseline(inp, flags, B, H):
     ords = [h for h in range(H) if not flags[h]][:3]
     fixs = [h for h in range(H) if flags[h]][:1]
     jobs = []
+    group = H // (Hkv or H)
     for h in ords + fixs:
         fx = bool(flags[h])
-        jobs.append((None if fx else inp["Q"][0, h], None if fx else inp["K"][0, h], inp["V"][0, h], inp["dO"][0, h],
+        g = h // group
+        jobs.append((None if fx else inp["Q"][0, h], None if fx else inp["K"][0, g], inp["V"][0, g], inp["dO"][0, h],
                      fx, inp["a"][h] if fx else None, inp["r"][h] if fx else None))
     workers = max(1, min(MAX_HOST_WORKERS, len(os.sched_getaffinity(0)), len(jobs)))
     ctx = threadpool_limits(limits=1) if threadpool_limits else None
@@ -852,35 +861,55 @@ def layer1b_cpu_baseline(inp, flags, B, H):
                       f"{wall:.1f} s wall on {workers} processes, scaled by {scale:g} to the layer's {B * H} slices"}
 
 
-def main_layer1b(args, torch):
+TRAIN_LAYERS = {
+    # name: (B, Hq, Hkv, N, d, stream id, metric, workload text)
+    "layer1b": (2, 16, 16, 8192, 96, 62,
+                "1B-shape hybrid layer fwd+bwd ms/layer (B=2, H=16, T=8192, d=96, 25% fixed)",
+                "layer1b_8k: hybrid causal attention layer fwd+bwd at head dimension 96"),
+    "layer128": (4, 32, 8, 4096, 128, 64,
+                 "grouped-query hybrid layer fwd+bwd ms/layer (B=4, 32 query / 8 kv heads, T=4096, d=128, "
+                 "25% fixed)",
+                 "gqa_train_4k: grouped-query hybrid causal attention layer fwd+bwd at head dimension 128"),
+}
+
+
+def main_train_layer(args, torch, which):
+    """One training layer (forward + backward) through the grouped-query entry
+    points at 25 % and 50 % fixed query heads against all-ordinary."""
     from paper_2609_34650_amd import binding
-    B, H, N, d = 2, 16, 8192, 96
-    inp = gen.make_inputs(B, H, N, d, [], "bf16", stream_id=62, backward=True)
+    B, H, Hkv, N, d, sid, metric, text = TRAIN_LAYERS[which]
+    inp = gen.make_inputs(B, H, N, d, [], "bf16", stream_id=sid, backward=True)
     dev = torch.device("cuda", 0)
-    t = {k: torch.from_numpy(inp[k]).to(dev).to(torch.bfloat16) for k in ("Q", "K", "V", "dO")}
+    t = {k: torch.from_numpy(np.ascontiguousarray(inp[k] if k in ("Q", "dO") else inp[k][:, :Hkv])).to(dev).to(
+        torch.bfloat16) for k in ("Q", "K", "V", "dO")}
     a = torch.from_numpy(inp["a"]).to(dev)
     r = torch.from_numpy(inp["r"]).to(dev)
     O = torch.empty_like(t["Q"])
     LSE = torch.empty((B, H, N), dtype=torch.float32, device=dev)
-    dQ, dK, dV = (torch.empty_like(t["Q"]) for _ in range(3))
+    dQ = torch.empty_like(t["Q"])
+    dK, dV = torch.empty_like(t["K"]), torch.empty_like(t["V"])
     code = binding.SAF_DTYPE_BF16
-    ws = torch.empty(max(256, int(binding.load().saf_hybrid_attn_bwd_gqa_workspace_bytes(code, B, H, H, N, d))),
+    ws = torch.empty(max(256, int(binding.load().saf_hybrid_attn_bwd_gqa_workspace_bytes(code, B, H, Hkv, N, d))),
                      dtype=torch.uint8, device=dev)
     C = contraction_flop(N, d) * B
 
     def flags_for(n_fixed):
         f = np.zeros(H, np.uint8)
-        f[gen.fixed_heads(H, n_fixed, stream_id=62)] = 1
+        f[gen.fixed_heads(H, n_fixed, stream_id=sid)] = 1
         return f
 
-    def step(fl):
+    def step(fl, ev=None):
+        if ev is not None:
+            ev[0].record()
         binding.saf_hybrid_attn_fwd_gqa(t["Q"], t["K"], t["V"], fl, a, r, O=O, LSE=LSE)
+        if ev is not None:
+            ev[1].record()
         binding.saf_hybrid_attn_bwd_gqa(t["Q"], t["K"], t["V"], O, t["dO"], LSE, fl, a, r, dQ=dQ, dK=dK, dV=dV,
                                         workspace=ws)
+        if ev is not None:
+            ev[2].record()
 
     def timed(fl, steps):
-        for _ in range(args.warmup):
-            step(fl)
         torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
@@ -892,22 +921,38 @@ def main_layer1b(args, torch):
 
     steps = max(1, args.steps // 3)
     n25, n50 = H // 4, H // 2
-    f25 = flags_for(n25)
+    f25, f50, f0 = flags_for(n25), flags_for(n50), flags_for(0)
+    t_w = time.perf_counter()
     for _ in range(args.warmup):
         step(f25)
     torch.cuda.synchronize()
+    while time.perf_counter() - t_w < args.warmup_floor_s:
+        for fl in (f25, f50, f0):
+            for _ in range(3):
+                step(fl)
+        torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(steps):
         step(f25)
     torch.cuda.synchronize()
     ms = (time.perf_counter() - t0) * 1e3 / steps
-    ms25 = timed(f25, steps)
-    ms50 = timed(flags_for(n50), steps)
-    ms0 = timed(flags_for(0), steps)
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
+    for e in evs:
+        step(f25, e)
+    torch.cuda.synchronize()
+    ms_fwd = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    ms_bwd = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    # Rates alternate in blocks (25 %, 50 %, 0 %) twice; medians per rate.
+    t25, t50, t0_ = [], [], []
+    for _ in range(2):
+        t25.append(timed(f25, steps))
+        t50.append(timed(f50, steps))
+        t0_.append(timed(f0, steps))
+    ms25, ms50, ms0 = float(np.median(t25)), float(np.median(t50)), float(np.median(t0_))
     flop25 = C * (7 * (H - n25) + 2 * n25)
     tflops = flop25 / (ms25 * 1e-3) / 1e12
     result = {
-        "metric": "1B-shape hybrid layer fwd+bwd ms/layer (B=2, H=16, T=8192, d=96, 25% fixed)",
+        "metric": metric,
         "value": round(ms, 3),
         "unit": "ms/layer",
         "n_gpus": 1,
@@ -919,15 +964,16 @@ def main_layer1b(args, torch):
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": "layer1b_8k: hybrid causal attention layer fwd+bwd at head dimension 96", "B": B,
-                   "H": H, "N": N, "d": d, "n_fixed": n25, "parallelism": "single GPU"},
+        "config": {"workload": text, "B": B, "Hq": H, "Hkv": Hkv, "N": N, "d": d, "n_fixed": n25,
+                   "parallelism": "single GPU"},
         "tflops": round(tflops, 1),
+        "kernels": {"fwd": {"ms": round(ms_fwd, 4)}, "bwd (query-block + key-block passes)": {"ms": round(ms_bwd, 4)}},
         "ms_25pct": round(ms25, 3),
         "ms_50pct": round(ms50, 3),
         "ms_all_ordinary": round(ms0, 3),
         "speedup_25pct": round(ms0 / ms25, 3),
         "speedup_50pct": round(ms0 / ms50, 3),
-        "cpu_baseline": layer1b_cpu_baseline(inp, f25, B, H) if args.cpu_baseline else None,
+        "cpu_baseline": layer1b_cpu_baseline(inp, f25, B, H, Hkv) if args.cpu_baseline else None,
         "roofline": {"bound": "mfma", "kernel": "gqa fwd+bwd (layer)", "achieved": round(tflops, 1),
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(tflops / PEAK_BF16_TFLOPS, 4),
                      "traffic": None},
@@ -972,7 +1018,10 @@ def main():
         main_gqa(args, torch)
         return
     if args.layer1b:
-        main_layer1b(args, torch)
+        main_train_layer(args, torch, "layer1b")
+        return
+    if args.layer128:
+        main_train_layer(args, torch, "layer128")
         return
 
     w = gen.WORKLOADS[args.workload]
@@ -1080,8 +1129,11 @@ def main():
         ms_h, ms_o = float(np.median(th)), float(np.median(to))
         flop_o = sum(layer_flop(B, H, N, d, 0, w.backward).values())
         c_med = float(np.median(ctrl))
+        _, st_o = timed_block(torch, layer, ordinary_flags, blk, with_events=True)
+        st_o.pop("layer_median")
         result["all_ordinary"] = {"ms": round(ms_o, 4), "tflops": round(flop_o / (ms_o * 1e-3) / 1e12, 1),
-                                  "hybrid_ms_same_blocks": round(ms_h, 4)}
+                                  "hybrid_ms_same_blocks": round(ms_h, 4),
+                                  "kernels_ms": {k: round(v, 4) for k, v in st_o.items()}}
         result["speedup_vs_all_ordinary"] = round(float(np.median(ratios)), 4)
         result["speedup_protocol"] = {
             "pairs": pairs, "steps_per_block": blk, "statistic": "median of within-pair ratios",
