@@ -103,11 +103,7 @@ template <typename T, bool MASK, bool M2, typename Q0, typename Q1, typename K0,
 __device__ __forceinline__ void calib_input(Q0 qa, Q1 qb, K0 ka, K1 kb, LS ls, int b, const CalibArgs& p,
                                             const CalLane& L, bool diag, int rows_valid, f32x16 (&mean)[4],
                                             INC& inc, float& inc_s, float& ent) {
-    typedef typename Vec<T>::x8 frag;
     const T* kt = (L.w >> 1) ? kb : ka;
-    frag kf[4];
-#pragma unroll
-    for (int dc = 0; dc < 4; ++dc) kf[dc] = ld_row<T>(kt, 32 * (L.w & 1) + L.c, 16 * dc + 8 * L.hf);
     const float rn = 1.0f / (float)(p.n_seen + b + 1);
     const float scale = p.scale;
 #pragma unroll
@@ -117,8 +113,13 @@ __device__ __forceinline__ void calib_input(Q0 qa, Q1 qb, K0 ka, K1 kb, LS ls, i
         f32x16 s;
 #pragma unroll
         for (int v = 0; v < 16; ++v) s[v] = 0.0f;
+        // K's fragments are read again for every row block (the kernel is
+        // bound by the state traffic, not by LDS), so they do not hold 16
+        // registers across the whole input.
 #pragma unroll
-        for (int dc = 0; dc < 4; ++dc) mma(s, ld_row<T>(qt, 32 * (rb & 1) + L.c, 16 * dc + 8 * L.hf), kf[dc]);
+        for (int dc = 0; dc < 4; ++dc)
+            mma(s, ld_row<T>(qt, 32 * (rb & 1) + L.c, 16 * dc + 8 * L.hf),
+                ld_row<T>(kt, 32 * (L.w & 1) + L.c, 16 * dc + 8 * L.hf));
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
             const f32x4 l4 = *reinterpret_cast<const f32x4*>(ls + 32 * rb + 8 * g + 4 * L.hf);
