@@ -198,6 +198,9 @@ def parse():
     ap.add_argument("--abba-pairs", type=int, default=8,
                     help="pairs of (hybrid, all-ordinary) blocks for the speedup, alternating the order")
     ap.add_argument("--abba-block", type=int, default=10, help="steps per ABBA block")
+    ap.add_argument("--no-clock", dest="clock", action="store_false", default=True,
+                    help="skip the shader-clock probe block after the timed steps (a profiler run then sees the "
+                         "timed steps as the last dispatches of each kernel)")
     ap.add_argument("--workload", default="gpt124m_4k", choices=sorted(gen.WORKLOADS))
     ap.add_argument("--cpu-baseline", dest="cpu_baseline", action="store_true", default=True)
     ap.add_argument("--no-cpu-baseline", dest="cpu_baseline", action="store_false")
@@ -1096,8 +1099,8 @@ def main():
     # library's counter probe spans about 30 ms of layer steps.
     n_clk = max(10, int(30.0 / max(ms, 0.05)))
     mhz = shader_clock_during(torch, lambda: [layer.step(hybrid_flags) for _ in range(n_clk)],
-                              int(n_clk * ms * 1e3 * 0.8))
-    result["shader_clock_mhz"] = {
+                              int(n_clk * ms * 1e3 * 0.8)) if args.clock else None
+    result["shader_clock_mhz"] = None if not args.clock else {
         "during_layer_steps": mhz,
         "method": "s_memtime / s_memrealtime (100 MHz) on a one-wavefront probe on a second stream, "
                   f"spanning {n_clk} layer steps after the timed region",

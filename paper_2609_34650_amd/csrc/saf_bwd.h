@@ -75,10 +75,12 @@ __global__ __launch_bounds__(PRE_THREADS) void bwd_pre_kernel(BwdArgs p) {
 // sub-blocks per wavefront: with one, a wavefront stays under 256 VGPRs and
 // two of them share a SIMD.
 //
-// Ordinary heads: scores are formed as S (queries x keys), so a lane holds one
-// key (l % 32) and 16 queries of each 32-query half: P and dS feed directly
-// into the B operand of dV^T += dO^T P and dK^T += Q^T dS, whose accumulators
-// again hold one key per lane.  K and V of the wavefront's keys stay in
+// Ordinary heads: scores are formed as S (queries x keys) on 16 x 16 tiles,
+// so a lane holds one key of each 16-key tile (l % 16) and eight queries of
+// each 32-query half: P and dS feed directly into the B operand of
+// dV^T += dO^T P and dK^T += Q^T dS, whose accumulators again hold one key
+// per lane.  (With 32 x 32 tiles a lane would hold 16 queries, and read twice
+// the per-row LSE and D values from LDS for the same products.)  K and V of the wavefront's keys stay in
 // registers; Q and dO tiles are copied by buffer loads straight into
 // column-slab LDS tiles (A operands of S and dP, and, through transposing
 // reads, of the dV/dK products), double-buffered so the next tile is in
@@ -109,7 +111,7 @@ static_assert(BAND_COPIES * KV_BAND_STRIDE * 4 <= tile_elems<bf16>() * 2, "float
 static_assert((KV_BM + KV_BAND + 1) * 4 <= tile_elems<bf16>() * 2, "exact-program rows fit in a tile");
 
 struct KvLane {
-    int tid, w, lane, c, hf, n0, kw, N;
+    int tid, w, lane, c, hf, n, g, n0, kw, N;
 };
 
 template <typename T>
@@ -146,85 +148,107 @@ __device__ __forceinline__ void kv_store_zero(T* base, const KvLane& L) {
 
 // --- ordinary heads ---------------------------------------------------------
 
-// One query tile: qt / gt are the Q / dO tiles, rows holds LSE * log2(e)
-// (first KV_BM floats) and -D (next KV_BM).  Per 32-query half the row
-// operands and row values are read first; the transposed operands of dV and
-// dK are issued right after the S and dP products, so they arrive while the
-// softmax runs instead of stalling the dV / dK products.
+// One query tile: q_tile / g_tile are the Q / dO tiles, rows holds
+// LSE * log2(e) (first KV_BM floats) and -D (next KV_BM).  The products run on
+// 16 x 16 tiles: per 32-query half, S and dP are 2 x 2 tiles (queries x the
+// wavefront's 32 keys), so a lane holds eight query rows (four of each
+// 16-query tile) and reads only those rows' LSE and D; the two query tiles of
+// a key column, stacked, are the B operand of dV^T += dO^T P and
+// dK^T += Q^T dS (k-slot t <-> query 16*(t/4) + 4*g + t%4, the order the
+// transposed reads of dO and Q follow).  The row operands and row values are
+// read first; the transposed operands are issued right after the S and dP
+// products, so they arrive while the softmax runs.
 template <typename T, bool MASK>
-__device__ __forceinline__ void kv_tile(const T* qt, const T* gt, const float* rows, int mq, const KvLane& L,
-                                        const typename Vec<T>::x8 (&kf)[KV_KB][4],
-                                        const typename Vec<T>::x8 (&vf)[KV_KB][4], f32x16 (&dv)[KV_KB][2],
-                                        f32x16 (&dk)[KV_KB][2], float scale_log2) {
+__device__ __forceinline__ void kv_tile(const T* q_tile, const T* g_tile, const float* rows, int mq, const KvLane& L,
+                                        const typename Vec<T>::x8 (&kf)[2][2], const typename Vec<T>::x8 (&vf)[2][2],
+                                        f32x4 (&dv)[4][2], f32x4 (&dk)[4][2], float scale_log2) {
     typedef typename Vec<T>::x8 frag;
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
         const int qs = mq + 32 * qb;
         if (MASK && (qs + 31 < L.kw || qs >= L.N)) continue;  // no query of this half sees these keys
-        frag qa[4], ga[4], gta[2][2], qta[2][2];
-        f32x4 l4[4], nd4[4];
+        frag qa[2][2], ga[2][2], gta[4], qta[4];
+        f32x4 l4[2], nd4[2];
 #pragma unroll
-        for (int dc = 0; dc < 4; ++dc) qa[dc] = ld_row<T>(qt, 32 * qb + L.c, 16 * dc + 8 * L.hf);
+        for (int qt = 0; qt < 2; ++qt)
 #pragma unroll
-        for (int dc = 0; dc < 4; ++dc) ga[dc] = ld_row<T>(gt, 32 * qb + L.c, 16 * dc + 8 * L.hf);
+            for (int dc = 0; dc < 2; ++dc) qa[qt][dc] = ld_row<T>(q_tile, 32 * qb + 16 * qt + L.n, 32 * dc + 8 * L.g);
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-            nd4[g] = *reinterpret_cast<const f32x4*>(rows + KV_BM + 32 * qb + 8 * g + 4 * L.hf);
-            l4[g] = *reinterpret_cast<const f32x4*>(rows + 32 * qb + 8 * g + 4 * L.hf);
+        for (int qt = 0; qt < 2; ++qt)
+#pragma unroll
+            for (int dc = 0; dc < 2; ++dc) ga[qt][dc] = ld_row<T>(g_tile, 32 * qb + 16 * qt + L.n, 32 * dc + 8 * L.g);
+#pragma unroll
+        for (int qt = 0; qt < 2; ++qt) {
+            nd4[qt] = *reinterpret_cast<const f32x4*>(rows + KV_BM + 32 * qb + 16 * qt + 4 * L.g);
+            l4[qt] = *reinterpret_cast<const f32x4*>(rows + 32 * qb + 16 * qt + 4 * L.g);
         }
-        f32x16 s[KV_KB], dp[KV_KB];
+        f32x4 s[2][2], dp[2][2];
 #pragma unroll
-        for (int kb = 0; kb < KV_KB; ++kb) {
+        for (int qt = 0; qt < 2; ++qt)
 #pragma unroll
-            for (int v = 0; v < 16; ++v) s[kb][v] = 0.0f;
+            for (int kt = 0; kt < 2; ++kt) {
+                s[qt][kt] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+                dp[qt][kt] = nd4[qt];  // dP - D in one go: the accumulator starts at -D of its rows
+            }
 #pragma unroll
-            for (int dc = 0; dc < 4; ++dc) mma(s[kb], qa[dc], kf[kb][dc]);
-            // dP - D in one go: the accumulator starts at -D of its rows.
+        for (int dc = 0; dc < 2; ++dc)
 #pragma unroll
-            for (int g = 0; g < 4; ++g)
+            for (int qt = 0; qt < 2; ++qt)
 #pragma unroll
-                for (int u = 0; u < 4; ++u) dp[kb][4 * g + u] = nd4[g][u];
+                for (int kt = 0; kt < 2; ++kt) mma16(s[qt][kt], qa[qt][dc], kf[kt][dc]);
 #pragma unroll
-            for (int dc = 0; dc < 4; ++dc) mma(dp[kb], ga[dc], vf[kb][dc]);
-        }
+        for (int dc = 0; dc < 2; ++dc)
+#pragma unroll
+            for (int qt = 0; qt < 2; ++qt)
+#pragma unroll
+                for (int kt = 0; kt < 2; ++kt) mma16(dp[qt][kt], ga[qt][dc], vf[kt][dc]);
         // The transposed operands of dV and dK, in flight during the softmax.
 #pragma unroll
-        for (int kc = 0; kc < 2; ++kc)
-#pragma unroll
-            for (int db = 0; db < 2; ++db) {
-                gta[kc][db] = ld_tile_t<true>(gt, 32 * qb + 16 * kc, 32 * db);
-                qta[kc][db] = ld_tile_t<true>(qt, 32 * qb + 16 * kc, 32 * db);
-            }
+        for (int dt = 0; dt < 4; ++dt) {
+            gta[dt] = ld_tile_t16(g_tile, 32 * qb, 16 * dt);
+            qta[dt] = ld_tile_t16(q_tile, 32 * qb, 16 * dt);
+        }
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
+        for (int qt = 0; qt < 2; ++qt)
 #pragma unroll
-            for (int kb = 0; kb < KV_KB; ++kb)
+            for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
                 for (int u = 0; u < 4; ++u) {
-                    const int v = 4 * g + u;
-                    float pv = fast_exp2(fmaf(s[kb][v], scale_log2, -l4[g][u]));
+                    float pv = fast_exp2(fmaf(s[qt][kt][u], scale_log2, -l4[qt][u]));
                     if (MASK) {
-                        const int row = qs + 8 * g + 4 * L.hf + u;
-                        if (row < L.kw + 32 * kb + L.c) pv = 0.0f;
+                        const int row = qs + 16 * qt + 4 * L.g + u;
+                        if (row < L.kw + 16 * kt + L.n) pv = 0.0f;
                     }
-                    s[kb][v] = pv;
-                    dp[kb][v] = pv * dp[kb][v];
+                    s[qt][kt][u] = pv;
+                    dp[qt][kt][u] = pv * dp[qt][kt][u];
                 }
-        }
 #pragma unroll
-        for (int kc = 0; kc < 2; ++kc) {
+        for (int kt = 0; kt < 2; ++kt) {
+            const frag pb = to_operand16<T>(s[0][kt], s[1][kt]);
+            const frag sb = to_operand16<T>(dp[0][kt], dp[1][kt]);
 #pragma unroll
-            for (int kb = 0; kb < KV_KB; ++kb) {
-                const frag pb = to_operand<T>(s[kb], 8 * kc);
-                const frag sb = to_operand<T>(dp[kb], 8 * kc);
-#pragma unroll
-                for (int db = 0; db < 2; ++db) {
-                    mma(dv[kb][db], gta[kc][db], pb);
-                    mma(dk[kb][db], qta[kc][db], sb);
-                }
+            for (int dt = 0; dt < 4; ++dt) {
+                mma16(dv[dt][kt], gta[dt], pb);
+                mma16(dk[dt][kt], qta[dt], sb);
             }
         }
+    }
+}
+
+// dV or dK rows of the wavefront's 32 keys from 16 x 16 accumulators
+// (acc[dt][kt]: head dimensions 16 dt .., keys 16 kt ..), times `scale`.
+template <typename T>
+__device__ __forceinline__ void kv_store_rows16(T* base, const KvLane& L, const f32x4 (&acc)[4][2], float scale) {
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt) {
+        const int key = L.kw + 16 * kt + L.n;
+        if (key >= L.N) continue;
+        T* row = base + (size_t)key * HEAD_DIM;
+#pragma unroll
+        for (int dt = 0; dt < 4; ++dt)
+            st4<T>(row + 16 * dt + 4 * L.g, acc[dt][kt][0] * scale, acc[dt][kt][1] * scale, acc[dt][kt][2] * scale,
+                   acc[dt][kt][3] * scale);
     }
 }
 
@@ -240,27 +264,28 @@ __device__ __forceinline__ void kv_ordinary(const Tiles<T>& sm, const BwdArgs& p
     const __amdgpu_buffer_rsrc_t rg = slice_rsrc<T>(reinterpret_cast<const T*>(p.dO) + base, L.N);
     const float* __restrict__ LSE = p.lse + row_base;
     const float* __restrict__ Dsum = p.dsum + row_base;
+    static_assert(KV_KB == 1, "the ordinary program's tiles cover 32 keys per wavefront");
     typedef typename Vec<T>::x8 frag;
-    frag kf[KV_KB][4], vf[KV_KB][4];
+    // B operands of S and dP: key 16 kt + n of the wavefront, head dimensions
+    // 32 dc + 8 g .. 32 dc + 8 g + 7.
+    frag kf[2][2], vf[2][2];
 #pragma unroll
-    for (int kb = 0; kb < KV_KB; ++kb) {
-        const int key = L.kw + 32 * kb + L.c;
+    for (int kt = 0; kt < 2; ++kt) {
+        const int key = L.kw + 16 * kt + L.n;
 #pragma unroll
-        for (int dc = 0; dc < 4; ++dc) {
-            kf[kb][dc] = key < L.N ? ld8<T>(K + (size_t)key * HEAD_DIM + 16 * dc + 8 * L.hf) : zero8<T>();
-            vf[kb][dc] = key < L.N ? ld8<T>(V + (size_t)key * HEAD_DIM + 16 * dc + 8 * L.hf) : zero8<T>();
+        for (int dc = 0; dc < 2; ++dc) {
+            kf[kt][dc] = key < L.N ? ld8<T>(K + (size_t)key * HEAD_DIM + 32 * dc + 8 * L.g) : zero8<T>();
+            vf[kt][dc] = key < L.N ? ld8<T>(V + (size_t)key * HEAD_DIM + 32 * dc + 8 * L.g) : zero8<T>();
         }
     }
-    f32x16 dv[KV_KB][2], dk[KV_KB][2];
+    f32x4 dv[4][2], dk[4][2];
 #pragma unroll
-    for (int kb = 0; kb < KV_KB; ++kb)
+    for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
-        for (int db = 0; db < 2; ++db)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                dv[kb][db][v] = 0.0f;
-                dk[kb][db][v] = 0.0f;
-            }
+        for (int kt = 0; kt < 2; ++kt) {
+            dv[dt][kt] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+            dk[dt][kt] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+        }
 
     // Steps of two 64-query tiles (one barrier per 128 queries): the step
     // that meets the diagonal first (masked), then the rest.  Rows past N
@@ -294,14 +319,8 @@ __device__ __forceinline__ void kv_ordinary(const Tiles<T>& sm, const BwdArgs& p
                 kv_tile<T, decltype(mask)::value>(sm.t[4 + b], sm.t[6 + b], sm.aux[b] + 2 * KV_BM, mq + KV_BM, L, kf,
                                                   vf, dv, dk, p.scale_log2);
         });
-    float one[KV_KB], ks[KV_KB];
-#pragma unroll
-    for (int kb = 0; kb < KV_KB; ++kb) {
-        one[kb] = 1.0f;
-        ks[kb] = p.scale;
-    }
-    kv_store_rows<T>(reinterpret_cast<T*>(p.dv) + base, L, dv, one);
-    kv_store_rows<T>(reinterpret_cast<T*>(p.dk) + base, L, dk, ks);
+    kv_store_rows16<T>(reinterpret_cast<T*>(p.dv) + base, L, dv, 1.0f);
+    kv_store_rows16<T>(reinterpret_cast<T*>(p.dk) + base, L, dk, p.scale);
 }
 
 // --- fixed heads: exact per-element program (fallback) ----------------------
@@ -578,14 +597,20 @@ __global__ __launch_bounds__(KV_THREADS) __attribute__((amdgpu_waves_per_eu(size
     L.lane = L.tid & 63;
     L.c = L.tid & 31;
     L.hf = (L.tid >> 5) & 1;
+    L.n = L.tid & 15;
+    L.g = (L.tid >> 4) & 3;
     L.n0 = kblk * KV_BN;
     L.kw = L.n0 + 32 * KV_KB * L.w;
     L.N = p.N;
     if ((p.fixed_mask >> h) & 1ull) {
-        // Batch elements pair up as in the forward: one workgroup of the pair
-        // (the one whose batch parity matches the key block's) forms the
-        // weights once and serves both; an unpaired last element (odd B) is
-        // served alone.
+        // Batch elements pair up (b0 = b with its low bit cleared, b0 + 1):
+        // one workgroup of the pair, the one whose batch parity matches the
+        // key block's, forms the pattern's weights once and applies them to
+        // both, so the active workgroups alternate between the pair's two
+        // places in the grid from block to block.  An unpaired last element
+        // (odd B) is served alone.  The forward does not pair: its fixed
+        // program forms fewer weights per product, and holding two elements'
+        // accumulators costs the whole forward kernel registers.
         const int b0 = sl.b & ~1;
         const bool paired = b0 + 1 < p.B;
         if (paired && (sl.b & 1) != (kblk & 1)) return;

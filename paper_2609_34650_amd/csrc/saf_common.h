@@ -68,6 +68,18 @@ __device__ __forceinline__ void mma(f32x16& acc, const f32x8& a, const f32x8& b)
     for (int t = 0; t < 8; ++t) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a[t], b[t], acc, 0, 0, 0);
 }
 
+// 16 x 16 tiles (v_mfma_f32_16x16x32_bf16): an accumulator lane l holds
+// column l % 16 and rows 4 (l / 16) .. 4 (l / 16) + 3; an operand lane holds
+// row (A) or column (B) l % 16 and eight k-slots of its group l / 16.  The
+// float32 form takes eight 16x16x4 steps, slot t of every group in step t.
+__device__ __forceinline__ void mma16(f32x4& acc, const bf16x8& a, const bf16x8& b) {
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc, 0, 0, 0);
+}
+__device__ __forceinline__ void mma16(f32x4& acc, const f32x8& a, const f32x8& b) {
+#pragma unroll
+    for (int t = 0; t < 8; ++t) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[t], b[t], acc, 0, 0, 0);
+}
+
 template <typename T>
 __device__ __forceinline__ typename Vec<T>::x8 zero8() {
     typename Vec<T>::x8 z;
@@ -82,6 +94,19 @@ __device__ __forceinline__ typename Vec<T>::x8 to_operand(const f32x16& acc, int
     typename Vec<T>::x8 o;
 #pragma unroll
     for (int t = 0; t < 8; ++t) o[t] = (T)acc[v0 + t];
+    return o;
+}
+
+// Two 16 x 16 accumulator tiles stacked along k as one operand: slots 0-3
+// from lo, 4-7 from hi.
+template <typename T>
+__device__ __forceinline__ typename Vec<T>::x8 to_operand16(const f32x4& lo, const f32x4& hi) {
+    typename Vec<T>::x8 o;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+        o[t] = (T)lo[t];
+        o[4 + t] = (T)hi[t];
+    }
     return o;
 }
 
@@ -303,6 +328,31 @@ __device__ __forceinline__ f32x8 ld_tile_t(const float* tile, int row0, int col0
         const int r = row0 + (ACC_ORDER ? 8 * (t >> 2) + 4 * hf + (t & 3) : 8 * hf + t);
         v[t] = tile[toff<float>(r, col0 + c)];
     }
+    return v;
+}
+
+// Transposed operand of a 16 x 16 product from a column-slab tile: row m of
+// the A operand is tile column col0 + m (m = lane % 16), and k-slot t of lane
+// group g = lane / 16 is tile row row0 + 16*(t/4) + 4*g + (t%4), the order in
+// which two stacked 16 x 16 accumulator tiles hold their rows.  bf16: two
+// ds_read_b64_tr_b16 (lane i of a 16-lane group addresses row base + i/4 at
+// column col0 + 4*(i%4) and receives four rows of column col0 + i); float32:
+// eight scalar LDS reads.
+__device__ __forceinline__ bf16x8 ld_tile_t16(const bf16* tile, int row0, int col0) {
+    const int l = threadIdx.x & 63;
+    const int i = l & 15;
+    const int r = row0 + 4 * (l >> 4) + (i >> 2);
+    const int col = col0 + 4 * (i & 3);
+    const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(tile + toff<bf16>(r, col)));
+    const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(tile + toff<bf16>(r + 16, col)));
+    const s16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    return __builtin_bit_cast(bf16x8, v);
+}
+__device__ __forceinline__ f32x8 ld_tile_t16(const float* tile, int row0, int col0) {
+    const int l = threadIdx.x & 63;
+    f32x8 v;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) v[t] = tile[toff<float>(row0 + 16 * (t >> 2) + 4 * (l >> 4) + (t & 3), col0 + (l & 15))];
     return v;
 }
 

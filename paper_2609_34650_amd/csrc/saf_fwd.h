@@ -403,70 +403,51 @@ __device__ __forceinline__ void fix_store(float* eas, float* band, const FixStag
     }
 }
 
-// O^T += V^T (band ea)^T for NB batch elements at once: four 16-key chunks;
-// the weight operand of lane (query column c, half hf) in chunk G is band
-// entries u0 .. u0 + 7 times ea of keys 16G + 8hf .. 16G + 8hf + 7, formed in
-// float32 and rounded once, then fed to the MFMAs of every batch element's V
-// tile (the pattern does not depend on the input).  z[qb] collects this
-// lane's share of the row sum Z'(i) of the float32 weights (the other lane
-// half holds the other eight keys of each chunk).
-template <typename T, int NB, bool MASK>
-__device__ __forceinline__ void fix_tile(const T* const (&vs)[NB], const float* band, const float* eas, int n0,
-                                         const FwdLane& L, f32x16 (&oacc)[NB][2][2], float (&z)[2]) {
+// O^T += V^T (band ea)^T: four 16-key chunks; the weight operand of lane
+// (query column c, half hf) in chunk G is band entries u0 .. u0 + 7 times ea
+// of keys 16G + 8hf .. 16G + 8hf + 7, formed in float32 and rounded once.
+// z[qb] collects this lane's share of the row sum Z'(i) of the float32
+// weights (the other lane half holds the other eight keys of each chunk).
+template <typename T, bool MASK>
+__device__ __forceinline__ void fix_tile(const T* vs, const float* band, const float* eas, int n0, const FwdLane& L,
+                                         f32x16 (&oacc)[2][2], float (&z)[2]) {
     typedef typename Vec<T>::x8 frag;
 #pragma unroll
     for (int G = 0; G < 4; ++G) {
         if (MASK && n0 + 16 * G > L.q0 + FWD_QW - 1) continue;  // chunk wholly after this wavefront's queries
+        frag vf[2];
+#pragma unroll
+        for (int db = 0; db < 2; ++db) vf[db] = ld_tile_t<false>(vs, 16 * G, 32 * db);
         const f32x4 e0 = *reinterpret_cast<const f32x4*>(eas + 16 * G + 8 * L.hf);
         const f32x4 e1 = *reinterpret_cast<const f32x4*>(eas + 16 * G + 8 * L.hf + 4);
-        // The weights of both query blocks first, then each batch element's V
-        // fragments and products (fewer operands live at once).
-        frag w[2];
-        bool live[2];
 #pragma unroll
         for (int qb = 0; qb < 2; ++qb) {
-            live[qb] = !(MASK && n0 + 16 * G > L.q0 + 32 * qb + 31);
-            if (!live[qb]) continue;
+            if (MASK && n0 + 16 * G > L.q0 + 32 * qb + 31) continue;
             const int ql = L.q0 - L.m0 + 32 * qb + L.c;  // query within the block
             const int u0 = (FWD_BM - 1) - ql + 16 * G + 8 * L.hf;
             const int s = u0 & (FIX_BAND_COPIES - 1);
             const float* bp = band + s * FWD_BAND_STRIDE + u0 - s;
             const f32x4 b0 = *reinterpret_cast<const f32x4*>(bp);
             const f32x4 b1 = *reinterpret_cast<const f32x4*>(bp + 4);
+            frag w;
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
                 const float x0 = b0[t] * e0[t], x1 = b1[t] * e1[t];
-                w[qb][t] = (T)x0;
-                w[qb][4 + t] = (T)x1;
+                w[t] = (T)x0;
+                w[4 + t] = (T)x1;
                 z[qb] += x0 + x1;
             }
+#pragma unroll
+            for (int db = 0; db < 2; ++db) mma(oacc[qb][db], vf[db], w);
         }
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb) {
-            frag vf[2];
-#pragma unroll
-            for (int db = 0; db < 2; ++db) vf[db] = ld_tile_t<false>(vs[nb], 16 * G, 32 * db);
-#pragma unroll
-            for (int qb = 0; qb < 2; ++qb)
-                if (live[qb]) {
-#pragma unroll
-                    for (int db = 0; db < 2; ++db) mma(oacc[nb][qb][db], vf[db], w[qb]);
-                }
-        }
-        // One chunk's operands live at a time (NB = 2 holds 128 accumulators).
-        if (NB > 1) __builtin_amdgcn_sched_barrier(0);
     }
 }
 
-// NB batch elements b, b + 1, .. of one fixed head and query block (slice
-// offsets base + nb * slice, row_base + nb * rows).
-template <typename T, int NB>
+template <typename T>
 __device__ __forceinline__ void fwd_fixed(const Tiles<T>& sm, const FwdArgs& p, const FwdLane& L, size_t base,
                                           size_t row_base, int h) {
-    // Tiles: V of batch element nb in t[2 nb] / t[2 nb + 1], the float32 band
-    // in t[4] / t[5], ea in aux.
-    const size_t slice = (size_t)p.H * p.N * HEAD_DIM;
-    const size_t rows = (size_t)p.H * p.N;
+    // Tiles: V in t[0] / t[1], the float32 band in t[2] / t[3], ea in aux.
+    const T* __restrict__ V = reinterpret_cast<const T*>(p.v) + base;
     const float* __restrict__ arow = p.a + (size_t)h * p.ld_prior;
     const float* __restrict__ rrow = p.r + (size_t)h * p.ld_prior;
     const int N = L.N;
@@ -488,63 +469,48 @@ __device__ __forceinline__ void fwd_fixed(const Tiles<T>& sm, const FwdArgs& p, 
         ok = fmaxf(arow[i] + rrow[0], arow[0] + rrow[i]) - A - R >= -FAST_GUARD;
     }
     if (!__syncthreads_and(ok)) {
-        for (int nb = 0; nb < NB; ++nb) {
-            if (nb > 0) __syncthreads();
-            fwd_fixed_exact<T>(sm, p, L, base + nb * slice, row_base + nb * rows, arow, rrow);
-        }
+        fwd_fixed_exact<T>(sm, p, L, base, row_base, arow, rrow);
         return;
     }
     const float a_sh = A * LOG2E, r_sh = R * LOG2E;
 
-    f32x16 oacc[NB][2][2];
+    f32x16 oacc[2][2];
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
+    for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
-        for (int qb = 0; qb < 2; ++qb)
+        for (int db = 0; db < 2; ++db)
 #pragma unroll
-            for (int db = 0; db < 2; ++db)
-#pragma unroll
-                for (int v = 0; v < 16; ++v) oacc[nb][qb][db][v] = 0.0f;
+            for (int v = 0; v < 16; ++v) oacc[qb][db][v] = 0.0f;
 
     const int n_tiles = (m1 + FWD_BN - 1) / FWD_BN;
     const int n_full = L.m0 / FWD_BN;
     const int n_mask = n_tiles - n_full;
     const int P = (n_mask + 1) & ~1;
-    __amdgpu_buffer_rsrc_t rv[NB];
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) rv[nb] = slice_rsrc<T>(reinterpret_cast<const T*>(p.v) + base + nb * slice, N);
+    const __amdgpu_buffer_rsrc_t rv = slice_rsrc<T>(V, N);
     float z[2] = {0.0f, 0.0f};
     FixStage st;
     run_slots(
         P, P + n_full, [&](int i) { return i < P ? (i < n_mask ? n_full + i : -1) : i - P; },
         [&](auto buf, int t) {
-            constexpr int b = decltype(buf)::value;
-#pragma unroll
-            for (int nb = 0; nb < NB; ++nb) tile_load_lds<T>(sm.t[2 * nb + b], rv[nb], t * FWD_BN, L.w, L.lane);
+            tile_load_lds<T>(sm.t[decltype(buf)::value], rv, t * FWD_BN, L.w, L.lane);
             fix_load(st, arow, rrow, t * FWD_BN, L);
         },
         [&](auto buf) {
             constexpr int b = decltype(buf)::value;
-            fix_store(sm.aux[b], reinterpret_cast<float*>(sm.t[4 + b]), st, L, a_sh, r_sh);
+            fix_store(sm.aux[b], reinterpret_cast<float*>(sm.t[2 + b]), st, L, a_sh, r_sh);
         },
         [&](auto buf, int t, auto mask) {
             constexpr int b = decltype(buf)::value;
-            const T* vs[NB];
-#pragma unroll
-            for (int nb = 0; nb < NB; ++nb) vs[nb] = sm.t[2 * nb + b];
-            fix_tile<T, NB, decltype(mask)::value>(vs, reinterpret_cast<const float*>(sm.t[4 + b]), sm.aux[b],
-                                                   t * FWD_BN, L, oacc, z);
+            fix_tile<T, decltype(mask)::value>(sm.t[b], reinterpret_cast<const float*>(sm.t[2 + b]), sm.aux[b],
+                                               t * FWD_BN, L, oacc, z);
         });
     // O(i) = acc(i) / Z'(i) and log Z(i) = A + R + ln Z'(i), with Z'(i) the
     // sum of the same float32 weights (the guard keeps it above e^-40).
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
         const float zt = pair_sum(z[qb]);
-        const float lse = A + R + __log2f(zt) * LN2;
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb)
-            store_rows<T>(reinterpret_cast<T*>(p.o) + base + nb * slice, p.lse + row_base + nb * rows, L,
-                          L.q0 + 32 * qb + L.c, oacc[nb][qb], 1.0f / zt, lse, true);
+        store_rows<T>(reinterpret_cast<T*>(p.o) + base, p.lse + row_base, L, L.q0 + 32 * qb + L.c, oacc[qb],
+                      1.0f / zt, A + R + __log2f(zt) * LN2, true);
     }
 }
 
@@ -683,12 +649,10 @@ __global__ __launch_bounds__(FWD_THREADS) __attribute__((amdgpu_waves_per_eu(2))
     __shared__ __attribute__((aligned(16))) T t1[tile_elems<T>()];
     __shared__ __attribute__((aligned(16))) T t2[tile_elems<T>()];
     __shared__ __attribute__((aligned(16))) T t3[tile_elems<T>()];
-    __shared__ __attribute__((aligned(16))) float band0[FIX_BAND_COPIES * FWD_BAND_STRIDE];
-    __shared__ __attribute__((aligned(16))) float band1[FIX_BAND_COPIES * FWD_BAND_STRIDE];
     __shared__ __attribute__((aligned(16))) float ea0[FWD_BN];
     __shared__ __attribute__((aligned(16))) float ea1[FWD_BN];
     __shared__ float red[4];
-    const Tiles<T> sm = {{t0, t1, t2, t3, reinterpret_cast<T*>(band0), reinterpret_cast<T*>(band1)}, {ea0, ea1}, red};
+    const Tiles<T> sm = {{t0, t1, t2, t3}, {ea0, ea1}, red};
     // Longest blocks first: level -> query block in descending order.
     const SliceOf sl = slice_of(blockIdx.x, p.B, p.H, 1, [&](int k) { return (int)p.head_order[k]; });
     const int qblk = p.n_qblocks - 1 - sl.level;
@@ -704,25 +668,12 @@ __global__ __launch_bounds__(FWD_THREADS) __attribute__((amdgpu_waves_per_eu(2))
     L.m0 = qblk * FWD_BM;
     L.q0 = L.m0 + FWD_QW * L.w;
     L.N = p.N;
-    if (fixed) {
-        // Batch elements pair up (b0 = b with its low bit cleared, b0 + 1):
-        // one workgroup of the pair forms the pattern's weights once and
-        // applies them to both, the one whose batch parity matches the query
-        // block's, so the active workgroups alternate between the pair's two
-        // places in the grid from block to block.  An unpaired last element
-        // (odd B) is served alone.
-        const int b0 = sl.b & ~1;
-        const bool paired = b0 + 1 < p.B;
-        if (paired && (sl.b & 1) != (qblk & 1)) return;
-        const size_t base = ((size_t)b0 * p.H + h) * p.N * HEAD_DIM;
-        const size_t row_base = ((size_t)b0 * p.H + h) * p.N;
-        if (paired)
-            fwd_fixed<T, 2>(sm, p, L, base, row_base, h);
-        else
-            fwd_fixed<T, 1>(sm, p, L, base, row_base, h);
-    } else {
-        fwd_ordinary<T>(sm, p, L, (size_t)bh * p.N * HEAD_DIM, (size_t)bh * p.N);
-    }
+    const size_t base = (size_t)bh * p.N * HEAD_DIM;
+    const size_t row_base = (size_t)bh * p.N;
+    if (fixed)
+        fwd_fixed<T>(sm, p, L, base, row_base, h);
+    else
+        fwd_ordinary<T>(sm, p, L, base, row_base);
 }
 
 }  // namespace saf

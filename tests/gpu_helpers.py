@@ -3,7 +3,8 @@ C ABI through the binding, and compare with the fp64 oracle at the stated
 tolerances.
 
 Tolerances (elementwise, on O, LSE, dQ, dK, dV):
-* float32 path: ``max |gpu - oracle| <= 1e-4``;
+* float32 path: ``max |gpu - oracle| <= 1e-4 * max(1, max |oracle|)`` per
+  tensor (float32 rounding of sums whose size follows the tensor's);
 * bf16 path:    ``|gpu - oracle| <= 1e-2 + 2e-2 * |oracle|``.
 """
 
@@ -66,7 +67,8 @@ def check_close(name: str, got: np.ndarray, ref: np.ndarray, dtype: str, extra=0
     err = np.abs(got - ref)
     if dtype == "f32":
         worst = float(err.max()) if err.size else 0.0
-        assert worst <= F32_ATOL, f"{name}: max abs err {worst:.3e} > {F32_ATOL}"
+        bar = F32_ATOL * max(1.0, float(np.abs(ref).max()) if ref.size else 1.0)
+        assert worst <= bar, f"{name}: max abs err {worst:.3e} > {bar:.3e}"
     else:
         bound = BF16_ATOL + BF16_RTOL * np.abs(ref) + extra
         ratio = err / bound

@@ -64,10 +64,10 @@ def test_uniform_head_sets(dtype, fixed):
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("B,N", [(3, 300), (5, 517), (1, 700)])
 def test_fixed_heads_batch_pairs(dtype, B, N):
-    """Fixed-head workgroups serve two batch elements at once (the weights do
-    not depend on the input); odd B leaves the last element unpaired.  Every
-    element of every slice, forward and backward, with several query and key
-    blocks (both parities of the pair-serving rule)."""
+    """Fixed-head workgroups of the key-block pass serve two batch elements
+    at once (the weights do not depend on the input); odd B leaves the last
+    element unpaired.  Every element of every slice, forward and backward,
+    with several key blocks (both parities of the pair-serving rule)."""
     announce(f"batch pairs {dtype} B={B} N={N}")
     inp = _inp(B, 3, N, [0, 2], dtype, seed=17)
     compare_layer(run_gpu(inp, dtype), inp, dtype)
