@@ -131,10 +131,11 @@ size_t saf_hybrid_attn_bwd_gqa_workspace_bytes(saf_dtype_t dt, int B, int Hq, in
  * saf_hybrid_attn_bwd, fixed query heads add P^T dO to dV only and get exact
  * zeros in dQ (the grouped-query path keeps every shared key/value head and
  * maps each ordinary query head to its group, Appendix "Mixed-head execution
- * and numerical checks").  Two launches: the query-block pass, which also
- * forms D = rowsum(dO * O) of the ordinary heads and writes it to the
- * workspace, then the key-block pass (one workgroup per batch element,
- * key/value head and 128 keys, looping over the group).
+ * and numerical checks").  Two launches (three at d = 128): the query-block
+ * pass, which also forms D = rowsum(dO * O) of the ordinary heads and writes
+ * it to the workspace, then the key-block pass (one workgroup per batch
+ * element, key/value head and 128 keys, looping over the group); at d = 128
+ * the key-block pass runs once for dK and once for dV.
  *   Q, O, dO : [B, Hq, N, d] `dt` (O and LSE as written by
  *              saf_hybrid_attn_fwd_gqa);  LSE : [B, Hq, N] float32;
  *   K, V     : [B, Hkv, N, d] `dt`;

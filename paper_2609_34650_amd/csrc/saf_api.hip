@@ -330,8 +330,14 @@ void launch_gqa_bwd(const saf::GqaBwdArgs& base, hipStream_t stream) {
     hipLaunchKernelGGL((saf::gqa_bwd_dq_kernel<T, D>), dim3((unsigned)((size_t)args.n_blocks * args.B * args.Hq)),
                        dim3(saf::GDQ_THREADS), 0, stream, args);
     args.n_blocks = (args.N + saf::GKV_BN - 1) / saf::GKV_BN;
-    hipLaunchKernelGGL((saf::gqa_bwd_kv_kernel<T, D>), dim3((unsigned)((size_t)args.n_blocks * args.B * args.Hkv)),
-                       dim3(saf::GKV_THREADS), 0, stream, args);
+    const dim3 grid((unsigned)((size_t)args.n_blocks * args.B * args.Hkv));
+    if constexpr (saf::gkv_split<D>()) {
+        hipLaunchKernelGGL((saf::gqa_bwd_kv_kernel<T, D, saf::GKV_DK>), grid, dim3(saf::GKV_THREADS), 0, stream, args);
+        hipLaunchKernelGGL((saf::gqa_bwd_kv_kernel<T, D, saf::GKV_DV>), grid, dim3(saf::GKV_THREADS), 0, stream, args);
+    } else {
+        hipLaunchKernelGGL((saf::gqa_bwd_kv_kernel<T, D, saf::GKV_BOTH>), grid, dim3(saf::GKV_THREADS), 0, stream,
+                           args);
+    }
 }
 
 }  // namespace

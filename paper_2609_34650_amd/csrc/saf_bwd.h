@@ -240,9 +240,17 @@ __device__ __forceinline__ void kv_tile(const T* q_tile, const T* g_tile, const 
 // (acc[dt][kt]: head dimensions 16 dt .., keys 16 kt ..), times `scale`.
 template <typename T>
 __device__ __forceinline__ void kv_store_rows16(T* base, const KvLane& L, const f32x4 (&acc)[4][2], float scale) {
+    // The lane's key column, recomputed here from the lane index (an
+    // instruction pair the compiler cannot merge with the prologue's):
+    // otherwise it keeps the K / V row offsets of the prologue, or the
+    // column itself, live across the whole query loop for these stores and
+    // spills them.
+    int lane;
+    asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(lane));
+    const int n = lane & 15;
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt) {
-        const int key = L.kw + 16 * kt + L.n;
+        const int key = L.kw + 16 * kt + n;
         if (key >= L.N) continue;
         T* row = base + (size_t)key * HEAD_DIM;
 #pragma unroll

@@ -13,11 +13,13 @@
 // band times a scaled dO, or, behind a guard, P(i, j) = exp(a[j] + r[i - j] -
 // log Z(i)) per entry); they get exact zeros in dQ.
 //
-// Three launches: the row pre-pass D_i = sum_c dO * O for ordinary query
-// heads; the key-block pass (workgroup = (b, key/value head, 128 keys), one
-// 32-key block per wavefront, looping over the group's query heads with dK
-// and dV accumulated in registers); the query-block pass (workgroup = (b,
-// query head, 128 queries)).
+// Launches: the query-block pass (workgroup = (b, query head, 128 queries)),
+// which also forms D_i = sum_c dO * O of the ordinary heads' rows; then the
+// key-block pass (workgroup = (b, key/value head, 128 keys), one 32-key block
+// per wavefront, looping over the group's query heads with dK and dV
+// accumulated in registers).  At D = 128 the key-block pass is two launches,
+// one for dK and one for dV: both gradients' accumulators plus the block's K
+// and V fragments would not leave room for two wavefronts per SIMD.
 #pragma once
 
 #include "saf_common.h"
@@ -61,7 +63,11 @@ struct GkvLane {
     int tid, w, lane, c, hf, n0, kw, N;
 };
 
-template <typename T, int D, bool MASK>
+// The gradients one key-block launch accumulates.
+enum GkvPart { GKV_BOTH = 0, GKV_DK = 1, GKV_DV = 2 };
+template <int D> constexpr bool gkv_split() { return D > 96; }
+
+template <typename T, int D, int PART, bool MASK>
 __device__ __forceinline__ void gkv_tile(const T* qt, const T* gt, const float* rows, int mq, const GkvLane& L,
                                          const typename Vec<T>::x8 (&kf)[D / 16],
                                          const typename Vec<T>::x8 (&vf)[D / 16], f32x16 (&dv)[D / 32],
@@ -76,15 +82,17 @@ __device__ __forceinline__ void gkv_tile(const T* qt, const T* gt, const float* 
         for (int v = 0; v < 16; ++v) s[v] = 0.0f;
 #pragma unroll
         for (int dc = 0; dc < D / 16; ++dc) mma(s, ld_row<T>(qt, 32 * qb + L.c, 16 * dc + 8 * L.hf), kf[dc]);
-        // dP - D in one go: the accumulator starts at -D of its rows.
+        if constexpr (PART != GKV_DV) {
+            // dP - D in one go: the accumulator starts at -D of its rows.
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-            const f32x4 nd4 = *reinterpret_cast<const f32x4*>(rows + GKV_BM + 32 * qb + 8 * g + 4 * L.hf);
+            for (int g = 0; g < 4; ++g) {
+                const f32x4 nd4 = *reinterpret_cast<const f32x4*>(rows + GKV_BM + 32 * qb + 8 * g + 4 * L.hf);
 #pragma unroll
-            for (int u = 0; u < 4; ++u) dp[4 * g + u] = nd4[u];
+                for (int u = 0; u < 4; ++u) dp[4 * g + u] = nd4[u];
+            }
+#pragma unroll
+            for (int dc = 0; dc < D / 16; ++dc) mma(dp, ld_row<T>(gt, 32 * qb + L.c, 16 * dc + 8 * L.hf), vf[dc]);
         }
-#pragma unroll
-        for (int dc = 0; dc < D / 16; ++dc) mma(dp, ld_row<T>(gt, 32 * qb + L.c, 16 * dc + 8 * L.hf), vf[dc]);
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
             const f32x4 l4 = *reinterpret_cast<const f32x4*>(rows + 32 * qb + 8 * g + 4 * L.hf);
@@ -94,17 +102,20 @@ __device__ __forceinline__ void gkv_tile(const T* qt, const T* gt, const float* 
                 float pv = fast_exp2(fmaf(s[v], scale_log2, -l4[u]));
                 if (MASK && qs + 8 * g + 4 * L.hf + u < L.kw + L.c) pv = 0.0f;
                 s[v] = pv;
-                dp[v] = pv * dp[v];
+                if constexpr (PART != GKV_DV) dp[v] = pv * dp[v];
             }
         }
 #pragma unroll
         for (int kc = 0; kc < 2; ++kc) {
-            const frag pb = to_operand<T>(s, 8 * kc);
-            const frag sb = to_operand<T>(dp, 8 * kc);
+            if constexpr (PART != GKV_DK) {
+                const frag pb = to_operand<T>(s, 8 * kc);
 #pragma unroll
-            for (int db = 0; db < D / 32; ++db) {
-                mma(dv[db], ld_tile_t<true>(gt, 32 * qb + 16 * kc, 32 * db), pb);
-                mma(dk[db], ld_tile_t<true>(qt, 32 * qb + 16 * kc, 32 * db), sb);
+                for (int db = 0; db < D / 32; ++db) mma(dv[db], ld_tile_t<true>(gt, 32 * qb + 16 * kc, 32 * db), pb);
+            }
+            if constexpr (PART != GKV_DV) {
+                const frag sb = to_operand<T>(dp, 8 * kc);
+#pragma unroll
+                for (int db = 0; db < D / 32; ++db) mma(dk[db], ld_tile_t<true>(qt, 32 * qb + 16 * kc, 32 * db), sb);
             }
         }
     }
@@ -221,9 +232,10 @@ __device__ __forceinline__ void gkv_store(T* base, const GkvLane& L, const f32x1
                    acc[db][4 * g + 2] * sc, acc[db][4 * g + 3] * sc);
 }
 
-template <typename T, int D>
-__global__ __launch_bounds__(GKV_THREADS) __attribute__((amdgpu_waves_per_eu(D * sizeof(T) <= 192 ? 2 : 1))) void gqa_bwd_kv_kernel(
+template <typename T, int D, int PART>
+__global__ __launch_bounds__(GKV_THREADS) __attribute__((amdgpu_waves_per_eu(sizeof(T) == 2 ? 2 : 1))) void gqa_bwd_kv_kernel(
     GqaBwdArgs p) {
+    static_assert((PART == GKV_BOTH) != gkv_split<D>(), "D = 128 runs the key-block pass as two launches");
     __shared__ __attribute__((aligned(16))) T q0s[tile_elems<T, D>()];
     __shared__ __attribute__((aligned(16))) T q1s[tile_elems<T, D>()];
     __shared__ __attribute__((aligned(16))) T g0s[tile_elems<T, D>()];
@@ -266,7 +278,7 @@ __global__ __launch_bounds__(GKV_THREADS) __attribute__((amdgpu_waves_per_eu(D *
     // Fixed query heads first (only dV is live), then the ordinary ones with K
     // and V of the block's keys in registers.
     for (int i = 0; i < group; ++i) {
-        if (!((gmask >> i) & 1ull)) continue;
+        if (PART == GKV_DK || !((gmask >> i) & 1ull)) continue;  // fixed heads add to dV only
         const int h = hkv * group + i;
         const size_t qbase = ((size_t)b * p.Hq + h) * N * D;
         const size_t row_base = ((size_t)b * p.Hq + h) * N;
@@ -351,7 +363,7 @@ __global__ __launch_bounds__(GKV_THREADS) __attribute__((amdgpu_waves_per_eu(D *
 #pragma unroll
         for (int dc = 0; dc < D / 16; ++dc) {
             kf[dc] = key < N ? ld8<T>(K + (size_t)key * D + 16 * dc + 8 * L.hf) : zero8<T>();
-            vf[dc] = key < N ? ld8<T>(V + (size_t)key * D + 16 * dc + 8 * L.hf) : zero8<T>();
+            vf[dc] = (PART != GKV_DV && key < N) ? ld8<T>(V + (size_t)key * D + 16 * dc + 8 * L.hf) : zero8<T>();
         }
         for (int i = 0; i < group; ++i) {
             if ((gmask >> i) & 1ull) continue;
@@ -379,13 +391,13 @@ __global__ __launch_bounds__(GKV_THREADS) __attribute__((amdgpu_waves_per_eu(D *
                 [&](auto) {},
                 [&](auto buf, int t, auto mask) {
                     constexpr int B_ = decltype(buf)::value;
-                    gkv_tile<T, D, decltype(mask)::value>(B_ ? q1s : q0s, B_ ? g1s : g0s, B_ ? x1 : x0,
-                                                          L.n0 + t * GKV_BM, L, kf, vf, dv, dk, p.scale_log2);
+                    gkv_tile<T, D, PART, decltype(mask)::value>(B_ ? q1s : q0s, B_ ? g1s : g0s, B_ ? x1 : x0,
+                                                                L.n0 + t * GKV_BM, L, kf, vf, dv, dk, p.scale_log2);
                 });
         }
     }
-    gkv_store<T, D>(reinterpret_cast<T*>(p.dv) + kvbase, L, dv, 1.0f);
-    gkv_store<T, D>(reinterpret_cast<T*>(p.dk) + kvbase, L, dk, p.scale);
+    if (PART != GKV_DK) gkv_store<T, D>(reinterpret_cast<T*>(p.dv) + kvbase, L, dv, 1.0f);
+    if (PART != GKV_DV) gkv_store<T, D>(reinterpret_cast<T*>(p.dk) + kvbase, L, dk, p.scale);
 }
 
 // ---------------------------------------------------------------------------
