@@ -121,55 +121,21 @@ __device__ __forceinline__ void ord_rescale(const float (&mx)[2], float (&m_run)
     }
 }
 
-// exp2(s * sl2 - m) for both query blocks.
-__device__ __forceinline__ void ord_probs(const f32x16 (&s)[2], const float (&m_run)[2], float sl2,
-                                          f32x16 (&pr)[2]) {
+// exp2(s * sl2 - m) for both query blocks, with this lane's partial sums.
+__device__ __forceinline__ void ord_probs(const f32x16 (&s)[2], const float (&m_run)[2], float sl2, f32x16 (&pr)[2],
+                                          float (&ts)[2]) {
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
         const float neg_m = -m_run[qb];
+        float t0 = 0.0f, t1 = 0.0f;
 #pragma unroll
-        for (int v = 0; v < 16; ++v) pr[qb][v] = fast_exp2(fmaf(s[qb][v], sl2, neg_m));
-    }
-}
-
-// This lane's share of a row sum: its 16 probabilities as they enter the
-// product with V.  bf16: the rounded operands, two per v_dot2c_f32_bf16
-// against (1, 1) (half the instructions of float32 adds, and the sum is that
-// of the weights the product applies); float32: plain adds.
-__device__ __forceinline__ float operand_sum(const bf16x8 (&pb)[2]) {
-    const bf16x2 one = {(bf16)1.0f, (bf16)1.0f};
-    float t0 = 0.0f, t1 = 0.0f;
-#pragma unroll
-    for (int kc = 0; kc < 2; ++kc)
-#pragma unroll
-        for (int t = 0; t < 8; t += 4) {
-            t0 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pb[kc][t], pb[kc][t + 1]}, one, t0, false);
-            t1 = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pb[kc][t + 2], pb[kc][t + 3]}, one, t1, false);
+        for (int v = 0; v < 16; v += 2) {
+            pr[qb][v] = fast_exp2(fmaf(s[qb][v], sl2, neg_m));
+            pr[qb][v + 1] = fast_exp2(fmaf(s[qb][v + 1], sl2, neg_m));
+            t0 += pr[qb][v];
+            t1 += pr[qb][v + 1];
         }
-    return t0 + t1;
-}
-__device__ __forceinline__ float operand_sum(const f32x8 (&pb)[2]) {
-    float t0 = 0.0f, t1 = 0.0f;
-#pragma unroll
-    for (int kc = 0; kc < 2; ++kc)
-#pragma unroll
-        for (int t = 0; t < 8; t += 2) {
-            t0 += pb[kc][t];
-            t1 += pb[kc][t + 1];
-        }
-    return t0 + t1;
-}
-
-// MFMA operands of both query blocks (pb[qb][kc]: keys 16 kc .. of the
-// sub-block) and this lane's partial row sums over them.
-template <typename T>
-__device__ __forceinline__ void ord_operands(const f32x16 (&pr)[2], typename Vec<T>::x8 (&pb)[2][2],
-                                             float (&ts)[2]) {
-#pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
-#pragma unroll
-        for (int kc = 0; kc < 2; ++kc) pb[qb][kc] = to_operand<T>(pr[qb], 8 * kc);
-        ts[qb] = operand_sum(pb[qb]);
+        ts[qb] = t0 + t1;
     }
 }
 
@@ -215,10 +181,8 @@ __device__ __forceinline__ void ord_tile(const T* kt, const T* vt, int n0, const
         // sub-block exceeds it by a wide margin (or on the first visible
         // sub-block, where the maximum is still NEG_BIG and the sums are inf).
         f32x16 pr[2];
-        frag pb[2][2];  // [qb][kc]
         float ts[2];
-        ord_probs(s, m_run, sl2, pr);
-        ord_operands<T>(pr, pb, ts);
+        ord_probs(s, m_run, sl2, pr, ts);
         if (__any(ts[0] > RESCALE_SUM || ts[1] > RESCALE_SUM)) {
             float mx[2];
 #pragma unroll
@@ -229,11 +193,15 @@ __device__ __forceinline__ void ord_tile(const T* kt, const T* vt, int n0, const
                 mx[qb] = pair_max(m) * sl2;
             }
             ord_rescale(mx, m_run, l_run, oacc);
-            ord_probs(s, m_run, sl2, pr);
-            ord_operands<T>(pr, pb, ts);
+            ord_probs(s, m_run, sl2, pr, ts);
         }
+        frag pb[2][2];  // [qb][kc]
 #pragma unroll
-        for (int qb = 0; qb < 2; ++qb) l_run[qb] += ts[qb];
+        for (int qb = 0; qb < 2; ++qb) {
+            l_run[qb] += ts[qb];  // float32 row sum, before rounding to the operand type
+#pragma unroll
+            for (int kc = 0; kc < 2; ++kc) pb[qb][kc] = to_operand<T>(pr[qb], 8 * kc);
+        }
 #pragma unroll
         for (int kc = 0; kc < 2; ++kc)
 #pragma unroll
