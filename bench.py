@@ -71,6 +71,14 @@ and causal entry, one exponential and three operations for the column sum
 and again for the diagonal sum: 8 operations) against the float32 vector
 rate.
 
+``--chip`` runs the library's two chip probes instead of a layer
+(include/saf_measure.h): the MFMA rate of the two bf16 tile shapes the
+kernels use (32x32x16 and 16x16x32, one and two wavefronts per SIMD, with the
+shader clock of the run), and the layer kernels' LDS operand reads one
+pattern per launch, timed with HIP events; under rocprofv3 --pmc
+SQ_INSTS_LDS SQ_LDS_BANK_CONFLICT the latter give each pattern's
+bank-conflict cycles per read.
+
 ``--calib`` times the calibration statistics instead (include/saf_calib.h):
 one step = folding 32 calibration inputs of one 12-head layer (T = 4096) into
 the running statistics (mean attention, scalar sums; no per-entry squared
@@ -223,6 +231,8 @@ def parse():
                     help="time the compact fit (targets + 400 Adam steps) of a 12-head layer at T=4096 instead")
     ap.add_argument("--calib", action="store_true",
                     help="time the calibration statistics (workload calib124m_4k) instead of the layer")
+    ap.add_argument("--chip", action="store_true",
+                    help="run the MFMA-rate and LDS read-pattern probes (include/saf_measure.h) instead")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run one plain 64 MiB read + 64 MiB write elementwise kernel (torch.neg), then one "
                          "64 MiB read through buffer loads straight to LDS (saf_lds_read_probe), before the "
@@ -876,6 +886,59 @@ TRAIN_LAYERS = {
 }
 
 
+def main_chip(args, torch):
+    """The chip probes of include/saf_measure.h: MFMA rate per tile shape and
+    occupancy, and the time of each LDS read pattern of the layer kernels."""
+    from paper_2609_34650_amd import binding
+    dev = torch.device("cuda", 0)
+    clk = torch.zeros(2, dtype=torch.int64, device=dev)
+    fsink = torch.zeros(256 * 64, dtype=torch.float32, device=dev)
+    isink = torch.zeros(65536, dtype=torch.int32, device=dev)
+
+    def timed(fn, reps):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    # Long enough runs that the clock has settled: warm the chip for the floor first.
+    t_w = time.perf_counter()
+    while time.perf_counter() - t_w < args.warmup_floor_s:
+        binding.saf_mfma_rate_probe(0, 2, 2000, clk, fsink)
+        torch.cuda.synchronize()
+    iters = 20000
+    mfma = []
+    for shape, name in ((0, "32x32x16 bf16"), (1, "16x16x32 bf16")):
+        for waves in (1, 2):
+            ms = timed(lambda: binding.saf_mfma_rate_probe(shape, waves, iters, clk, fsink), 3)
+            c = clk.cpu().tolist()
+            mhz = c[0] / c[1] * 100.0 if c[1] else None
+            flop = 2.0 * 131072 * iters * 1024 * waves
+            mfma.append({"shape": name, "waves_per_simd": waves, "ms": round(ms, 4),
+                         "tflops": round(flop / (ms * 1e-3) / 1e12, 1),
+                         "shader_clock_mhz": round(mhz, 1) if mhz else None})
+    lds = []
+    reads = (4, 8, 4, 8, 4, 2, 8)  # LDS read instructions per iteration and wavefront
+    for pat, name in enumerate(binding.LDS_PATTERNS):
+        it = 4000
+        ms = timed(lambda: binding.saf_lds_pattern_probe(pat, it, isink), 3)
+        waves = 256 * 4
+        lds.append({"pattern": pat, "what": name, "ms": round(ms, 4),
+                    "ns_per_wave_iteration": round(ms * 1e6 / it, 2),
+                    "lds_reads_per_wave_iteration": reads[pat],
+                    "note": f"{waves} wavefronts x {it} iterations"})
+    result = {"metric": "chip probes: MFMA rate per bf16 tile shape, LDS read patterns of the layer kernels",
+              "value": mfma[-1]["tflops"], "unit": "TFLOP/s (16x16x32 bf16, two wavefronts per SIMD)",
+              "n_gpus": 1, "higher_is_better": True, "data": "synthetic", "dtype": "bf16",
+              "config": {"workload": "chip probes"}, "mfma": mfma, "lds_patterns": lds}
+    print(json.dumps(result), flush=True)
+
+
 def main_train_layer(args, torch, which):
     """One training layer (forward + backward) through the grouped-query entry
     points at 25 % and 50 % fixed query heads against all-ordinary."""
@@ -1008,6 +1071,9 @@ def main():
         binding.saf_lds_read_probe(src)
         torch.cuda.synchronize()
         del src, dst
+    if args.chip:
+        main_chip(args, torch)
+        return
     if args.calib:
         main_calib(args, torch)
         return

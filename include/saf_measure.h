@@ -1,14 +1,16 @@
 /*
  * saf_measure.h -- measurement aids of libsaf.so.  They compute nothing of
- * the layer; they give the benchmark two reference readings that the layer's
- * own kernels cannot:
+ * the layer; they give the benchmark reference readings that the layer's own
+ * kernels cannot:
  *
  * - the shader clock while the layer runs (the bf16 MFMA peak scales with it:
  *   the published 2.5 PFLOP/s is quoted at 2.4 GHz), from the GPU's two
  *   hardware counters rather than a driver's DPM table;
  * - a known number of bytes read through the same load path the layer
  *   kernels use (buffer loads straight into LDS), so that a profiler's HBM
- *   byte counters can be scaled by what they read for a known size.
+ *   byte counters can be scaled by what they read for a known size;
+ * - the layer kernels' LDS operand reads one pattern at a time (which of
+ *   them meet bank conflicts), and the MFMA rate of the two tile shapes.
  *
  * Conventions as in saf.h: device pointers owned by the caller, nothing
  * allocated, nothing synchronised, arguments checked before any launch.
@@ -56,6 +58,44 @@ saf_status_t saf_clock_probe(uint64_t* out, int duration_us, hipStream_t stream)
  * Errors: SAF_ERR_NULL, SAF_ERR_SHAPE, SAF_ERR_ALIGNMENT, SAF_ERR_LAUNCH.
  */
 saf_status_t saf_lds_read_probe(const void* src, size_t bytes, float* sink, hipStream_t stream);
+
+/*
+ * LDS read patterns of the layer kernels, one per launch, for bank-conflict
+ * counters (SQ_LDS_BANK_CONFLICT / SQ_INSTS_LDS) and timing.  256 workgroups
+ * of 256 threads; each wavefront runs `iters` iterations of one pattern on a
+ * 64 x 64 bf16 tile in the kernels' column-slab layout, addressed by the
+ * kernels' own helpers:
+ *   0  row operand of a 32 x 32 product (lane c reads row c, its 16-byte
+ *      half chosen by the lane half; 4 reads per iteration)
+ *   1  transposed operand of a 32 x 32 product, accumulator order (4 x 2)
+ *   2  row operand of a 16 x 16 product (lanes i and i + 16 read the two
+ *      halves of one row; 4)
+ *   3  transposed operand of a 16 x 16 product (4 x 2)
+ *   4  16-byte reads of per-row floats in the 32 x 32 accumulator order (4)
+ *   5  16-byte reads of per-row floats in the 16 x 16 accumulator order (2)
+ *   6  transposed operand of a 32 x 32 product, natural order (4 x 2)
+ *   pattern : 0 .. 6;   iters : 1 .. 2^20;
+ *   sink    : DEVICE uint32 [65536], 4-byte aligned; written only under a
+ *             condition no pattern meets (it keeps the reads live).
+ * Errors: SAF_ERR_NULL, SAF_ERR_SHAPE, SAF_ERR_ALIGNMENT, SAF_ERR_LAUNCH.
+ */
+saf_status_t saf_lds_pattern_probe(int pattern, int iters, uint32_t* sink, hipStream_t stream);
+
+/*
+ * MFMA rate of the two bf16 tile shapes the kernels use.  256 workgroups, one
+ * per CU, each of 4 * waves_per_simd wavefronts; every wavefront issues
+ * `iters` rounds of 131072 multiply-adds on independent accumulators:
+ * 8 v_mfma_f32_32x32x16_bf16 (shape 0) or 16 v_mfma_f32_16x16x32_bf16
+ * (shape 1).  FLOP per launch = 2 * 131072 * iters * 1024 * waves_per_simd.
+ *   clk  : DEVICE 2 x uint64, 8-byte aligned: shader cycles and 100 MHz
+ *          reference ticks of workgroup 0's run (its mean shader clock);
+ *   sink : DEVICE float [256 * 64], written only under a condition the
+ *          accumulators never meet.
+ *   shape: 0 or 1;  waves_per_simd: 1 or 2;  iters: 1 .. 2^20.
+ * Errors: SAF_ERR_NULL, SAF_ERR_SHAPE, SAF_ERR_ALIGNMENT, SAF_ERR_LAUNCH.
+ */
+saf_status_t saf_mfma_rate_probe(int shape, int waves_per_simd, int iters, uint64_t* clk, float* sink,
+                                 hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -59,6 +59,8 @@ EXPORTS = (
     "saf_hybrid_attn_bwd_noalloc",
     "saf_clock_probe",
     "saf_lds_read_probe",
+    "saf_lds_pattern_probe",
+    "saf_mfma_rate_probe",
 )
 
 
@@ -128,6 +130,10 @@ def load() -> ctypes.CDLL:
     lib.saf_clock_probe.argtypes = [vp, i, vp]
     lib.saf_lds_read_probe.restype = ctypes.c_int
     lib.saf_lds_read_probe.argtypes = [vp, ctypes.c_size_t, vp, vp]
+    lib.saf_lds_pattern_probe.restype = ctypes.c_int
+    lib.saf_lds_pattern_probe.argtypes = [i, i, vp, vp]
+    lib.saf_mfma_rate_probe.restype = ctypes.c_int
+    lib.saf_mfma_rate_probe.argtypes = [i, i, i, vp, vp, vp]
     lib.saf_status_str.restype = ctypes.c_char_p
     lib.saf_status_str.argtypes = [i]
     del f32p
@@ -610,3 +616,31 @@ def saf_lds_read_probe(src: torch.Tensor, sink: Optional[torch.Tensor] = None) -
            "saf_lds_read_probe")
     return sink
 
+
+LDS_PATTERNS = ("row operand 32x32", "transposed 32x32 (accumulator order)", "row operand 16x16",
+                "transposed 16x16", "row floats 32x32 order", "row floats 16x16 order",
+                "transposed 32x32 (natural order)")
+
+
+def saf_lds_pattern_probe(pattern: int, iters: int, sink: torch.Tensor):
+    """Enqueue one LDS read pattern of the layer kernels (LDS_PATTERNS) on the
+    current stream; `sink` is a device int32 tensor of at least 65536
+    elements (written only under a condition no pattern meets)."""
+    if sink.dtype != torch.int32 or sink.numel() < 65536 or not sink.is_cuda:
+        raise ValueError("sink must be a device int32 tensor with at least 65536 elements")
+    _raise(load().saf_lds_pattern_probe(int(pattern), int(iters), sink.data_ptr(), _stream(sink.device)),
+           "saf_lds_pattern_probe")
+
+
+def saf_mfma_rate_probe(shape: int, waves_per_simd: int, iters: int, clk: torch.Tensor, sink: torch.Tensor):
+    """Enqueue the MFMA rate probe (shape 0: 32x32x16 bf16, 1: 16x16x32 bf16)
+    on the current stream.  `clk`: device int64 tensor of 2 (shader cycles and
+    100 MHz ticks of workgroup 0); `sink`: device float32 tensor of at least
+    16384 elements.  FLOP per launch: 2 * 131072 * iters * 1024 *
+    waves_per_simd."""
+    if clk.dtype != torch.int64 or clk.numel() < 2 or not clk.is_cuda:
+        raise ValueError("clk must be a device int64 tensor with 2 elements")
+    if sink.dtype != torch.float32 or sink.numel() < 16384 or not sink.is_cuda:
+        raise ValueError("sink must be a device float32 tensor with at least 16384 elements")
+    _raise(load().saf_mfma_rate_probe(int(shape), int(waves_per_simd), int(iters), clk.data_ptr(), sink.data_ptr(),
+                                      _stream(clk.device)), "saf_mfma_rate_probe")

@@ -849,6 +849,38 @@ SAF_EXPORT saf_status_t saf_lds_read_probe(const void* src, size_t bytes, float*
     return launched();
 }
 
+SAF_EXPORT saf_status_t saf_lds_pattern_probe(int pattern, int iters, uint32_t* sink, hipStream_t stream) {
+    if (sink == nullptr) return SAF_ERR_NULL;
+    if (pattern < 0 || pattern >= saf::LDS_PATTERN_COUNT || iters < 1 || iters > (1 << 20)) return SAF_ERR_SHAPE;
+    if ((reinterpret_cast<uintptr_t>(sink) & 3u) != 0) return SAF_ERR_ALIGNMENT;
+    const dim3 grid(saf::LDS_PATTERN_BLOCKS), block(saf::LDS_PATTERN_THREADS);
+    switch (pattern) {
+        case 0: hipLaunchKernelGGL(saf::lds_pattern_kernel<0>, grid, block, 0, stream, sink, iters); break;
+        case 1: hipLaunchKernelGGL(saf::lds_pattern_kernel<1>, grid, block, 0, stream, sink, iters); break;
+        case 2: hipLaunchKernelGGL(saf::lds_pattern_kernel<2>, grid, block, 0, stream, sink, iters); break;
+        case 3: hipLaunchKernelGGL(saf::lds_pattern_kernel<3>, grid, block, 0, stream, sink, iters); break;
+        case 4: hipLaunchKernelGGL(saf::lds_pattern_kernel<4>, grid, block, 0, stream, sink, iters); break;
+        case 5: hipLaunchKernelGGL(saf::lds_pattern_kernel<5>, grid, block, 0, stream, sink, iters); break;
+        default: hipLaunchKernelGGL(saf::lds_pattern_kernel<6>, grid, block, 0, stream, sink, iters); break;
+    }
+    return launched();
+}
+
+SAF_EXPORT saf_status_t saf_mfma_rate_probe(int shape, int waves_per_simd, int iters, uint64_t* clk, float* sink,
+                                            hipStream_t stream) {
+    if (clk == nullptr || sink == nullptr) return SAF_ERR_NULL;
+    if (shape < 0 || shape > 1 || waves_per_simd < 1 || waves_per_simd > 2 || iters < 1 || iters > (1 << 20))
+        return SAF_ERR_SHAPE;
+    if ((reinterpret_cast<uintptr_t>(clk) & 7u) != 0 || (reinterpret_cast<uintptr_t>(sink) & 3u) != 0)
+        return SAF_ERR_ALIGNMENT;
+    const dim3 grid(saf::MFMA_PROBE_BLOCKS), block(256 * waves_per_simd);
+    if (shape == 0)
+        hipLaunchKernelGGL(saf::mfma_rate_kernel<0>, grid, block, 0, stream, clk, sink, iters);
+    else
+        hipLaunchKernelGGL(saf::mfma_rate_kernel<1>, grid, block, 0, stream, clk, sink, iters);
+    return launched();
+}
+
 SAF_EXPORT const char* saf_status_str(saf_status_t s) {
     switch (s) {
         case SAF_OK: return "ok";

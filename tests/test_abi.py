@@ -317,3 +317,19 @@ def test_measurement_probe_argument_errors(lib):
     assert lib.saf_lds_read_probe(FAKE, (1 << 40) + 4096, FAKE, None) == 2
     assert lib.saf_lds_read_probe(FAKE + 8, 4096, FAKE, None) == 6
     assert lib.saf_lds_read_probe(FAKE, 4096, FAKE + 2, None) == 6
+    # LDS read patterns
+    assert lib.saf_lds_pattern_probe(0, 10, None, None) == 1
+    assert lib.saf_lds_pattern_probe(-1, 10, FAKE, None) == 2
+    assert lib.saf_lds_pattern_probe(7, 10, FAKE, None) == 2
+    assert lib.saf_lds_pattern_probe(0, 0, FAKE, None) == 2
+    assert lib.saf_lds_pattern_probe(0, (1 << 20) + 1, FAKE, None) == 2
+    assert lib.saf_lds_pattern_probe(0, 10, FAKE + 2, None) == 6
+    # MFMA rate
+    assert lib.saf_mfma_rate_probe(0, 1, 10, None, FAKE, None) == 1
+    assert lib.saf_mfma_rate_probe(0, 1, 10, FAKE, None, None) == 1
+    assert lib.saf_mfma_rate_probe(2, 1, 10, FAKE, FAKE, None) == 2
+    assert lib.saf_mfma_rate_probe(0, 3, 10, FAKE, FAKE, None) == 2
+    assert lib.saf_mfma_rate_probe(0, 0, 10, FAKE, FAKE, None) == 2
+    assert lib.saf_mfma_rate_probe(1, 2, 0, FAKE, FAKE, None) == 2
+    assert lib.saf_mfma_rate_probe(0, 1, 10, FAKE + 4, FAKE, None) == 6
+    assert lib.saf_mfma_rate_probe(0, 1, 10, FAKE, FAKE + 2, None) == 6
