@@ -80,7 +80,8 @@ def check_close(name: str, got: np.ndarray, ref: np.ndarray, dtype: str, extra=0
 
 
 def compare_layer(gpu: dict, inp: dict, dtype: str, backward: bool = True, heads=None, extra=None):
-    """Compare every listed (b, h) slice (all if ``heads`` is None).
+    """Compare every listed (b, h) slice (all if ``heads`` is None); returns
+    per tensor the largest absolute error and the relative L2 error.
     ``extra``: optional per-element additions to the bf16 bar for dQ, dK, dV
     (``bf16_rounding_bound``)."""
     from oracle import saf_oracle as orc
@@ -98,7 +99,12 @@ def compare_layer(gpu: dict, inp: dict, dtype: str, backward: bool = True, heads
         got = np.stack([gpu[name][b, h] for b, h in sel])
         want = np.stack([ref[b, h] for b, h in sel])
         add = np.stack([ex[name][b, h] for b, h in sel]) if name in ex else 0.0
-        errs[name] = check_close(name, got, want, dtype, add)
+        worst = check_close(name, got, want, dtype, add)
+        # The paper's gradient check reports the largest absolute error and
+        # the relative L2 error ||got - want|| / max(||want||, 1e-8) of each
+        # tensor; both are returned.
+        rel_l2 = float(np.linalg.norm(got - want)) / max(float(np.linalg.norm(want)), 1e-8)
+        errs[name] = {"max_abs": worst, "rel_l2": rel_l2}
     if backward:
         fixed = np.asarray(inp["is_fixed"]).astype(bool)
         for b, h in sel:

@@ -33,10 +33,18 @@ def test_tiny_f32_workload_all_elements():
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_paper_unaligned_shape(dtype):
     """B=2, T=129, H=4, d=64, prior length 192, heads 1 and 3 fixed (the mixed
-    layer of the paper's gradient-agreement check)."""
+    layer of the paper's gradient-agreement check), elementwise at the usual
+    bars, and by the check's second measure, the relative L2 error of each
+    tensor: the paper's float32 values are 2-3e-7 and its bf16-autocast
+    values 1.5-4.5e-3 (a whole layer with projections), so float32 is held
+    to 1e-5 and bf16 to 1e-2."""
     announce(f"paper shape {dtype}")
     inp = _inp(2, 4, 129, [1, 3], dtype, prior_len=192)
-    compare_layer(run_gpu(inp, dtype), inp, dtype)
+    errs = compare_layer(run_gpu(inp, dtype), inp, dtype)
+    print(errs)
+    bar = 1e-5 if dtype == "f32" else 1e-2
+    for name, e in errs.items():
+        assert e["rel_l2"] <= bar, (name, e)
 
 
 @pytest.mark.parametrize("N", [1, 2, 31, 32, 33, 63, 64, 65, 127, 128, 129, 191, 255, 256, 257, 300])
