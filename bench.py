@@ -95,6 +95,7 @@ import argparse
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -154,14 +155,24 @@ KERNEL_SOURCES = {
 }
 
 
+def _code_only(text: str) -> str:
+    """Source text without comments and blank-line or trailing-space
+    differences, so that editing a comment does not mark the counters
+    stale.  (The sources hold no string literal containing // or /*.)"""
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", "", text)
+    return "\n".join(ln.rstrip() for ln in text.splitlines() if ln.strip())
+
+
 def kernel_source_digest(group: str = "layer") -> str:
-    """sha256 over the device sources of one kernel group (in the listed order)."""
+    """sha256 over the code (comments removed) of the device sources of one
+    kernel group, in the listed order."""
     csrc = os.path.join(ROOT, "paper_2609_34650_amd", "csrc")
     h = hashlib.sha256()
     for name in KERNEL_SOURCES[group]:
         h.update(name.encode())
-        with open(os.path.join(csrc, name), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(csrc, name), encoding="utf-8") as f:
+            h.update(_code_only(f.read()).encode())
     return h.hexdigest()
 
 

@@ -8,8 +8,9 @@
 // reads neither queries nor keys.
 //
 // Ordinary heads use the FlashAttention-2 recurrences: with P recomputed from
-// the forward's LSE, dP = dO V^T, D_i = rowsum(dO * O)_i (row pre-pass),
-// dS = P * (dP - D), dQ = dS K / sqrt(d), dK = dS^T Q / sqrt(d).
+// the forward's LSE, dP = dO V^T, D_i = rowsum(dO * O)_i (formed by the
+// query-block pass, which runs first, or by a row pre-pass), dS = P * (dP - D),
+// dQ = dS K / sqrt(d), dK = dS^T Q / sqrt(d).
 #pragma once
 
 #include "saf_common.h"
@@ -71,21 +72,21 @@ __global__ __launch_bounds__(PRE_THREADS) void bwd_pre_kernel(BwdArgs p) {
 
 // ---------------------------------------------------------------------------
 // Key-block pass: workgroup = (b, h, 128 keys); 4 wavefronts x 32 keys,
-// streaming query tiles of 64 from the block's first key to N.  KV_KB 32-key
-// sub-blocks per wavefront: with one, a wavefront stays under 256 VGPRs and
-// two of them share a SIMD.
+// streaming steps of two 64-query tiles from the block's first key to N.
+// KV_KB 32-key sub-blocks per wavefront: with one, a wavefront stays within
+// 256 VGPRs and two of them share a SIMD.
 //
 // Ordinary heads: scores are formed as S (queries x keys) on 16 x 16 tiles,
 // so a lane holds one key of each 16-key tile (l % 16) and eight queries of
 // each 32-query half: P and dS feed directly into the B operand of
 // dV^T += dO^T P and dK^T += Q^T dS, whose accumulators again hold one key
-// per lane.  (With 32 x 32 tiles a lane would hold 16 queries, and read twice
-// the per-row LSE and D values from LDS for the same products.)  K and V of the wavefront's keys stay in
-// registers; Q and dO tiles are copied by buffer loads straight into
-// column-slab LDS tiles (A operands of S and dP, and, through transposing
-// reads, of the dV/dK products), double-buffered so the next tile is in
-// flight while this one is used.  The first tiles meet the diagonal and run a
-// masked body; the rest run mask-free.
+// per lane.  (With 32 x 32 tiles a lane would hold 16 queries, and read
+// twice the per-row LSE and D values from LDS for the same products.)  K and
+// V of the wavefront's keys stay in registers; Q and dO tiles are copied by
+// buffer loads straight into column-slab LDS tiles (A operands of S and dP,
+// and, through transposing reads, of the dV/dK products), double-buffered so
+// the next step is in flight while this one is used.  The first step meets
+// the diagonal and runs a masked body; the rest run mask-free.
 //
 // Fixed heads: dV[j] = sum_i P(i,j) dO[i] with P(i,j) = ea(j) er(i-j) g(i),
 // ea = exp(a - A), er = exp(r - R), g(i) = exp(A + R - log Z(i)) (A: maximum

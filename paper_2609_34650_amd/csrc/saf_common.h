@@ -160,11 +160,16 @@ __device__ __forceinline__ unsigned int pack_bf16(float lo, float hi) {
 // slabs of 32 bytes of columns (16 bf16 or 8 float); each slab stores its 64
 // rows 32 bytes apart, and slabs are SLAB_BYTES apart, 128 bytes more than
 // 2 KB so that neighbouring slabs sit in opposite halves of the LDS banks.
-// In this layout the two operand reads of the kernels are linear and free of
-// bank conflicts: a row operand (eight consecutive columns of row c, lanes
-// c = 0..31 in each lane half) is one 1 KB run, and each 16-lane group of a
-// transposed read (four rows x 32 bytes) is one 128-byte run.  It is also the
-// order in which a buffer load to LDS writes 64 lanes x 16 bytes.
+// A row operand (eight consecutive columns of a row per lane) is one linear
+// run, and each 16-lane group of a transposed read (four rows x 32 bytes) is
+// one 128-byte run.  Measured bank conflicts (saf_lds_pattern_probe): none
+// for the transposed reads and for the row operand of a 16 x 16 product
+// (lanes i and i + 16 read the two halves of one row); 4 cycles per read for
+// the row operand of a 32 x 32 product (lane c reads row c, so lanes i and
+// i + 16, served together, read rows 16 apart at the same half, which share
+// banks); a layout that swaps the halves of rows 16-31 and 48-63 removes
+// those without making the kernels faster.  It is also the order in which a
+// buffer load to LDS writes 64 lanes x 16 bytes.
 // ---------------------------------------------------------------------------
 constexpr int SLAB_BYTES = 32 * 64 + 128;
 constexpr int TILE_ROWS = 64;
