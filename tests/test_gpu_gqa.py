@@ -225,3 +225,64 @@ def test_gqa_autograd_wrapper_matches_abi():
     torch.cuda.synchronize()
     assert torch.equal(o.detach(), O)
     assert torch.equal(q.grad, dQ) and torch.equal(k.grad, dK) and torch.equal(v.grad, dV)
+
+
+# ---------------------------------------------------------------------------
+# The grouped-query training layers the benchmark times, at full size
+# ---------------------------------------------------------------------------
+
+TRAIN_SHAPES = {
+    # name: (B, Hq, Hkv, N, d, stream id, fixed query heads) -- bench.py's --layer128 and --layer1b
+    "gqa_train_4k_d128": (4, 32, 8, 4096, 128, 64, 8),
+    "layer1b_8k_d96": (2, 16, 16, 8192, 96, 62, 4),
+}
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("name", list(TRAIN_SHAPES))
+def test_gqa_training_layer_full_size_sampled(name):
+    """Forward and backward of a whole training layer in the benchmark's
+    launch configuration (at d = 128 the key-block pass runs as its dK and dV
+    launches), then, for two (batch element, key/value group) pairs -- the
+    first group holding a fixed head, and in the last batch element the last
+    group holding an ordinary head -- every element of O, LSE and dQ of the
+    group's query heads and
+    of the group's dK and dV against the oracle, at the bf16 bar plus the
+    worst-case effect of the bf16 operand rounding (gpu_helpers)."""
+    torch = torch_cuda()
+    from oracle import saf_oracle as orc
+    from paper_2609_34650_amd import binding, inputs
+    B, Hq, Hkv, N, d, sid, n_fixed = TRAIN_SHAPES[name]
+    announce(f"gqa training layer full size {name}")
+    inp = inputs.make_inputs(B, Hq, N, d, [], "bf16", stream_id=sid, backward=True)
+    flags = np.zeros(Hq, np.uint8)
+    flags[inputs.fixed_heads(Hq, n_fixed, stream_id=sid)] = 1
+    inp["K"] = np.ascontiguousarray(inp["K"][:, :Hkv])
+    inp["V"] = np.ascontiguousarray(inp["V"][:, :Hkv])
+    inp["is_fixed"] = flags
+    dev = torch.device("cuda", 0)
+    t = {k: torch.from_numpy(inp[k]).to(dev).to(torch.bfloat16).contiguous() for k in ("Q", "K", "V", "dO")}
+    a = torch.from_numpy(inp["a"]).to(dev)
+    r = torch.from_numpy(inp["r"]).to(dev)
+    O, LSE = binding.saf_hybrid_attn_fwd_gqa(t["Q"], t["K"], t["V"], flags, a, r)
+    dQ, dK, dV = binding.saf_hybrid_attn_bwd_gqa(t["Q"], t["K"], t["V"], O, t["dO"], LSE, flags, a, r)
+    torch.cuda.synchronize()
+    group = Hq // Hkv
+    g_fixed = next(g for g in range(Hkv) if flags[g * group:(g + 1) * group].any())
+    g_ordinary = next(g for g in reversed(range(Hkv)) if not flags[g * group:(g + 1) * group].all())
+    for b, g in ((0, g_fixed), (B - 1, g_ordinary)):
+        hs = slice(g * group, (g + 1) * group)
+        sub = {"Q": inp["Q"][b:b + 1, hs], "K": inp["K"][b:b + 1, g:g + 1], "V": inp["V"][b:b + 1, g:g + 1],
+               "dO": inp["dO"][b:b + 1, hs], "is_fixed": flags[hs], "a": inp["a"][hs], "r": inp["r"][hs]}
+        announce(f"  oracle for b={b} group={g} heads {hs.start}..{hs.stop - 1} fixed={flags[hs].tolist()}")
+        Oo, Lo = orc.layer_forward_gqa(sub["Q"], sub["K"], sub["V"], sub["is_fixed"], sub["a"], sub["r"])
+        dQo, dKo, dVo = orc.layer_backward_gqa(sub["Q"], sub["K"], sub["V"], sub["dO"], sub["is_fixed"], sub["a"],
+                                               sub["r"])
+        wq, wk, wv = bf16_rounding_bound(sub, 1)
+        _check("bf16", O[b:b + 1, hs].double().cpu().numpy(), Oo)
+        _check("bf16", LSE[b:b + 1, hs].double().cpu().numpy(), Lo)
+        _check("bf16", dQ[b:b + 1, hs].double().cpu().numpy(), dQo, wq)
+        _check("bf16", dK[b:b + 1, g:g + 1].double().cpu().numpy(), dKo, wk)
+        _check("bf16", dV[b:b + 1, g:g + 1].double().cpu().numpy(), dVo, wv)
+        fixed_q = flags[hs].astype(bool)
+        assert not dQ[b, hs][torch.from_numpy(fixed_q).to(dev)].any(), "fixed heads must get zero dQ"
