@@ -61,3 +61,30 @@ def test_noalloc_rejects_problems_beyond_its_scratch():
                                            N, 2, 1, N, 64, fake, fake, fake, None)
     assert code == 2
     torch.cuda.synchronize()
+
+
+def test_noalloc_at_its_largest_problem():
+    """B * H * N = 2^22 rows exactly (B = 16, H = 64, the largest head mask,
+    N = 4096, bf16, fixed heads on mask bits 0 and 63): the whole scratch
+    array is used, and the result is bit-identical to the workspace entry
+    point's.  Inputs are drawn on the device from a seeded generator."""
+    torch = torch_cuda()
+    from paper_2609_34650_amd import binding
+    B, H, N, d = 16, 64, 4096, 64
+    assert B * H * N == 1 << 22
+    announce(f"noalloc at the limit B={B} H={H} N={N}")
+    dev = torch.device("cuda", 0)
+    gen_ = torch.Generator(device=dev).manual_seed(1337)
+    t = {k: torch.randn((B, H, N, d), generator=gen_, device=dev).to(torch.bfloat16) for k in ("Q", "K", "V", "dO")}
+    flags = np.zeros(H, np.uint8)
+    flags[[0, 63]] = 1
+    t["is_fixed"] = flags
+    t["a"] = torch.randn((H, N), generator=gen_, device=dev)
+    t["r"] = -torch.log1p(torch.arange(N, device=dev, dtype=torch.float32)).expand(H, N).contiguous()
+    O, LSE = binding.saf_hybrid_attn_fwd(t["Q"], t["K"], t["V"], t["is_fixed"], t["a"], t["r"])
+    ref = _grads(binding, t, O, LSE, noalloc=False)
+    got = _grads(binding, t, O, LSE, noalloc=True)
+    torch.cuda.synchronize()
+    for name, g, r in zip(("dQ", "dK", "dV"), got, ref):
+        assert torch.isfinite(r).all(), name
+        assert torch.equal(g, r), f"{name} differs from saf_hybrid_attn_bwd at the scratch limit"
